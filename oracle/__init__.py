@@ -1,0 +1,45 @@
+"""CPU oracle for the BASE-layer balanced assignment path.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path imports, calls, links
+or executes anything under this directory; only the tests, the smoke check
+and the benchmark's CPU-baseline leg do. It shares no code with the GPU
+path: its own C sources (plain C, gcc), numpy and scipy.
+
+What it computes, each function citing the passage it follows:
+  affinity          token-expert scores h_t . w_e in fp64        (Sec. 3.1, Eq. 2)
+  solve_ssp         exact optimum of the balanced assignment    (Sec. 3.2.1, Eq. 2)
+  solve_hungarian   the same on the expert-replicated matrix    (Sec. 3.2.1, Eq. 2)
+  solve_bruteforce  the same by enumeration, tiny inputs        (Sec. 3.2.1, Eq. 2)
+  greedy_argmax     test-time assignment, best expert per token (Sec. 3.2.2)
+  dual_bound        LP-duality upper bound of Eq. 2 for prices p
+  optimum_gap       second-best gap / uniqueness of an optimum
+  stable_perm       sort vector grouping tokens by expert        (Fig. 2 caption)
+  gather / scatter  routing into expert-contiguous rows and back (Fig. 2, Sec. 3)
+"""
+from .affinity import affinity
+from .assign import (
+    balanced_counts_ok,
+    dual_bound,
+    greedy_argmax,
+    objective,
+    optimum_gap,
+    solve_bruteforce,
+    solve_hungarian,
+    solve_ssp,
+)
+from .permute import gather, scatter, stable_perm
+
+__all__ = [
+    "affinity",
+    "balanced_counts_ok",
+    "dual_bound",
+    "gather",
+    "greedy_argmax",
+    "objective",
+    "optimum_gap",
+    "scatter",
+    "solve_bruteforce",
+    "solve_hungarian",
+    "solve_ssp",
+    "stable_perm",
+]
