@@ -1,0 +1,191 @@
+/*
+ * base.h -- C ABI of the balanced token-to-expert assignment path of BASE
+ * layers (Lewis et al., "BASE Layers: Simplifying Training of Large, Sparse
+ * Models", ICML 2021), built for AMD Instinct MI355X (gfx950).
+ *
+ * The path has three calls, in the order a BASE layer makes them during
+ * training (Sec. 3, Fig. 2):
+ *   base_affinity  token-expert scores S = H . W^T              (Sec. 3.1, Eq. 2)
+ *   base_assign    balanced assignment maximising sum_t S[t,a_t],
+ *                  every expert receiving exactly T/E tokens     (Sec. 3.2.1, Eq. 2)
+ *   base_permute   rows routed into expert-contiguous order and back
+ *                  (Fig. 2 caption; Sec. 3, third stage)
+ *
+ * Conventions shared by every entry point
+ *   - Pointers marked [device] are HIP device pointers (hipMalloc / torch
+ *     CUDA tensors); [host] pointers are ordinary host memory.
+ *   - Matrices are dense, row-major, contiguous. Index ranges are half-open:
+ *     tokens t in [0, T), experts e in [0, E).
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Work is enqueued on it and the call returns without waiting, except
+ *     where a flag below asks for a synchronous result.
+ *   - The caller owns every buffer. The library allocates no device memory
+ *     in these calls and keeps no state between calls beyond the loaded
+ *     kernels of each device.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     call that returns an error has enqueued nothing, unless the error is
+ *     BASE_ERR_HIP or one reported by a synchronous flag. Outputs are
+ *     unspecified after an error.
+ *   - Device buffers must be 16-byte aligned.
+ *   - Calls on one stream are ordered; calls that share a workspace must not
+ *     run concurrently on different streams.
+ */
+#ifndef BASE_MI355X_H
+#define BASE_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every int-valued entry point. */
+typedef enum {
+    BASE_OK = 0,
+    BASE_ERR_INVALID_ARG = -1,      /* null pointer, size <= 0, misaligned pointer, bad option */
+    BASE_ERR_NOT_DIVISIBLE = -2,    /* T is not a multiple of E (Eq. 2 needs T/E tokens per expert) */
+    BASE_ERR_UNSUPPORTED_DTYPE = -3,/* dtype not accepted by this entry point */
+    BASE_ERR_NONFINITE = -4,        /* a score is NaN or infinite (only with BASE_ASSIGN_CHECK_FINITE) */
+    BASE_ERR_NOT_CONVERGED = -5,    /* the round limit was reached before every expert was full */
+    BASE_ERR_WORKSPACE = -6,        /* workspace missing or smaller than base_assign_workspace_size */
+    BASE_ERR_HIP = -7,              /* a HIP runtime call failed */
+    BASE_ERR_RANGE = -8             /* a size or value outside what the kernels represent */
+} base_status;
+
+/* Element types. BASE_I16 is accepted for scores only (the integer variant). */
+typedef enum { BASE_F32 = 0, BASE_BF16 = 1, BASE_I16 = 2 } base_dtype;
+
+/* Returns a static, human-readable name for a status code. Never NULL. */
+const char *base_status_string(int status);
+
+/* ------------------------------------------------------------------------ */
+/* base_affinity: S[t, e] = sum_k H[t, k] * W[e, k]                          */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. 3.1 and Eq. 2: the score of token t for expert e is the dot product of
+ * the token representation h_t and the expert embedding w_e. No sigmoid,
+ * softmax or bias is applied (the sigmoid of Eq. 1 gates the expert output,
+ * not the assignment).
+ *
+ *   H  [device] T x d, in_dtype (BASE_BF16 or BASE_F32), row-major
+ *   W  [device] E x d, same dtype as H, row-major
+ *   S  [device] T x E float32, row-major, written entirely
+ *   T, E, d > 0; T, E <= 2^31 - 1; d % 8 == 0
+ *
+ * Arithmetic: BASE_BF16 multiplies bf16 values on the matrix cores and
+ * accumulates in fp32; BASE_F32 multiplies and accumulates in fp32 (no
+ * reduced-precision products). The summation order over k is unspecified.
+ * Errors: BASE_ERR_INVALID_ARG (null/misaligned pointer, size <= 0,
+ * d % 8 != 0), BASE_ERR_UNSUPPORTED_DTYPE, BASE_ERR_RANGE, BASE_ERR_HIP.
+ */
+int base_affinity(const void *H, const void *W, float *S, int64_t T, int64_t E, int64_t d,
+                  int in_dtype, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* base_assign: balanced assignment of Eq. 2                                  */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. 3.2.1, Eq. 2: choose a_t in [0, E) maximising sum_t S[t, a_t] subject to
+ * every expert receiving exactly C = T/E tokens. The paper solves it with an
+ * auction algorithm (Sec. 3.2.1; appendix figure on the assignment algorithm).
+ * This implementation is a forward auction with epsilon scaling in which
+ * every expert is C identical objects: each round, every unassigned token
+ * bids for its best expert (top-2 over the values S[t,e] - p[e]); each expert
+ * keeps its C highest bids (ties: lower token index wins), evicts the rest,
+ * and once full sets its price to its lowest held bid. A phase ends when
+ * every expert holds C tokens; epsilon then shrinks by eps_factor until
+ * eps_final. The result satisfies epsilon-complementary slackness with the
+ * returned prices, so
+ *     sum_t max_e (S[t,e] - p[e]) + C * sum_e p[e] - sum_t S[t, a_t] <= T * eps_final
+ * (up to fp32 rounding in float mode), i.e. the assignment is within
+ * T * eps_final of the optimum.
+ *
+ * Integer mode (s_dtype == BASE_I16): scores are int16; the solve runs in
+ * int64 on the scores scaled by K = 2^ceil(log2(T + 1)) with eps_final = 1
+ * (one scaled unit, 1/K of a score unit), so T * eps_final < 1 score unit and
+ * the assignment is an exact optimum of Eq. 2. Requires T < 2^21.
+ *
+ *   S          [device] T x E scores, s_dtype (BASE_F32 or BASE_I16), row-major
+ *   T, E       T > 0, E > 0, T % E == 0, T < 2^24
+ *   opts       [host] options, NULL for the defaults below
+ *   assign     [device] int32 [T] out: a_t in [0, E)
+ *   perm       [device] int32 [T] out: the sort vector of Fig. 2; perm[k] is
+ *              the token placed at row k when tokens are grouped by expert in
+ *              ascending expert order and ascending token order inside an
+ *              expert, so rows [e*C, (e+1)*C) hold expert e's tokens
+ *   prices     [device] out, may be NULL: E float32 (float mode) or E int64
+ *              (integer mode, in scaled units); the dual prices certifying
+ *              the bound above
+ *   workspace  [device] at least base_assign_workspace_size(T, E) bytes,
+ *              256-byte aligned; contents on entry are ignored
+ *   stats      [host] out, may be NULL; filled only with BASE_ASSIGN_SYNC_STATS
+ *
+ * Errors: BASE_ERR_INVALID_ARG, BASE_ERR_NOT_DIVISIBLE, BASE_ERR_UNSUPPORTED_DTYPE,
+ * BASE_ERR_WORKSPACE, BASE_ERR_RANGE, BASE_ERR_HIP; with BASE_ASSIGN_SYNC_STATS
+ * also BASE_ERR_NOT_CONVERGED (max_rounds reached without the fallback flag)
+ * and BASE_ERR_RANGE (a price left the representable range); with
+ * BASE_ASSIGN_CHECK_FINITE also BASE_ERR_NONFINITE.
+ */
+enum {
+    BASE_ASSIGN_GREEDY_FALLBACK = 1, /* when max_rounds is reached, fill the free slots
+                                        with the still-unassigned tokens (balance kept,
+                                        the epsilon bound void; stats.fell_back = 1) */
+    BASE_ASSIGN_SYNC_STATS = 2,      /* wait for the solve, fill *stats, report
+                                        NOT_CONVERGED / RANGE */
+    BASE_ASSIGN_CHECK_FINITE = 4     /* scan S first (synchronous); NaN/Inf -> BASE_ERR_NONFINITE */
+};
+
+typedef struct {
+    double eps_final;    /* float mode: final epsilon in score units; <= 0 -> 1e-4.
+                            Ignored in integer mode (always 1 scaled unit). */
+    double eps_initial;  /* first-phase epsilon; <= 0 -> (max S - min S) / 8 computed on the device */
+    double eps_factor;   /* epsilon divisor between phases; <= 1 -> 8 */
+    int32_t max_rounds;  /* bound on bidding rounds over all phases; <= 0 -> 4,000,000 */
+    uint32_t flags;      /* BASE_ASSIGN_* */
+} base_assign_opts;
+
+typedef struct {
+    int32_t phases;      /* epsilon phases run */
+    int32_t rounds;      /* bidding rounds over all phases */
+    int64_t bids;        /* bids placed over all phases */
+    double eps_final;    /* epsilon of the last phase, in score units */
+    int32_t fell_back;   /* 1 if the greedy completion was used */
+    int32_t converged;   /* 1 if every expert holds exactly T/E tokens */
+} base_assign_stats;
+
+/* Bytes of device workspace base_assign needs for T tokens and E experts
+ * (0 if T or E is not positive). */
+size_t base_assign_workspace_size(int64_t T, int64_t E);
+
+int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_assign_opts *opts,
+                int32_t *assign, int32_t *perm, void *prices, void *workspace,
+                size_t workspace_bytes, base_assign_stats *stats, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* base_permute: route rows into expert-contiguous order, or back            */
+/* ------------------------------------------------------------------------ */
+/*
+ * Fig. 2 caption: the assignment vector sorts tokens by expert so that row k
+ * of the sorted features goes to expert floor(k E / T). Sec. 3: the expert
+ * output returns to the token's original position afterwards.
+ *
+ *   in, out  [device] T x d rows of dtype (BASE_BF16 or BASE_F32); must not overlap
+ *   perm     [device] int32 [T], a permutation of [0, T) (e.g. from base_assign)
+ *   inverse  0: out[k, :] = in[perm[k], :]   (gather into expert order)
+ *            1: out[perm[k], :] = in[k, :]   (scatter back to token order)
+ *   T > 0, d > 0, d % 8 == 0
+ *
+ * Rows are copied bit for bit. perm is not checked on the device: an entry
+ * outside [0, T) is undefined behaviour, a repeated entry leaves rows of out
+ * unwritten (gather) or written twice (scatter).
+ * Errors: BASE_ERR_INVALID_ARG, BASE_ERR_UNSUPPORTED_DTYPE, BASE_ERR_RANGE, BASE_ERR_HIP.
+ */
+int base_permute(const void *in, const int32_t *perm, void *out, int64_t T, int64_t d, int dtype,
+                 int inverse, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BASE_MI355X_H */

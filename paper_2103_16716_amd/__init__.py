@@ -1,0 +1,206 @@
+"""Balanced token-to-expert assignment of BASE layers on AMD Instinct MI355X.
+
+Python binding of the C ABI in include/base.h (libbase_mi355x.so, built from
+csrc/ by `python -m paper_2103_16716_amd.build`). The functions below only
+marshal torch tensors into the C calls; every step of the path runs in the
+library's HIP kernels. There is no fallback: if the library is missing or
+fails to load, every call raises.
+
+    S = affinity(H, W)                 # Sec. 3.1 / Eq. 2: S[t, e] = h_t . w_e
+    res = assign(S)                    # Sec. 3.2.1 / Eq. 2: balanced assignment
+    X = permute(H, res.perm)           # Fig. 2: rows grouped by expert
+    Y = permute(X, res.perm, inverse=True)   # Sec. 3: back to token order
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libbase_mi355x.so")
+
+# Status codes and enums of include/base.h.
+BASE_OK = 0
+BASE_ERR_INVALID_ARG = -1
+BASE_ERR_NOT_DIVISIBLE = -2
+BASE_ERR_UNSUPPORTED_DTYPE = -3
+BASE_ERR_NONFINITE = -4
+BASE_ERR_NOT_CONVERGED = -5
+BASE_ERR_WORKSPACE = -6
+BASE_ERR_HIP = -7
+BASE_ERR_RANGE = -8
+
+BASE_F32 = 0
+BASE_BF16 = 1
+BASE_I16 = 2
+
+BASE_ASSIGN_GREEDY_FALLBACK = 1
+BASE_ASSIGN_SYNC_STATS = 2
+BASE_ASSIGN_CHECK_FINITE = 4
+
+# Every symbol include/base.h declares.
+EXPORTED = ("base_status_string", "base_affinity", "base_assign_workspace_size", "base_assign",
+            "base_permute")
+
+
+class AssignOpts(ctypes.Structure):
+    _fields_ = [("eps_final", ctypes.c_double), ("eps_initial", ctypes.c_double),
+                ("eps_factor", ctypes.c_double), ("max_rounds", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
+
+
+class AssignStats(ctypes.Structure):
+    _fields_ = [("phases", ctypes.c_int32), ("rounds", ctypes.c_int32), ("bids", ctypes.c_int64),
+                ("eps_final", ctypes.c_double), ("fell_back", ctypes.c_int32),
+                ("converged", ctypes.c_int32)]
+
+
+class BaseError(RuntimeError):
+    """A non-zero status returned by the library."""
+
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run `python -m paper_2103_16716_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+        L.base_status_string.argtypes = [i32]
+        L.base_status_string.restype = ctypes.c_char_p
+        L.base_affinity.argtypes = [vp, vp, vp, i64, i64, i64, i32, vp]
+        L.base_affinity.restype = i32
+        L.base_assign_workspace_size.argtypes = [i64, i64]
+        L.base_assign_workspace_size.restype = ctypes.c_size_t
+        L.base_assign.argtypes = [vp, i32, i64, i64, ctypes.POINTER(AssignOpts), vp, vp, vp, vp,
+                                  ctypes.c_size_t, ctypes.POINTER(AssignStats), vp]
+        L.base_assign.restype = i32
+        L.base_permute.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
+        L.base_permute.restype = i32
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().base_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != BASE_OK:
+        raise BaseError(status, where)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return BASE_BF16
+    if t.dtype == torch.float32:
+        return BASE_F32
+    if t.dtype == torch.int16:
+        return BASE_I16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream_ptr(stream) -> int:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _need_device(*ts) -> None:
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("tensors must be on the GPU")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+
+
+def affinity(H, W, out=None, stream=None):
+    """S = H . W^T as float32 [T, E] (base_affinity)."""
+    torch = _torch()
+    _need_device(H, W)
+    T, d = H.shape
+    E, d2 = W.shape
+    if d != d2 or H.dtype != W.dtype:
+        raise ValueError("H [T, d] and W [E, d] must share d and dtype")
+    if out is None:
+        out = torch.empty((T, E), dtype=torch.float32, device=H.device)
+    _need_device(out)
+    _check(lib().base_affinity(H.data_ptr(), W.data_ptr(), out.data_ptr(), T, E, d,
+                               _dtype_code(H), _stream_ptr(stream)), "base_affinity")
+    return out
+
+
+def assign_workspace_size(T: int, E: int) -> int:
+    return int(lib().base_assign_workspace_size(T, E))
+
+
+@dataclasses.dataclass
+class AssignResult:
+    assign: object      # int32 [T]
+    perm: object        # int32 [T]
+    prices: object      # float32 [E] (int64 [E] in integer mode)
+    stats: AssignStats | None
+
+
+def assign(S, *, eps_final: float = 0.0, eps_initial: float = 0.0, eps_factor: float = 0.0,
+           max_rounds: int = 0, flags: int = 0, sync_stats: bool = True, workspace=None,
+           out_assign=None, out_perm=None, out_prices=None, stream=None) -> AssignResult:
+    """Balanced assignment of Eq. 2 (base_assign). Zero-valued options take
+    the library defaults. With sync_stats (the default) the call waits for the
+    solve and returns its statistics; pass False to keep it asynchronous."""
+    torch = _torch()
+    _need_device(S)
+    T, E = S.shape
+    dev = S.device
+    integer = S.dtype == torch.int16
+    if out_assign is None:
+        out_assign = torch.empty(T, dtype=torch.int32, device=dev)
+    if out_perm is None:
+        out_perm = torch.empty(T, dtype=torch.int32, device=dev)
+    if out_prices is None:
+        out_prices = torch.empty(E, dtype=torch.int64 if integer else torch.float32, device=dev)
+    ws_bytes = assign_workspace_size(T, E)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    opts = AssignOpts(eps_final, eps_initial, eps_factor, max_rounds,
+                      flags | (BASE_ASSIGN_SYNC_STATS if sync_stats else 0))
+    stats = AssignStats()
+    _check(lib().base_assign(S.data_ptr(), _dtype_code(S), T, E, ctypes.byref(opts),
+                             out_assign.data_ptr(), out_perm.data_ptr(), out_prices.data_ptr(),
+                             workspace.data_ptr(), workspace.numel(), ctypes.byref(stats),
+                             _stream_ptr(stream)), "base_assign")
+    return AssignResult(out_assign, out_perm, out_prices, stats if sync_stats else None)
+
+
+def permute(x, perm, inverse: bool = False, out=None, stream=None):
+    """Gather rows into expert order (out[k] = x[perm[k]]) or, with inverse,
+    scatter them back (out[perm[k]] = x[k]) (base_permute)."""
+    torch = _torch()
+    _need_device(x, perm)
+    T, d = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    _need_device(out)
+    _check(lib().base_permute(x.data_ptr(), perm.data_ptr(), out.data_ptr(), T, d, _dtype_code(x),
+                              1 if inverse else 0, _stream_ptr(stream)), "base_permute")
+    return out
+
+
+__all__ = ["affinity", "assign", "permute", "assign_workspace_size", "AssignResult", "AssignOpts",
+           "AssignStats", "BaseError", "lib", "status_string", "EXPORTED"]

@@ -1,0 +1,168 @@
+// C ABI of the assignment path: argument validation on the host, then the
+// HIP launchers. Nothing is enqueued when validation fails.
+#include <math.h>
+#include <stdint.h>
+
+#include "base.h"
+#include "internal.hpp"
+
+namespace {
+
+constexpr int64_t kMaxTokens = (int64_t)1 << 24;      // token index field of a bid key
+constexpr int64_t kMaxTokensInt = (int64_t)1 << 21;   // integer mode: scaled scores stay < 2^37
+constexpr int64_t kMaxExperts = 2048;                 // per-expert tables staged in LDS
+constexpr int64_t kMaxDim = (int64_t)1 << 30;
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? BASE_OK : BASE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char *base_status_string(int status) {
+    switch (status) {
+        case BASE_OK: return "ok";
+        case BASE_ERR_INVALID_ARG: return "invalid argument";
+        case BASE_ERR_NOT_DIVISIBLE: return "T is not a multiple of E";
+        case BASE_ERR_UNSUPPORTED_DTYPE: return "unsupported dtype";
+        case BASE_ERR_NONFINITE: return "non-finite score";
+        case BASE_ERR_NOT_CONVERGED: return "assignment did not converge within max_rounds";
+        case BASE_ERR_WORKSPACE: return "workspace missing or too small";
+        case BASE_ERR_HIP: return "HIP runtime error";
+        case BASE_ERR_RANGE: return "size or value out of the supported range";
+        default: return "unknown status";
+    }
+}
+
+int base_affinity(const void *H, const void *W, float *S, int64_t T, int64_t E, int64_t d,
+                  int in_dtype, void *stream) {
+    if (H == nullptr || W == nullptr || S == nullptr) return BASE_ERR_INVALID_ARG;
+    if (T <= 0 || E <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
+    if (!aligned(H, 16) || !aligned(W, 16) || !aligned(S, 16)) return BASE_ERR_INVALID_ARG;
+    if (in_dtype != BASE_BF16 && in_dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
+    if (T > INT32_MAX || E > 65535 * 128 || d > kMaxDim) return BASE_ERR_RANGE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (in_dtype == BASE_BF16)
+        return hip_status(base::launch_affinity_bf16(static_cast<const uint16_t *>(H),
+                                                     static_cast<const uint16_t *>(W), S, T, E, d,
+                                                     s));
+    return hip_status(base::launch_affinity_f32(static_cast<const float *>(H),
+                                                static_cast<const float *>(W), S, T, E, d, s));
+}
+
+size_t base_assign_workspace_size(int64_t T, int64_t E) {
+    if (T <= 0 || E <= 0 || T % E != 0 || T >= kMaxTokens || E > kMaxExperts) return 0;
+    return base::assign_workspace_size(T, E);
+}
+
+int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_assign_opts *opts,
+                int32_t *assign, int32_t *perm, void *prices, void *workspace,
+                size_t workspace_bytes, base_assign_stats *stats, void *stream) {
+    if (S == nullptr || assign == nullptr || perm == nullptr) return BASE_ERR_INVALID_ARG;
+    if (T <= 0 || E <= 0) return BASE_ERR_INVALID_ARG;
+    if (s_dtype != BASE_F32 && s_dtype != BASE_I16) return BASE_ERR_UNSUPPORTED_DTYPE;
+    if (T % E != 0) return BASE_ERR_NOT_DIVISIBLE;
+    const bool integer = s_dtype == BASE_I16;
+    if (T >= kMaxTokens || E > kMaxExperts) return BASE_ERR_RANGE;
+    if (integer && T >= kMaxTokensInt) return BASE_ERR_RANGE;
+    if (!aligned(S, 16) || !aligned(assign, 4) || !aligned(perm, 4)) return BASE_ERR_INVALID_ARG;
+    if (prices != nullptr && !aligned(prices, integer ? 8 : 4)) return BASE_ERR_INVALID_ARG;
+
+    base_assign_opts o{1e-4, 0.0, 8.0, 4000000, 0u};
+    if (opts != nullptr) {
+        o = *opts;
+        if (isnan(o.eps_final) || isnan(o.eps_initial) || isnan(o.eps_factor) ||
+            isinf(o.eps_final) || isinf(o.eps_initial) || isinf(o.eps_factor))
+            return BASE_ERR_INVALID_ARG;
+        if (!(o.eps_final > 0.0)) o.eps_final = 1e-4;
+        if (!(o.eps_factor > 1.0)) o.eps_factor = 8.0;
+        if (o.max_rounds <= 0) o.max_rounds = 4000000;
+        const uint32_t known =
+            BASE_ASSIGN_GREEDY_FALLBACK | BASE_ASSIGN_SYNC_STATS | BASE_ASSIGN_CHECK_FINITE;
+        if (o.flags & ~known) return BASE_ERR_INVALID_ARG;
+    }
+
+    const size_t need = base::assign_workspace_size(T, E);
+    if (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 256))
+        return BASE_ERR_WORKSPACE;
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    base::AssignParams p{};
+    p.T = T;
+    p.E = E;
+    p.C = T / E;
+    p.integer = integer;
+    p.scale = 1;
+    if (integer) {
+        int64_t K = 1;
+        while (K < T + 1) K <<= 1;
+        p.scale = K;
+        p.eps_final = 1.0;
+        p.eps_initial = o.eps_initial > 0.0 ? floor(o.eps_initial * (double)K) : 0.0;
+    } else {
+        p.eps_final = o.eps_final;
+        p.eps_initial = o.eps_initial;
+    }
+    p.eps_factor = o.eps_factor;
+    p.max_rounds = o.max_rounds;
+    p.flags = o.flags;
+
+    if ((o.flags & BASE_ASSIGN_CHECK_FINITE) && !integer) {
+        int bad = 0;
+        hipError_t e = base::check_scores_finite(static_cast<const float *>(S), T * E, workspace,
+                                                 &bad, s);
+        if (e != hipSuccess) return BASE_ERR_HIP;
+        if (bad) return BASE_ERR_NONFINITE;
+    }
+
+    hipError_t e = base::launch_assign(S, p, assign, perm, prices, workspace, s);
+    if (e != hipSuccess) return BASE_ERR_HIP;
+
+    if (o.flags & BASE_ASSIGN_SYNC_STATS) {
+        base::SolveCtrl c{};
+        e = base::read_assign_stats(workspace, T, E, &c, s);
+        if (e != hipSuccess) return BASE_ERR_HIP;
+        const int unconverged = c.unconverged_experts & ~(1 << 30);
+        if (stats != nullptr) {
+            stats->phases = c.phase;
+            stats->rounds = c.rounds;
+            stats->bids = (int64_t)c.bids;
+            stats->eps_final = integer ? c.eps / (double)p.scale : c.eps;
+            stats->fell_back = c.fell_back;
+            stats->converged = (E == 1) || (unconverged == 0 && !c.not_converged) ? 1 : 0;
+            if (E == 1) {
+                stats->phases = 0;
+                stats->rounds = 0;
+                stats->bids = 0;
+                stats->eps_final = 0.0;
+                stats->fell_back = 0;
+            }
+        }
+        if (E > 1) {
+            if (c.overflow) return BASE_ERR_RANGE;
+            if (unconverged != 0 || (c.not_converged && !c.fell_back)) return BASE_ERR_NOT_CONVERGED;
+        }
+    }
+    return BASE_OK;
+}
+
+int base_permute(const void *in, const int32_t *perm, void *out, int64_t T, int64_t d, int dtype,
+                 int inverse, void *stream) {
+    if (in == nullptr || perm == nullptr || out == nullptr) return BASE_ERR_INVALID_ARG;
+    if (T <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
+    if (inverse != 0 && inverse != 1) return BASE_ERR_INVALID_ARG;
+    if (!aligned(in, 16) || !aligned(out, 16) || !aligned(perm, 4)) return BASE_ERR_INVALID_ARG;
+    if (dtype != BASE_BF16 && dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
+    if (T > INT32_MAX || d > kMaxDim) return BASE_ERR_RANGE;
+    const int64_t row_bytes = d * (dtype == BASE_BF16 ? 2 : 4);
+    const char *ib = static_cast<const char *>(in);
+    const char *ob = static_cast<const char *>(out);
+    const int64_t bytes = T * row_bytes;
+    if (ib < ob + bytes && ob < ib + bytes) return BASE_ERR_INVALID_ARG;   // overlap
+    return hip_status(
+        base::launch_permute(in, perm, out, T, row_bytes, inverse, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

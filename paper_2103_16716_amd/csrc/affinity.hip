@@ -1,0 +1,192 @@
+// Token-expert affinity S = H . W^T (Sec. 3.1, Eq. 2), S[t, e] = h_t . w_e.
+//
+// bf16 path: a tiled GEMM on the CDNA4 matrix cores (v_mfma_f32_32x32x16_bf16,
+// fp32 accumulation). The contraction dimension is the model dimension d,
+// contiguous in both H and W, so both operands are loaded the same way: eight
+// bf16 of one row per 16-byte vector. A block owns 64 tokens x 128 experts;
+// H is streamed from HBM exactly once, W (at most a few MiB) is re-read from
+// L2 by every block. The GEMM is bandwidth-bound at every shape of interest
+// (arithmetic intensity about 2E/(2+4E/d) flop per byte, well below the MFMA
+// ridge), so the kernel is organised around keeping HBM reads in flight:
+// the next K-chunk is fetched into registers while the current one is
+// multiplied out of LDS.
+//
+// fp32 path: a plain LDS-tiled FMA kernel (fp32 products and sums, no
+// reduced-precision matrix instructions).
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace base {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kBM = 64;             // tokens per block
+constexpr int kBN = 128;            // experts per block
+constexpr int kBK = 64;             // bf16 elements of d per chunk
+constexpr int kLdsRow = kBK + 8;    // padded LDS row (elements): 144 B, shifts 4 banks per row
+
+__global__ __launch_bounds__(256) void affinity_bf16_kernel(const uint16_t *__restrict__ H,
+                                                            const uint16_t *__restrict__ W,
+                                                            float *__restrict__ S, int T, int E,
+                                                            int d) {
+    __shared__ __attribute__((aligned(16))) uint16_t As[kBM * kLdsRow];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[kBN * kLdsRow];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int m0 = blockIdx.x * kBM;
+    const int n0 = blockIdx.y * kBN;
+
+    // Global -> register staging: chunk c covers row c/8, elements (c%8)*8 .. +8.
+    uint4 ra[2], rb[4];
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int c = tid + 256 * i;
+            const int r = c >> 3;
+            const int k = k0 + (c & 7) * 8;
+            ra[i] = make_uint4(0, 0, 0, 0);
+            if (m0 + r < T && k < d)
+                ra[i] = *reinterpret_cast<const uint4 *>(H + (int64_t)(m0 + r) * d + k);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 256 * i;
+            const int r = c >> 3;
+            const int k = k0 + (c & 7) * 8;
+            rb[i] = make_uint4(0, 0, 0, 0);
+            if (n0 + r < E && k < d)
+                rb[i] = *reinterpret_cast<const uint4 *>(W + (int64_t)(n0 + r) * d + k);
+        }
+    };
+    auto sstore = [&]() {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int c = tid + 256 * i;
+            *reinterpret_cast<uint4 *>(&As[(c >> 3) * kLdsRow + (c & 7) * 8]) = ra[i];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 256 * i;
+            *reinterpret_cast<uint4 *>(&Bs[(c >> 3) * kLdsRow + (c & 7) * 8]) = rb[i];
+        }
+    };
+
+    // Wave layout: 2 x 2 waves, each 32 tokens x 64 experts = two 32x32 MFMA tiles.
+    const int wm = wave & 1;
+    const int wn = wave >> 1;
+    f32x16_t acc[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[j][i] = 0.0f;
+
+    const int lrow = lane & 31;     // operand row inside a 32-row tile
+    const int lk = (lane >> 5) * 8; // this lane's 8 elements of the 16-wide k step
+
+    gload(0);
+    for (int k0 = 0; k0 < d; k0 += kBK) {
+        __syncthreads();
+        sstore();
+        __syncthreads();
+        if (k0 + kBK < d) gload(k0 + kBK);
+#pragma unroll
+        for (int ks = 0; ks < kBK; ks += 16) {
+            const bf16x8_t a =
+                *reinterpret_cast<const bf16x8_t *>(&As[(32 * wm + lrow) * kLdsRow + ks + lk]);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const bf16x8_t b = *reinterpret_cast<const bf16x8_t *>(
+                    &Bs[(64 * wn + 32 * j + lrow) * kLdsRow + ks + lk]);
+                acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+            }
+        }
+    }
+
+    // 32x32 accumulator layout: lane holds column lane%32; register i holds
+    // row 8*(i/4) + 4*(lane/32) + i%4.
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int e = n0 + 64 * wn + 32 * j + lrow;
+        if (e >= E) continue;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int t = m0 + 32 * wm + 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+            if (t < T) S[(int64_t)t * E + e] = acc[j][i];
+        }
+    }
+}
+
+// fp32: 64 x 64 output tile per block, 16 x 16 threads, 4 x 4 outputs each.
+constexpr int kFT = 64;
+constexpr int kFK = 16;
+
+__global__ __launch_bounds__(256) void affinity_f32_kernel(const float *__restrict__ H,
+                                                           const float *__restrict__ W,
+                                                           float *__restrict__ S, int T, int E,
+                                                           int d) {
+    __shared__ float As[kFK][kFT + 4];   // As[k][token]
+    __shared__ float Bs[kFK][kFT + 4];   // Bs[k][expert]
+    const int tid = threadIdx.x;
+    const int tx = tid & 15, ty = tid >> 4;
+    const int m0 = blockIdx.x * kFT, n0 = blockIdx.y * kFT;
+    // Loader: thread covers row tid/4, elements (tid%4)*4 .. +4 of the chunk.
+    const int lr = tid >> 2, lk = (tid & 3) * 4;
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < d; k0 += kFK) {
+        float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+        if (m0 + lr < T && k0 + lk < d)
+            a = *reinterpret_cast<const float4 *>(H + (int64_t)(m0 + lr) * d + k0 + lk);
+        if (n0 + lr < E && k0 + lk < d)
+            b = *reinterpret_cast<const float4 *>(W + (int64_t)(n0 + lr) * d + k0 + lk);
+        __syncthreads();
+        As[lk + 0][lr] = a.x; As[lk + 1][lr] = a.y; As[lk + 2][lr] = a.z; As[lk + 3][lr] = a.w;
+        Bs[lk + 0][lr] = b.x; Bs[lk + 1][lr] = b.y; Bs[lk + 2][lr] = b.z; Bs[lk + 3][lr] = b.w;
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kFK; ++k) {
+            float av[4], bv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) av[i] = As[k][ty * 4 + i];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) bv[j] = Bs[k][tx * 4 + j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int t = m0 + ty * 4 + i;
+        if (t >= T) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int e = n0 + tx * 4 + j;
+            if (e < E) S[(int64_t)t * E + e] = acc[i][j];
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_affinity_bf16(const uint16_t *H, const uint16_t *W, float *S, int64_t T,
+                                int64_t E, int64_t d, hipStream_t stream) {
+    dim3 grid((unsigned)((T + kBM - 1) / kBM), (unsigned)((E + kBN - 1) / kBN));
+    hipLaunchKernelGGL(affinity_bf16_kernel, grid, dim3(256), 0, stream, H, W, S, (int)T, (int)E,
+                       (int)d);
+    return hipGetLastError();
+}
+
+hipError_t launch_affinity_f32(const float *H, const float *W, float *S, int64_t T, int64_t E,
+                               int64_t d, hipStream_t stream) {
+    dim3 grid((unsigned)((T + kFT - 1) / kFT), (unsigned)((E + kFT - 1) / kFT));
+    hipLaunchKernelGGL(affinity_f32_kernel, grid, dim3(256), 0, stream, H, W, S, (int)T, (int)E,
+                       (int)d);
+    return hipGetLastError();
+}
+
+}  // namespace base

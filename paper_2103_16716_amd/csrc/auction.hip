@@ -1,0 +1,908 @@
+// Balanced token-to-expert assignment (Sec. 3.2.1, Eq. 2) by a forward
+// auction with epsilon scaling, every expert being C = T/E identical objects.
+//
+// State (all in the caller's workspace):
+//   prices[E]          expert prices p_e (fp32, or int64 in integer mode)
+//   holders[2][E][C]   each expert's held bid keys (two buffers, per-expert
+//                      selector hsel[e]; hcount[e] valid entries)
+//   bucket[E][cap]     the bids an expert received this round (bcount[e]);
+//                      bids beyond `cap` go to one shared overflow list
+//   active[2][T]       tokens without an expert (ping-pong between rounds)
+//   ctrl               round/phase counters, epsilon, flags
+//
+// One round:
+//   bid     every active token t finds its best and second-best values
+//           v_e = S[t,e] - p_e over all experts and bids S[t,e1] - v2 + eps
+//           for its best expert e1 (lowest index on ties).
+//   update  every expert that received bids keeps the C highest keys among
+//           its holders and the new bids (ties: lower token index), sends
+//           the others back to the active list, and, once full, sets its
+//           price to its lowest held bid.
+// A phase ends when no token is active (every expert holds C); epsilon is
+// then divided by eps_factor down to eps_final and all tokens bid again
+// against the prices reached so far.
+//
+// Invariant behind the guarantee: a held token's bid was computed against
+// prices no higher than the current ones and its expert's price never
+// exceeds that bid, so S[t,a_t] - p[a_t] >= max_e (S[t,e] - p_e) - eps for
+// every token; summed over tokens this bounds the distance to the optimum by
+// T * eps.
+//
+// Execution: the first rounds of a phase (many active tokens) run as grid-wide
+// bid and update kernels; the remaining rounds, which typically have a
+// handful of active tokens each, run inside one workgroup that loops with
+// block barriers instead of kernel launches.
+#include <math.h>
+
+#include "common.hpp"
+#include "internal.hpp"
+#include "base.h"
+
+namespace base {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kCandLds = 4096;   // candidates of one expert staged in LDS when they fit
+constexpr int kCountTile = 256;  // tokens per block in the permutation build
+
+inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+    size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
+        total;
+    int64_t cap, nblk;
+};
+
+Layout make_layout(int64_t T, int64_t E) {
+    Layout L{};
+    const int64_t C = T / E;
+    L.cap = 16 * C + 4096;
+    if (L.cap > T) L.cap = T;
+    L.nblk = (T + kCountTile - 1) / kCountTile;
+    size_t off = 0;
+    L.ctrl = off;    off += align_up(sizeof(SolveCtrl));
+    L.prices = off;  off += align_up((size_t)E * 8);
+    L.hcount = off;  off += align_up((size_t)E * 4);
+    L.hsel = off;    off += align_up((size_t)E * 4);
+    L.bcount = off;  off += align_up((size_t)E * 4);
+    L.holders = off; off += align_up((size_t)2 * T * 8);
+    L.bucket = off;  off += align_up((size_t)E * L.cap * 8);
+    L.ovf_key = off; off += align_up((size_t)T * 8);
+    L.ovf_exp = off; off += align_up((size_t)T * 4);
+    L.active = off;  off += align_up((size_t)2 * T * 4);
+    L.blk = off;     off += align_up((size_t)L.nblk * E * 4);
+    L.total = off;
+    return L;
+}
+
+template <class M>
+struct Ctx {
+    using value_t = typename M::value_t;
+    const typename M::score_t *S;
+    int T, E, C, cap;
+    int64_t scale;
+    SolveCtrl *ctrl;
+    value_t *prices;
+    int *hcount, *hsel, *bcount;
+    uint64_t *holders, *bucket, *ovf_key;
+    int *ovf_exp, *active;
+    int *ovf_count;   // lives in ctrl->pad0
+};
+
+template <class M>
+Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
+    const Layout L = make_layout(p.T, p.E);
+    Ctx<M> c;
+    c.S = static_cast<const typename M::score_t *>(S);
+    c.T = (int)p.T;
+    c.E = (int)p.E;
+    c.C = (int)p.C;
+    c.cap = (int)L.cap;
+    c.scale = p.scale;
+    c.ctrl = reinterpret_cast<SolveCtrl *>(ws + L.ctrl);
+    c.prices = reinterpret_cast<typename M::value_t *>(ws + L.prices);
+    c.hcount = reinterpret_cast<int *>(ws + L.hcount);
+    c.hsel = reinterpret_cast<int *>(ws + L.hsel);
+    c.bcount = reinterpret_cast<int *>(ws + L.bcount);
+    c.holders = reinterpret_cast<uint64_t *>(ws + L.holders);
+    c.bucket = reinterpret_cast<uint64_t *>(ws + L.bucket);
+    c.ovf_key = reinterpret_cast<uint64_t *>(ws + L.ovf_key);
+    c.ovf_exp = reinterpret_cast<int *>(ws + L.ovf_exp);
+    c.active = reinterpret_cast<int *>(ws + L.active);
+    c.ovf_count = &c.ctrl->pad0;
+    return c;
+}
+
+// ---------------------------------------------------------------- helpers --
+
+__device__ inline int lane_id() { return threadIdx.x & 63; }
+
+// Counters that other waves update with atomics are read with atomic loads so
+// that no stale cached copy is used.
+__device__ inline int ld_relaxed(const int *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline uint64_t lanemask_lt() {
+    const int l = lane_id();
+    return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+
+// Appends `tok` to active list `which` for every lane with want == true.
+// Must be reached by all lanes of the wave together.
+template <class M>
+__device__ inline void append_active(const Ctx<M> &c, int which, bool want, int tok) {
+    const uint64_t mask = __ballot(want);
+    if (mask == 0) return;
+    const int leader = __ffsll((long long)mask) - 1;
+    int base = 0;
+    if (lane_id() == leader) base = atomicAdd(&c.ctrl->active_count[which], __popcll(mask));
+    base = __shfl(base, leader);
+    if (want) c.active[(int64_t)which * c.T + base + __popcll(mask & lanemask_lt())] = tok;
+}
+
+// -------------------------------------------------------------------- bid --
+
+// One group of G lanes evaluates one token. VEC: rows are read as 16-byte
+// vectors (E % 8 == 0 for int16, E % 4 == 0 for fp32).
+template <class M, int G>
+__device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const typename M::value_t *pr,
+                                  typename M::value_t &v1, int &e1, typename M::value_t &v2) {
+    using value_t = typename M::value_t;
+    const int gl = lane_id() & (G - 1);
+    v1 = M::lowest();
+    v2 = M::lowest();
+    e1 = 0x7fffffff;
+    if (valid) {
+        const int64_t row = (int64_t)t * c.E;
+        for (int e = gl; e < c.E; e += G) {
+            const value_t v = M::load(c.S, row + e, c.scale) - pr[e];
+            if (v > v1) {
+                v2 = v1;
+                v1 = v;
+                e1 = e;
+            } else if (v > v2) {
+                v2 = v;
+            }
+        }
+    }
+#pragma unroll
+    for (int off = G / 2; off > 0; off >>= 1) {
+        const value_t ov1 = __shfl_xor(v1, off);
+        const int oe1 = __shfl_xor(e1, off);
+        const value_t ov2 = __shfl_xor(v2, off);
+        if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
+            v2 = v1 > ov2 ? v1 : ov2;
+            v1 = ov1;
+            e1 = oe1;
+        } else {
+            v2 = v2 > ov1 ? v2 : ov1;
+        }
+    }
+}
+
+// Bids of active tokens [i0, n) with stride `ngroups` groups. `touched`
+// (LDS, may be null) collects experts receiving their first bid this round.
+template <class M, int G>
+__device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *list,
+                          typename M::value_t eps, const typename M::value_t *pr, int gid,
+                          int ngroups, int *touched, int *ntouched) {
+    using value_t = typename M::value_t;
+    const int gl = lane_id() & (G - 1);
+    const int n_round = ((n + ngroups - 1) / ngroups) * ngroups;
+    for (int i = gid; i < n_round; i += ngroups) {
+        const bool valid = i < n;
+        const int t = valid ? (all_active ? i : list[i]) : 0;
+        value_t v1, v2;
+        int e1;
+        top2_token<M, G>(c, t, valid, pr, v1, e1, v2);
+        if (valid && gl == 0) {
+            if (e1 >= c.E) e1 = 0;   // every value non-finite: any expert, the bid overflows
+            const value_t s1 = M::load(c.S, (int64_t)t * c.E + e1, c.scale);
+            const value_t bid = (c.E > 1) ? (value_t)((s1 - v2) + eps) : (value_t)(s1 + eps);
+            int overflow = 0;
+            const uint64_t key = M::make_key(bid, t, &overflow);
+            if (overflow) c.ctrl->overflow = 1;
+            const int pos = atomicAdd(&c.bcount[e1], 1);
+            if (pos < c.cap) {
+                c.bucket[(int64_t)e1 * c.cap + pos] = key;
+            } else {
+                const int q = atomicAdd(c.ovf_count, 1);
+                c.ovf_key[q] = key;
+                c.ovf_exp[q] = e1;
+            }
+            if (touched != nullptr && pos == 0) touched[atomicAdd(ntouched, 1)] = e1;
+        }
+    }
+}
+
+// ----------------------------------------------------------------- update --
+
+struct UpdateSmem {
+    uint64_t cand[kCandLds];
+    uint32_t hist[256];
+    uint64_t minkey;
+    int sel_digit, need, kept, pos;
+};
+
+// Calls fn(key) for every candidate of expert e (holders, bucket, overflow)
+// with a wave-uniform trip count: fn(key, valid) is called by all lanes.
+template <class M, class F>
+__device__ inline void for_each_candidate(const Ctx<M> &c, int e, const uint64_t *hold, int h,
+                                          int nb, int novf, F fn) {
+    for (int b = 0; b < h; b += blockDim.x) {
+        const int i = b + threadIdx.x;
+        const bool v = i < h;
+        fn(v ? hold[i] : 0ull, v);
+    }
+    const uint64_t *bk = c.bucket + (int64_t)e * c.cap;
+    for (int b = 0; b < nb; b += blockDim.x) {
+        const int i = b + threadIdx.x;
+        const bool v = i < nb;
+        fn(v ? bk[i] : 0ull, v);
+    }
+    for (int b = 0; b < novf; b += blockDim.x) {
+        const int i = b + threadIdx.x;
+        const bool v = i < novf && c.ovf_exp[i] == e;
+        fn(v ? c.ovf_key[i] : 0ull, v);
+    }
+}
+
+// Suffix scan of sm.hist by wave 0: finds the digit holding the need-th
+// largest candidate; stores it in sm.sel_digit and the remaining rank in sm.need.
+__device__ inline void pick_digit(UpdateSmem &sm, int need) {
+    if (threadIdx.x < 64) {
+        const int l = threadIdx.x;
+        // Lane l owns digits 255-4l .. 252-4l (descending).
+        uint32_t h[4];
+        uint32_t s = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            h[j] = sm.hist[255 - 4 * l - j];
+            s += h[j];
+        }
+        // Exclusive prefix (over lanes below l) of the per-lane sums.
+        uint32_t incl = s;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t o = __shfl_up(incl, off);
+            if (l >= off) incl += o;
+        }
+        uint32_t before = incl - s;
+        if ((int)before < need && (int)incl >= need) {
+            uint32_t cum = before;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if ((int)(cum + h[j]) >= need) {
+                    sm.sel_digit = 255 - 4 * l - j;
+                    sm.need = need - (int)cum;
+                    break;
+                }
+                cum += h[j];
+            }
+        }
+    }
+}
+
+// Merges the new bids of expert e into its holder table. Executed by a whole
+// block; `next` is the active list that receives evicted tokens.
+template <class M>
+__device__ void update_expert(const Ctx<M> &c, int e, int next, int novf, UpdateSmem &sm) {
+    const int n = ld_relaxed(&c.bcount[e]);
+    if (n == 0) return;
+    const int h = ld_relaxed(&c.hcount[e]);
+    const int sel = ld_relaxed(&c.hsel[e]);
+    uint64_t *hold = c.holders + (int64_t)sel * c.T + (int64_t)e * c.C;
+    const int nb = n < c.cap ? n : c.cap;
+    const int novf_e = (n > c.cap) ? novf : 0;
+    const int total = h + n;
+    const int tid = threadIdx.x;
+
+    if (total <= c.C) {
+        // Room for every bid: append them after the current holders.
+        if (tid == 0) {
+            sm.pos = h;
+            sm.minkey = ~0ull;
+        }
+        __syncthreads();
+        const uint64_t *bk = c.bucket + (int64_t)e * c.cap;
+        for (int i = tid; i < nb; i += blockDim.x) hold[h + i] = bk[i];
+        if (tid == 0) sm.pos = h + nb;
+        __syncthreads();
+        if (novf_e) {
+            for (int i = tid; i < novf_e; i += blockDim.x)
+                if (c.ovf_exp[i] == e) {
+                    const int at = atomicAdd(&sm.pos, 1);
+                    if (at < c.C) hold[at] = c.ovf_key[i];
+                }
+        }
+        __syncthreads();
+        if (total == c.C) {
+            // Full now: the price becomes the lowest held bid.
+            uint64_t m = ~0ull;
+            for (int i = tid; i < c.C; i += blockDim.x) {
+                const uint64_t k = hold[i];
+                m = k < m ? k : m;
+            }
+            atomicMin(reinterpret_cast<unsigned long long *>(&sm.minkey), (unsigned long long)m);
+            __syncthreads();
+            if (tid == 0) c.prices[e] = M::key_bid(sm.minkey);
+        }
+        if (tid == 0) {
+            c.hcount[e] = total;
+            c.bcount[e] = 0;
+        }
+        __syncthreads();
+        return;
+    }
+
+    // More candidates than slots: find the C-th largest key by MSD radix
+    // select (8 bits per pass), keep keys >= it, evict the rest.
+    const bool staged = total <= kCandLds;
+    if (staged) {
+        if (tid == 0) sm.pos = 0;
+        __syncthreads();
+        for_each_candidate<M>(c, e, hold, h, nb, novf_e, [&](uint64_t k, bool v) {
+            const uint64_t m = __ballot(v);
+            if (m == 0) return;
+            const int leader = __ffsll((long long)m) - 1;
+            int base = 0;
+            if (lane_id() == leader) base = atomicAdd(&sm.pos, __popcll(m));
+            base = __shfl(base, leader);
+            const int at = base + __popcll(m & lanemask_lt());
+            if (v && at < kCandLds) sm.cand[at] = k;
+        });
+        __syncthreads();
+    }
+    uint64_t prefix = 0, pmask = 0;
+    int need = c.C;
+    for (int shift = 56; shift >= 0; shift -= 8) {
+        for (int i = tid; i < 256; i += blockDim.x) sm.hist[i] = 0;
+        __syncthreads();
+        auto count = [&](uint64_t k, bool v) {
+            if (v && (k & pmask) == prefix) atomicAdd(&sm.hist[(k >> shift) & 255], 1u);
+        };
+        if (staged) {
+            for (int i = tid; i < total; i += blockDim.x) count(sm.cand[i], true);
+        } else {
+            for_each_candidate<M>(c, e, hold, h, nb, novf_e, count);
+        }
+        __syncthreads();
+        pick_digit(sm, need);
+        __syncthreads();
+        prefix |= (uint64_t)sm.sel_digit << shift;
+        pmask |= 255ull << shift;
+        need = sm.need;
+        __syncthreads();
+    }
+    const uint64_t kstar = prefix;   // keys are unique, so this is a key
+
+    uint64_t *alt = c.holders + (int64_t)(sel ^ 1) * c.T + (int64_t)e * c.C;
+    if (tid == 0) sm.kept = 0;
+    __syncthreads();
+    auto split = [&](uint64_t k, bool v) {
+        const bool keep = v && k >= kstar;
+        const uint64_t m = __ballot(keep);
+        if (m) {
+            const int leader = __ffsll((long long)m) - 1;
+            int base = 0;
+            if (lane_id() == leader) base = atomicAdd(&sm.kept, __popcll(m));
+            base = __shfl(base, leader);
+            const int at = base + __popcll(m & lanemask_lt());
+            if (keep && at < c.C) alt[at] = k;
+        }
+        append_active<M>(c, next, v && k < kstar, key_token(k));
+    };
+    if (staged) {
+        const int trips = ((total + blockDim.x - 1) / blockDim.x) * blockDim.x;
+        for (int i = tid; i < trips; i += blockDim.x) {
+            const bool v = i < total;
+            split(v ? sm.cand[i] : 0ull, v);
+        }
+    } else {
+        for_each_candidate<M>(c, e, hold, h, nb, novf_e, split);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        c.hsel[e] = sel ^ 1;
+        c.hcount[e] = c.C;
+        c.prices[e] = M::key_bid(kstar);
+        c.bcount[e] = 0;
+    }
+    __syncthreads();
+}
+
+// ------------------------------------------------------- round bookkeeping --
+
+// Called by one thread once a round's updates are complete and visible.
+__device__ inline void end_round(SolveCtrl *ctrl, int T) {
+    const int old = ctrl->cur;
+    const int nw = old ^ 1;
+    const int n = ctrl->all_active ? T : ld_relaxed(&ctrl->active_count[old]);
+    if (n == 0) return;
+    ctrl->bids += (unsigned long long)n;
+    ctrl->rounds += 1;
+    ctrl->active_count[old] = 0;
+    ctrl->cur = nw;
+    ctrl->all_active = 0;
+    ctrl->pad0 = 0;   // overflow list count
+    if (ld_relaxed(&ctrl->active_count[nw]) == 0 && ctrl->last_phase) ctrl->done = 1;
+}
+
+// Starts the next epsilon phase (one thread). Returns false if the solve is done.
+__device__ inline void begin_phase_scalar(SolveCtrl *ctrl, const AssignParams &p, int T) {
+    double eps;
+    if (ctrl->phase == 0) {
+        eps = p.eps_initial;
+        if (!(eps > 0.0)) {
+            double range;
+            if (p.integer)
+                range = ((double)(int32_t)(ctrl->smax_ord ^ 0x80000000u) -
+                         (double)(int32_t)(ctrl->smin_ord ^ 0x80000000u)) *
+                        (double)p.scale;
+            else
+                range = (double)f32_unord(ctrl->smax_ord) - (double)f32_unord(ctrl->smin_ord);
+            eps = range / 8.0;
+        }
+    } else {
+        eps = ctrl->eps / p.eps_factor;
+    }
+    if (p.integer) eps = floor(eps);
+    if (!(eps > ctrl->eps_final_eff)) eps = ctrl->eps_final_eff;
+    ctrl->eps = eps;
+    ctrl->last_phase = eps <= ctrl->eps_final_eff ? 1 : 0;
+    ctrl->phase += 1;
+    ctrl->all_active = 1;
+    ctrl->active_count[ctrl->cur] = 0;
+    ctrl->active_count[ctrl->cur ^ 1] = 0;
+    ctrl->pad0 = 0;
+}
+
+// ---------------------------------------------------------------- kernels --
+
+__global__ void init_kernel(SolveCtrl *ctrl, void *prices, int E, AssignParams p) {
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        SolveCtrl z{};
+        z.smax_ord = 0u;
+        z.smin_ord = 0xffffffffu;
+        z.eps_final_eff = p.eps_final;
+        *ctrl = z;
+    }
+    for (int e = tid; e < E; e += blockDim.x) reinterpret_cast<int64_t *>(prices)[e] = 0;
+}
+
+// Score range (order-preserving images) and a non-finite count.
+template <class M>
+__global__ void range_kernel(const typename M::score_t *S, int64_t n, SolveCtrl *ctrl) {
+    uint32_t mx = 0u, mn = 0xffffffffu;
+    int bad = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        uint32_t o;
+        if constexpr (M::kInteger) {
+            o = (uint32_t)((int32_t)S[i]) ^ 0x80000000u;
+        } else {
+            const float x = S[i];
+            if (!isfinite(x)) {
+                bad = 1;
+                continue;
+            }
+            o = f32_ord(x);
+        }
+        mx = o > mx ? o : mx;
+        mn = o < mn ? o : mn;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t a = __shfl_xor(mx, off), b = __shfl_xor(mn, off);
+        mx = a > mx ? a : mx;
+        mn = b < mn ? b : mn;
+        bad |= __shfl_xor(bad, off);
+    }
+    if (lane_id() == 0) {
+        atomicMax(&ctrl->smax_ord, mx);
+        atomicMin(&ctrl->smin_ord, mn);
+        if (bad) atomicOr(&ctrl->unconverged_experts, 1 << 30);
+    }
+}
+
+// Float mode: raise eps_final so that it stays far above fp32 rounding at the
+// magnitude prices and bids reach (scores plus a few score ranges).
+__global__ void eps_floor_kernel(SolveCtrl *ctrl, int integer) {
+    if (integer) {
+        ctrl->eps_final_eff = 1.0;
+        return;
+    }
+    const double smax = (double)f32_unord(ctrl->smax_ord);
+    const double smin = (double)f32_unord(ctrl->smin_ord);
+    const double mag = fmax(fabs(smax), fabs(smin)) + 3.0 * (smax - smin) + 1e-30;
+    const double floor_eps = ldexp(mag, -20);
+    if (ctrl->eps_final_eff < floor_eps) ctrl->eps_final_eff = floor_eps;
+}
+
+template <class M>
+__global__ void phase_begin_kernel(Ctx<M> c, AssignParams p) {
+    __shared__ int skip;
+    if (threadIdx.x == 0) {
+        skip = c.ctrl->done;
+        if (!skip) begin_phase_scalar(c.ctrl, p, c.T);
+    }
+    __syncthreads();
+    if (skip) return;
+    for (int e = threadIdx.x; e < c.E; e += blockDim.x) {
+        c.hcount[e] = 0;
+        c.bcount[e] = 0;
+    }
+}
+
+template <class M, int G>
+__global__ __launch_bounds__(kThreads) void bid_wide_kernel(Ctx<M> c) {
+    using value_t = typename M::value_t;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
+    SolveCtrl *ctrl = c.ctrl;
+    if (ctrl->done) return;
+    const int cur = ctrl->cur;
+    const bool all = ctrl->all_active != 0;
+    const int n = all ? c.T : ld_relaxed(&ctrl->active_count[cur]);
+    if (n == 0) return;
+    for (int e = threadIdx.x; e < c.E; e += blockDim.x) pr[e] = c.prices[e];
+    __syncthreads();
+    const value_t eps = (value_t)ctrl->eps;
+    const int per_block = kThreads / G;
+    const int gid = blockIdx.x * per_block + threadIdx.x / G;
+    bid_range<M, G>(c, n, all, c.active + (int64_t)cur * c.T, eps, pr, gid,
+                    gridDim.x * per_block, nullptr, nullptr);
+}
+
+template <class M>
+__global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c) {
+    __shared__ UpdateSmem sm;
+    __shared__ int last;
+    SolveCtrl *ctrl = c.ctrl;
+    if (ctrl->done) return;
+    const int cur = ctrl->cur;
+    const int novf = ld_relaxed(c.ovf_count);
+    for (int e = blockIdx.x; e < c.E; e += gridDim.x) update_expert<M>(c, e, cur ^ 1, novf, sm);
+    // The last block to finish closes the round.
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) last = atomicAdd(&ctrl->blocks_done, 1) == (int)gridDim.x - 1;
+    __syncthreads();
+    if (last && threadIdx.x == 0) {
+        __threadfence();
+        ctrl->blocks_done = 0;
+        end_round(ctrl, c.T);
+    }
+}
+
+// Remaining rounds of the current phase inside one workgroup. With
+// `continue_phases` the block also runs every later phase to the end.
+template <class M, int G>
+__global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p,
+                                                        int continue_phases) {
+    using value_t = typename M::value_t;
+    __shared__ UpdateSmem sm;
+    __shared__ int st_n, st_cur, st_all, st_stop, st_begin, ntouched;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
+    int *touched = reinterpret_cast<int *>(pr + c.E);
+    SolveCtrl *ctrl = c.ctrl;
+    const int tid = threadIdx.x;
+    for (;;) {
+        if (tid == 0) {
+            st_stop = 0;
+            st_begin = 0;
+            if (ctrl->done) {
+                st_stop = 1;
+            } else {
+                st_cur = ctrl->cur;
+                st_all = ctrl->all_active;
+                st_n = st_all ? c.T : ld_relaxed(&ctrl->active_count[st_cur]);
+                if (st_n == 0) {
+                    if (ctrl->last_phase) {
+                        ctrl->done = 1;
+                        st_stop = 1;
+                    } else if (!continue_phases) {
+                        st_stop = 1;
+                    } else {
+                        begin_phase_scalar(ctrl, p, c.T);
+                        st_begin = 1;
+                    }
+                } else if (ctrl->rounds >= p.max_rounds) {
+                    ctrl->not_converged = 1;
+                    ctrl->done = 1;
+                    st_stop = 1;
+                }
+            }
+            ntouched = 0;
+        }
+        __syncthreads();
+        if (st_stop) break;
+        if (st_begin) {
+            for (int e = tid; e < c.E; e += blockDim.x) {
+                c.hcount[e] = 0;
+                c.bcount[e] = 0;
+            }
+            __threadfence_block();
+            __syncthreads();
+            continue;
+        }
+        for (int e = tid; e < c.E; e += blockDim.x) pr[e] = c.prices[e];
+        __syncthreads();
+        const value_t eps = (value_t)ctrl->eps;
+        bid_range<M, G>(c, st_n, st_all != 0, c.active + (int64_t)st_cur * c.T, eps, pr,
+                        tid / G, kThreads / G, touched, &ntouched);
+        __threadfence_block();
+        __syncthreads();
+        const int novf = ld_relaxed(c.ovf_count);
+        const int nt = ntouched;
+        for (int i = 0; i < nt; ++i) update_expert<M>(c, touched[i], st_cur ^ 1, novf, sm);
+        __threadfence_block();
+        __syncthreads();
+        if (tid == 0) end_round(ctrl, c.T);
+        __threadfence_block();
+        __syncthreads();
+    }
+}
+
+// ------------------------------------------------------------- finalising --
+
+// assign[t] = e for every held token; counts experts that are not full.
+template <class M>
+__global__ void holders_to_assign_kernel(Ctx<M> c, int32_t *assign) {
+    const int e = blockIdx.x;
+    const int h = c.hcount[e];
+    const uint64_t *hold = c.holders + (int64_t)c.hsel[e] * c.T + (int64_t)e * c.C;
+    for (int i = threadIdx.x; i < h; i += blockDim.x) assign[key_token(hold[i])] = e;
+    if (threadIdx.x == 0 && h != c.C) atomicAdd(&c.ctrl->unconverged_experts, 1);
+}
+
+// Greedy completion after max_rounds (one block, sequential in token order):
+// every still-unassigned token takes its best expert among those with room.
+template <class M>
+__global__ void greedy_fill_kernel(Ctx<M> c, int32_t *assign, uint32_t flags) {
+    using value_t = typename M::value_t;
+    SolveCtrl *ctrl = c.ctrl;
+    if (!ctrl->not_converged || !(flags & BASE_ASSIGN_GREEDY_FALLBACK)) return;
+    __shared__ int room_left;
+    if (threadIdx.x == 0) {
+        ctrl->fell_back = 1;
+        ctrl->unconverged_experts &= (1 << 30);
+    }
+    // One wave scans tokens in ascending order.
+    if (threadIdx.x >= 64) return;
+    for (int t = 0; t < c.T; ++t) {
+        if (assign[t] >= 0) continue;
+        value_t best = M::lowest();
+        int be = 0x7fffffff;
+        for (int e = threadIdx.x; e < c.E; e += 64) {
+            if (c.hcount[e] >= c.C) continue;
+            const value_t v = M::load(c.S, (int64_t)t * c.E + e, c.scale) - c.prices[e];
+            if (v > best || (v == best && e < be)) {
+                best = v;
+                be = e;
+            }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const value_t ob = __shfl_xor(best, off);
+            const int oe = __shfl_xor(be, off);
+            if (ob > best || (ob == best && oe < be)) {
+                best = ob;
+                be = oe;
+            }
+        }
+        if (threadIdx.x == 0 && be < c.E) {
+            assign[t] = be;
+            c.hcount[be] += 1;
+        }
+        __threadfence_block();
+    }
+    (void)room_left;
+}
+
+// Per block of kCountTile tokens: how many go to each expert.
+__global__ __launch_bounds__(kCountTile) void block_count_kernel(const int32_t *assign, int T,
+                                                                 int E, int32_t *blk) {
+    extern __shared__ int hist[];
+    for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
+    __syncthreads();
+    const int t = blockIdx.x * kCountTile + threadIdx.x;
+    if (t < T) {
+        const int a = assign[t];
+        if (a >= 0 && a < E) atomicAdd(&hist[a], 1);
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += blockDim.x) blk[(int64_t)blockIdx.x * E + e] = hist[e];
+}
+
+// Exclusive scan over blocks for each expert, offset by the expert's first row e*C.
+__global__ void block_scan_kernel(int32_t *blk, int nblk, int E, int C) {
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= E) return;
+    int run = e * C;
+    for (int b = 0; b < nblk; ++b) {
+        const int v = blk[(int64_t)b * E + e];
+        blk[(int64_t)b * E + e] = run;
+        run += v;
+    }
+}
+
+// perm[offset(block, a_t) + rank of t among the block's tokens of a_t] = t:
+// a stable counting sort by expert.
+__global__ __launch_bounds__(kCountTile) void perm_scatter_kernel(const int32_t *assign, int T,
+                                                                  int E, const int32_t *blk,
+                                                                  int32_t *perm) {
+    __shared__ int loc[kCountTile];
+    const int t = blockIdx.x * kCountTile + threadIdx.x;
+    const int a = t < T ? assign[t] : -1;
+    loc[threadIdx.x] = a;
+    __syncthreads();
+    if (a < 0 || a >= E) return;
+    int rank = 0;
+    for (int j = 0; j < (int)threadIdx.x; ++j) rank += (loc[j] == a);
+    const int pos = blk[(int64_t)blockIdx.x * E + a] + rank;
+    if (pos < T) perm[pos] = t;
+}
+
+__global__ void fill_kernel(int32_t *p, int64_t n, int32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+// E == 1: every token goes to expert 0 and the sort vector is the identity.
+__global__ void single_expert_kernel(int32_t *assign, int32_t *perm, int64_t T) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < T;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        assign[i] = 0;
+        perm[i] = (int32_t)i;
+    }
+}
+
+// ------------------------------------------------------------------ driver --
+
+int lanes_per_token(int64_t E) {
+    if (E <= 1) return 1;
+    if (E <= 2) return 2;
+    if (E <= 8) return 4;
+    if (E <= 32) return 8;
+    if (E <= 128) return 16;
+    if (E <= 256) return 32;
+    return 64;
+}
+
+template <class M, int G>
+hipError_t run_solve(const Ctx<M> &c, const AssignParams &p, hipStream_t s) {
+    using value_t = typename M::value_t;
+    const size_t pr_bytes = (size_t)c.E * sizeof(value_t);
+    const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
+    // Phase slots enqueued up front; the last one continues on its own if
+    // the epsilon schedule needs more phases than were enqueued.
+    int slots = 8;
+    if (p.eps_initial > 0.0) {
+        double e = p.eps_initial;
+        slots = 1;
+        while (e > p.eps_final && slots < 64) {
+            e /= p.eps_factor;
+            ++slots;
+        }
+    }
+    const int wide_rounds = 2;
+    const int per_block = kThreads / G;
+    int bid_blocks = (int)((c.T + per_block - 1) / per_block);
+    if (bid_blocks > 4096) bid_blocks = 4096;
+    int upd_blocks = c.E < 2048 ? c.E : 2048;
+    for (int slot = 0; slot < slots; ++slot) {
+        hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1), dim3(1024), 0, s, c, p);
+        for (int r = 0; r < wide_rounds; ++r) {
+            hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks), dim3(kThreads), pr_bytes,
+                               s, c);
+            hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks), dim3(kThreads), 0, s, c);
+        }
+        hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1), dim3(kThreads), tail_smem, s, c, p,
+                           slot == slots - 1 ? 1 : 0);
+    }
+    return hipGetLastError();
+}
+
+template <class M>
+hipError_t solve_mode(const void *S, const AssignParams &p, int32_t *assign, int32_t *perm,
+                      void *prices_out, void *workspace, hipStream_t s) {
+    using value_t = typename M::value_t;
+    char *ws = static_cast<char *>(workspace);
+    const Layout L = make_layout(p.T, p.E);
+    Ctx<M> c = make_ctx<M>(S, p, ws);
+    hipLaunchKernelGGL(init_kernel, dim3(1), dim3(256), 0, s, c.ctrl, (void *)c.prices, c.E, p);
+    const int64_t n = p.T * p.E;
+    int rblocks = (int)((n + 255) / 256);
+    if (rblocks > 1024) rblocks = 1024;
+    hipLaunchKernelGGL(range_kernel<M>, dim3(rblocks), dim3(256), 0, s, c.S, n, c.ctrl);
+    hipLaunchKernelGGL(eps_floor_kernel, dim3(1), dim3(1), 0, s, c.ctrl, p.integer ? 1 : 0);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+
+    switch (lanes_per_token(p.E)) {
+        case 1: err = run_solve<M, 1>(c, p, s); break;
+        case 2: err = run_solve<M, 2>(c, p, s); break;
+        case 4: err = run_solve<M, 4>(c, p, s); break;
+        case 8: err = run_solve<M, 8>(c, p, s); break;
+        case 16: err = run_solve<M, 16>(c, p, s); break;
+        case 32: err = run_solve<M, 32>(c, p, s); break;
+        default: err = run_solve<M, 64>(c, p, s); break;
+    }
+    if (err != hipSuccess) return err;
+
+    int fblocks = (int)((p.T + 255) / 256);
+    if (fblocks > 2048) fblocks = 2048;
+    hipLaunchKernelGGL(fill_kernel, dim3(fblocks), dim3(256), 0, s, assign, p.T, -1);
+    hipLaunchKernelGGL(holders_to_assign_kernel<M>, dim3(c.E), dim3(256), 0, s, c, assign);
+    hipLaunchKernelGGL(greedy_fill_kernel<M>, dim3(1), dim3(64), 0, s, c, assign, p.flags);
+    int32_t *blk = reinterpret_cast<int32_t *>(ws + L.blk);
+    hipLaunchKernelGGL(block_count_kernel, dim3((unsigned)L.nblk), dim3(kCountTile),
+                       (size_t)p.E * sizeof(int), s, assign, c.T, c.E, blk);
+    hipLaunchKernelGGL(block_scan_kernel, dim3((unsigned)((p.E + 255) / 256)), dim3(256), 0, s,
+                       blk, (int)L.nblk, c.E, c.C);
+    hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)L.nblk), dim3(kCountTile), 0, s,
+                       assign, c.T, c.E, blk, perm);
+    if (prices_out != nullptr) {
+        err = hipMemcpyAsync(prices_out, c.prices, (size_t)p.E * sizeof(value_t),
+                             hipMemcpyDeviceToDevice, s);
+        if (err != hipSuccess) return err;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t assign_workspace_size(int64_t T, int64_t E) {
+    if (T <= 0 || E <= 0 || T % E) return 0;
+    return make_layout(T, E).total;
+}
+
+hipError_t launch_assign(const void *S, const AssignParams &p, int32_t *assign, int32_t *perm,
+                         void *prices_out, void *workspace, hipStream_t stream) {
+    if (p.E == 1) {
+        SolveCtrl *ctrl = static_cast<SolveCtrl *>(workspace);
+        hipError_t err = hipMemsetAsync(ctrl, 0, sizeof(SolveCtrl), stream);
+        if (err != hipSuccess) return err;
+        int blocks = (int)((p.T + 255) / 256);
+        if (blocks > 2048) blocks = 2048;
+        hipLaunchKernelGGL(single_expert_kernel, dim3(blocks), dim3(256), 0, stream, assign, perm,
+                           p.T);
+        if (prices_out != nullptr) {
+            err = hipMemsetAsync(prices_out, 0, p.integer ? 8 : 4, stream);
+            if (err != hipSuccess) return err;
+        }
+        return hipGetLastError();
+    }
+    if (p.integer) return solve_mode<IntMode>(S, p, assign, perm, prices_out, workspace, stream);
+    return solve_mode<FloatMode>(S, p, assign, perm, prices_out, workspace, stream);
+}
+
+hipError_t read_assign_stats(const void *workspace, int64_t /*T*/, int64_t /*E*/, SolveCtrl *out,
+                             hipStream_t stream) {
+    hipError_t err = hipMemcpyAsync(out, workspace, sizeof(SolveCtrl), hipMemcpyDeviceToHost,
+                                    stream);
+    if (err != hipSuccess) return err;
+    return hipStreamSynchronize(stream);
+}
+
+hipError_t check_scores_finite(const float *S, int64_t n, void *workspace, int *bad,
+                               hipStream_t stream) {
+    SolveCtrl *ctrl = static_cast<SolveCtrl *>(workspace);
+    AssignParams p{};
+    hipLaunchKernelGGL(init_kernel, dim3(1), dim3(256), 0, stream, ctrl, (void *)nullptr, 0, p);
+    int blocks = (int)((n + 255) / 256);
+    if (blocks > 1024) blocks = 1024;
+    hipLaunchKernelGGL(range_kernel<FloatMode>, dim3(blocks), dim3(256), 0, stream, S, n, ctrl);
+    SolveCtrl h{};
+    hipError_t err = read_assign_stats(workspace, 0, 0, &h, stream);
+    if (err != hipSuccess) return err;
+    *bad = (h.unconverged_experts & (1 << 30)) ? 1 : 0;
+    return hipSuccess;
+}
+
+}  // namespace base

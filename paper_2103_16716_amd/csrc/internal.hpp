@@ -1,0 +1,66 @@
+// Host-side launchers of the HIP kernels. Arguments are validated by the
+// C-ABI layer before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace base {
+
+hipError_t launch_affinity_bf16(const uint16_t *H, const uint16_t *W, float *S, int64_t T,
+                                int64_t E, int64_t d, hipStream_t stream);
+hipError_t launch_affinity_f32(const float *H, const float *W, float *S, int64_t T, int64_t E,
+                               int64_t d, hipStream_t stream);
+
+hipError_t launch_permute(const void *in, const int32_t *perm, void *out, int64_t T,
+                          int64_t row_bytes, int inverse, hipStream_t stream);
+
+struct AssignParams {
+    int64_t T, E, C;
+    bool integer;         // int16 scores, int64 arithmetic
+    int64_t scale;        // integer mode: K; float mode: 1
+    double eps_final;     // score units (float) / scaled units (integer)
+    double eps_initial;   // <= 0: derived from the score range on the device
+    double eps_factor;
+    int32_t max_rounds;
+    uint32_t flags;
+};
+
+// Device-side solver state and statistics, at the head of the workspace.
+struct SolveCtrl {
+    int32_t active_count[2];
+    int32_t cur;            // which active list the next round reads
+    int32_t all_active;     // 1: every token is active (first round of a phase)
+    int32_t phase;          // phases started
+    int32_t rounds;         // rounds run over all phases
+    int32_t done;           // 1 once the last phase has finished
+    int32_t overflow;       // a bid left the key's range
+    int32_t not_converged;  // max_rounds reached
+    int32_t fell_back;
+    int32_t last_phase;     // the current phase runs at eps_final
+    int32_t blocks_done;    // last-block counter of the wide update kernel
+    uint32_t smax_ord, smin_ord;   // score range (order-preserving images)
+    int32_t unconverged_experts;
+    int32_t pad0;
+    unsigned long long bids;
+    double eps;             // epsilon of the current phase (score or scaled units)
+    double eps_final_eff;
+    int64_t pad1[4];
+};
+
+size_t assign_workspace_size(int64_t T, int64_t E);
+
+// Enqueues the whole solve; returns the first HIP error of the launches.
+hipError_t launch_assign(const void *S, const AssignParams &p, int32_t *assign, int32_t *perm,
+                         void *prices_out, void *workspace, hipStream_t stream);
+
+// Reads the statistics back (synchronises the stream).
+hipError_t read_assign_stats(const void *workspace, int64_t T, int64_t E, SolveCtrl *out,
+                             hipStream_t stream);
+
+// Scans S for NaN/Inf (synchronous). *bad is set to 1 when one is found.
+hipError_t check_scores_finite(const float *S, int64_t n, void *workspace, int *bad,
+                               hipStream_t stream);
+
+}  // namespace base

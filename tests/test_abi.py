@@ -1,0 +1,134 @@
+"""The C-ABI library without a GPU: it loads, exports every symbol
+include/base.h declares, and rejects bad arguments on the host before
+anything reaches HIP. No call here carries a full set of valid arguments, so
+nothing is ever enqueued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2103_16716_amd as pb
+from paper_2103_16716_amd import build as pbuild
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "base.h")
+FAKE = 0x10000   # a 64 KiB-aligned stand-in address: never dereferenced by these calls
+
+
+@pytest.fixture(scope="module")
+def L():
+    if pbuild.is_stale():
+        pbuild.build()
+    return pb.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(base_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_path_calls():
+    names = declared_functions()
+    for n in ("base_affinity", "base_assign", "base_permute", "base_assign_workspace_size",
+              "base_status_string"):
+        assert n in names
+    assert set(names) == set(pb.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    out = os.popen(f"nm -D --defined-only {pb.LIB_PATH}").read()
+    for name in declared_functions():
+        assert re.search(rf"\bT {name}\b", out), name
+
+
+def test_status_strings(L):
+    for code in range(0, -9, -1):
+        s = pb.status_string(code)
+        assert s and s != "unknown status"
+    assert pb.status_string(-99) == "unknown status"
+
+
+def test_workspace_size_rules(L):
+    assert pb.assign_workspace_size(0, 1) == 0
+    assert pb.assign_workspace_size(10, 3) == 0           # T % E != 0
+    assert pb.assign_workspace_size(-4, 2) == 0
+    assert pb.assign_workspace_size(1 << 24, 1) == 0       # beyond the token-index field
+    assert pb.assign_workspace_size(4096, 4096 * 2) == 0   # E > T is not divisible
+    a = pb.assign_workspace_size(4096, 16)
+    b = pb.assign_workspace_size(32768, 128)
+    assert 0 < a < b and a % 256 == 0 and b % 256 == 0
+    # the per-expert tables and token lists grow with T at fixed E
+    assert pb.assign_workspace_size(8192, 16) > a
+
+
+def test_affinity_validation(L):
+    f = L.base_affinity
+    assert f(None, FAKE, FAKE, 4, 2, 8, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 4, 2, 7, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG   # d % 8
+    assert f(FAKE, FAKE, FAKE, 0, 2, 8, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    assert f(FAKE + 4, FAKE, FAKE, 4, 2, 8, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 4, 2, 8, pb.BASE_I16, None) == pb.BASE_ERR_UNSUPPORTED_DTYPE
+    assert f(FAKE, FAKE, FAKE, 4, 2, 8, 7, None) == pb.BASE_ERR_UNSUPPORTED_DTYPE
+
+
+def _assign(L, S=FAKE, dtype=pb.BASE_F32, T=8, E=2, opts=None, a=FAKE, p=FAKE, pr=None,
+            ws=FAKE, wsb=None):
+    if wsb is None:
+        wsb = 0
+    o = ctypes.byref(opts) if opts is not None else None
+    return L.base_assign(S, dtype, T, E, o, a, p, pr, ws, wsb, None, None)
+
+
+def test_assign_validation(L):
+    assert _assign(L, S=None) == pb.BASE_ERR_INVALID_ARG
+    assert _assign(L, a=None) == pb.BASE_ERR_INVALID_ARG
+    assert _assign(L, p=None) == pb.BASE_ERR_INVALID_ARG
+    assert _assign(L, T=0) == pb.BASE_ERR_INVALID_ARG
+    assert _assign(L, E=-1) == pb.BASE_ERR_INVALID_ARG
+    assert _assign(L, T=10, E=3) == pb.BASE_ERR_NOT_DIVISIBLE
+    assert _assign(L, dtype=pb.BASE_BF16) == pb.BASE_ERR_UNSUPPORTED_DTYPE
+    assert _assign(L, T=1 << 24, E=1) == pb.BASE_ERR_RANGE
+    assert _assign(L, T=4096, E=4096) == pb.BASE_ERR_RANGE          # E above the table limit
+    assert _assign(L, dtype=pb.BASE_I16, T=1 << 21, E=2) == pb.BASE_ERR_RANGE
+    assert _assign(L, S=FAKE + 8) == pb.BASE_ERR_INVALID_ARG         # S must be 16-byte aligned
+    assert _assign(L, a=FAKE + 2) == pb.BASE_ERR_INVALID_ARG
+    assert _assign(L, dtype=pb.BASE_I16, pr=FAKE + 4) == pb.BASE_ERR_INVALID_ARG
+    # workspace: missing, too small, misaligned
+    need = pb.assign_workspace_size(8, 2)
+    assert _assign(L, ws=None, wsb=need) == pb.BASE_ERR_WORKSPACE
+    assert _assign(L, wsb=need - 1) == pb.BASE_ERR_WORKSPACE
+    assert _assign(L, ws=FAKE + 16, wsb=need) == pb.BASE_ERR_WORKSPACE
+    # options: unknown flag bits and non-finite epsilons are rejected
+    bad = pb.AssignOpts(1e-4, 0.0, 8.0, 0, 1 << 7)
+    assert _assign(L, opts=bad, wsb=need) == pb.BASE_ERR_INVALID_ARG
+    bad = pb.AssignOpts(float("nan"), 0.0, 8.0, 0, 0)
+    assert _assign(L, opts=bad, wsb=need) == pb.BASE_ERR_INVALID_ARG
+    bad = pb.AssignOpts(1e-4, float("inf"), 8.0, 0, 0)
+    assert _assign(L, opts=bad, wsb=need) == pb.BASE_ERR_INVALID_ARG
+
+
+def test_assign_expert_limit(L):
+    # more experts than the per-expert tables support
+    assert _assign(L, T=4096 * 2, E=4096) == pb.BASE_ERR_RANGE
+
+
+def test_permute_validation(L):
+    f = L.base_permute
+    assert f(None, FAKE, FAKE + (1 << 20), 4, 8, pb.BASE_BF16, 0, None) == pb.BASE_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE + (1 << 20), 4, 6, pb.BASE_BF16, 0, None) == pb.BASE_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE + (1 << 20), 4, 8, pb.BASE_BF16, 2, None) == pb.BASE_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE + (1 << 20), 4, 8, pb.BASE_I16, 0, None) == pb.BASE_ERR_UNSUPPORTED_DTYPE
+    assert f(FAKE + 8, FAKE, FAKE + (1 << 20), 4, 8, pb.BASE_BF16, 0, None) == pb.BASE_ERR_INVALID_ARG
+    # in and out overlap
+    assert f(FAKE, FAKE, FAKE + 16, 4, 8, pb.BASE_BF16, 0, None) == pb.BASE_ERR_INVALID_ARG
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(pb, "_lib", None)
+    monkeypatch.setattr(pb, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        pb.lib()

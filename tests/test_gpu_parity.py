@@ -1,0 +1,259 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Affinity: elementwise within 2e-3 (bf16 inputs) / 1e-5 (fp32 inputs) of
+sum_k |H W|; bit-exact on integer-valued inputs. Assignment: every expert
+holds exactly T/E tokens, perm is the stable sort vector of the assignment
+bit for bit, the objective is at least the oracle optimum minus T * eps, the
+returned prices certify the same bound by LP duality, and the assignment is
+identical to the oracle's wherever the optimum is unique by more than T * eps
+(always in integer mode). Permute: bit-exact gather and scatter."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2103_16716_amd as pb
+import workloads as wl
+from gpu_common import (AFF_TOL, EPS_FINAL, affinity_bound, dev, host, inputs_on_device,
+                        rounding_slack)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "the GPU tests need an MI355X"
+    pb.lib()
+
+
+def gpu_affinity(H: np.ndarray, W: np.ndarray) -> np.ndarray:
+    S = pb.affinity(dev(H), dev(W))
+    torch.cuda.synchronize()
+    return host(S)
+
+
+def check_assignment(S: np.ndarray, res, eps: float, opt=None, unique_gap=None):
+    """The properties every float-mode solve must have, against the oracle."""
+    T, E = S.shape
+    a = host(res.assign)
+    perm = host(res.perm)
+    p = host(res.prices).astype(np.float64)
+    assert res.stats.converged == 1
+    assert oracle.balanced_counts_ok(a, E)
+    np.testing.assert_array_equal(perm, oracle.stable_perm(a, E))
+    obj = oracle.objective(S, a)
+    eps_used = res.stats.eps_final
+    assert eps_used <= eps * (1 + 1e-12) or eps_used <= 1e-3 * float(np.abs(S).max())
+    gap = oracle.dual_bound(S, p) - obj
+    assert gap >= -1e-9 * max(1.0, abs(obj))            # weak duality
+    assert gap <= T * eps_used + rounding_slack(T, S, p)
+    if opt is not None:
+        a_opt, obj_opt = opt
+        assert obj >= obj_opt - T * eps_used
+        if unique_gap is not None and unique_gap > T * eps_used + rounding_slack(T, S, p):
+            np.testing.assert_array_equal(a, a_opt)
+    return a, obj
+
+
+# ---------------------------------------------------------------- affinity --
+
+def test_affinity_bf16_integer_inputs_bit_exact():
+    # T, E and d all ragged against the 64 x 128 x 64 tiling
+    H, W = wl.small_integer_inputs(300, 200, 264, seed=7)
+    S = gpu_affinity(wl.f32_to_bf16_bits(H), wl.f32_to_bf16_bits(W))
+    np.testing.assert_array_equal(S.astype(np.float64), oracle.affinity(H, W))
+
+
+def test_affinity_f32_integer_inputs_bit_exact():
+    H, W = wl.small_integer_inputs(130, 70, 40, seed=8)
+    S = gpu_affinity(H, W)
+    np.testing.assert_array_equal(S.astype(np.float64), oracle.affinity(H, W))
+
+
+@pytest.mark.parametrize("T,E,d", [(1000, 200, 520), (64, 128, 64), (1, 1, 8), (77, 3, 2048)])
+def test_affinity_bf16_random_ragged(T, E, d):
+    rng = np.random.Generator(np.random.PCG64(T * 7 + E))
+    Hb = wl.f32_to_bf16_bits(rng.standard_normal((T, d), dtype=np.float32))
+    Wb = wl.f32_to_bf16_bits(rng.standard_normal((E, d), dtype=np.float32) / np.sqrt(d))
+    H, W = wl.bf16_bits_to_f32(Hb), wl.bf16_bits_to_f32(Wb)
+    S = gpu_affinity(Hb, Wb)
+    err = np.abs(S - oracle.affinity(H, W))
+    assert np.all(err <= affinity_bound(H, W, AFF_TOL["bf16"]))
+
+
+@pytest.mark.parametrize("T,E,d", [(512, 8, 128), (100, 70, 40), (65, 65, 1032)])
+def test_affinity_f32_random_ragged(T, E, d):
+    rng = np.random.Generator(np.random.PCG64(T + 3 * E))
+    H = rng.standard_normal((T, d), dtype=np.float32)
+    W = rng.standard_normal((E, d), dtype=np.float32) / np.float32(np.sqrt(d))
+    S = gpu_affinity(H, W)
+    err = np.abs(S - oracle.affinity(H, W))
+    assert np.all(err <= affinity_bound(H, W, AFF_TOL["f32"]))
+
+
+@pytest.mark.parametrize("name", ["t512-e8-d128-f32", "t4096-e16-d512", "t8192-e64-d1024",
+                                  "t2048-e128-d2048-worker"])
+def test_affinity_workloads(name):
+    inp = wl.make_inputs(name)
+    S = gpu_affinity(inp.H_store, inp.W_store)
+    err = np.abs(S - oracle.affinity(inp.H, inp.W))
+    assert np.all(err <= affinity_bound(inp.H, inp.W, AFF_TOL[inp.wl.dtype]))
+
+
+# ---------------------------------------------------------------- assign ---
+
+TINY = [(8, 2), (9, 3), (8, 4), (6, 6), (10, 5), (12, 4), (2, 2), (4, 1)]
+
+
+@pytest.mark.parametrize("T,E", TINY)
+def test_assign_tiny_against_bruteforce(T, E):
+    for kind in ("int", "normal"):
+        S = wl.random_scores(T, E, seed=1000 + 10 * T + E, kind=kind)
+        best, winners = oracle.solve_bruteforce(S)
+        res = pb.assign(dev(S))
+        a, obj = check_assignment(S.astype(np.float64), res, EPS_FINAL)
+        assert obj >= best - T * res.stats.eps_final
+        if kind == "int" and len(winners) == 1:
+            np.testing.assert_array_equal(a, winners[0])
+
+
+@pytest.mark.parametrize("T,E", TINY)
+def test_assign_tiny_integer_mode_exact(T, E):
+    S = wl.random_scores(T, E, seed=2000 + 10 * T + E, kind="int16")
+    best, winners = oracle.solve_bruteforce(S.astype(np.float64))
+    res = pb.assign(dev(S))
+    a = host(res.assign)
+    assert oracle.balanced_counts_ok(a, E)
+    assert oracle.objective(S, a) == best
+    if len(winners) == 1:
+        np.testing.assert_array_equal(a, winners[0])
+    np.testing.assert_array_equal(host(res.perm), oracle.stable_perm(a, E))
+
+
+@pytest.mark.parametrize("T,E", [(600, 12), (1000, 40), (64, 64), (17, 1), (2048, 128),
+                                 (256, 2)])
+def test_assign_ragged_shapes_against_ssp(T, E):
+    S = wl.random_scores(T, E, seed=T + E)
+    S64 = S.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    res = pb.assign(dev(S))
+    check_assignment(S64, res, EPS_FINAL, opt=(a_opt, obj_opt),
+                     unique_gap=oracle.optimum_gap(S64, a_opt))
+
+
+@pytest.mark.parametrize("name", ["t512-e8-d128-f32", "t4096-e16-d512", "t8192-e64-d1024",
+                                  "t2048-e128-d2048-worker"])
+def test_assign_workloads_against_ssp(name):
+    inp = wl.make_inputs(name)
+    Sg = pb.affinity(*inputs_on_device(inp))
+    res = pb.assign(Sg)
+    S = host(Sg).astype(np.float64)   # the oracle solves the scores the GPU solved
+    a_opt, obj_opt, _ = oracle.solve_ssp(S)
+    check_assignment(S, res, EPS_FINAL, opt=(a_opt, obj_opt),
+                     unique_gap=oracle.optimum_gap(S, a_opt))
+
+
+def test_assign_integer_variant_identical_to_oracle():
+    # The int16-quantised scores of the T=4096, E=16 workload: the optimum is
+    # unique, and the integer-mode solve is exact, so the assignments match.
+    inp = wl.make_inputs("t4096-e16-d512")
+    Sq, _ = wl.quantize_scores_int16(oracle.affinity(inp.H, inp.W))
+    a_opt, obj_opt, _ = oracle.solve_ssp(Sq.astype(np.float64))
+    assert oracle.optimum_gap(Sq.astype(np.float64), a_opt) > 0
+    res = pb.assign(dev(Sq))
+    a = host(res.assign)
+    np.testing.assert_array_equal(a, a_opt)
+    np.testing.assert_array_equal(host(res.perm), oracle.stable_perm(a_opt, 16))
+    # integer prices certify exact optimality: D(p / K) == OPT
+    K = 8192
+    p = host(res.prices)
+    assert oracle.dual_bound(Sq.astype(np.int64) * K, p) - int(obj_opt) * K < 4096 + 1
+
+
+@pytest.mark.parametrize("T,E", [(600, 12), (240, 8), (512, 64)])
+def test_assign_integer_mode_random_matches_ssp(T, E):
+    S = wl.random_scores(T, E, seed=3 * T + E, kind="int16")
+    S64 = S.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    res = pb.assign(dev(S))
+    a = host(res.assign)
+    assert oracle.balanced_counts_ok(a, E)
+    assert oracle.objective(S64, a) == obj_opt
+    if oracle.optimum_gap(S64, a_opt) > 0:
+        np.testing.assert_array_equal(a, a_opt)
+
+
+def test_assign_deterministic():
+    inp = wl.make_inputs("t4096-e16-d512")
+    Sg = pb.affinity(*inputs_on_device(inp))
+    runs = [pb.assign(Sg) for _ in range(3)]
+    for r in runs[1:]:
+        assert torch.equal(r.assign, runs[0].assign)
+        assert torch.equal(r.perm, runs[0].perm)
+        assert torch.equal(r.prices, runs[0].prices)
+        assert (r.stats.rounds, r.stats.bids, r.stats.phases) == (
+            runs[0].stats.rounds, runs[0].stats.bids, runs[0].stats.phases)
+
+
+def test_assign_greedy_balanced_case_is_argmax():
+    T, E = 960, 12
+    S = wl.random_scores(T, E, seed=21)
+    S[np.arange(T), np.arange(T) % E] += 10.0
+    res = pb.assign(dev(S))
+    np.testing.assert_array_equal(host(res.assign), oracle.greedy_argmax(S))
+
+
+def test_assign_not_converged_and_greedy_fallback():
+    S = wl.random_scores(512, 8, seed=5)
+    with pytest.raises(pb.BaseError) as ei:
+        pb.assign(dev(S), max_rounds=1)
+    assert ei.value.status == pb.BASE_ERR_NOT_CONVERGED
+    res = pb.assign(dev(S), max_rounds=1, flags=pb.BASE_ASSIGN_GREEDY_FALLBACK)
+    assert res.stats.fell_back == 1 and res.stats.converged == 1
+    a = host(res.assign)
+    assert oracle.balanced_counts_ok(a, 8)
+    np.testing.assert_array_equal(host(res.perm), oracle.stable_perm(a, 8))
+
+
+def test_assign_nonfinite_scores_rejected():
+    S = wl.random_scores(64, 8, seed=6)
+    S[10, 3] = np.nan
+    with pytest.raises(pb.BaseError) as ei:
+        pb.assign(dev(S), flags=pb.BASE_ASSIGN_CHECK_FINITE)
+    assert ei.value.status == pb.BASE_ERR_NONFINITE
+    S[10, 3] = np.inf
+    with pytest.raises(pb.BaseError) as ei:
+        pb.assign(dev(S), flags=pb.BASE_ASSIGN_CHECK_FINITE)
+    assert ei.value.status == pb.BASE_ERR_NONFINITE
+
+
+def test_assign_user_epsilon_schedule():
+    S = wl.random_scores(1024, 16, seed=12)
+    S64 = S.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    res = pb.assign(dev(S), eps_final=1e-3, eps_initial=0.5, eps_factor=4.0)
+    assert res.stats.eps_final == pytest.approx(1e-3)
+    check_assignment(S64, res, 1e-3, opt=(a_opt, obj_opt))
+
+
+# ---------------------------------------------------------------- permute --
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 2048), ("bf16", 24), ("f32", 40), ("f32", 8)])
+def test_permute_gather_scatter_bitwise(dtype, d):
+    T, E = 1000, 20
+    rng = np.random.Generator(np.random.PCG64(d))
+    x = rng.standard_normal((T, d), dtype=np.float32)
+    xs = wl.f32_to_bf16_bits(x) if dtype == "bf16" else x
+    a = rng.permutation(np.repeat(np.arange(E), T // E)).astype(np.int32)
+    perm = oracle.stable_perm(a, E)
+    X = pb.permute(dev(xs), dev(perm))
+    np.testing.assert_array_equal(host(X), oracle.gather(xs, perm))
+    Y = pb.permute(X, dev(perm), inverse=True)
+    np.testing.assert_array_equal(host(Y), oracle.scatter(oracle.gather(xs, perm), perm))
+    np.testing.assert_array_equal(host(Y), xs)
+
+
+def test_permute_single_row():
+    x = wl.f32_to_bf16_bits(np.arange(8, dtype=np.float32)[None, :])
+    X = pb.permute(dev(x), dev(np.zeros(1, np.int32)))
+    np.testing.assert_array_equal(host(X), x)
