@@ -50,7 +50,8 @@ typedef enum {
     BASE_ERR_NOT_CONVERGED = -5,    /* the round limit was reached before every expert was full */
     BASE_ERR_WORKSPACE = -6,        /* workspace missing or smaller than base_assign_workspace_size */
     BASE_ERR_HIP = -7,              /* a HIP runtime call failed */
-    BASE_ERR_RANGE = -8             /* a size or value outside what the kernels represent */
+    BASE_ERR_RANGE = -8,            /* a size or value outside what the kernels represent */
+    BASE_ERR_INTERNAL = -9          /* a device-side consistency check failed (a bug, not bad input) */
 } base_status;
 
 /* Element types. BASE_I16 is accepted for scores only (the integer variant). */

@@ -30,6 +30,7 @@ BASE_ERR_NOT_CONVERGED = -5
 BASE_ERR_WORKSPACE = -6
 BASE_ERR_HIP = -7
 BASE_ERR_RANGE = -8
+BASE_ERR_INTERNAL = -9
 
 BASE_F32 = 0
 BASE_BF16 = 1

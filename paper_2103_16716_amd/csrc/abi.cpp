@@ -32,6 +32,7 @@ const char *base_status_string(int status) {
         case BASE_ERR_WORKSPACE: return "workspace missing or too small";
         case BASE_ERR_HIP: return "HIP runtime error";
         case BASE_ERR_RANGE: return "size or value out of the supported range";
+        case BASE_ERR_INTERNAL: return "device-side consistency check failed";
         default: return "unknown status";
     }
 }
@@ -141,6 +142,7 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
             }
         }
         if (E > 1) {
+            if (c.internal_error) return BASE_ERR_INTERNAL;
             if (c.overflow) return BASE_ERR_RANGE;
             if (unconverged != 0 || (c.not_converged && !c.fell_back)) return BASE_ERR_NOT_CONVERGED;
         }

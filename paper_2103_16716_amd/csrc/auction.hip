@@ -123,6 +123,10 @@ __device__ inline int ld_relaxed(const int *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// A consistency check failed: the access is skipped and the call reports
+// BASE_ERR_INTERNAL instead of touching memory outside the workspace.
+__device__ inline void flag_internal(SolveCtrl *ctrl) { ctrl->internal_error = 1; }
+
 __device__ inline uint64_t lanemask_lt() {
     const int l = lane_id();
     return l == 0 ? 0ull : (~0ull >> (64 - l));
@@ -138,7 +142,11 @@ __device__ inline void append_active(const Ctx<M> &c, int which, bool want, int 
     int base = 0;
     if (lane_id() == leader) base = atomicAdd(&c.ctrl->active_count[which], __popcll(mask));
     base = __shfl(base, leader);
-    if (want) c.active[(int64_t)which * c.T + base + __popcll(mask & lanemask_lt())] = tok;
+    const int at = base + __popcll(mask & lanemask_lt());
+    if (want) {
+        if (at < c.T && tok >= 0 && tok < c.T) c.active[(int64_t)which * c.T + at] = tok;
+        else flag_internal(c.ctrl);
+    }
 }
 
 // -------------------------------------------------------------------- bid --
@@ -191,8 +199,12 @@ __device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *li
     const int gl = lane_id() & (G - 1);
     const int n_round = ((n + ngroups - 1) / ngroups) * ngroups;
     for (int i = gid; i < n_round; i += ngroups) {
-        const bool valid = i < n;
-        const int t = valid ? (all_active ? i : list[i]) : 0;
+        int t = (i < n) ? (all_active ? i : list[i]) : 0;
+        if (t < 0 || t >= c.T) {
+            if (i < n && gl == 0) flag_internal(c.ctrl);
+            t = 0;
+        }
+        const bool valid = i < n && t >= 0;
         value_t v1, v2;
         int e1;
         top2_token<M, G>(c, t, valid, pr, v1, e1, v2);
@@ -208,10 +220,18 @@ __device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *li
                 c.bucket[(int64_t)e1 * c.cap + pos] = key;
             } else {
                 const int q = atomicAdd(c.ovf_count, 1);
-                c.ovf_key[q] = key;
-                c.ovf_exp[q] = e1;
+                if (q < c.T) {
+                    c.ovf_key[q] = key;
+                    c.ovf_exp[q] = e1;
+                } else {
+                    flag_internal(c.ctrl);
+                }
             }
-            if (touched != nullptr && pos == 0) touched[atomicAdd(ntouched, 1)] = e1;
+            if (touched != nullptr && pos == 0) {
+                const int at = atomicAdd(ntouched, 1);
+                if (at < c.E) touched[at] = e1;
+                else flag_internal(c.ctrl);
+            }
         }
     }
 }
@@ -288,10 +308,21 @@ __device__ inline void pick_digit(UpdateSmem &sm, int need) {
 // block; `next` is the active list that receives evicted tokens.
 template <class M>
 __device__ void update_expert(const Ctx<M> &c, int e, int next, int novf, UpdateSmem &sm) {
-    const int n = ld_relaxed(&c.bcount[e]);
+    if (e < 0 || e >= c.E) {
+        if (threadIdx.x == 0) flag_internal(c.ctrl);
+        return;
+    }
+    int n = ld_relaxed(&c.bcount[e]);
     if (n == 0) return;
-    const int h = ld_relaxed(&c.hcount[e]);
-    const int sel = ld_relaxed(&c.hsel[e]);
+    int h = ld_relaxed(&c.hcount[e]);
+    int sel = ld_relaxed(&c.hsel[e]);
+    if (n < 0 || n > c.T || h < 0 || h > c.C || (sel & ~1)) {
+        if (threadIdx.x == 0) flag_internal(c.ctrl);
+        n = n < 0 ? 0 : (n > c.T ? c.T : n);
+        h = h < 0 ? 0 : (h > c.C ? c.C : h);
+        sel &= 1;
+        if (n == 0) return;
+    }
     uint64_t *hold = c.holders + (int64_t)sel * c.T + (int64_t)e * c.C;
     const int nb = n < c.cap ? n : c.cap;
     const int novf_e = (n > c.cap) ? novf : 0;
@@ -532,6 +563,7 @@ __global__ void phase_begin_kernel(Ctx<M> c, AssignParams p) {
     if (skip) return;
     for (int e = threadIdx.x; e < c.E; e += blockDim.x) {
         c.hcount[e] = 0;
+        c.hsel[e] = 0;
         c.bcount[e] = 0;
     }
 }
@@ -563,7 +595,7 @@ __global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c) {
     SolveCtrl *ctrl = c.ctrl;
     if (ctrl->done) return;
     const int cur = ctrl->cur;
-    const int novf = ld_relaxed(c.ovf_count);
+    const int novf = min(ld_relaxed(c.ovf_count), c.T);
     for (int e = blockIdx.x; e < c.E; e += gridDim.x) update_expert<M>(c, e, cur ^ 1, novf, sm);
     // The last block to finish closes the round.
     __threadfence();
@@ -623,6 +655,7 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
         if (st_begin) {
             for (int e = tid; e < c.E; e += blockDim.x) {
                 c.hcount[e] = 0;
+                c.hsel[e] = 0;
                 c.bcount[e] = 0;
             }
             __threadfence_block();
@@ -636,8 +669,8 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
                         tid / G, kThreads / G, touched, &ntouched);
         __threadfence_block();
         __syncthreads();
-        const int novf = ld_relaxed(c.ovf_count);
-        const int nt = ntouched;
+        const int novf = min(ld_relaxed(c.ovf_count), c.T);
+        const int nt = ntouched < c.E ? ntouched : c.E;
         for (int i = 0; i < nt; ++i) update_expert<M>(c, touched[i], st_cur ^ 1, novf, sm);
         __threadfence_block();
         __syncthreads();
@@ -653,9 +686,17 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
 template <class M>
 __global__ void holders_to_assign_kernel(Ctx<M> c, int32_t *assign) {
     const int e = blockIdx.x;
-    const int h = c.hcount[e];
-    const uint64_t *hold = c.holders + (int64_t)c.hsel[e] * c.T + (int64_t)e * c.C;
-    for (int i = threadIdx.x; i < h; i += blockDim.x) assign[key_token(hold[i])] = e;
+    int h = c.hcount[e];
+    if (h < 0 || h > c.C) {
+        if (threadIdx.x == 0) flag_internal(c.ctrl);
+        h = h < 0 ? 0 : c.C;
+    }
+    const uint64_t *hold = c.holders + (int64_t)(c.hsel[e] & 1) * c.T + (int64_t)e * c.C;
+    for (int i = threadIdx.x; i < h; i += blockDim.x) {
+        const int t = key_token(hold[i]);
+        if (t >= 0 && t < c.T) assign[t] = e;
+        else flag_internal(c.ctrl);
+    }
     if (threadIdx.x == 0 && h != c.C) atomicAdd(&c.ctrl->unconverged_experts, 1);
 }
 

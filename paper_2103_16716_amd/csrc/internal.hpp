@@ -46,7 +46,9 @@ struct SolveCtrl {
     unsigned long long bids;
     double eps;             // epsilon of the current phase (score or scaled units)
     double eps_final_eff;
-    int64_t pad1[4];
+    int32_t internal_error; // a device-side consistency check failed
+    int32_t pad2;
+    int64_t pad1[3];
 };
 
 size_t assign_workspace_size(int64_t T, int64_t E);

@@ -46,7 +46,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_status_strings(L):
-    for code in range(0, -9, -1):
+    for code in range(0, -10, -1):
         s = pb.status_string(code)
         assert s and s != "unknown status"
     assert pb.status_string(-99) == "unknown status"
