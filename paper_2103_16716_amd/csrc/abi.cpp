@@ -132,7 +132,8 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
             stats->bids = (int64_t)c.bids;
             stats->eps_final = integer ? c.eps / (double)p.scale : c.eps;
             stats->fell_back = c.fell_back;
-            stats->converged = (E == 1) || (unconverged == 0 && !c.not_converged) ? 1 : 0;
+            stats->converged =
+                (E == 1) || (unconverged == 0 && (!c.not_converged || c.fell_back)) ? 1 : 0;
             if (E == 1) {
                 stats->phases = 0;
                 stats->rounds = 0;

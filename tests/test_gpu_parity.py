@@ -257,3 +257,38 @@ def test_permute_single_row():
     x = wl.f32_to_bf16_bits(np.arange(8, dtype=np.float32)[None, :])
     X = pb.permute(dev(x), dev(np.zeros(1, np.int32)))
     np.testing.assert_array_equal(host(X), x)
+
+
+# ------------------------------------------------- full sizes, bench setup --
+
+@pytest.mark.parametrize("name", ["t32768-e128-d2048-mix8", "t65536-e256-d4096"])
+def test_full_pipeline_against_oracle(name):
+    """The whole path at full size, in the launch configuration bench.py times
+    (one stream, caller-provided workspace): affinity elementwise, the solve
+    against the exact optimum of the scores it solved, the sort vector and
+    the permute bit for bit, and the un-permute round trip."""
+    inp = wl.make_inputs(name)
+    w = inp.wl
+    H, W = inputs_on_device(inp)
+    S = torch.empty((w.T, w.E), dtype=torch.float32, device="cuda")
+    ws = torch.empty(pb.assign_workspace_size(w.T, w.E), dtype=torch.uint8, device="cuda")
+    a = torch.empty(w.T, dtype=torch.int32, device="cuda")
+    perm = torch.empty(w.T, dtype=torch.int32, device="cuda")
+    prices = torch.empty(w.E, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    pb.affinity(H, W, out=S, stream=stream)
+    res = pb.assign(S, workspace=ws, out_assign=a, out_perm=perm, out_prices=prices,
+                    stream=stream)
+    X = pb.permute(H, perm, stream=stream)
+    Y = pb.permute(X, perm, inverse=True, stream=stream)
+    torch.cuda.synchronize()
+
+    Sh = host(S)
+    err = np.abs(Sh - oracle.affinity(inp.H, inp.W))
+    assert np.all(err <= affinity_bound(inp.H, inp.W, AFF_TOL["bf16"]))
+    S64 = Sh.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    a_h, _ = check_assignment(S64, res, EPS_FINAL, opt=(a_opt, obj_opt))
+    Xh = host(X)
+    np.testing.assert_array_equal(Xh, oracle.gather(inp.H_store, host(perm)))
+    assert torch.equal(Y.view(torch.int16), H.view(torch.int16))
