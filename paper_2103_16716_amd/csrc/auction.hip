@@ -87,6 +87,7 @@ struct Ctx {
     uint64_t *holders, *bucket, *ovf_key;
     int *ovf_exp, *active;
     int *ovf_count;   // lives in ctrl->pad0
+    int engine_cap;   // > 0: rounds with at most this many active tokens go to the engine
 };
 
 template <class M>
@@ -110,6 +111,7 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.ovf_exp = reinterpret_cast<int *>(ws + L.ovf_exp);
     c.active = reinterpret_cast<int *>(ws + L.active);
     c.ovf_count = &c.ctrl->pad0;
+    c.engine_cap = 0;
     return c;
 }
 
@@ -579,6 +581,7 @@ __global__ __launch_bounds__(kThreads) void bid_wide_kernel(Ctx<M> c) {
     const bool all = ctrl->all_active != 0;
     const int n = all ? c.T : ld_relaxed(&ctrl->active_count[cur]);
     if (n == 0) return;
+    if (!all && n <= c.engine_cap) return;   // left to the tail engine
     for (int e = threadIdx.x; e < c.E; e += blockDim.x) pr[e] = c.prices[e];
     __syncthreads();
     const value_t eps = (value_t)ctrl->eps;
@@ -595,6 +598,11 @@ __global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c) {
     SolveCtrl *ctrl = c.ctrl;
     if (ctrl->done) return;
     const int cur = ctrl->cur;
+    {
+        const bool all = ctrl->all_active != 0;
+        const int n = all ? c.T : ld_relaxed(&ctrl->active_count[cur]);
+        if (!all && n <= c.engine_cap) return;   // the bid kernel skipped this round too
+    }
     const int novf = min(ld_relaxed(c.ovf_count), c.T);
     for (int e = blockIdx.x; e < c.E; e += gridDim.x) update_expert<M>(c, e, cur ^ 1, novf, sm);
     // The last block to finish closes the round.
@@ -677,6 +685,392 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
         if (tid == 0) end_round(ctrl, c.T);
         __threadfence_block();
         __syncthreads();
+    }
+}
+
+// ------------------------------------------------------------ tail engine --
+//
+// The rounds left once at most kEngCap tokens are active run inside one
+// workgroup with all mutable state in LDS:
+//   prices and holder counts of every expert,
+//   the kCache lowest held keys of every expert (sorted ascending) with the
+//   slot each occupies in the expert's holder table in global memory,
+//   the active tokens and the round's bids grouped by expert.
+// Bids are computed against the prices at the start of the round (Jacobi),
+// then one wave per touched expert streams that expert's bids through the
+// rule "a new key replaces the lowest held key when it is larger"; for any
+// arrival order this leaves the C largest keys of holders and bids, i.e. the
+// same result as a selection. The lowest held key is the expert's price once
+// it is full. A cached list that runs empty is refilled from the holder table.
+
+constexpr int kEngThreads = 512;
+constexpr int kEngWaves = kEngThreads / 64;
+constexpr int kCache = 8;
+constexpr int kEngCap = 2048;
+constexpr int kEngMaxE = 512;
+constexpr int kEngMaxC = 512;
+constexpr int kRefillRegs = kEngMaxC / 64;
+
+struct EngLayout {
+    size_t pr, cnt, cn, sel, bcnt, boff, bfill, tch, ck, cs, bkey, bexp, bsort, actA, actB, total;
+};
+
+__host__ __device__ inline size_t eng_align(size_t x) { return (x + 15) & ~size_t(15); }
+
+__host__ __device__ inline EngLayout eng_layout(int E, int value_bytes) {
+    EngLayout L{};
+    size_t off = 0;
+    L.pr = off;    off = eng_align(off + (size_t)E * value_bytes);
+    L.cnt = off;   off = eng_align(off + (size_t)E * 4);
+    L.cn = off;    off = eng_align(off + (size_t)E * 4);
+    L.sel = off;   off = eng_align(off + (size_t)E * 4);
+    L.bcnt = off;  off = eng_align(off + (size_t)E * 4);
+    L.boff = off;  off = eng_align(off + (size_t)E * 4);
+    L.bfill = off; off = eng_align(off + (size_t)E * 4);
+    L.tch = off;   off = eng_align(off + (size_t)E * 4);
+    L.ck = off;    off = eng_align(off + (size_t)E * kCache * 8);
+    L.cs = off;    off = eng_align(off + (size_t)E * kCache * 4);
+    L.bkey = off;  off = eng_align(off + (size_t)kEngCap * 8);
+    L.bexp = off;  off = eng_align(off + (size_t)kEngCap * 4);
+    L.bsort = off; off = eng_align(off + (size_t)kEngCap * 8);
+    L.actA = off;  off = eng_align(off + (size_t)kEngCap * 4);
+    L.actB = off;  off = eng_align(off + (size_t)kEngCap * 4);
+    L.total = off;
+    return L;
+}
+
+template <class M>
+struct Eng {
+    typename M::value_t *pr;
+    int *cnt, *cn, *sel, *bcnt, *boff, *bfill, *tch;
+    uint64_t *ck;
+    int *cs;
+    uint64_t *bkey, *bsort;
+    int *bexp;
+};
+
+__device__ inline uint64_t wave_min_u64(uint64_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint64_t o = __shfl_xor(v, off);
+        v = o < v ? o : v;
+    }
+    return v;
+}
+
+// One wave: the kCache lowest keys of expert e's holder table, sorted.
+template <class M>
+__device__ void eng_refill(const Ctx<M> &c, const Eng<M> &s, int e) {
+    __threadfence_block();   // this wave's holder-table stores before the reads below
+    const int lane = lane_id();
+    const int count = s.cnt[e];
+    const uint64_t *hold = c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
+    uint64_t kk[kRefillRegs];
+#pragma unroll
+    for (int r = 0; r < kRefillRegs; ++r) {
+        const int idx = lane + 64 * r;
+        kk[r] = idx < count ? hold[idx] : ~0ull;
+    }
+    const int take = count < kCache ? count : kCache;
+    for (int q = 0; q < take; ++q) {
+        uint64_t mk = ~0ull;
+        int mr = 0;
+#pragma unroll
+        for (int r = 0; r < kRefillRegs; ++r)
+            if (kk[r] < mk) {
+                mk = kk[r];
+                mr = r;
+            }
+        const uint64_t g = wave_min_u64(mk);
+        const uint64_t owners = __ballot(mk == g && g != ~0ull);
+        const int owner = owners ? __ffsll((long long)owners) - 1 : 0;
+        int slot = 0;
+        if (lane == owner) {
+            slot = lane + 64 * mr;
+#pragma unroll
+            for (int r = 0; r < kRefillRegs; ++r)
+                if (r == mr) kk[r] = ~0ull;
+        }
+        slot = __shfl(slot, owner);
+        if (lane == 0) {
+            s.ck[e * kCache + q] = g;
+            s.cs[e * kCache + q] = slot;
+        }
+    }
+    if (lane == 0) s.cn[e] = take;
+}
+
+// One wave: inserts key b (held in `slot`) into expert e's sorted list if it
+// belongs to the lowest kCache keys. `complete` says every holder other than
+// b is in the list.
+template <class M>
+__device__ inline void eng_cache_insert(const Eng<M> &s, int e, uint64_t b, int slot, bool complete) {
+    const int lane = lane_id();
+    const int nc = s.cn[e];
+    if (!complete && (nc == 0 || b > s.ck[e * kCache + nc - 1])) return;   // stays outside
+    uint64_t v = ~0ull;
+    int sl = 0;
+    if (lane < nc) {
+        v = s.ck[e * kCache + lane];
+        sl = s.cs[e * kCache + lane];
+    }
+    const int pos = __popcll(__ballot(lane < nc && v < b));
+    if (pos >= kCache) return;   // larger than a full list of keys
+    if (lane >= pos && lane < nc && lane + 1 < kCache) {
+        s.ck[e * kCache + lane + 1] = v;
+        s.cs[e * kCache + lane + 1] = sl;
+    }
+    if (lane == pos) {
+        s.ck[e * kCache + pos] = b;
+        s.cs[e * kCache + pos] = slot;
+    }
+    if (lane == 0) s.cn[e] = nc + 1 < kCache ? nc + 1 : kCache;
+}
+
+template <class M>
+__device__ inline void eng_cache_pop(const Eng<M> &s, int e) {
+    const int lane = lane_id();
+    const int nc = s.cn[e];
+    uint64_t v = 0;
+    int sl = 0;
+    if (lane >= 1 && lane < nc) {
+        v = s.ck[e * kCache + lane];
+        sl = s.cs[e * kCache + lane];
+    }
+    if (lane >= 1 && lane < nc) {
+        s.ck[e * kCache + lane - 1] = v;
+        s.cs[e * kCache + lane - 1] = sl;
+    }
+    if (lane == 0) s.cn[e] = nc > 0 ? nc - 1 : 0;
+}
+
+// One wave: streams expert e's bids of this round into its holders.
+template <class M>
+__device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *bids, int nb,
+                           int *nxt, int *nnext) {
+    const int lane = lane_id();
+    uint64_t *hold = c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
+    for (int j = 0; j < nb; ++j) {
+        const uint64_t b = bids[j];
+        const int count = s.cnt[e];
+        int out_tok = -1;
+        if (count < c.C) {
+            const bool complete = s.cn[e] == count;
+            if (lane == 0) {
+                hold[count] = b;
+                s.cnt[e] = count + 1;
+            }
+            eng_cache_insert<M>(s, e, b, count, complete);
+            if (count + 1 == c.C) {
+                if (s.cn[e] == 0) eng_refill<M>(c, s, e);
+                if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * kCache]);
+            }
+        } else {
+            if (s.cn[e] == 0) eng_refill<M>(c, s, e);
+            const uint64_t m = s.ck[e * kCache];
+            if (b > m) {
+                const int slot = s.cs[e * kCache];
+                out_tok = key_token(m);
+                eng_cache_pop<M>(s, e);
+                if (lane == 0) {
+                    if (slot >= 0 && slot < c.C) hold[slot] = b;
+                    else flag_internal(c.ctrl);
+                }
+                eng_cache_insert<M>(s, e, b, slot, s.cn[e] == count - 1);
+                __threadfence_block();
+                if (s.cn[e] == 0) eng_refill<M>(c, s, e);
+                if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * kCache]);
+            } else {
+                out_tok = key_token(b);
+            }
+        }
+        if (out_tok >= 0 && lane == 0) {
+            const int at = atomicAdd(nnext, 1);
+            if (at < kEngCap && out_tok < c.T) nxt[at] = out_tok;
+            else flag_internal(c.ctrl);
+        }
+    }
+}
+
+template <class M, int G>
+__global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignParams p) {
+    using value_t = typename M::value_t;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    const EngLayout L = eng_layout(c.E, (int)sizeof(value_t));
+    Eng<M> s;
+    s.pr = reinterpret_cast<value_t *>(smem_raw + L.pr);
+    s.cnt = reinterpret_cast<int *>(smem_raw + L.cnt);
+    s.cn = reinterpret_cast<int *>(smem_raw + L.cn);
+    s.sel = reinterpret_cast<int *>(smem_raw + L.sel);
+    s.bcnt = reinterpret_cast<int *>(smem_raw + L.bcnt);
+    s.boff = reinterpret_cast<int *>(smem_raw + L.boff);
+    s.bfill = reinterpret_cast<int *>(smem_raw + L.bfill);
+    s.tch = reinterpret_cast<int *>(smem_raw + L.tch);
+    s.ck = reinterpret_cast<uint64_t *>(smem_raw + L.ck);
+    s.cs = reinterpret_cast<int *>(smem_raw + L.cs);
+    s.bkey = reinterpret_cast<uint64_t *>(smem_raw + L.bkey);
+    s.bexp = reinterpret_cast<int *>(smem_raw + L.bexp);
+    s.bsort = reinterpret_cast<uint64_t *>(smem_raw + L.bsort);
+    int *act = reinterpret_cast<int *>(smem_raw + L.actA);
+    int *nxt = reinterpret_cast<int *>(smem_raw + L.actB);
+    __shared__ int s_go, s_cur, s_n, s_nnext, s_ntouched, s_rounds, s_stop;
+    __shared__ unsigned long long s_bids;
+
+    SolveCtrl *ctrl = c.ctrl;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    if (tid == 0) {
+        s_go = 0;
+        if (!ctrl->done && !ctrl->all_active) {
+            s_cur = ctrl->cur;
+            const int n = ld_relaxed(&ctrl->active_count[s_cur]);
+            if (n > 0 && n <= kEngCap) {
+                s_go = 1;
+                s_n = n;
+            }
+        }
+        s_nnext = 0;
+        s_ntouched = 0;
+        s_rounds = 0;
+        s_stop = 0;
+        s_bids = 0;
+    }
+    __syncthreads();
+    if (!s_go) return;
+    const int max_rounds_left = p.max_rounds - ctrl->rounds;
+    const value_t eps = (value_t)ctrl->eps;
+    for (int e = tid; e < c.E; e += kEngThreads) {
+        s.pr[e] = c.prices[e];
+        s.cnt[e] = ld_relaxed(&c.hcount[e]);
+        s.sel[e] = ld_relaxed(&c.hsel[e]) & 1;
+        s.bcnt[e] = 0;
+        s.bfill[e] = 0;
+    }
+    for (int i = tid; i < s_n; i += kEngThreads) {
+        const int t = c.active[(int64_t)s_cur * c.T + i];
+        act[i] = (t >= 0 && t < c.T) ? t : 0;
+        if (t < 0 || t >= c.T) flag_internal(ctrl);
+    }
+    __syncthreads();
+    for (int e = wave; e < c.E; e += kEngWaves) {
+        if (s.cnt[e] < 0 || s.cnt[e] > c.C) {
+            if (lane == 0) flag_internal(ctrl);
+            if (lane == 0) s.cnt[e] = 0;
+        }
+        eng_refill<M>(c, s, e);
+    }
+    __syncthreads();
+
+    const int per_pass = kEngThreads / G;
+    const int gid = tid / G;
+    const int gl = lane & (G - 1);
+    for (;;) {
+        const int n = s_n;
+        if (n == 0) break;
+        if (s_rounds >= max_rounds_left) {
+            if (tid == 0) s_stop = 1;
+            break;
+        }
+        // Bids against the prices at the start of the round.
+        const int n_round = ((n + per_pass - 1) / per_pass) * per_pass;
+        for (int i = gid; i < n_round; i += per_pass) {
+            const bool valid = i < n;
+            const int t = valid ? act[i] : 0;
+            value_t v1, v2;
+            int e1;
+            top2_token<M, G>(c, t, valid, s.pr, v1, e1, v2);
+            if (valid && gl == 0) {
+                if (e1 >= c.E) e1 = 0;
+                const value_t s1 = M::load(c.S, (int64_t)t * c.E + e1, c.scale);
+                const value_t bid = (value_t)((s1 - v2) + eps);
+                int overflow = 0;
+                const uint64_t key = M::make_key(bid, t, &overflow);
+                if (overflow) ctrl->overflow = 1;
+                s.bkey[i] = key;
+                s.bexp[i] = e1;
+                if (atomicAdd(&s.bcnt[e1], 1) == 0) {
+                    const int at = atomicAdd(&s_ntouched, 1);
+                    if (at < c.E) s.tch[at] = e1;
+                }
+            }
+        }
+        __syncthreads();
+        const int nt = s_ntouched < c.E ? s_ntouched : c.E;
+        if (wave == 0) {
+            int base = 0;
+            for (int j0 = 0; j0 < nt; j0 += 64) {
+                const int j = j0 + lane;
+                const int cj = j < nt ? s.bcnt[s.tch[j]] : 0;
+                int incl = cj;
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int o = __shfl_up(incl, off);
+                    if (lane >= off) incl += o;
+                }
+                if (j < nt) s.boff[s.tch[j]] = base + incl - cj;
+                base += __shfl(incl, 63);
+            }
+        }
+        __syncthreads();
+        for (int i = tid; i < n; i += kEngThreads) {
+            const int e = s.bexp[i];
+            const int pos = s.boff[e] + atomicAdd(&s.bfill[e], 1);
+            if (pos < kEngCap) s.bsort[pos] = s.bkey[i];
+            else flag_internal(ctrl);
+        }
+        __syncthreads();
+        for (int j = wave; j < nt; j += kEngWaves) {
+            const int e = s.tch[j];
+            int nb = s.bcnt[e];
+            const int off = s.boff[e];
+            if (off + nb > kEngCap) {
+                if (lane == 0) flag_internal(ctrl);
+                nb = kEngCap - off;
+            }
+            eng_update<M>(c, s, e, s.bsort + off, nb, nxt, &s_nnext);
+        }
+        __threadfence_block();
+        __syncthreads();
+        for (int j = tid; j < nt; j += kEngThreads) {
+            const int e = s.tch[j];
+            s.bcnt[e] = 0;
+            s.bfill[e] = 0;
+        }
+        if (tid == 0) {
+            s_rounds += 1;
+            s_bids += (unsigned long long)n;
+            s_n = s_nnext < kEngCap ? s_nnext : kEngCap;
+            s_nnext = 0;
+            s_ntouched = 0;
+        }
+        int *tmp = act;
+        act = nxt;
+        nxt = tmp;
+        __syncthreads();
+    }
+
+    // Hand the state back.
+    for (int e = tid; e < c.E; e += kEngThreads) {
+        c.prices[e] = s.pr[e];
+        c.hcount[e] = s.cnt[e];
+        c.bcount[e] = 0;
+    }
+    for (int i = tid; i < s_n; i += kEngThreads) c.active[(int64_t)s_cur * c.T + i] = act[i];
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) {
+        ctrl->rounds += s_rounds;
+        ctrl->bids += s_bids;
+        ctrl->active_count[s_cur] = s_n;
+        ctrl->active_count[s_cur ^ 1] = 0;
+        ctrl->pad0 = 0;
+        if (s_stop) {
+            ctrl->not_converged = 1;
+            ctrl->done = 1;
+        } else if (s_n == 0 && ctrl->last_phase) {
+            ctrl->done = 1;
+        }
     }
 }
 
@@ -816,8 +1210,22 @@ int lanes_per_token(int64_t E) {
 }
 
 template <class M, int G>
-hipError_t run_solve(const Ctx<M> &c, const AssignParams &p, hipStream_t s) {
+hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     using value_t = typename M::value_t;
+    Ctx<M> c = c0;
+    const size_t eng_bytes = eng_layout(c.E, (int)sizeof(value_t)).total;
+    const bool engine = c.E <= kEngMaxE && c.C <= kEngMaxC && eng_bytes <= 160 * 1024;
+    if (engine) {
+        static bool attr_set = false;
+        if (!attr_set) {
+            hipError_t err = hipFuncSetAttribute(
+                reinterpret_cast<const void *>(&engine_kernel<M, G>),
+                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+            if (err != hipSuccess) return err;
+            attr_set = true;
+        }
+        c.engine_cap = kEngCap;
+    }
     const size_t pr_bytes = (size_t)c.E * sizeof(value_t);
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
     // Phase slots enqueued up front; the last one continues on its own if
@@ -831,7 +1239,7 @@ hipError_t run_solve(const Ctx<M> &c, const AssignParams &p, hipStream_t s) {
             ++slots;
         }
     }
-    const int wide_rounds = 2;
+    const int wide_rounds = engine ? 3 : 2;
     const int per_block = kThreads / G;
     int bid_blocks = (int)((c.T + per_block - 1) / per_block);
     if (bid_blocks > 4096) bid_blocks = 4096;
@@ -843,6 +1251,9 @@ hipError_t run_solve(const Ctx<M> &c, const AssignParams &p, hipStream_t s) {
                                s, c);
             hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks), dim3(kThreads), 0, s, c);
         }
+        if (engine)
+            hipLaunchKernelGGL((engine_kernel<M, G>), dim3(1), dim3(kEngThreads), eng_bytes, s, c,
+                               p);
         hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1), dim3(kThreads), tail_smem, s, c, p,
                            slot == slots - 1 ? 1 : 0);
     }
