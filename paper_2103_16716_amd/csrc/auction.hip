@@ -33,6 +33,8 @@
 // handful of active tokens each, run inside one workgroup that loops with
 // block barriers instead of kernel launches.
 #include <math.h>
+#include <stdio.h>
+#include <stdlib.h>
 
 #include "common.hpp"
 #include "internal.hpp"
@@ -46,6 +48,13 @@ constexpr int kCandLds = 4096;   // candidates of one expert staged in LDS when 
 constexpr int kCountTile = 256;  // tokens per block in the permutation build
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+// With BASE_DEBUG set in the environment, notes why a launch path was taken
+// or which HIP call failed, on stderr.
+inline void debug_note(const char *what, hipError_t err) {
+    static const bool on = getenv("BASE_DEBUG") != nullptr;
+    if (on) fprintf(stderr, "[base] %s: %s\n", what, hipGetErrorString(err));
+}
 
 struct Layout {
     size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
@@ -706,7 +715,7 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
 constexpr int kEngThreads = 512;
 constexpr int kEngWaves = kEngThreads / 64;
 constexpr int kCache = 8;
-constexpr int kEngCap = 2048;
+constexpr int kEngCap = 1024;
 constexpr int kEngMaxE = 512;
 constexpr int kEngMaxC = 512;
 constexpr int kRefillRegs = kEngMaxC / 64;
@@ -1214,18 +1223,20 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     using value_t = typename M::value_t;
     Ctx<M> c = c0;
     const size_t eng_bytes = eng_layout(c.E, (int)sizeof(value_t)).total;
-    const bool engine = c.E <= kEngMaxE && c.C <= kEngMaxC && eng_bytes <= 160 * 1024;
-    if (engine) {
-        static bool attr_set = false;
-        if (!attr_set) {
-            hipError_t err = hipFuncSetAttribute(
-                reinterpret_cast<const void *>(&engine_kernel<M, G>),
-                hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-            if (err != hipSuccess) return err;
-            attr_set = true;
+    bool engine = c.E <= kEngMaxE && c.C <= kEngMaxC;
+    if (engine && eng_bytes > 64 * 1024) {
+        // Layouts above the default per-block LDS need the opt-in; without it
+        // the rounds stay with the grid-wide kernels and the fallback tail.
+        const hipError_t err = hipFuncSetAttribute(
+            reinterpret_cast<const void *>(&engine_kernel<M, G>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, (int)eng_bytes);
+        if (err != hipSuccess) {
+            (void)hipGetLastError();
+            debug_note("engine LDS opt-in refused", err);
+            engine = false;
         }
-        c.engine_cap = kEngCap;
     }
+    if (engine) c.engine_cap = kEngCap;
     const size_t pr_bytes = (size_t)c.E * sizeof(value_t);
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
     // Phase slots enqueued up front; the last one continues on its own if
@@ -1285,7 +1296,10 @@ hipError_t solve_mode(const void *S, const AssignParams &p, int32_t *assign, int
         case 32: err = run_solve<M, 32>(c, p, s); break;
         default: err = run_solve<M, 64>(c, p, s); break;
     }
-    if (err != hipSuccess) return err;
+    if (err != hipSuccess) {
+        debug_note("solver launches", err);
+        return err;
+    }
 
     int fblocks = (int)((p.T + 255) / 256);
     if (fblocks > 2048) fblocks = 2048;
