@@ -164,22 +164,27 @@ __device__ inline void append_active(const Ctx<M> &c, int which, bool want, int 
 
 // One group of G lanes evaluates one token. VEC: rows are read as 16-byte
 // vectors (E % 8 == 0 for int16, E % 4 == 0 for fp32).
+// s1 returns the score S[t, e1] itself, so the bid needs no second read.
 template <class M, int G>
 __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const typename M::value_t *pr,
-                                  typename M::value_t &v1, int &e1, typename M::value_t &v2) {
+                                  typename M::value_t &v1, int &e1, typename M::value_t &v2,
+                                  typename M::value_t &s1) {
     using value_t = typename M::value_t;
     const int gl = lane_id() & (G - 1);
     v1 = M::lowest();
     v2 = M::lowest();
+    s1 = 0;
     e1 = 0x7fffffff;
     if (valid) {
         const int64_t row = (int64_t)t * c.E;
         for (int e = gl; e < c.E; e += G) {
-            const value_t v = M::load(c.S, row + e, c.scale) - pr[e];
+            const value_t sv = M::load(c.S, row + e, c.scale);
+            const value_t v = sv - pr[e];
             if (v > v1) {
                 v2 = v1;
                 v1 = v;
                 e1 = e;
+                s1 = sv;
             } else if (v > v2) {
                 v2 = v;
             }
@@ -190,10 +195,12 @@ __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const type
         const value_t ov1 = __shfl_xor(v1, off);
         const int oe1 = __shfl_xor(e1, off);
         const value_t ov2 = __shfl_xor(v2, off);
+        const value_t os1 = __shfl_xor(s1, off);
         if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
             v2 = v1 > ov2 ? v1 : ov2;
             v1 = ov1;
             e1 = oe1;
+            s1 = os1;
         } else {
             v2 = v2 > ov1 ? v2 : ov1;
         }
@@ -216,12 +223,14 @@ __device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *li
             t = 0;
         }
         const bool valid = i < n && t >= 0;
-        value_t v1, v2;
+        value_t v1, v2, s1;
         int e1;
-        top2_token<M, G>(c, t, valid, pr, v1, e1, v2);
+        top2_token<M, G>(c, t, valid, pr, v1, e1, v2, s1);
         if (valid && gl == 0) {
-            if (e1 >= c.E) e1 = 0;   // every value non-finite: any expert, the bid overflows
-            const value_t s1 = M::load(c.S, (int64_t)t * c.E + e1, c.scale);
+            if (e1 >= c.E) {   // every value non-finite: any expert, the bid overflows
+                e1 = 0;
+                s1 = M::load(c.S, (int64_t)t * c.E, c.scale);
+            }
             const value_t bid = (c.E > 1) ? (value_t)((s1 - v2) + eps) : (value_t)(s1 + eps);
             int overflow = 0;
             const uint64_t key = M::make_key(bid, t, &overflow);
@@ -698,6 +707,15 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
 }
 
 // ------------------------------------------------------------ tail engine --
+
+// Workgroup barrier that orders LDS only: in-flight global stores are not
+// waited for (the engine's one full barrier per round, after the bids, covers
+// the holder-table stores before any later refill reads them).
+__device__ inline void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 //
 // The rounds left once at most kEngCap tokens are active run inside one
 // workgroup with all mutable state in LDS:
@@ -716,6 +734,7 @@ constexpr int kEngThreads = 512;
 constexpr int kEngWaves = kEngThreads / 64;
 constexpr int kCache = 8;
 constexpr int kEngCap = 1024;
+constexpr int kEngDirect = 64;   // rounds with at most this many bids skip the grouping
 constexpr int kEngMaxE = 512;
 constexpr int kEngMaxC = 512;
 constexpr int kRefillRegs = kEngMaxC / 64;
@@ -854,12 +873,15 @@ __device__ inline void eng_cache_pop(const Eng<M> &s, int e) {
 }
 
 // One wave: streams expert e's bids of this round into its holders.
+// Bids are bids[0..nb), or, with `exps`, the entries of bids[0..nb) whose
+// expert exps[j] is e.
 template <class M>
-__device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *bids, int nb,
-                           int *nxt, int *nnext) {
+__device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *bids,
+                           const int *exps, int nb, int *nxt, int *nnext) {
     const int lane = lane_id();
     uint64_t *hold = c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
     for (int j = 0; j < nb; ++j) {
+        if (exps != nullptr && exps[j] != e) continue;
         const uint64_t b = bids[j];
         const int count = s.cnt[e];
         int out_tok = -1;
@@ -886,7 +908,6 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
                     else flag_internal(c.ctrl);
                 }
                 eng_cache_insert<M>(s, e, b, slot, s.cn[e] == count - 1);
-                __threadfence_block();
                 if (s.cn[e] == 0) eng_refill<M>(c, s, e);
                 if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * kCache]);
             } else {
@@ -986,12 +1007,14 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
         for (int i = gid; i < n_round; i += per_pass) {
             const bool valid = i < n;
             const int t = valid ? act[i] : 0;
-            value_t v1, v2;
+            value_t v1, v2, s1;
             int e1;
-            top2_token<M, G>(c, t, valid, s.pr, v1, e1, v2);
+            top2_token<M, G>(c, t, valid, s.pr, v1, e1, v2, s1);
             if (valid && gl == 0) {
-                if (e1 >= c.E) e1 = 0;
-                const value_t s1 = M::load(c.S, (int64_t)t * c.E + e1, c.scale);
+                if (e1 >= c.E) {
+                    e1 = 0;
+                    s1 = M::load(c.S, (int64_t)t * c.E, c.scale);
+                }
                 const value_t bid = (value_t)((s1 - v2) + eps);
                 int overflow = 0;
                 const uint64_t key = M::make_key(bid, t, &overflow);
@@ -1004,8 +1027,13 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
                 }
             }
         }
-        __syncthreads();
+        __syncthreads();   // also completes the previous round's holder-table stores
         const int nt = s_ntouched < c.E ? s_ntouched : c.E;
+        if (n <= kEngDirect) {
+            // Few bids: every wave reads them all and keeps its experts' ones.
+            for (int j = wave; j < nt; j += kEngWaves)
+                eng_update<M>(c, s, s.tch[j], s.bkey, s.bexp, n, nxt, &s_nnext);
+        } else {
         if (wave == 0) {
             int base = 0;
             for (int j0 = 0; j0 < nt; j0 += 64) {
@@ -1021,14 +1049,14 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
                 base += __shfl(incl, 63);
             }
         }
-        __syncthreads();
+        lds_barrier();
         for (int i = tid; i < n; i += kEngThreads) {
             const int e = s.bexp[i];
             const int pos = s.boff[e] + atomicAdd(&s.bfill[e], 1);
             if (pos < kEngCap) s.bsort[pos] = s.bkey[i];
             else flag_internal(ctrl);
         }
-        __syncthreads();
+        lds_barrier();
         for (int j = wave; j < nt; j += kEngWaves) {
             const int e = s.tch[j];
             int nb = s.bcnt[e];
@@ -1037,10 +1065,10 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
                 if (lane == 0) flag_internal(ctrl);
                 nb = kEngCap - off;
             }
-            eng_update<M>(c, s, e, s.bsort + off, nb, nxt, &s_nnext);
+            eng_update<M>(c, s, e, s.bsort + off, nullptr, nb, nxt, &s_nnext);
         }
-        __threadfence_block();
-        __syncthreads();
+        }
+        lds_barrier();
         for (int j = tid; j < nt; j += kEngThreads) {
             const int e = s.tch[j];
             s.bcnt[e] = 0;
@@ -1056,7 +1084,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
         int *tmp = act;
         act = nxt;
         nxt = tmp;
-        __syncthreads();
+        lds_barrier();
     }
 
     // Hand the state back.
