@@ -164,7 +164,39 @@ __device__ inline void append_active(const Ctx<M> &c, int which, bool want, int 
 
 // One group of G lanes evaluates one token. VEC: rows are read as 16-byte
 // vectors (E % 8 == 0 for int16, E % 4 == 0 for fp32).
-// s1 returns the score S[t, e1] itself, so the bid needs no second read.
+// One group of G lanes evaluates one token: lane gl owns experts
+// [8 gl, 8 gl + 8) of every chunk of 8 G experts and loads them with
+// 16-byte vector reads issued before any comparison, so a row costs one
+// memory latency. Ties keep the lowest expert index (ascending scan inside a
+// lane, index comparison across lanes). s1 returns the score S[t, e1]
+// itself, so the bid needs no second read.
+template <class M>
+__device__ inline void load8(const typename M::score_t *S, int64_t base, int e0, int E, int64_t scale,
+                             typename M::value_t (&sv)[8]) {
+    using score_t = typename M::score_t;
+    constexpr int kVecElems = 16 / sizeof(score_t);   // 4 fp32 or 8 int16 per 16 bytes
+    const bool vec = (e0 + 8 <= E) && ((base + e0) % kVecElems == 0);
+    if (vec) {
+        if constexpr (sizeof(score_t) == 4) {
+            const float4 a = *reinterpret_cast<const float4 *>(S + base + e0);
+            const float4 b = *reinterpret_cast<const float4 *>(S + base + e0 + 4);
+            const float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) sv[j] = (typename M::value_t)f[j];
+        } else {
+            const uint4 a = *reinterpret_cast<const uint4 *>(S + base + e0);
+            const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                sv[j] = (typename M::value_t)(int16_t)(uint16_t)(w[j >> 1] >> (16 * (j & 1))) * scale;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            sv[j] = (e0 + j < E) ? M::load(S, base + e0 + j, scale) : (typename M::value_t)0;
+    }
+}
+
 template <class M, int G>
 __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const typename M::value_t *pr,
                                   typename M::value_t &v1, int &e1, typename M::value_t &v2,
@@ -177,16 +209,24 @@ __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const type
     e1 = 0x7fffffff;
     if (valid) {
         const int64_t row = (int64_t)t * c.E;
-        for (int e = gl; e < c.E; e += G) {
-            const value_t sv = M::load(c.S, row + e, c.scale);
-            const value_t v = sv - pr[e];
-            if (v > v1) {
-                v2 = v1;
-                v1 = v;
-                e1 = e;
-                s1 = sv;
-            } else if (v > v2) {
-                v2 = v;
+        for (int base = 0; base < c.E; base += 8 * G) {
+            const int e0 = base + 8 * gl;
+            if (e0 >= c.E) break;
+            value_t sv[8];
+            load8<M>(c.S, row, e0, c.E, c.scale, sv);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int e = e0 + j;
+                if (e >= c.E) break;
+                const value_t v = sv[j] - pr[e];
+                if (v > v1) {
+                    v2 = v1;
+                    v1 = v;
+                    e1 = e;
+                    s1 = sv[j];
+                } else if (v > v2) {
+                    v2 = v;
+                }
             }
         }
     }
@@ -1236,14 +1276,11 @@ __global__ void single_expert_kernel(int32_t *assign, int32_t *perm, int64_t T) 
 
 // ------------------------------------------------------------------ driver --
 
+// Lanes per token: 8 experts per lane, a power of two up to a whole wave.
 int lanes_per_token(int64_t E) {
-    if (E <= 1) return 1;
-    if (E <= 2) return 2;
-    if (E <= 8) return 4;
-    if (E <= 32) return 8;
-    if (E <= 128) return 16;
-    if (E <= 256) return 32;
-    return 64;
+    int g = 1;
+    while (g < 64 && 8 * g < E) g <<= 1;
+    return g;
 }
 
 template <class M, int G>
