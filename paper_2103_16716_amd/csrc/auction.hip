@@ -58,7 +58,7 @@ inline void debug_note(const char *what, hipError_t err) {
 
 struct Layout {
     size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
-        total;
+        eck, ecs, ecn, total;
     int64_t cap, nblk;
 };
 
@@ -80,6 +80,9 @@ Layout make_layout(int64_t T, int64_t E) {
     L.ovf_exp = off; off += align_up((size_t)T * 4);
     L.active = off;  off += align_up((size_t)2 * T * 4);
     L.blk = off;     off += align_up((size_t)L.nblk * E * 4);
+    L.eck = off;     off += align_up((size_t)E * 64 * 8);   // engine entry lists (K <= 64)
+    L.ecs = off;     off += align_up((size_t)E * 64 * 2);
+    L.ecn = off;     off += align_up((size_t)E * 4);
     L.total = off;
     return L;
 }
@@ -97,6 +100,10 @@ struct Ctx {
     int *ovf_exp, *active;
     int *ovf_count;   // lives in ctrl->pad0
     int engine_cap;   // > 0: rounds with at most this many active tokens go to the engine
+    int eng_k;        // length of the engine's per-expert lists of lowest keys
+    uint64_t *eng_ck; // the lists as built at the engine's entry
+    uint16_t *eng_cs;
+    int *eng_cn;
 };
 
 template <class M>
@@ -121,6 +128,10 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.active = reinterpret_cast<int *>(ws + L.active);
     c.ovf_count = &c.ctrl->pad0;
     c.engine_cap = 0;
+    c.eng_k = 8;
+    c.eng_ck = reinterpret_cast<uint64_t *>(ws + L.eck);
+    c.eng_cs = reinterpret_cast<uint16_t *>(ws + L.ecs);
+    c.eng_cn = reinterpret_cast<int *>(ws + L.ecn);
     return c;
 }
 
@@ -747,6 +758,19 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
 }
 
 // ------------------------------------------------------------ tail engine --
+//
+// The rounds left once at most kEngCap tokens are active run inside one
+// workgroup with all mutable state in LDS:
+//   prices and holder counts of every expert,
+//   the K lowest held keys of every expert (sorted ascending) with the slot
+//   each occupies in the expert's holder table in global memory,
+//   the active tokens and the round's bids grouped by expert.
+// Bids are computed against the prices at the start of the round (Jacobi),
+// then one wave per touched expert streams that expert's bids through the
+// rule "a new key replaces the lowest held key when it is larger"; for any
+// arrival order this leaves the C largest keys of holders and bids, i.e. the
+// same result as a selection. The lowest held key is the expert's price once
+// it is full. A cached list that runs empty is refilled from the holder table.
 
 // Workgroup barrier that orders LDS only: in-flight global stores are not
 // waited for (the engine's one full barrier per round, after the bids, covers
@@ -756,36 +780,24 @@ __device__ inline void lds_barrier() {
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
-//
-// The rounds left once at most kEngCap tokens are active run inside one
-// workgroup with all mutable state in LDS:
-//   prices and holder counts of every expert,
-//   the kCache lowest held keys of every expert (sorted ascending) with the
-//   slot each occupies in the expert's holder table in global memory,
-//   the active tokens and the round's bids grouped by expert.
-// Bids are computed against the prices at the start of the round (Jacobi),
-// then one wave per touched expert streams that expert's bids through the
-// rule "a new key replaces the lowest held key when it is larger"; for any
-// arrival order this leaves the C largest keys of holders and bids, i.e. the
-// same result as a selection. The lowest held key is the expert's price once
-// it is full. A cached list that runs empty is refilled from the holder table.
 
 constexpr int kEngThreads = 512;
 constexpr int kEngWaves = kEngThreads / 64;
-constexpr int kCache = 8;
 constexpr int kEngCap = 1024;
 constexpr int kEngDirect = 64;   // rounds with at most this many bids skip the grouping
 constexpr int kEngMaxE = 512;
-constexpr int kEngMaxC = 512;
-constexpr int kRefillRegs = kEngMaxC / 64;
+constexpr int kEngMaxC = 512;    // holder tables a wave holds in registers (8 keys per lane)
+constexpr int kEngMaxK = 64;     // longest per-expert list of lowest keys
+constexpr int kPend = 32;        // holder-table stores a wave batches per expert
 
 struct EngLayout {
-    size_t pr, cnt, cn, sel, bcnt, boff, bfill, tch, ck, cs, bkey, bexp, bsort, actA, actB, total;
+    size_t pr, cnt, cn, sel, bcnt, boff, bfill, tch, ck, cs, bkey, bexp, bsort, actA, actB, pslot,
+        pkey, pn, total;
 };
 
 __host__ __device__ inline size_t eng_align(size_t x) { return (x + 15) & ~size_t(15); }
 
-__host__ __device__ inline EngLayout eng_layout(int E, int value_bytes) {
+__host__ __device__ inline EngLayout eng_layout(int E, int value_bytes, int K) {
     EngLayout L{};
     size_t off = 0;
     L.pr = off;    off = eng_align(off + (size_t)E * value_bytes);
@@ -796,13 +808,16 @@ __host__ __device__ inline EngLayout eng_layout(int E, int value_bytes) {
     L.boff = off;  off = eng_align(off + (size_t)E * 4);
     L.bfill = off; off = eng_align(off + (size_t)E * 4);
     L.tch = off;   off = eng_align(off + (size_t)E * 4);
-    L.ck = off;    off = eng_align(off + (size_t)E * kCache * 8);
-    L.cs = off;    off = eng_align(off + (size_t)E * kCache * 4);
+    L.ck = off;    off = eng_align(off + (size_t)E * K * 8);
+    L.cs = off;    off = eng_align(off + (size_t)E * K * 2);
     L.bkey = off;  off = eng_align(off + (size_t)kEngCap * 8);
     L.bexp = off;  off = eng_align(off + (size_t)kEngCap * 4);
     L.bsort = off; off = eng_align(off + (size_t)kEngCap * 8);
     L.actA = off;  off = eng_align(off + (size_t)kEngCap * 4);
     L.actB = off;  off = eng_align(off + (size_t)kEngCap * 4);
+    L.pslot = off; off = eng_align(off + (size_t)kEngWaves * kPend * 4);
+    L.pkey = off;  off = eng_align(off + (size_t)kEngWaves * kPend * 8);
+    L.pn = off;    off = eng_align(off + (size_t)kEngWaves * 4);
     L.total = off;
     return L;
 }
@@ -812,9 +827,13 @@ struct Eng {
     typename M::value_t *pr;
     int *cnt, *cn, *sel, *bcnt, *boff, *bfill, *tch;
     uint64_t *ck;
-    int *cs;
+    uint16_t *cs;
     uint64_t *bkey, *bsort;
     int *bexp;
+    int *pslot;      // per wave: batched holder-table stores (slot, key)
+    uint64_t *pkey;
+    int *pn;
+    int K;
 };
 
 __device__ inline uint64_t wave_min_u64(uint64_t v) {
@@ -826,99 +845,157 @@ __device__ inline uint64_t wave_min_u64(uint64_t v) {
     return v;
 }
 
-// One wave: the kCache lowest keys of expert e's holder table, sorted.
+__device__ inline void cswap(uint64_t &a, int &sa, uint64_t &b, int &sb) {
+    if (b < a) {
+        const uint64_t t = a;
+        a = b;
+        b = t;
+        const int u = sa;
+        sa = sb;
+        sb = u;
+    }
+}
+
+// Stores the wave's batched holder-table writes for expert e.
 template <class M>
-__device__ void eng_refill(const Ctx<M> &c, const Eng<M> &s, int e) {
-    __threadfence_block();   // this wave's holder-table stores before the reads below
+__device__ inline void eng_flush(const Ctx<M> &c, const Eng<M> &s, int e, uint64_t *hold) {
     const int lane = lane_id();
+    const int w = threadIdx.x >> 6;
+    const int np = s.pn[w];
+    if (lane < np) {
+        const int slot = s.pslot[w * kPend + lane];
+        if (slot >= 0 && slot < c.C) hold[slot] = s.pkey[w * kPend + lane];
+        else flag_internal(c.ctrl);
+    }
+    if (lane == 0) s.pn[w] = 0;
+}
+
+// Records hold[slot] = key for expert e (stored by eng_flush).
+template <class M>
+__device__ inline void eng_write(const Ctx<M> &c, const Eng<M> &s, int e, uint64_t *hold, int slot,
+                                 uint64_t key) {
+    const int w = threadIdx.x >> 6;
+    if (s.pn[w] >= kPend) eng_flush<M>(c, s, e, hold);
+    if (lane_id() == 0) {
+        const int np = s.pn[w];
+        s.pslot[w * kPend + np] = slot;
+        s.pkey[w * kPend + np] = key;
+        s.pn[w] = np + 1;
+    }
+}
+
+// One wave: the K lowest keys of expert e's holder table, sorted. The table
+// is read from global memory and patched with this wave's batched writes.
+template <class M>
+__device__ void eng_refill(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *hold) {
+    __threadfence_block();   // this wave's earlier flushed stores before the reads below
+    const int lane = lane_id();
+    const int w = threadIdx.x >> 6;
     const int count = s.cnt[e];
-    const uint64_t *hold = c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
-    uint64_t kk[kRefillRegs];
+    uint64_t kk[8];
+    int ss[8];
 #pragma unroll
-    for (int r = 0; r < kRefillRegs; ++r) {
+    for (int r = 0; r < 8; ++r) {
         const int idx = lane + 64 * r;
         kk[r] = idx < count ? hold[idx] : ~0ull;
+        ss[r] = idx;
     }
-    const int take = count < kCache ? count : kCache;
-    for (int q = 0; q < take; ++q) {
-        uint64_t mk = ~0ull;
-        int mr = 0;
+    const int np = s.pn[w];
+    for (int j = 0; j < np; ++j) {
+        const int slot = s.pslot[w * kPend + j];
+        const uint64_t key = s.pkey[w * kPend + j];
+        if ((slot & 63) == lane) {
 #pragma unroll
-        for (int r = 0; r < kRefillRegs; ++r)
-            if (kk[r] < mk) {
-                mk = kk[r];
-                mr = r;
-            }
-        const uint64_t g = wave_min_u64(mk);
-        const uint64_t owners = __ballot(mk == g && g != ~0ull);
-        const int owner = owners ? __ffsll((long long)owners) - 1 : 0;
-        int slot = 0;
-        if (lane == owner) {
-            slot = lane + 64 * mr;
-#pragma unroll
-            for (int r = 0; r < kRefillRegs; ++r)
-                if (r == mr) kk[r] = ~0ull;
+            for (int r = 0; r < 8; ++r)
+                if ((slot >> 6) == r) kk[r] = key;
         }
-        slot = __shfl(slot, owner);
+    }
+    // Sort the lane's 8 entries (Batcher's network), then merge across lanes.
+    cswap(kk[0], ss[0], kk[1], ss[1]); cswap(kk[2], ss[2], kk[3], ss[3]);
+    cswap(kk[4], ss[4], kk[5], ss[5]); cswap(kk[6], ss[6], kk[7], ss[7]);
+    cswap(kk[0], ss[0], kk[2], ss[2]); cswap(kk[1], ss[1], kk[3], ss[3]);
+    cswap(kk[4], ss[4], kk[6], ss[6]); cswap(kk[5], ss[5], kk[7], ss[7]);
+    cswap(kk[1], ss[1], kk[2], ss[2]); cswap(kk[5], ss[5], kk[6], ss[6]);
+    cswap(kk[0], ss[0], kk[4], ss[4]); cswap(kk[1], ss[1], kk[5], ss[5]);
+    cswap(kk[2], ss[2], kk[6], ss[6]); cswap(kk[3], ss[3], kk[7], ss[7]);
+    cswap(kk[2], ss[2], kk[4], ss[4]); cswap(kk[3], ss[3], kk[5], ss[5]);
+    cswap(kk[1], ss[1], kk[2], ss[2]); cswap(kk[3], ss[3], kk[4], ss[4]);
+    cswap(kk[5], ss[5], kk[6], ss[6]);
+    const int take = count < s.K ? count : s.K;
+    for (int q = 0; q < take; ++q) {
+        const uint64_t g = wave_min_u64(kk[0]);
+        const uint64_t owners = __ballot(kk[0] == g);
+        const int owner = owners ? __ffsll((long long)owners) - 1 : 0;
+        const int slot = __shfl(ss[0], owner);
+        if (lane == owner) {
+#pragma unroll
+            for (int r = 0; r < 7; ++r) {
+                kk[r] = kk[r + 1];
+                ss[r] = ss[r + 1];
+            }
+            kk[7] = ~0ull;
+        }
         if (lane == 0) {
-            s.ck[e * kCache + q] = g;
-            s.cs[e * kCache + q] = slot;
+            s.ck[e * s.K + q] = g;
+            s.cs[e * s.K + q] = (uint16_t)slot;
         }
     }
     if (lane == 0) s.cn[e] = take;
 }
 
 // One wave: inserts key b (held in `slot`) into expert e's sorted list if it
-// belongs to the lowest kCache keys. `complete` says every holder other than
-// b is in the list.
+// belongs to the lowest K keys. `complete` says every holder other than b is
+// in the list.
 template <class M>
 __device__ inline void eng_cache_insert(const Eng<M> &s, int e, uint64_t b, int slot, bool complete) {
     const int lane = lane_id();
+    const int K = s.K;
     const int nc = s.cn[e];
-    if (!complete && (nc == 0 || b > s.ck[e * kCache + nc - 1])) return;   // stays outside
+    if (!complete && (nc == 0 || b > s.ck[e * K + nc - 1])) return;   // stays outside
     uint64_t v = ~0ull;
-    int sl = 0;
+    uint16_t sl = 0;
     if (lane < nc) {
-        v = s.ck[e * kCache + lane];
-        sl = s.cs[e * kCache + lane];
+        v = s.ck[e * K + lane];
+        sl = s.cs[e * K + lane];
     }
     const int pos = __popcll(__ballot(lane < nc && v < b));
-    if (pos >= kCache) return;   // larger than a full list of keys
-    if (lane >= pos && lane < nc && lane + 1 < kCache) {
-        s.ck[e * kCache + lane + 1] = v;
-        s.cs[e * kCache + lane + 1] = sl;
+    if (pos >= K) return;   // larger than a full list of keys
+    if (lane >= pos && lane < nc && lane + 1 < K) {
+        s.ck[e * K + lane + 1] = v;
+        s.cs[e * K + lane + 1] = sl;
     }
     if (lane == pos) {
-        s.ck[e * kCache + pos] = b;
-        s.cs[e * kCache + pos] = slot;
+        s.ck[e * K + pos] = b;
+        s.cs[e * K + pos] = (uint16_t)slot;
     }
-    if (lane == 0) s.cn[e] = nc + 1 < kCache ? nc + 1 : kCache;
+    if (lane == 0) s.cn[e] = nc + 1 < K ? nc + 1 : K;
 }
 
 template <class M>
 __device__ inline void eng_cache_pop(const Eng<M> &s, int e) {
     const int lane = lane_id();
+    const int K = s.K;
     const int nc = s.cn[e];
     uint64_t v = 0;
-    int sl = 0;
+    uint16_t sl = 0;
     if (lane >= 1 && lane < nc) {
-        v = s.ck[e * kCache + lane];
-        sl = s.cs[e * kCache + lane];
+        v = s.ck[e * K + lane];
+        sl = s.cs[e * K + lane];
     }
     if (lane >= 1 && lane < nc) {
-        s.ck[e * kCache + lane - 1] = v;
-        s.cs[e * kCache + lane - 1] = sl;
+        s.ck[e * K + lane - 1] = v;
+        s.cs[e * K + lane - 1] = sl;
     }
     if (lane == 0) s.cn[e] = nc > 0 ? nc - 1 : 0;
 }
 
-// One wave: streams expert e's bids of this round into its holders.
-// Bids are bids[0..nb), or, with `exps`, the entries of bids[0..nb) whose
-// expert exps[j] is e.
+// One wave: streams expert e's bids of this round into its holders. Bids are
+// bids[0..nb), or, with `exps`, the entries of bids[0..nb) whose expert is e.
 template <class M>
 __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *bids,
                            const int *exps, int nb, int *nxt, int *nnext) {
     const int lane = lane_id();
+    const int K = s.K;
     uint64_t *hold = c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
     for (int j = 0; j < nb; ++j) {
         if (exps != nullptr && exps[j] != e) continue;
@@ -927,29 +1004,24 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
         int out_tok = -1;
         if (count < c.C) {
             const bool complete = s.cn[e] == count;
-            if (lane == 0) {
-                hold[count] = b;
-                s.cnt[e] = count + 1;
-            }
+            eng_write<M>(c, s, e, hold, count, b);
+            if (lane == 0) s.cnt[e] = count + 1;
             eng_cache_insert<M>(s, e, b, count, complete);
             if (count + 1 == c.C) {
-                if (s.cn[e] == 0) eng_refill<M>(c, s, e);
-                if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * kCache]);
+                if (s.cn[e] == 0) eng_refill<M>(c, s, e, hold);
+                if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * K]);
             }
         } else {
-            if (s.cn[e] == 0) eng_refill<M>(c, s, e);
-            const uint64_t m = s.ck[e * kCache];
+            if (s.cn[e] == 0) eng_refill<M>(c, s, e, hold);
+            const uint64_t m = s.ck[e * K];
             if (b > m) {
-                const int slot = s.cs[e * kCache];
+                const int slot = s.cs[e * K];
                 out_tok = key_token(m);
                 eng_cache_pop<M>(s, e);
-                if (lane == 0) {
-                    if (slot >= 0 && slot < c.C) hold[slot] = b;
-                    else flag_internal(c.ctrl);
-                }
+                eng_write<M>(c, s, e, hold, slot, b);
                 eng_cache_insert<M>(s, e, b, slot, s.cn[e] == count - 1);
-                if (s.cn[e] == 0) eng_refill<M>(c, s, e);
-                if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * kCache]);
+                if (s.cn[e] == 0) eng_refill<M>(c, s, e, hold);
+                if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * K]);
             } else {
                 out_tok = key_token(b);
             }
@@ -960,14 +1032,75 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
             else flag_internal(c.ctrl);
         }
     }
+    eng_flush<M>(c, s, e, hold);
+}
+
+// The engine's phase entry, one block per expert: sorts the expert's holder
+// table and stores its K lowest keys (with slots) for the engine to load.
+template <class M>
+__global__ __launch_bounds__(256) void cache_build_kernel(Ctx<M> c) {
+    __shared__ uint64_t keys[kEngMaxC];
+    __shared__ uint16_t slots[kEngMaxC];
+    __shared__ int go;
+    SolveCtrl *ctrl = c.ctrl;
+    if (threadIdx.x == 0) {
+        go = 0;
+        if (!ctrl->done && !ctrl->all_active) {
+            const int n = ld_relaxed(&ctrl->active_count[ctrl->cur]);
+            if (n > 0 && n <= c.engine_cap) go = 1;
+        }
+    }
+    __syncthreads();
+    if (!go) return;
+    const int e = blockIdx.x;
+    int cnt = ld_relaxed(&c.hcount[e]);
+    if (cnt < 0 || cnt > c.C) {
+        if (threadIdx.x == 0) flag_internal(ctrl);
+        cnt = cnt < 0 ? 0 : c.C;
+    }
+    const uint64_t *hold = c.holders + (int64_t)(ld_relaxed(&c.hsel[e]) & 1) * c.T + (int64_t)e * c.C;
+    int P = 1;
+    while (P < cnt) P <<= 1;
+    for (int i = threadIdx.x; i < P; i += blockDim.x) {
+        keys[i] = i < cnt ? hold[i] : ~0ull;
+        slots[i] = (uint16_t)i;
+    }
+    __syncthreads();
+    for (int k = 2; k <= P; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = threadIdx.x; i < P; i += blockDim.x) {
+                const int ixj = i ^ j;
+                if (ixj > i) {
+                    const bool up = (i & k) == 0;
+                    const uint64_t a = keys[i], b = keys[ixj];
+                    if ((a > b) == up) {
+                        keys[i] = b;
+                        keys[ixj] = a;
+                        const uint16_t t = slots[i];
+                        slots[i] = slots[ixj];
+                        slots[ixj] = t;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    const int take = cnt < c.eng_k ? cnt : c.eng_k;
+    for (int q = threadIdx.x; q < take; q += blockDim.x) {
+        c.eng_ck[(int64_t)e * c.eng_k + q] = keys[q];
+        c.eng_cs[(int64_t)e * c.eng_k + q] = slots[q];
+    }
+    if (threadIdx.x == 0) c.eng_cn[e] = take;
 }
 
 template <class M, int G>
 __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignParams p) {
     using value_t = typename M::value_t;
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    const EngLayout L = eng_layout(c.E, (int)sizeof(value_t));
+    const int K = c.eng_k;
+    const EngLayout L = eng_layout(c.E, (int)sizeof(value_t), K);
     Eng<M> s;
+    s.K = K;
     s.pr = reinterpret_cast<value_t *>(smem_raw + L.pr);
     s.cnt = reinterpret_cast<int *>(smem_raw + L.cnt);
     s.cn = reinterpret_cast<int *>(smem_raw + L.cn);
@@ -977,10 +1110,13 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
     s.bfill = reinterpret_cast<int *>(smem_raw + L.bfill);
     s.tch = reinterpret_cast<int *>(smem_raw + L.tch);
     s.ck = reinterpret_cast<uint64_t *>(smem_raw + L.ck);
-    s.cs = reinterpret_cast<int *>(smem_raw + L.cs);
+    s.cs = reinterpret_cast<uint16_t *>(smem_raw + L.cs);
     s.bkey = reinterpret_cast<uint64_t *>(smem_raw + L.bkey);
     s.bexp = reinterpret_cast<int *>(smem_raw + L.bexp);
     s.bsort = reinterpret_cast<uint64_t *>(smem_raw + L.bsort);
+    s.pslot = reinterpret_cast<int *>(smem_raw + L.pslot);
+    s.pkey = reinterpret_cast<uint64_t *>(smem_raw + L.pkey);
+    s.pn = reinterpret_cast<int *>(smem_raw + L.pn);
     int *act = reinterpret_cast<int *>(smem_raw + L.actA);
     int *nxt = reinterpret_cast<int *>(smem_raw + L.actB);
     __shared__ int s_go, s_cur, s_n, s_nnext, s_ntouched, s_rounds, s_stop;
@@ -1012,23 +1148,28 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
     const value_t eps = (value_t)ctrl->eps;
     for (int e = tid; e < c.E; e += kEngThreads) {
         s.pr[e] = c.prices[e];
-        s.cnt[e] = ld_relaxed(&c.hcount[e]);
+        int cnt = ld_relaxed(&c.hcount[e]);
+        int cn = c.eng_cn[e];
+        if (cnt < 0 || cnt > c.C || cn < 0 || cn > K || cn > cnt) {
+            flag_internal(ctrl);
+            cnt = cnt < 0 ? 0 : (cnt > c.C ? c.C : cnt);
+            cn = 0;
+        }
+        s.cnt[e] = cnt;
+        s.cn[e] = cn;
         s.sel[e] = ld_relaxed(&c.hsel[e]) & 1;
         s.bcnt[e] = 0;
         s.bfill[e] = 0;
     }
+    for (int i = tid; i < c.E * K; i += kEngThreads) {
+        s.ck[i] = c.eng_ck[i];
+        s.cs[i] = c.eng_cs[i];
+    }
+    if (tid < kEngWaves) s.pn[tid] = 0;
     for (int i = tid; i < s_n; i += kEngThreads) {
         const int t = c.active[(int64_t)s_cur * c.T + i];
         act[i] = (t >= 0 && t < c.T) ? t : 0;
         if (t < 0 || t >= c.T) flag_internal(ctrl);
-    }
-    __syncthreads();
-    for (int e = wave; e < c.E; e += kEngWaves) {
-        if (s.cnt[e] < 0 || s.cnt[e] > c.C) {
-            if (lane == 0) flag_internal(ctrl);
-            if (lane == 0) s.cnt[e] = 0;
-        }
-        eng_refill<M>(c, s, e);
     }
     __syncthreads();
 
@@ -1074,39 +1215,39 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
             for (int j = wave; j < nt; j += kEngWaves)
                 eng_update<M>(c, s, s.tch[j], s.bkey, s.bexp, n, nxt, &s_nnext);
         } else {
-        if (wave == 0) {
-            int base = 0;
-            for (int j0 = 0; j0 < nt; j0 += 64) {
-                const int j = j0 + lane;
-                const int cj = j < nt ? s.bcnt[s.tch[j]] : 0;
-                int incl = cj;
+            if (wave == 0) {
+                int base = 0;
+                for (int j0 = 0; j0 < nt; j0 += 64) {
+                    const int j = j0 + lane;
+                    const int cj = j < nt ? s.bcnt[s.tch[j]] : 0;
+                    int incl = cj;
 #pragma unroll
-                for (int off = 1; off < 64; off <<= 1) {
-                    const int o = __shfl_up(incl, off);
-                    if (lane >= off) incl += o;
+                    for (int off = 1; off < 64; off <<= 1) {
+                        const int o = __shfl_up(incl, off);
+                        if (lane >= off) incl += o;
+                    }
+                    if (j < nt) s.boff[s.tch[j]] = base + incl - cj;
+                    base += __shfl(incl, 63);
                 }
-                if (j < nt) s.boff[s.tch[j]] = base + incl - cj;
-                base += __shfl(incl, 63);
             }
-        }
-        lds_barrier();
-        for (int i = tid; i < n; i += kEngThreads) {
-            const int e = s.bexp[i];
-            const int pos = s.boff[e] + atomicAdd(&s.bfill[e], 1);
-            if (pos < kEngCap) s.bsort[pos] = s.bkey[i];
-            else flag_internal(ctrl);
-        }
-        lds_barrier();
-        for (int j = wave; j < nt; j += kEngWaves) {
-            const int e = s.tch[j];
-            int nb = s.bcnt[e];
-            const int off = s.boff[e];
-            if (off + nb > kEngCap) {
-                if (lane == 0) flag_internal(ctrl);
-                nb = kEngCap - off;
+            lds_barrier();
+            for (int i = tid; i < n; i += kEngThreads) {
+                const int e = s.bexp[i];
+                const int pos = s.boff[e] + atomicAdd(&s.bfill[e], 1);
+                if (pos < kEngCap) s.bsort[pos] = s.bkey[i];
+                else flag_internal(ctrl);
             }
-            eng_update<M>(c, s, e, s.bsort + off, nullptr, nb, nxt, &s_nnext);
-        }
+            lds_barrier();
+            for (int j = wave; j < nt; j += kEngWaves) {
+                const int e = s.tch[j];
+                int nb = s.bcnt[e];
+                const int off = s.boff[e];
+                if (off + nb > kEngCap) {
+                    if (lane == 0) flag_internal(ctrl);
+                    nb = kEngCap - off;
+                }
+                eng_update<M>(c, s, e, s.bsort + off, nullptr, nb, nxt, &s_nnext);
+            }
         }
         lds_barrier();
         for (int j = tid; j < nt; j += kEngThreads) {
@@ -1287,18 +1428,37 @@ template <class M, int G>
 hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     using value_t = typename M::value_t;
     Ctx<M> c = c0;
-    const size_t eng_bytes = eng_layout(c.E, (int)sizeof(value_t)).total;
+    // The engine's LDS: the longest per-expert lists that fit the device's
+    // per-block limit (with the opt-in above the default 64 KiB).
     bool engine = c.E <= kEngMaxE && c.C <= kEngMaxC;
-    if (engine && eng_bytes > 64 * 1024) {
-        // Layouts above the default per-block LDS need the opt-in; without it
-        // the rounds stay with the grid-wide kernels and the fallback tail.
-        const hipError_t err = hipFuncSetAttribute(
-            reinterpret_cast<const void *>(&engine_kernel<M, G>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, (int)eng_bytes);
-        if (err != hipSuccess) {
-            (void)hipGetLastError();
-            debug_note("engine LDS opt-in refused", err);
+    size_t eng_bytes = 0;
+    if (engine) {
+        int dev = 0, optin = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) != hipSuccess ||
+            optin <= 0)
+            optin = 64 * 1024;
+        const size_t limit = (size_t)optin - 1024;   // room for the kernel's static LDS
+        int K = kEngMaxK;
+        while (K >= 8 && eng_layout(c.E, (int)sizeof(value_t), K).total > limit) K >>= 1;
+        if (K < 8) {
             engine = false;
+        } else {
+            eng_bytes = eng_layout(c.E, (int)sizeof(value_t), K).total;
+            if (eng_bytes > 64 * 1024) {
+                const hipError_t err = hipFuncSetAttribute(
+                    reinterpret_cast<const void *>(&engine_kernel<M, G>),
+                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)eng_bytes);
+                if (err != hipSuccess) {
+                    (void)hipGetLastError();
+                    debug_note("engine LDS opt-in refused", err);
+                    while (K >= 8 && eng_layout(c.E, (int)sizeof(value_t), K).total > 64 * 1024)
+                        K >>= 1;
+                    engine = K >= 8;
+                    if (engine) eng_bytes = eng_layout(c.E, (int)sizeof(value_t), K).total;
+                }
+            }
+            c.eng_k = K;
         }
     }
     if (engine) c.engine_cap = kEngCap;
@@ -1327,9 +1487,11 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
                                s, c);
             hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks), dim3(kThreads), 0, s, c);
         }
-        if (engine)
+        if (engine) {
+            hipLaunchKernelGGL(cache_build_kernel<M>, dim3(c.E), dim3(256), 0, s, c);
             hipLaunchKernelGGL((engine_kernel<M, G>), dim3(1), dim3(kEngThreads), eng_bytes, s, c,
                                p);
+        }
         hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1), dim3(kThreads), tail_smem, s, c, p,
                            slot == slots - 1 ? 1 : 0);
     }
