@@ -945,7 +945,9 @@ __device__ void eng_refill(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
 
 // One wave: inserts key b (held in `slot`) into expert e's sorted list if it
 // belongs to the lowest K keys. `complete` says every holder other than b is
-// in the list.
+// in the list. Entries move between lanes through shuffles, so every lane
+// reads and writes only its own list position (no lane reads an LDS word
+// another lane writes in the same step).
 template <class M>
 __device__ inline void eng_cache_insert(const Eng<M> &s, int e, uint64_t b, int slot, bool complete) {
     const int lane = lane_id();
@@ -953,38 +955,40 @@ __device__ inline void eng_cache_insert(const Eng<M> &s, int e, uint64_t b, int 
     const int nc = s.cn[e];
     if (!complete && (nc == 0 || b > s.ck[e * K + nc - 1])) return;   // stays outside
     uint64_t v = ~0ull;
-    uint16_t sl = 0;
+    int sl = 0;
     if (lane < nc) {
         v = s.ck[e * K + lane];
         sl = s.cs[e * K + lane];
     }
     const int pos = __popcll(__ballot(lane < nc && v < b));
     if (pos >= K) return;   // larger than a full list of keys
-    if (lane >= pos && lane < nc && lane + 1 < K) {
-        s.ck[e * K + lane + 1] = v;
-        s.cs[e * K + lane + 1] = sl;
+    const uint64_t vprev = __shfl_up(v, 1);
+    const int slprev = __shfl_up(sl, 1);
+    const int nn = nc + 1 < K ? nc + 1 : K;
+    if (lane >= pos && lane < nn) {
+        s.ck[e * K + lane] = lane == pos ? b : vprev;
+        s.cs[e * K + lane] = (uint16_t)(lane == pos ? slot : slprev);
     }
-    if (lane == pos) {
-        s.ck[e * K + pos] = b;
-        s.cs[e * K + pos] = (uint16_t)slot;
-    }
-    if (lane == 0) s.cn[e] = nc + 1 < K ? nc + 1 : K;
+    if (lane == 0) s.cn[e] = nn;
 }
 
+// One wave: removes the lowest entry of expert e's list.
 template <class M>
 __device__ inline void eng_cache_pop(const Eng<M> &s, int e) {
     const int lane = lane_id();
     const int K = s.K;
     const int nc = s.cn[e];
-    uint64_t v = 0;
-    uint16_t sl = 0;
-    if (lane >= 1 && lane < nc) {
+    uint64_t v = ~0ull;
+    int sl = 0;
+    if (lane < nc) {
         v = s.ck[e * K + lane];
         sl = s.cs[e * K + lane];
     }
-    if (lane >= 1 && lane < nc) {
-        s.ck[e * K + lane - 1] = v;
-        s.cs[e * K + lane - 1] = sl;
+    const uint64_t vnext = __shfl_down(v, 1);
+    const int slnext = __shfl_down(sl, 1);
+    if (lane + 1 < nc) {
+        s.ck[e * K + lane] = vnext;
+        s.cs[e * K + lane] = (uint16_t)slnext;
     }
     if (lane == 0) s.cn[e] = nc > 0 ? nc - 1 : 0;
 }
