@@ -788,11 +788,9 @@ constexpr int kEngDirect = 64;   // rounds with at most this many bids skip the 
 constexpr int kEngMaxE = 512;
 constexpr int kEngMaxC = 512;    // holder tables a wave holds in registers (8 keys per lane)
 constexpr int kEngMaxK = 64;     // longest per-expert list of lowest keys
-constexpr int kPend = 32;        // holder-table stores a wave batches per expert
 
 struct EngLayout {
-    size_t pr, cnt, cn, sel, bcnt, boff, bfill, tch, ck, cs, bkey, bexp, bsort, actA, actB, pslot,
-        pkey, pn, total;
+    size_t pr, cnt, cn, sel, bcnt, boff, bfill, tch, ck, cs, bkey, bexp, bsort, actA, actB, total;
 };
 
 __host__ __device__ inline size_t eng_align(size_t x) { return (x + 15) & ~size_t(15); }
@@ -815,9 +813,6 @@ __host__ __device__ inline EngLayout eng_layout(int E, int value_bytes, int K) {
     L.bsort = off; off = eng_align(off + (size_t)kEngCap * 8);
     L.actA = off;  off = eng_align(off + (size_t)kEngCap * 4);
     L.actB = off;  off = eng_align(off + (size_t)kEngCap * 4);
-    L.pslot = off; off = eng_align(off + (size_t)kEngWaves * kPend * 4);
-    L.pkey = off;  off = eng_align(off + (size_t)kEngWaves * kPend * 8);
-    L.pn = off;    off = eng_align(off + (size_t)kEngWaves * 4);
     L.total = off;
     return L;
 }
@@ -830,9 +825,6 @@ struct Eng {
     uint16_t *cs;
     uint64_t *bkey, *bsort;
     int *bexp;
-    int *pslot;      // per wave: batched holder-table stores (slot, key)
-    uint64_t *pkey;
-    int *pn;
     int K;
 };
 
@@ -856,58 +848,64 @@ __device__ inline void cswap(uint64_t &a, int &sa, uint64_t &b, int &sb) {
     }
 }
 
-// Stores the wave's batched holder-table writes for expert e.
+// Expert state while one wave updates it, held in registers: lane q owns
+// entry q of the sorted list of lowest keys (key, slot), and lane q also
+// owns pending holder-table store q. Every lane keeps identical copies of
+// the scalar fields, and every exchange between lanes is a shuffle, so no
+// lane ever depends on an LDS word another lane wrote.
 template <class M>
-__device__ inline void eng_flush(const Ctx<M> &c, const Eng<M> &s, int e, uint64_t *hold) {
-    const int lane = lane_id();
-    const int w = threadIdx.x >> 6;
-    const int np = s.pn[w];
-    if (lane < np) {
-        const int slot = s.pslot[w * kPend + lane];
-        if (slot >= 0 && slot < c.C) hold[slot] = s.pkey[w * kPend + lane];
+struct ExpertRegs {
+    uint64_t key;    // this lane's list entry (~0 when unused)
+    int slot;
+    int cn;          // list length (uniform)
+    int cnt;         // holders (uniform)
+    uint64_t pkey;   // this lane's pending store
+    int pslot;
+    int np;          // pending stores (uniform)
+    typename M::value_t price;
+};
+
+template <class M>
+__device__ inline void er_flush(const Ctx<M> &c, uint64_t *hold, ExpertRegs<M> &r) {
+    if (lane_id() < r.np) {
+        if (r.pslot >= 0 && r.pslot < c.C) hold[r.pslot] = r.pkey;
         else flag_internal(c.ctrl);
     }
-    if (lane == 0) s.pn[w] = 0;
+    r.np = 0;
 }
 
-// Records hold[slot] = key for expert e (stored by eng_flush).
+// Records hold[slot] = key (stored by er_flush).
 template <class M>
-__device__ inline void eng_write(const Ctx<M> &c, const Eng<M> &s, int e, uint64_t *hold, int slot,
-                                 uint64_t key) {
-    const int w = threadIdx.x >> 6;
-    if (s.pn[w] >= kPend) eng_flush<M>(c, s, e, hold);
-    if (lane_id() == 0) {
-        const int np = s.pn[w];
-        s.pslot[w * kPend + np] = slot;
-        s.pkey[w * kPend + np] = key;
-        s.pn[w] = np + 1;
+__device__ inline void er_write(const Ctx<M> &c, uint64_t *hold, ExpertRegs<M> &r, int slot,
+                                uint64_t key) {
+    if (r.np == 64) er_flush<M>(c, hold, r);
+    if (lane_id() == r.np) {
+        r.pslot = slot;
+        r.pkey = key;
     }
+    r.np += 1;
 }
 
-// One wave: the K lowest keys of expert e's holder table, sorted. The table
-// is read from global memory and patched with this wave's batched writes.
+// The K lowest keys of the expert's holder table, sorted, into the lanes.
+// The table is read from global memory and patched with the pending stores.
 template <class M>
-__device__ void eng_refill(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *hold) {
-    __threadfence_block();   // this wave's earlier flushed stores before the reads below
+__device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRegs<M> &r) {
     const int lane = lane_id();
-    const int w = threadIdx.x >> 6;
-    const int count = s.cnt[e];
     uint64_t kk[8];
     int ss[8];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-        const int idx = lane + 64 * r;
-        kk[r] = idx < count ? hold[idx] : ~0ull;
-        ss[r] = idx;
+    for (int q = 0; q < 8; ++q) {
+        const int idx = lane + 64 * q;
+        kk[q] = idx < r.cnt ? hold[idx] : ~0ull;
+        ss[q] = idx;
     }
-    const int np = s.pn[w];
-    for (int j = 0; j < np; ++j) {
-        const int slot = s.pslot[w * kPend + j];
-        const uint64_t key = s.pkey[w * kPend + j];
+    for (int j = 0; j < r.np; ++j) {
+        const int slot = __shfl(r.pslot, j);
+        const uint64_t key = __shfl(r.pkey, j);
         if ((slot & 63) == lane) {
 #pragma unroll
-            for (int r = 0; r < 8; ++r)
-                if ((slot >> 6) == r) kk[r] = key;
+            for (int q = 0; q < 8; ++q)
+                if ((slot >> 6) == q) kk[q] = key;
         }
     }
     // Sort the lane's 8 entries (Batcher's network), then merge across lanes.
@@ -921,7 +919,9 @@ __device__ void eng_refill(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
     cswap(kk[2], ss[2], kk[4], ss[4]); cswap(kk[3], ss[3], kk[5], ss[5]);
     cswap(kk[1], ss[1], kk[2], ss[2]); cswap(kk[3], ss[3], kk[4], ss[4]);
     cswap(kk[5], ss[5], kk[6], ss[6]);
-    const int take = count < s.K ? count : s.K;
+    const int take = r.cnt < K ? r.cnt : K;
+    r.key = ~0ull;
+    r.slot = 0;
     for (int q = 0; q < take; ++q) {
         const uint64_t g = wave_min_u64(kk[0]);
         const uint64_t owners = __ballot(kk[0] == g);
@@ -929,68 +929,46 @@ __device__ void eng_refill(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
         const int slot = __shfl(ss[0], owner);
         if (lane == owner) {
 #pragma unroll
-            for (int r = 0; r < 7; ++r) {
-                kk[r] = kk[r + 1];
-                ss[r] = ss[r + 1];
+            for (int u = 0; u < 7; ++u) {
+                kk[u] = kk[u + 1];
+                ss[u] = ss[u + 1];
             }
             kk[7] = ~0ull;
         }
-        if (lane == 0) {
-            s.ck[e * s.K + q] = g;
-            s.cs[e * s.K + q] = (uint16_t)slot;
+        if (lane == q) {
+            r.key = g;
+            r.slot = slot;
         }
     }
-    if (lane == 0) s.cn[e] = take;
+    r.cn = take;
 }
 
-// One wave: inserts key b (held in `slot`) into expert e's sorted list if it
-// belongs to the lowest K keys. `complete` says every holder other than b is
-// in the list. Entries move between lanes through shuffles, so every lane
-// reads and writes only its own list position (no lane reads an LDS word
-// another lane writes in the same step).
+// Inserts key b (held in `slot`) if it belongs to the lowest K keys;
+// `complete` says every holder other than b is in the list.
 template <class M>
-__device__ inline void eng_cache_insert(const Eng<M> &s, int e, uint64_t b, int slot, bool complete) {
+__device__ inline void er_insert(ExpertRegs<M> &r, int K, uint64_t b, int slot, bool complete) {
     const int lane = lane_id();
-    const int K = s.K;
-    const int nc = s.cn[e];
-    if (!complete && (nc == 0 || b > s.ck[e * K + nc - 1])) return;   // stays outside
-    uint64_t v = ~0ull;
-    int sl = 0;
-    if (lane < nc) {
-        v = s.ck[e * K + lane];
-        sl = s.cs[e * K + lane];
-    }
-    const int pos = __popcll(__ballot(lane < nc && v < b));
+    if (!complete && (r.cn == 0 || b > __shfl(r.key, r.cn - 1))) return;   // stays outside
+    const int pos = __popcll(__ballot(lane < r.cn && r.key < b));
     if (pos >= K) return;   // larger than a full list of keys
-    const uint64_t vprev = __shfl_up(v, 1);
-    const int slprev = __shfl_up(sl, 1);
-    const int nn = nc + 1 < K ? nc + 1 : K;
+    const uint64_t kprev = __shfl_up(r.key, 1);
+    const int sprev = __shfl_up(r.slot, 1);
+    const int nn = r.cn + 1 < K ? r.cn + 1 : K;
     if (lane >= pos && lane < nn) {
-        s.ck[e * K + lane] = lane == pos ? b : vprev;
-        s.cs[e * K + lane] = (uint16_t)(lane == pos ? slot : slprev);
+        r.key = lane == pos ? b : kprev;
+        r.slot = lane == pos ? slot : sprev;
     }
-    if (lane == 0) s.cn[e] = nn;
+    r.cn = nn;
 }
 
-// One wave: removes the lowest entry of expert e's list.
 template <class M>
-__device__ inline void eng_cache_pop(const Eng<M> &s, int e) {
+__device__ inline void er_pop(ExpertRegs<M> &r) {
     const int lane = lane_id();
-    const int K = s.K;
-    const int nc = s.cn[e];
-    uint64_t v = ~0ull;
-    int sl = 0;
-    if (lane < nc) {
-        v = s.ck[e * K + lane];
-        sl = s.cs[e * K + lane];
-    }
-    const uint64_t vnext = __shfl_down(v, 1);
-    const int slnext = __shfl_down(sl, 1);
-    if (lane + 1 < nc) {
-        s.ck[e * K + lane] = vnext;
-        s.cs[e * K + lane] = (uint16_t)slnext;
-    }
-    if (lane == 0) s.cn[e] = nc > 0 ? nc - 1 : 0;
+    const uint64_t knext = __shfl_down(r.key, 1);
+    const int snext = __shfl_down(r.slot, 1);
+    r.key = lane + 1 < r.cn ? knext : ~0ull;
+    r.slot = lane + 1 < r.cn ? snext : 0;
+    r.cn = r.cn > 0 ? r.cn - 1 : 0;
 }
 
 // One wave: streams expert e's bids of this round into its holders. Bids are
@@ -1001,31 +979,40 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
     const int lane = lane_id();
     const int K = s.K;
     uint64_t *hold = c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
+    ExpertRegs<M> r;
+    r.cn = s.cn[e];
+    r.cnt = s.cnt[e];
+    r.key = lane < r.cn ? s.ck[e * K + lane] : ~0ull;
+    r.slot = lane < r.cn ? (int)s.cs[e * K + lane] : 0;
+    r.price = s.pr[e];
+    r.np = 0;
+    r.pkey = 0;
+    r.pslot = 0;
     for (int j = 0; j < nb; ++j) {
         if (exps != nullptr && exps[j] != e) continue;
         const uint64_t b = bids[j];
-        const int count = s.cnt[e];
         int out_tok = -1;
-        if (count < c.C) {
-            const bool complete = s.cn[e] == count;
-            eng_write<M>(c, s, e, hold, count, b);
-            if (lane == 0) s.cnt[e] = count + 1;
-            eng_cache_insert<M>(s, e, b, count, complete);
-            if (count + 1 == c.C) {
-                if (s.cn[e] == 0) eng_refill<M>(c, s, e, hold);
-                if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * K]);
+        if (r.cnt < c.C) {
+            const int slot = r.cnt;
+            const bool complete = r.cn == r.cnt;
+            er_write<M>(c, hold, r, slot, b);
+            r.cnt += 1;
+            er_insert<M>(r, K, b, slot, complete);
+            if (r.cnt == c.C) {
+                if (r.cn == 0) er_refill<M>(c, hold, K, r);
+                r.price = M::key_bid(__shfl(r.key, 0));
             }
         } else {
-            if (s.cn[e] == 0) eng_refill<M>(c, s, e, hold);
-            const uint64_t m = s.ck[e * K];
+            if (r.cn == 0) er_refill<M>(c, hold, K, r);
+            const uint64_t m = __shfl(r.key, 0);
             if (b > m) {
-                const int slot = s.cs[e * K];
+                const int slot = __shfl(r.slot, 0);
                 out_tok = key_token(m);
-                eng_cache_pop<M>(s, e);
-                eng_write<M>(c, s, e, hold, slot, b);
-                eng_cache_insert<M>(s, e, b, slot, s.cn[e] == count - 1);
-                if (s.cn[e] == 0) eng_refill<M>(c, s, e, hold);
-                if (lane == 0) s.pr[e] = M::key_bid(s.ck[e * K]);
+                er_pop<M>(r);
+                er_write<M>(c, hold, r, slot, b);
+                er_insert<M>(r, K, b, slot, r.cn == r.cnt - 1);
+                if (r.cn == 0) er_refill<M>(c, hold, K, r);
+                r.price = M::key_bid(__shfl(r.key, 0));
             } else {
                 out_tok = key_token(b);
             }
@@ -1036,7 +1023,16 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
             else flag_internal(c.ctrl);
         }
     }
-    eng_flush<M>(c, s, e, hold);
+    er_flush<M>(c, hold, r);
+    if (lane < r.cn) {
+        s.ck[e * K + lane] = r.key;
+        s.cs[e * K + lane] = (uint16_t)r.slot;
+    }
+    if (lane == 0) {
+        s.cn[e] = r.cn;
+        s.cnt[e] = r.cnt;
+        s.pr[e] = r.price;
+    }
 }
 
 // The engine's phase entry, one block per expert: sorts the expert's holder
@@ -1118,9 +1114,6 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
     s.bkey = reinterpret_cast<uint64_t *>(smem_raw + L.bkey);
     s.bexp = reinterpret_cast<int *>(smem_raw + L.bexp);
     s.bsort = reinterpret_cast<uint64_t *>(smem_raw + L.bsort);
-    s.pslot = reinterpret_cast<int *>(smem_raw + L.pslot);
-    s.pkey = reinterpret_cast<uint64_t *>(smem_raw + L.pkey);
-    s.pn = reinterpret_cast<int *>(smem_raw + L.pn);
     int *act = reinterpret_cast<int *>(smem_raw + L.actA);
     int *nxt = reinterpret_cast<int *>(smem_raw + L.actB);
     __shared__ int s_go, s_cur, s_n, s_nnext, s_ntouched, s_rounds, s_stop;
@@ -1169,7 +1162,6 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
         s.ck[i] = c.eng_ck[i];
         s.cs[i] = c.eng_cs[i];
     }
-    if (tid < kEngWaves) s.pn[tid] = 0;
     for (int i = tid; i < s_n; i += kEngThreads) {
         const int t = c.active[(int64_t)s_cur * c.T + i];
         act[i] = (t >= 0 && t < c.T) ? t : 0;
