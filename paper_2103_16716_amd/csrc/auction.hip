@@ -790,7 +790,8 @@ constexpr int kEngMaxC = 512;    // holder tables a wave holds in registers (8 k
 constexpr int kEngMaxK = 64;     // longest per-expert list of lowest keys
 
 struct EngLayout {
-    size_t pr, cnt, cn, sel, bcnt, boff, bfill, tch, ck, cs, bkey, bexp, bsort, actA, actB, total;
+    size_t pr, cnt, cn, sel, bcnt, boff, bfill, tch, ck, cs, bkey, bexp, bsort, actA, actB, skey,
+        sslot, total;
 };
 
 __host__ __device__ inline size_t eng_align(size_t x) { return (x + 15) & ~size_t(15); }
@@ -813,6 +814,8 @@ __host__ __device__ inline EngLayout eng_layout(int E, int value_bytes, int K) {
     L.bsort = off; off = eng_align(off + (size_t)kEngCap * 8);
     L.actA = off;  off = eng_align(off + (size_t)kEngCap * 4);
     L.actB = off;  off = eng_align(off + (size_t)kEngCap * 4);
+    L.skey = off;  off = eng_align(off + (size_t)kEngWaves * 64 * 8);   // per-wave scratch
+    L.sslot = off; off = eng_align(off + (size_t)kEngWaves * 64 * 4);
     L.total = off;
     return L;
 }
@@ -825,6 +828,8 @@ struct Eng {
     uint16_t *cs;
     uint64_t *bkey, *bsort;
     int *bexp;
+    uint64_t *scr_key;
+    int *scr_slot;
     int K;
 };
 
@@ -835,17 +840,6 @@ __device__ inline uint64_t wave_min_u64(uint64_t v) {
         v = o < v ? o : v;
     }
     return v;
-}
-
-__device__ inline void cswap(uint64_t &a, int &sa, uint64_t &b, int &sb) {
-    if (b < a) {
-        const uint64_t t = a;
-        a = b;
-        b = t;
-        const int u = sa;
-        sa = sb;
-        sb = u;
-    }
 }
 
 // Expert state while one wave updates it, held in registers: lane q owns
@@ -887,17 +881,19 @@ __device__ inline void er_write(const Ctx<M> &c, uint64_t *hold, ExpertRegs<M> &
 }
 
 // The K lowest keys of the expert's holder table, sorted, into the lanes.
-// The table is read from global memory and patched with the pending stores.
+// The table is read from global memory and patched with the pending stores;
+// the K-th smallest key is found by a bitwise search on ballot counts, the
+// keys up to it are compacted through the wave's LDS scratch, and a 64-lane
+// bitonic network sorts them.
 template <class M>
-__device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRegs<M> &r) {
+__device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRegs<M> &r,
+                          uint64_t *scr_key, int *scr_slot) {
     const int lane = lane_id();
     uint64_t kk[8];
-    int ss[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         const int idx = lane + 64 * q;
         kk[q] = idx < r.cnt ? hold[idx] : ~0ull;
-        ss[q] = idx;
     }
     for (int j = 0; j < r.np; ++j) {
         const int slot = __shfl(r.pslot, j);
@@ -908,39 +904,59 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
                 if ((slot >> 6) == q) kk[q] = key;
         }
     }
-    // Sort the lane's 8 entries (Batcher's network), then merge across lanes.
-    cswap(kk[0], ss[0], kk[1], ss[1]); cswap(kk[2], ss[2], kk[3], ss[3]);
-    cswap(kk[4], ss[4], kk[5], ss[5]); cswap(kk[6], ss[6], kk[7], ss[7]);
-    cswap(kk[0], ss[0], kk[2], ss[2]); cswap(kk[1], ss[1], kk[3], ss[3]);
-    cswap(kk[4], ss[4], kk[6], ss[6]); cswap(kk[5], ss[5], kk[7], ss[7]);
-    cswap(kk[1], ss[1], kk[2], ss[2]); cswap(kk[5], ss[5], kk[6], ss[6]);
-    cswap(kk[0], ss[0], kk[4], ss[4]); cswap(kk[1], ss[1], kk[5], ss[5]);
-    cswap(kk[2], ss[2], kk[6], ss[6]); cswap(kk[3], ss[3], kk[7], ss[7]);
-    cswap(kk[2], ss[2], kk[4], ss[4]); cswap(kk[3], ss[3], kk[5], ss[5]);
-    cswap(kk[1], ss[1], kk[2], ss[2]); cswap(kk[3], ss[3], kk[4], ss[4]);
-    cswap(kk[5], ss[5], kk[6], ss[6]);
     const int take = r.cnt < K ? r.cnt : K;
+    r.cn = take;
     r.key = ~0ull;
     r.slot = 0;
-    for (int q = 0; q < take; ++q) {
-        const uint64_t g = wave_min_u64(kk[0]);
-        const uint64_t owners = __ballot(kk[0] == g);
-        const int owner = owners ? __ffsll((long long)owners) - 1 : 0;
-        const int slot = __shfl(ss[0], owner);
-        if (lane == owner) {
+    if (take == 0) return;
+    // thr: the largest value with fewer than `take` keys below it, i.e. the
+    // take-th smallest key (keys are distinct).
+    uint64_t thr = 0;
+    for (int bit = 63; bit >= 0; --bit) {
+        const uint64_t trial = thr | (1ull << bit);
+        int below = 0;
 #pragma unroll
-            for (int u = 0; u < 7; ++u) {
-                kk[u] = kk[u + 1];
-                ss[u] = ss[u + 1];
+        for (int q = 0; q < 8; ++q) below += __popcll(__ballot(kk[q] < trial));
+        if (below < take) thr = trial;
+    }
+    int base = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const bool sel = kk[q] <= thr;
+        const uint64_t m = __ballot(sel);
+        if (sel) {
+            const int at = base + __popcll(m & lanemask_lt());
+            if (at < 64) {
+                scr_key[at] = kk[q];
+                scr_slot[at] = lane + 64 * q;
             }
-            kk[7] = ~0ull;
         }
-        if (lane == q) {
-            r.key = g;
-            r.slot = slot;
+        base += __popcll(m);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane < take) {
+        r.key = scr_key[lane];
+        r.slot = scr_slot[lane];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const uint64_t pk = __shfl_xor(r.key, j);
+            const int ps = __shfl_xor(r.slot, j);
+            const bool ascending = (lane & k) == 0;
+            const bool keep_min = ((lane & j) == 0) == ascending;
+            if (keep_min ? pk < r.key : pk > r.key) {
+                r.key = pk;
+                r.slot = ps;
+            }
         }
     }
-    r.cn = take;
 }
 
 // Inserts key b (held in `slot`) if it belongs to the lowest K keys;
@@ -979,6 +995,8 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
     const int lane = lane_id();
     const int K = s.K;
     uint64_t *hold = c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
+    uint64_t *scr_key = s.scr_key + (threadIdx.x >> 6) * 64;
+    int *scr_slot = s.scr_slot + (threadIdx.x >> 6) * 64;
     ExpertRegs<M> r;
     r.cn = s.cn[e];
     r.cnt = s.cnt[e];
@@ -999,11 +1017,11 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
             r.cnt += 1;
             er_insert<M>(r, K, b, slot, complete);
             if (r.cnt == c.C) {
-                if (r.cn == 0) er_refill<M>(c, hold, K, r);
+                if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
                 r.price = M::key_bid(__shfl(r.key, 0));
             }
         } else {
-            if (r.cn == 0) er_refill<M>(c, hold, K, r);
+            if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
             const uint64_t m = __shfl(r.key, 0);
             if (b > m) {
                 const int slot = __shfl(r.slot, 0);
@@ -1011,7 +1029,7 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
                 er_pop<M>(r);
                 er_write<M>(c, hold, r, slot, b);
                 er_insert<M>(r, K, b, slot, r.cn == r.cnt - 1);
-                if (r.cn == 0) er_refill<M>(c, hold, K, r);
+                if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
                 r.price = M::key_bid(__shfl(r.key, 0));
             } else {
                 out_tok = key_token(b);
@@ -1114,6 +1132,8 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
     s.bkey = reinterpret_cast<uint64_t *>(smem_raw + L.bkey);
     s.bexp = reinterpret_cast<int *>(smem_raw + L.bexp);
     s.bsort = reinterpret_cast<uint64_t *>(smem_raw + L.bsort);
+    s.scr_key = reinterpret_cast<uint64_t *>(smem_raw + L.skey);
+    s.scr_slot = reinterpret_cast<int *>(smem_raw + L.sslot);
     int *act = reinterpret_cast<int *>(smem_raw + L.actA);
     int *nxt = reinterpret_cast<int *>(smem_raw + L.actB);
     __shared__ int s_go, s_cur, s_n, s_nnext, s_ntouched, s_rounds, s_stop;
