@@ -208,6 +208,50 @@ __device__ inline void load8(const typename M::score_t *S, int64_t base, int e0,
     }
 }
 
+// Top-2 of one token whose lane-local scores sv (experts e0 .. e0 + 7) are
+// already in registers (rows that fit one chunk of 8 G experts).
+template <class M, int G>
+__device__ inline void top2_row(const typename M::value_t (&sv)[8], int e0, int E, bool valid,
+                                const typename M::value_t *pr, typename M::value_t &v1, int &e1,
+                                typename M::value_t &v2, typename M::value_t &s1) {
+    using value_t = typename M::value_t;
+    v1 = M::lowest();
+    v2 = M::lowest();
+    s1 = 0;
+    e1 = 0x7fffffff;
+    if (valid && e0 < E) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int e = e0 + j;
+            if (e >= E) break;
+            const value_t v = sv[j] - pr[e];
+            if (v > v1) {
+                v2 = v1;
+                v1 = v;
+                e1 = e;
+                s1 = sv[j];
+            } else if (v > v2) {
+                v2 = v;
+            }
+        }
+    }
+#pragma unroll
+    for (int off = G / 2; off > 0; off >>= 1) {
+        const value_t ov1 = __shfl_xor(v1, off);
+        const int oe1 = __shfl_xor(e1, off);
+        const value_t ov2 = __shfl_xor(v2, off);
+        const value_t os1 = __shfl_xor(s1, off);
+        if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
+            v2 = v1 > ov2 ? v1 : ov2;
+            v1 = ov1;
+            e1 = oe1;
+            s1 = os1;
+        } else {
+            v2 = v2 > ov1 ? v2 : ov1;
+        }
+    }
+}
+
 template <class M, int G>
 __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const typename M::value_t *pr,
                                   typename M::value_t &v1, int &e1, typename M::value_t &v2,
@@ -788,6 +832,7 @@ constexpr int kEngDirect = 64;   // rounds with at most this many bids skip the 
 constexpr int kEngMaxE = 512;
 constexpr int kEngMaxC = 512;    // holder tables a wave holds in registers (8 keys per lane)
 constexpr int kEngMaxK = 64;     // longest per-expert list of lowest keys
+constexpr int kEngRows = 4;      // score rows a bidding group keeps in flight
 
 struct EngLayout {
     size_t pr, cnt, cn, sel, bcnt, boff, bfill, tch, ck, cs, bkey, bexp, bsort, actA, actB, skey,
@@ -988,7 +1033,8 @@ __device__ inline void er_pop(ExpertRegs<M> &r) {
 }
 
 // One wave: streams expert e's bids of this round into its holders. Bids are
-// bids[0..nb), or, with `exps`, the entries of bids[0..nb) whose expert is e.
+// bids[0..nb), or, with `exps`, the entries of bids[0..nb) whose expert is e
+// (picked out by a ballot, 64 entries per step).
 template <class M>
 __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *bids,
                            const int *exps, int nb, int *nxt, int *nnext) {
@@ -1006,39 +1052,47 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
     r.np = 0;
     r.pkey = 0;
     r.pslot = 0;
-    for (int j = 0; j < nb; ++j) {
-        if (exps != nullptr && exps[j] != e) continue;
-        const uint64_t b = bids[j];
-        int out_tok = -1;
-        if (r.cnt < c.C) {
-            const int slot = r.cnt;
-            const bool complete = r.cn == r.cnt;
-            er_write<M>(c, hold, r, slot, b);
-            r.cnt += 1;
-            er_insert<M>(r, K, b, slot, complete);
-            if (r.cnt == c.C) {
-                if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-                r.price = M::key_bid(__shfl(r.key, 0));
-            }
-        } else {
-            if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-            const uint64_t m = __shfl(r.key, 0);
-            if (b > m) {
-                const int slot = __shfl(r.slot, 0);
-                out_tok = key_token(m);
-                er_pop<M>(r);
+    // Bids are read 64 at a time, one per lane, and taken in lane order.
+    for (int j0 = 0; j0 < nb; j0 += 64) {
+        const int j = j0 + lane;
+        const bool mine = j < nb && (exps == nullptr || exps[j] == e);
+        const uint64_t mykey = j < nb ? bids[j] : 0ull;
+        uint64_t mask = __ballot(mine);
+        while (mask) {
+            const int src = __ffsll((long long)mask) - 1;
+            mask &= mask - 1;
+            const uint64_t b = __shfl(mykey, src);
+            int out_tok = -1;
+            if (r.cnt < c.C) {
+                const int slot = r.cnt;
+                const bool complete = r.cn == r.cnt;
                 er_write<M>(c, hold, r, slot, b);
-                er_insert<M>(r, K, b, slot, r.cn == r.cnt - 1);
-                if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-                r.price = M::key_bid(__shfl(r.key, 0));
+                r.cnt += 1;
+                er_insert<M>(r, K, b, slot, complete);
+                if (r.cnt == c.C) {
+                    if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
+                    r.price = M::key_bid(__shfl(r.key, 0));
+                }
             } else {
-                out_tok = key_token(b);
+                if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
+                const uint64_t m = __shfl(r.key, 0);
+                if (b > m) {
+                    const int slot = __shfl(r.slot, 0);
+                    out_tok = key_token(m);
+                    er_pop<M>(r);
+                    er_write<M>(c, hold, r, slot, b);
+                    er_insert<M>(r, K, b, slot, r.cn == r.cnt - 1);
+                    if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
+                    r.price = M::key_bid(__shfl(r.key, 0));
+                } else {
+                    out_tok = key_token(b);
+                }
             }
-        }
-        if (out_tok >= 0 && lane == 0) {
-            const int at = atomicAdd(nnext, 1);
-            if (at < kEngCap && out_tok < c.T) nxt[at] = out_tok;
-            else flag_internal(c.ctrl);
+            if (out_tok >= 0 && lane == 0) {
+                const int at = atomicAdd(nnext, 1);
+                if (at < kEngCap && out_tok < c.T) nxt[at] = out_tok;
+                else flag_internal(c.ctrl);
+            }
         }
     }
     er_flush<M>(c, hold, r);
@@ -1200,13 +1254,31 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
             break;
         }
         // Bids against the prices at the start of the round.
-        const int n_round = ((n + per_pass - 1) / per_pass) * per_pass;
-        for (int i = gid; i < n_round; i += per_pass) {
+        // Each group keeps kEngRows score rows in flight: all loads first,
+        // then the reductions. With E <= kEngMaxE = 8 * 64 a row is one chunk
+        // of 8 experts per lane (lanes_per_token picks G >= E / 8).
+        const int stride = per_pass * kEngRows;
+        const int n_round = ((n + stride - 1) / stride) * stride;
+        for (int i0 = gid; i0 < n_round; i0 += stride) {
+          value_t rows[kEngRows][8];
+          int toks[kEngRows];
+#pragma unroll
+          for (int u = 0; u < kEngRows; ++u) {
+              const int i = i0 + u * per_pass;
+              toks[u] = i < n ? act[i] : 0;
+#pragma unroll
+              for (int q = 0; q < 8; ++q) rows[u][q] = 0;
+              if (i < n && 8 * gl < c.E)
+                  load8<M>(c.S, (int64_t)toks[u] * c.E, 8 * gl, c.E, c.scale, rows[u]);
+          }
+#pragma unroll
+          for (int u = 0; u < kEngRows; ++u) {
+            const int i = i0 + u * per_pass;
             const bool valid = i < n;
-            const int t = valid ? act[i] : 0;
+            const int t = toks[u];
             value_t v1, v2, s1;
             int e1;
-            top2_token<M, G>(c, t, valid, s.pr, v1, e1, v2, s1);
+            top2_row<M, G>(rows[u], 8 * gl, c.E, valid, s.pr, v1, e1, v2, s1);
             if (valid && gl == 0) {
                 if (e1 >= c.E) {
                     e1 = 0;
@@ -1223,6 +1295,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
                     if (at < c.E) s.tch[at] = e1;
                 }
             }
+          }
         }
         __syncthreads();   // also completes the previous round's holder-table stores
         const int nt = s_ntouched < c.E ? s_ntouched : c.E;
