@@ -1275,6 +1275,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
           for (int u = 0; u < kEngRows; ++u) {
             const int i = i0 + u * per_pass;
             const bool valid = i < n;
+            if (__ballot(valid) == 0) break;   // no token of this slot in the wave
             const int t = toks[u];
             value_t v1, v2, s1;
             int e1;
