@@ -878,13 +878,29 @@ struct Eng {
     int K;
 };
 
-__device__ inline uint64_t wave_min_u64(uint64_t v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const uint64_t o = __shfl_xor(v, off);
-        v = o < v ? o : v;
-    }
-    return v;
+// Cross-lane moves inside the engine's update, on the VALU instead of the
+// LDS crossbar: readlane broadcasts the value of one (uniform) lane; the DPP
+// wavefront shifts move every lane's value one lane up (lane i receives lane
+// i-1) or down (lane i receives lane i+1).
+__device__ inline int rl32(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
+__device__ inline uint64_t rl64(uint64_t v, int lane) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
+}
+constexpr int kDppWaveShr1 = 0x138;
+constexpr int kDppWaveShl1 = 0x130;
+__device__ inline int up1_i32(int v) { return __builtin_amdgcn_update_dpp(v, v, kDppWaveShr1, 0xf, 0xf, false); }
+__device__ inline int down1_i32(int v) { return __builtin_amdgcn_update_dpp(v, v, kDppWaveShl1, 0xf, 0xf, false); }
+__device__ inline uint64_t up1_u64(uint64_t v) {
+    const uint32_t lo = (uint32_t)up1_i32((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)up1_i32((int)(uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ inline uint64_t down1_u64(uint64_t v) {
+    const uint32_t lo = (uint32_t)down1_i32((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)down1_i32((int)(uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
 }
 
 // Expert state while one wave updates it, held in registers: lane q owns
@@ -941,8 +957,8 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
         kk[q] = idx < r.cnt ? hold[idx] : ~0ull;
     }
     for (int j = 0; j < r.np; ++j) {
-        const int slot = __shfl(r.pslot, j);
-        const uint64_t key = __shfl(r.pkey, j);
+        const int slot = rl32(r.pslot, j);
+        const uint64_t key = rl64(r.pkey, j);
         if ((slot & 63) == lane) {
 #pragma unroll
             for (int q = 0; q < 8; ++q)
@@ -1009,11 +1025,11 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
 template <class M>
 __device__ inline void er_insert(ExpertRegs<M> &r, int K, uint64_t b, int slot, bool complete) {
     const int lane = lane_id();
-    if (!complete && (r.cn == 0 || b > __shfl(r.key, r.cn - 1))) return;   // stays outside
+    if (!complete && (r.cn == 0 || b > rl64(r.key, r.cn - 1))) return;   // stays outside
     const int pos = __popcll(__ballot(lane < r.cn && r.key < b));
     if (pos >= K) return;   // larger than a full list of keys
-    const uint64_t kprev = __shfl_up(r.key, 1);
-    const int sprev = __shfl_up(r.slot, 1);
+    const uint64_t kprev = up1_u64(r.key);
+    const int sprev = up1_i32(r.slot);
     const int nn = r.cn + 1 < K ? r.cn + 1 : K;
     if (lane >= pos && lane < nn) {
         r.key = lane == pos ? b : kprev;
@@ -1025,8 +1041,8 @@ __device__ inline void er_insert(ExpertRegs<M> &r, int K, uint64_t b, int slot, 
 template <class M>
 __device__ inline void er_pop(ExpertRegs<M> &r) {
     const int lane = lane_id();
-    const uint64_t knext = __shfl_down(r.key, 1);
-    const int snext = __shfl_down(r.slot, 1);
+    const uint64_t knext = down1_u64(r.key);
+    const int snext = down1_i32(r.slot);
     r.key = lane + 1 < r.cn ? knext : ~0ull;
     r.slot = lane + 1 < r.cn ? snext : 0;
     r.cn = r.cn > 0 ? r.cn - 1 : 0;
@@ -1061,7 +1077,7 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
         while (mask) {
             const int src = __ffsll((long long)mask) - 1;
             mask &= mask - 1;
-            const uint64_t b = __shfl(mykey, src);
+            const uint64_t b = rl64(mykey, src);
             int out_tok = -1;
             if (r.cnt < c.C) {
                 const int slot = r.cnt;
@@ -1071,19 +1087,19 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
                 er_insert<M>(r, K, b, slot, complete);
                 if (r.cnt == c.C) {
                     if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-                    r.price = M::key_bid(__shfl(r.key, 0));
+                    r.price = M::key_bid(rl64(r.key, 0));
                 }
             } else {
                 if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-                const uint64_t m = __shfl(r.key, 0);
+                const uint64_t m = rl64(r.key, 0);
                 if (b > m) {
-                    const int slot = __shfl(r.slot, 0);
+                    const int slot = rl32(r.slot, 0);
                     out_tok = key_token(m);
                     er_pop<M>(r);
                     er_write<M>(c, hold, r, slot, b);
                     er_insert<M>(r, K, b, slot, r.cn == r.cnt - 1);
                     if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-                    r.price = M::key_bid(__shfl(r.key, 0));
+                    r.price = M::key_bid(rl64(r.key, 0));
                 } else {
                     out_tok = key_token(b);
                 }
