@@ -58,7 +58,7 @@ inline void debug_note(const char *what, hipError_t err) {
 
 struct Layout {
     size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
-        eck, ecs, ecn, total;
+        eck, ecs, ecn, sums, total;
     int64_t cap, nblk;
 };
 
@@ -83,6 +83,7 @@ Layout make_layout(int64_t T, int64_t E) {
     L.eck = off;     off += align_up((size_t)E * 64 * 8);   // engine entry lists (K <= 64)
     L.ecs = off;     off += align_up((size_t)E * 64 * 2);
     L.ecn = off;     off += align_up((size_t)E * 4);
+    L.sums = off;    off += align_up((size_t)T * 64);          // per-token score summaries
     L.total = off;
     return L;
 }
@@ -104,6 +105,7 @@ struct Ctx {
     uint64_t *eng_ck; // the lists as built at the engine's entry
     uint16_t *eng_cs;
     int *eng_cn;
+    uint32_t *sums;   // T x 16 words: each token's 8 best scores, their experts, a bound
 };
 
 template <class M>
@@ -132,6 +134,7 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.eng_ck = reinterpret_cast<uint64_t *>(ws + L.eck);
     c.eng_cs = reinterpret_cast<uint16_t *>(ws + L.ecs);
     c.eng_cn = reinterpret_cast<int *>(ws + L.ecn);
+    c.sums = reinterpret_cast<uint32_t *>(ws + L.sums);
     return c;
 }
 
@@ -801,6 +804,116 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
     }
 }
 
+// ---------------------------------------------------------- score summaries --
+//
+// A token's summary is 64 bytes: its 8 highest scores (words 0..7, fp32 bits or
+// the raw int16 score), their experts (words 8..11, two uint16 per word), the
+// 9th highest score (word 12; the lowest value when E <= 8, where the 8 cover
+// every expert) and the number of entries (word 13). Scores never change
+// during a solve, so the summaries are built once. For prices p, every expert
+// outside a summary has S[t,e] - p[e] <= bound - min_e p[e]; a top-2 taken
+// over the summary is therefore the top-2 over all experts whenever its best
+// value exceeds that limit and its second value reaches it.
+
+constexpr int kSumWords = 16;
+
+template <class M>
+__device__ inline uint32_t score_bits(typename M::value_t v, int64_t scale) {
+    if constexpr (M::kInteger) return (uint32_t)(int32_t)(v / scale);
+    else return __float_as_uint(v);
+}
+template <class M>
+__device__ inline typename M::value_t bits_score(uint32_t w, int64_t scale) {
+    if constexpr (M::kInteger) return (typename M::value_t)(int32_t)w * scale;
+    else return __uint_as_float(w);
+}
+
+// One group of G lanes per token: 9 rounds of a group maximum (ties to the
+// lowest expert) over the lanes' 8 scores each.
+template <class M, int G>
+__global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c) {
+    using value_t = typename M::value_t;
+    const int lane = lane_id();
+    const int gl = lane & (G - 1);
+    const int per_block = kThreads / G;
+    const int n_round = ((c.T + per_block * (int)gridDim.x - 1) / (per_block * (int)gridDim.x)) *
+                        per_block * (int)gridDim.x;
+    const int e0 = 8 * gl;
+    const int take = c.E < 8 ? c.E : 8;
+    for (int t = blockIdx.x * per_block + threadIdx.x / G; t < n_round;
+         t += per_block * gridDim.x) {
+        const bool valid = t < c.T;
+        value_t sv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) sv[q] = M::lowest();
+        if (valid && e0 < c.E) load8<M>(c.S, (int64_t)t * c.E, e0, c.E, c.scale, sv);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            if (e0 + q >= c.E) sv[q] = M::lowest();
+        uint32_t *out = c.sums + (int64_t)(valid ? t : 0) * kSumWords;
+        uint32_t pairs[4] = {0, 0, 0, 0};
+        for (int r = 0; r <= take; ++r) {
+            // Lane-local best, then the group's best (lowest expert on ties).
+            value_t bv = M::lowest();
+            int be = 0x7fffffff;
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (e0 + q < c.E && sv[q] > bv) {
+                    bv = sv[q];
+                    be = e0 + q;
+                }
+#pragma unroll
+            for (int off = G / 2; off > 0; off >>= 1) {
+                const value_t ov = __shfl_xor(bv, off);
+                const int oe = __shfl_xor(be, off);
+                if (ov > bv || (ov == bv && oe < be)) {
+                    bv = ov;
+                    be = oe;
+                }
+            }
+            if (r < take) {
+                if (be >= e0 && be < e0 + 8) {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        if (e0 + q == be) sv[q] = M::lowest();
+                }
+                if (valid && gl == 0) out[r] = score_bits<M>(bv, c.scale);
+                pairs[r >> 1] |= (uint32_t)(be & 0xffff) << (16 * (r & 1));
+            } else if (valid && gl == 0) {
+                // the 9th score bounds every expert outside the summary
+                out[12] = (take < c.E) ? score_bits<M>(bv, c.scale)
+                                       : (M::kInteger ? 0x80000000u : __float_as_uint(-INFINITY));
+            }
+        }
+        if (valid && gl == 0) {
+            for (int q = 0; q < 4; ++q) out[8 + q] = pairs[q];
+            out[13] = (uint32_t)take;
+        }
+    }
+}
+
+// Reads the summary table from blocks spread over every XCD, so that the
+// L2 of whichever XCD runs the one-workgroup engine holds it. Consecutive
+// workgroups go to consecutive XCDs; with a multiple of 8 blocks, the blocks
+// of any one XCD cover the whole table whatever XCD block 0 lands on.
+__global__ __launch_bounds__(256) void summary_prefill_kernel(const uint4 *sums, int64_t n16,
+                                                              const SolveCtrl *ctrl, int cap,
+                                                              uint32_t *sink) {
+    if (ctrl->done || ctrl->all_active) return;
+    const int n = ld_relaxed(&ctrl->active_count[ctrl->cur]);
+    if (n <= 0 || n > cap) return;
+    const int per_xcd = gridDim.x / 8;
+    const int64_t chunk = (n16 + per_xcd - 1) / per_xcd;
+    const int64_t lo = (int64_t)(blockIdx.x / 8) * chunk;
+    const int64_t hi = lo + chunk < n16 ? lo + chunk : n16;
+    uint32_t acc = 0;
+    for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
+        const uint4 v = sums[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x9e3779b9u && threadIdx.x == 0) *sink = acc;   // keeps the loads
+}
+
 // ------------------------------------------------------------ tail engine --
 //
 // The rounds left once at most kEngCap tokens are active run inside one
@@ -1258,6 +1371,21 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
         if (t < 0 || t >= c.T) flag_internal(ctrl);
     }
     __syncthreads();
+    // Lowest price at entry: prices only rise, so it stays a lower bound of
+    // every price for the whole run (used by the summary test).
+    __shared__ value_t s_pmin;
+    if (wave == 0) {
+        value_t m = s.pr[0];
+        for (int e = lane; e < c.E; e += 64) m = s.pr[e] < m ? s.pr[e] : m;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const value_t o = __shfl_xor(m, off);
+            m = o < m ? o : m;
+        }
+        if (lane == 0) s_pmin = m;
+    }
+    __syncthreads();
+    const value_t pmin = s_pmin;
 
     const int per_pass = kEngThreads / G;
     const int gid = tid / G;
@@ -1273,19 +1401,26 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
         // Each group keeps kEngRows score rows in flight: all loads first,
         // then the reductions. With E <= kEngMaxE = 8 * 64 a row is one chunk
         // of 8 experts per lane (lanes_per_token picks G >= E / 8).
+        // Summaries first (one 64-byte line per token, held in L2); a token
+        // whose summary cannot decide its top-2 reads its whole row.
         const int stride = per_pass * kEngRows;
         const int n_round = ((n + stride - 1) / stride) * stride;
         for (int i0 = gid; i0 < n_round; i0 += stride) {
-          value_t rows[kEngRows][8];
+          uint32_t sw[kEngRows][4];   // words gl, gl+G, .. of the summary; bound, count
           int toks[kEngRows];
 #pragma unroll
           for (int u = 0; u < kEngRows; ++u) {
               const int i = i0 + u * per_pass;
               toks[u] = i < n ? act[i] : 0;
-#pragma unroll
-              for (int q = 0; q < 8; ++q) rows[u][q] = 0;
-              if (i < n && 8 * gl < c.E)
-                  load8<M>(c.S, (int64_t)toks[u] * c.E, 8 * gl, c.E, c.scale, rows[u]);
+              sw[u][0] = sw[u][1] = sw[u][2] = sw[u][3] = 0;
+              if (i < n) {
+                  const uint32_t *sm = c.sums + (int64_t)toks[u] * kSumWords;
+                  const int q = gl & 7;
+                  sw[u][0] = sm[q];                       // score of entry q
+                  sw[u][1] = sm[8 + (q >> 1)];            // its expert (half word)
+                  sw[u][2] = sm[12];                      // bound
+                  sw[u][3] = sm[13];                      // entries
+              }
           }
 #pragma unroll
           for (int u = 0; u < kEngRows; ++u) {
@@ -1295,7 +1430,67 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
             const int t = toks[u];
             value_t v1, v2, s1;
             int e1;
-            top2_row<M, G>(rows[u], 8 * gl, c.E, valid, s.pr, v1, e1, v2, s1);
+            // Top-2 over the summary's entries (lane gl takes entry gl when gl < 8).
+            {
+                const int q = gl;
+                const int cnt = (int)sw[u][3];
+                value_t sv[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) sv[j] = M::lowest();
+                int ex = 0;
+                if (valid && q < 8 && q < cnt) {
+                    sv[0] = bits_score<M>(sw[u][0], c.scale);
+                    ex = (int)((sw[u][1] >> (16 * (q & 1))) & 0xffff);
+                    if (ex >= c.E) ex = 0;
+                }
+                v1 = M::lowest();
+                v2 = M::lowest();
+                s1 = 0;
+                e1 = 0x7fffffff;
+                if (valid && q < 8 && q < cnt) {
+                    v1 = sv[0] - s.pr[ex];
+                    e1 = ex;
+                    s1 = sv[0];
+                }
+#pragma unroll
+                for (int off = G / 2; off > 0; off >>= 1) {
+                    const value_t ov1 = __shfl_xor(v1, off);
+                    const int oe1 = __shfl_xor(e1, off);
+                    const value_t ov2 = __shfl_xor(v2, off);
+                    const value_t os1 = __shfl_xor(s1, off);
+                    if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
+                        v2 = v1 > ov2 ? v1 : ov2;
+                        v1 = ov1;
+                        e1 = oe1;
+                        s1 = os1;
+                    } else {
+                        v2 = v2 > ov1 ? v2 : ov1;
+                    }
+                }
+                bool exact = cnt >= c.E;
+                if (!exact) {
+                    const value_t lim = bits_score<M>(sw[u][2], c.scale) - pmin;
+                    exact = v1 > lim && v2 >= lim;
+                }
+                if (G < 8) exact = false;   // a group narrower than 8 lanes cannot hold the 8 entries
+                const bool need = valid && !exact;
+                if (__ballot(need)) {
+                    value_t row[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) row[j] = 0;
+                    if (need && 8 * gl < c.E)
+                        load8<M>(c.S, (int64_t)t * c.E, 8 * gl, c.E, c.scale, row);
+                    value_t w1, w2, ws1;
+                    int we1;
+                    top2_row<M, G>(row, 8 * gl, c.E, need, s.pr, w1, we1, w2, ws1);
+                    if (need) {
+                        v1 = w1;
+                        v2 = w2;
+                        e1 = we1;
+                        s1 = ws1;
+                    }
+                }
+            }
             if (valid && gl == 0) {
                 if (e1 >= c.E) {
                     e1 = 0;
@@ -1586,6 +1781,11 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     int bid_blocks = (int)((c.T + per_block - 1) / per_block);
     if (bid_blocks > 4096) bid_blocks = 4096;
     int upd_blocks = c.E < 2048 ? c.E : 2048;
+    if (engine) {
+        int sblocks = (int)((c.T + per_block - 1) / per_block);
+        if (sblocks > 4096) sblocks = 4096;
+        hipLaunchKernelGGL((summary_kernel<M, G>), dim3(sblocks), dim3(kThreads), 0, s, c);
+    }
     for (int slot = 0; slot < slots; ++slot) {
         hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1), dim3(1024), 0, s, c, p);
         for (int r = 0; r < wide_rounds; ++r) {
@@ -1595,6 +1795,9 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
         }
         if (engine) {
             hipLaunchKernelGGL(cache_build_kernel<M>, dim3(c.E), dim3(256), 0, s, c);
+            hipLaunchKernelGGL(summary_prefill_kernel, dim3(256), dim3(256), 0, s,
+                               reinterpret_cast<const uint4 *>(c.sums), (int64_t)c.T * 4, c.ctrl,
+                               kEngCap, reinterpret_cast<uint32_t *>(&c.ctrl->pad2));
             hipLaunchKernelGGL((engine_kernel<M, G>), dim3(1), dim3(kEngThreads), eng_bytes, s, c,
                                p);
         }
