@@ -211,6 +211,74 @@ __device__ inline void load8(const typename M::score_t *S, int64_t base, int e0,
     }
 }
 
+// Partner of a lane in step OFF (1, 2, 4, ...) of a butterfly reduction over
+// aligned groups of lanes. Inside a row of 16 lanes the partner comes from a
+// DPP move: swaps inside quads for OFF = 1, 2, then the mirror of the half
+// row (OFF = 4) and of the row (OFF = 8). A mirror pairs each lane with one
+// of the other half, which reduces as well as an xor once every half holds
+// one value. Wider steps go through ds_bpermute.
+template <int CTRL>
+__device__ inline uint32_t dpp_u32(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
+}
+template <int OFF, class T>
+__device__ inline T grp_partner(T v) {
+    constexpr int kCtrl = OFF == 1 ? 0xB1 : OFF == 2 ? 0x4E : OFF == 4 ? 0x141 : 0x140;
+    if constexpr (OFF <= 8) {
+        if constexpr (sizeof(T) == 8) {
+            uint64_t u;
+            __builtin_memcpy(&u, &v, 8);
+            const uint64_t r = (uint64_t)dpp_u32<kCtrl>((uint32_t)u) |
+                               ((uint64_t)dpp_u32<kCtrl>((uint32_t)(u >> 32)) << 32);
+            T out;
+            __builtin_memcpy(&out, &r, 8);
+            return out;
+        } else {
+            uint32_t u;
+            __builtin_memcpy(&u, &v, 4);
+            const uint32_t r = dpp_u32<kCtrl>(u);
+            T out;
+            __builtin_memcpy(&out, &r, 4);
+            return out;
+        }
+    } else {
+        return __shfl_xor(v, OFF);
+    }
+}
+
+// Merges the top-2 of the partner lane: (v1, e1) is the best value and its
+// expert (ties to the lower expert), v2 the best value of any other expert,
+// s1 the score of e1.
+template <int OFF, class M>
+__device__ inline void top2_step(typename M::value_t &v1, int &e1, typename M::value_t &v2,
+                                 typename M::value_t &s1) {
+    using value_t = typename M::value_t;
+    const value_t ov1 = grp_partner<OFF>(v1);
+    const int oe1 = grp_partner<OFF>(e1);
+    const value_t ov2 = grp_partner<OFF>(v2);
+    const value_t os1 = grp_partner<OFF>(s1);
+    if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
+        v2 = v1 > ov2 ? v1 : ov2;
+        v1 = ov1;
+        e1 = oe1;
+        s1 = os1;
+    } else {
+        v2 = v2 > ov1 ? v2 : ov1;
+    }
+}
+
+// Top-2 over a group of G lanes; every lane of the group ends with the result.
+template <class M, int G>
+__device__ inline void top2_reduce(typename M::value_t &v1, int &e1, typename M::value_t &v2,
+                                   typename M::value_t &s1) {
+    if constexpr (G > 1) top2_step<1, M>(v1, e1, v2, s1);
+    if constexpr (G > 2) top2_step<2, M>(v1, e1, v2, s1);
+    if constexpr (G > 4) top2_step<4, M>(v1, e1, v2, s1);
+    if constexpr (G > 8) top2_step<8, M>(v1, e1, v2, s1);
+    if constexpr (G > 16) top2_step<16, M>(v1, e1, v2, s1);
+    if constexpr (G > 32) top2_step<32, M>(v1, e1, v2, s1);
+}
+
 // Top-2 of one token whose lane-local scores sv (experts e0 .. e0 + 7) are
 // already in registers (rows that fit one chunk of 8 G experts).
 template <class M, int G>
@@ -238,21 +306,7 @@ __device__ inline void top2_row(const typename M::value_t (&sv)[8], int e0, int 
             }
         }
     }
-#pragma unroll
-    for (int off = G / 2; off > 0; off >>= 1) {
-        const value_t ov1 = __shfl_xor(v1, off);
-        const int oe1 = __shfl_xor(e1, off);
-        const value_t ov2 = __shfl_xor(v2, off);
-        const value_t os1 = __shfl_xor(s1, off);
-        if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
-            v2 = v1 > ov2 ? v1 : ov2;
-            v1 = ov1;
-            e1 = oe1;
-            s1 = os1;
-        } else {
-            v2 = v2 > ov1 ? v2 : ov1;
-        }
-    }
+    top2_reduce<M, G>(v1, e1, v2, s1);
 }
 
 template <class M, int G>
@@ -288,21 +342,7 @@ __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const type
             }
         }
     }
-#pragma unroll
-    for (int off = G / 2; off > 0; off >>= 1) {
-        const value_t ov1 = __shfl_xor(v1, off);
-        const int oe1 = __shfl_xor(e1, off);
-        const value_t ov2 = __shfl_xor(v2, off);
-        const value_t os1 = __shfl_xor(s1, off);
-        if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
-            v2 = v1 > ov2 ? v1 : ov2;
-            v1 = ov1;
-            e1 = oe1;
-            s1 = os1;
-        } else {
-            v2 = v2 > ov1 ? v2 : ov1;
-        }
-    }
+    top2_reduce<M, G>(v1, e1, v2, s1);
 }
 
 // Bids of active tokens [i0, n) with stride `ngroups` groups. `touched`
@@ -914,6 +954,66 @@ __global__ __launch_bounds__(256) void summary_prefill_kernel(const uint4 *sums,
     if (acc == 0x9e3779b9u && threadIdx.x == 0) *sink = acc;   // keeps the loads
 }
 
+// Loads words of token t's summary into sw: lane gl of the group takes
+// entry gl % 8 (score, expert half-word), the bound and the entry count.
+__device__ inline void load_summary(const uint32_t *sums, int t, int gl, uint32_t (&sw)[4]) {
+    const uint32_t *sm = sums + (int64_t)t * kSumWords;
+    const int q = gl & 7;
+    sw[0] = sm[q];
+    sw[1] = sm[8 + (q >> 1)];
+    const uint2 bc = *reinterpret_cast<const uint2 *>(sm + 12);
+    sw[2] = bc.x;
+    sw[3] = bc.y;
+}
+
+// Top-2 of token t from its summary words (called by the whole wave; groups
+// with valid == false take part in the shuffles only). A token whose summary
+// cannot decide (or any token when G < 8) reads its full row instead.
+// pmin is a lower bound of every price.
+template <class M, int G>
+__device__ inline void top2_summary(const Ctx<M> &c, const uint32_t (&sw)[4], int t, bool valid,
+                                    int gl, const typename M::value_t *pr,
+                                    typename M::value_t pmin, typename M::value_t &v1, int &e1,
+                                    typename M::value_t &v2, typename M::value_t &s1) {
+    using value_t = typename M::value_t;
+    const int cnt = (int)sw[3];
+    v1 = M::lowest();
+    v2 = M::lowest();
+    s1 = 0;
+    e1 = 0x7fffffff;
+    if (valid && gl < 8 && gl < cnt) {
+        const value_t sc = bits_score<M>(sw[0], c.scale);
+        int ex = (int)((sw[1] >> (16 * (gl & 1))) & 0xffff);
+        if (ex >= c.E) ex = 0;
+        v1 = sc - pr[ex];
+        e1 = ex;
+        s1 = sc;
+    }
+    top2_reduce<M, G>(v1, e1, v2, s1);
+    bool exact = cnt >= c.E;
+    if (!exact) {
+        const value_t lim = bits_score<M>(sw[2], c.scale) - pmin;
+        exact = v1 > lim && v2 >= lim;
+    }
+    if (G < 8) exact = false;   // a group narrower than 8 lanes cannot hold the 8 entries
+    const bool need = valid && !exact;
+    if (__ballot(need)) {
+        value_t row[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) row[j] = 0;
+        if (need && 8 * gl < c.E) load8<M>(c.S, (int64_t)t * c.E, 8 * gl, c.E, c.scale, row);
+        value_t w1, w2, ws1;
+        int we1;
+        top2_row<M, G>(row, 8 * gl, c.E, need, pr, w1, we1, w2, ws1);
+        if (need) {
+            v1 = w1;
+            v2 = w2;
+            e1 = we1;
+            s1 = ws1;
+        }
+    }
+}
+
 // ------------------------------------------------------------ tail engine --
 //
 // The rounds left once at most kEngCap tokens are active run inside one
@@ -1161,18 +1261,11 @@ __device__ inline void er_pop(ExpertRegs<M> &r) {
     r.cn = r.cn > 0 ? r.cn - 1 : 0;
 }
 
-// One wave: streams expert e's bids of this round into its holders. Bids are
-// bids[0..nb), or, with `exps`, the entries of bids[0..nb) whose expert is e
-// (picked out by a ballot, 64 entries per step).
+// Loads expert e's state into the wave's registers.
 template <class M>
-__device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *bids,
-                           const int *exps, int nb, int *nxt, int *nnext) {
+__device__ inline void er_load(const Eng<M> &s, int e, ExpertRegs<M> &r) {
     const int lane = lane_id();
     const int K = s.K;
-    uint64_t *hold = c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
-    uint64_t *scr_key = s.scr_key + (threadIdx.x >> 6) * 64;
-    int *scr_slot = s.scr_slot + (threadIdx.x >> 6) * 64;
-    ExpertRegs<M> r;
     r.cn = s.cn[e];
     r.cnt = s.cnt[e];
     r.key = lane < r.cn ? s.ck[e * K + lane] : ~0ull;
@@ -1181,49 +1274,14 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
     r.np = 0;
     r.pkey = 0;
     r.pslot = 0;
-    // Bids are read 64 at a time, one per lane, and taken in lane order.
-    for (int j0 = 0; j0 < nb; j0 += 64) {
-        const int j = j0 + lane;
-        const bool mine = j < nb && (exps == nullptr || exps[j] == e);
-        const uint64_t mykey = j < nb ? bids[j] : 0ull;
-        uint64_t mask = __ballot(mine);
-        while (mask) {
-            const int src = __ffsll((long long)mask) - 1;
-            mask &= mask - 1;
-            const uint64_t b = rl64(mykey, src);
-            int out_tok = -1;
-            if (r.cnt < c.C) {
-                const int slot = r.cnt;
-                const bool complete = r.cn == r.cnt;
-                er_write<M>(c, hold, r, slot, b);
-                r.cnt += 1;
-                er_insert<M>(r, K, b, slot, complete);
-                if (r.cnt == c.C) {
-                    if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-                    r.price = M::key_bid(rl64(r.key, 0));
-                }
-            } else {
-                if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-                const uint64_t m = rl64(r.key, 0);
-                if (b > m) {
-                    const int slot = rl32(r.slot, 0);
-                    out_tok = key_token(m);
-                    er_pop<M>(r);
-                    er_write<M>(c, hold, r, slot, b);
-                    er_insert<M>(r, K, b, slot, r.cn == r.cnt - 1);
-                    if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-                    r.price = M::key_bid(rl64(r.key, 0));
-                } else {
-                    out_tok = key_token(b);
-                }
-            }
-            if (out_tok >= 0 && lane == 0) {
-                const int at = atomicAdd(nnext, 1);
-                if (at < kEngCap && out_tok < c.T) nxt[at] = out_tok;
-                else flag_internal(c.ctrl);
-            }
-        }
-    }
+}
+
+// Stores the pending holder-table entries and expert e's state back.
+template <class M>
+__device__ inline void er_store(const Ctx<M> &c, const Eng<M> &s, int e, uint64_t *hold,
+                                ExpertRegs<M> &r) {
+    const int lane = lane_id();
+    const int K = s.K;
     er_flush<M>(c, hold, r);
     if (lane < r.cn) {
         s.ck[e * K + lane] = r.key;
@@ -1233,6 +1291,165 @@ __device__ void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64
         s.cn[e] = r.cn;
         s.cnt[e] = r.cnt;
         s.pr[e] = r.price;
+    }
+}
+
+// Streams one bid key b into the expert held in r: a free slot takes it;
+// otherwise it replaces the lowest held key when larger. Returns the token
+// that leaves (the displaced holder or the bidder itself), or -1. A full
+// expert always leaves with a non-empty list (its head is the price), so the
+// list is refilled in one place, at the end.
+template <class M>
+__device__ __attribute__((always_inline)) inline int er_bid(const Ctx<M> &c, uint64_t *hold,
+                                                            int K, ExpertRegs<M> &r, uint64_t b,
+                                                            uint64_t *scr_key, int *scr_slot) {
+    int out_tok = -1;
+    if (r.cnt < c.C) {
+        const int slot = r.cnt;
+        const bool complete = r.cn == r.cnt;
+        er_write<M>(c, hold, r, slot, b);
+        r.cnt += 1;
+        er_insert<M>(r, K, b, slot, complete);
+    } else {
+        // (an empty list here only follows a flagged inconsistency: every
+        // bid is then refused)
+        const uint64_t m = r.cn > 0 ? rl64(r.key, 0) : ~0ull;
+        if (b > m) {
+            const int slot = rl32(r.slot, 0);
+            out_tok = key_token(m);
+            er_pop<M>(r);
+            er_write<M>(c, hold, r, slot, b);
+            er_insert<M>(r, K, b, slot, r.cn == r.cnt - 1);
+        } else {
+            out_tok = key_token(b);
+        }
+    }
+    if (r.cnt == c.C) {
+        if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
+        r.price = M::key_bid(rl64(r.key, 0));
+    }
+    return out_tok;
+}
+
+template <class M>
+__device__ inline uint64_t *expert_holders(const Ctx<M> &c, const Eng<M> &s, int e) {
+    return c.holders + (int64_t)(s.sel[e] & 1) * c.T + (int64_t)e * c.C;
+}
+
+// One wave: streams expert e's bids of this round into its holders. Bids are
+// bids[0..nb), or, with `exps`, the entries of bids[0..nb) whose expert is e
+// (picked out by a ballot, 64 entries per step).
+template <class M>
+__device__ __attribute__((always_inline)) void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *bids,
+                           const int *exps, int nb, int *nxt, int *nnext) {
+    const int lane = lane_id();
+    uint64_t *hold = expert_holders<M>(c, s, e);
+    uint64_t *scr_key = s.scr_key + (threadIdx.x >> 6) * 64;
+    int *scr_slot = s.scr_slot + (threadIdx.x >> 6) * 64;
+    ExpertRegs<M> r;
+    er_load<M>(s, e, r);
+    // Bids are read 64 at a time, one per lane, and taken in lane order.
+    for (int j0 = 0; j0 < nb; j0 += 64) {
+        const int j = j0 + lane;
+        const bool mine = j < nb && (exps == nullptr || exps[j] == e);
+        const uint64_t mykey = j < nb ? bids[j] : 0ull;
+        uint64_t mask = __ballot(mine);
+        while (mask) {
+            const int src = __ffsll((long long)mask) - 1;
+            mask &= mask - 1;
+            const int out_tok = er_bid<M>(c, hold, s.K, r, rl64(mykey, src), scr_key, scr_slot);
+            if (out_tok >= 0 && lane == 0) {
+                const int at = atomicAdd(nnext, 1);
+                if (at < kEngCap && out_tok < c.T) nxt[at] = out_tok;
+                else flag_internal(c.ctrl);
+            }
+        }
+    }
+    er_store<M>(c, s, e, hold, r);
+}
+
+// Orders one wave's LDS (and global) accesses for the compiler: values one
+// lane stored are seen by every lane after it (the hardware keeps a wave's
+// accesses in order).
+__device__ inline void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Tokens one wave bids for at once: one group of G lanes each, at most 8.
+template <int G>
+constexpr int solo_tokens() { return (64 / G) < 8 ? (64 / G) : 8; }
+
+// Rounds with at most solo_tokens<G>() active tokens, run by one wave with
+// no workgroup barrier: each group bids for one token (same prices for all,
+// as in every round), then the wave streams the bids into their experts one
+// after another. A bid leaves at most one token active, so once a round fits
+// every later round of the phase fits as well; the loop runs until no token
+// is active or the round limit is reached. The other waves wait at the
+// caller's next barrier.
+template <class M, int G>
+__device__ __attribute__((always_inline)) void engine_solo(const Ctx<M> &c, const Eng<M> &s, int *act, typename M::value_t eps,
+                            typename M::value_t pmin, int max_rounds_left, int *s_n,
+                            int *s_rounds, unsigned long long *s_bids) {
+    using value_t = typename M::value_t;
+    const int lane = lane_id();
+    const int gl = lane & (G - 1);
+    const int g = lane / G;
+    int n = *s_n;
+    int rounds = *s_rounds;
+    unsigned long long bids = 0;
+    int tokv = lane < n ? act[lane] : 0;   // lane k holds active token k
+    int overflow = 0;
+    while (n > 0 && rounds < max_rounds_left) {
+        int t = 0;
+        for (int k = 0; k < n; ++k) {
+            const int tk = rl32(tokv, k);
+            if (g == k) t = tk;
+        }
+        const bool valid = g < n;
+        uint32_t sw[4] = {0, 0, 0, 0};
+        if (valid) load_summary(c.sums, t, gl, sw);
+        value_t v1, v2, s1;
+        int e1;
+        top2_summary<M, G>(c, sw, t, valid, gl, s.pr, pmin, v1, e1, v2, s1);
+        uint64_t key = 0;
+        int ex = 0;
+        if (valid && gl == 0) {
+            if (e1 >= c.E) {
+                e1 = 0;
+                s1 = M::load(c.S, (int64_t)t * c.E, c.scale);
+            }
+            const value_t bid = (value_t)((s1 - v2) + eps);
+            key = M::make_key(bid, t, &overflow);
+            ex = e1;
+        }
+        int nn = 0, nxt_tok = 0;
+        for (int k = 0; k < n; ++k) {
+            const int e = rl32(ex, k * G);
+            uint64_t *hold = expert_holders<M>(c, s, e);
+            ExpertRegs<M> r;
+            er_load<M>(s, e, r);
+            const int out = er_bid<M>(c, hold, s.K, r, rl64(key, k * G), s.scr_key, s.scr_slot);
+            er_store<M>(c, s, e, hold, r);
+            wave_sync();
+            if (out >= 0) {
+                if (out >= c.T) flag_internal(c.ctrl);
+                if (lane == nn) nxt_tok = out < c.T ? out : 0;
+                ++nn;
+            }
+        }
+        rounds += 1;
+        bids += (unsigned long long)n;
+        tokv = nxt_tok;
+        n = nn;
+    }
+    if (lane < n) act[lane] = tokv;
+    if (__ballot(overflow != 0) && lane == 0) c.ctrl->overflow = 1;
+    if (lane == 0) {
+        *s_n = n;
+        *s_rounds = rounds;
+        *s_bids += bids;
     }
 }
 
@@ -1397,6 +1614,12 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
             if (tid == 0) s_stop = 1;
             break;
         }
+        if (n <= solo_tokens<G>()) {
+            if (wave == 0)
+                engine_solo<M, G>(c, s, act, eps, pmin, max_rounds_left, &s_n, &s_rounds, &s_bids);
+            __syncthreads();
+            continue;
+        }
         // Bids against the prices at the start of the round.
         // Each group keeps kEngRows score rows in flight: all loads first,
         // then the reductions. With E <= kEngMaxE = 8 * 64 a row is one chunk
@@ -1406,21 +1629,14 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
         const int stride = per_pass * kEngRows;
         const int n_round = ((n + stride - 1) / stride) * stride;
         for (int i0 = gid; i0 < n_round; i0 += stride) {
-          uint32_t sw[kEngRows][4];   // words gl, gl+G, .. of the summary; bound, count
+          uint32_t sw[kEngRows][4];   // entry gl % 8 of the summary, bound, count
           int toks[kEngRows];
 #pragma unroll
           for (int u = 0; u < kEngRows; ++u) {
               const int i = i0 + u * per_pass;
               toks[u] = i < n ? act[i] : 0;
               sw[u][0] = sw[u][1] = sw[u][2] = sw[u][3] = 0;
-              if (i < n) {
-                  const uint32_t *sm = c.sums + (int64_t)toks[u] * kSumWords;
-                  const int q = gl & 7;
-                  sw[u][0] = sm[q];                       // score of entry q
-                  sw[u][1] = sm[8 + (q >> 1)];            // its expert (half word)
-                  sw[u][2] = sm[12];                      // bound
-                  sw[u][3] = sm[13];                      // entries
-              }
+              if (i < n) load_summary(c.sums, toks[u], gl, sw[u]);
           }
 #pragma unroll
           for (int u = 0; u < kEngRows; ++u) {
@@ -1430,67 +1646,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
             const int t = toks[u];
             value_t v1, v2, s1;
             int e1;
-            // Top-2 over the summary's entries (lane gl takes entry gl when gl < 8).
-            {
-                const int q = gl;
-                const int cnt = (int)sw[u][3];
-                value_t sv[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) sv[j] = M::lowest();
-                int ex = 0;
-                if (valid && q < 8 && q < cnt) {
-                    sv[0] = bits_score<M>(sw[u][0], c.scale);
-                    ex = (int)((sw[u][1] >> (16 * (q & 1))) & 0xffff);
-                    if (ex >= c.E) ex = 0;
-                }
-                v1 = M::lowest();
-                v2 = M::lowest();
-                s1 = 0;
-                e1 = 0x7fffffff;
-                if (valid && q < 8 && q < cnt) {
-                    v1 = sv[0] - s.pr[ex];
-                    e1 = ex;
-                    s1 = sv[0];
-                }
-#pragma unroll
-                for (int off = G / 2; off > 0; off >>= 1) {
-                    const value_t ov1 = __shfl_xor(v1, off);
-                    const int oe1 = __shfl_xor(e1, off);
-                    const value_t ov2 = __shfl_xor(v2, off);
-                    const value_t os1 = __shfl_xor(s1, off);
-                    if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
-                        v2 = v1 > ov2 ? v1 : ov2;
-                        v1 = ov1;
-                        e1 = oe1;
-                        s1 = os1;
-                    } else {
-                        v2 = v2 > ov1 ? v2 : ov1;
-                    }
-                }
-                bool exact = cnt >= c.E;
-                if (!exact) {
-                    const value_t lim = bits_score<M>(sw[u][2], c.scale) - pmin;
-                    exact = v1 > lim && v2 >= lim;
-                }
-                if (G < 8) exact = false;   // a group narrower than 8 lanes cannot hold the 8 entries
-                const bool need = valid && !exact;
-                if (__ballot(need)) {
-                    value_t row[8];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) row[j] = 0;
-                    if (need && 8 * gl < c.E)
-                        load8<M>(c.S, (int64_t)t * c.E, 8 * gl, c.E, c.scale, row);
-                    value_t w1, w2, ws1;
-                    int we1;
-                    top2_row<M, G>(row, 8 * gl, c.E, need, s.pr, w1, we1, w2, ws1);
-                    if (need) {
-                        v1 = w1;
-                        v2 = w2;
-                        e1 = we1;
-                        s1 = ws1;
-                    }
-                }
-            }
+            top2_summary<M, G>(c, sw[u], t, valid, gl, s.pr, pmin, v1, e1, v2, s1);
             if (valid && gl == 0) {
                 if (e1 >= c.E) {
                     e1 = 0;
