@@ -108,7 +108,8 @@ int base_affinity(const void *H, const void *W, float *S, int64_t T, int64_t E, 
  * the assignment is an exact optimum of Eq. 2. Requires T < 2^21.
  *
  *   S          [device] T x E scores, s_dtype (BASE_F32 or BASE_I16), row-major
- *   T, E       T > 0, E > 0, T % E == 0, T < 2^24
+ *   T, E       T > 0, 0 < E <= 2048, T % E == 0, T < 2^24 (T < 2^21 in integer
+ *              mode); other sizes return BASE_ERR_RANGE
  *   opts       [host] options, NULL for the defaults below
  *   assign     [device] int32 [T] out: a_t in [0, E)
  *   perm       [device] int32 [T] out: the sort vector of Fig. 2; perm[k] is
@@ -140,8 +141,10 @@ enum {
 typedef struct {
     double eps_final;    /* float mode: final epsilon in score units; <= 0 -> 1e-4.
                             Ignored in integer mode (always 1 scaled unit). */
-    double eps_initial;  /* first-phase epsilon; <= 0 -> (max S - min S) / 8 computed on the device */
-    double eps_factor;   /* epsilon divisor between phases; <= 1 -> 8 */
+    double eps_initial;  /* first-phase epsilon in score units (also in integer mode,
+                            where it is scaled by K); <= 0 -> (max S - min S) / 8
+                            computed on the device */
+    double eps_factor;   /* epsilon divisor between phases; <= 1 -> 24 */
     int32_t max_rounds;  /* bound on bidding rounds over all phases; <= 0 -> 4,000,000 */
     uint32_t flags;      /* BASE_ASSIGN_* */
 } base_assign_opts;

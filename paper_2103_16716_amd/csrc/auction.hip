@@ -46,6 +46,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kCandLds = 4096;   // candidates of one expert staged in LDS when they fit
 constexpr int kCountTile = 256;  // tokens per block in the permutation build
+constexpr int kWideLoopRounds = 1024;  // rounds one cooperative launch may run
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -58,7 +59,7 @@ inline void debug_note(const char *what, hipError_t err) {
 
 struct Layout {
     size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
-        eck, ecs, ecn, sums, total;
+        eck, ecs, ecn, sums, bar, total;
     int64_t cap, nblk;
 };
 
@@ -84,6 +85,7 @@ Layout make_layout(int64_t T, int64_t E) {
     L.ecs = off;     off += align_up((size_t)E * 64 * 2);
     L.ecn = off;     off += align_up((size_t)E * 4);
     L.sums = off;    off += align_up((size_t)T * 64);          // per-token score summaries
+    L.bar = off;     off += align_up(512);                      // grid barrier words
     L.total = off;
     return L;
 }
@@ -106,6 +108,7 @@ struct Ctx {
     uint16_t *eng_cs;
     int *eng_cn;
     uint32_t *sums;   // T x 16 words: each token's 8 best scores, their experts, a bound
+    uint64_t *bar;    // grid barrier: arrivals at bar[0], release at bar[32] (own lines)
 };
 
 template <class M>
@@ -135,6 +138,7 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.eng_cs = reinterpret_cast<uint16_t *>(ws + L.ecs);
     c.eng_cn = reinterpret_cast<int *>(ws + L.ecn);
     c.sums = reinterpret_cast<uint32_t *>(ws + L.sums);
+    c.bar = reinterpret_cast<uint64_t *>(ws + L.bar);
     return c;
 }
 
@@ -717,6 +721,10 @@ __global__ void phase_begin_kernel(Ctx<M> c, AssignParams p) {
         skip = c.ctrl->done;
         if (!skip) begin_phase_scalar(c.ctrl, p, c.T);
     }
+    if (threadIdx.x == 0) {
+        c.bar[0] = 0;    // the round loop's barrier counts from zero in every launch
+        c.bar[32] = 0;
+    }
     __syncthreads();
     if (skip) return;
     for (int e = threadIdx.x; e < c.E; e += blockDim.x) {
@@ -770,6 +778,98 @@ __global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c) {
         __threadfence();
         ctrl->blocks_done = 0;
         end_round(ctrl, c.T);
+    }
+}
+
+// ------------------------------------------------------ wide round loop --
+//
+// Rounds that still have more active tokens than the engine takes after
+// the fixed wide launches: all blocks of a cooperative launch (every block
+// resident) run them back to back with a grid barrier between the bids and
+// the updates and after the updates (the last block to finish closes the
+// round). All blocks read the same control words after a barrier and take
+// the same exit. The launch returns at once when there is nothing to do.
+
+// Barrier k of a launch completes when bar[0] reaches k * gridDim.x. Every
+// thread waits for its own stores first; one thread per block then writes
+// back its L2 (device-scope release), arrives, waits for the release word
+// (on its own line, stored by the last arrival) and invalidates its caches
+// (acquire). The wait gives up after ~2^24 polls: the block flags an
+// internal error and returns false.
+__device__ inline bool grid_barrier(uint64_t *bar, uint64_t target, SolveCtrl *ctrl) {
+    __shared__ int ok;
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this thread's stores are done
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        ok = 1;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        const uint64_t arrived =
+            __hip_atomic_fetch_add(bar, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+        if (arrived == target) {
+            __hip_atomic_store(bar + 32, target, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            uint32_t polls = 0;
+            while (__hip_atomic_load(bar + 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+                __builtin_amdgcn_s_sleep(2);
+                if (++polls == (1u << 24)) {
+                    flag_internal(ctrl);
+                    ok = 0;
+                    break;
+                }
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    __syncthreads();
+    return ok != 0;
+}
+
+template <class M, int G>
+__global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c, int max_wide,
+                                                             int32_t max_rounds) {
+    using value_t = typename M::value_t;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
+    __shared__ UpdateSmem sm;
+    __shared__ int st_go, st_cur, st_all, st_n, last;
+    SolveCtrl *ctrl = c.ctrl;
+    const int tid = threadIdx.x;
+    uint64_t target = 0;
+    for (int r = 0; r < max_wide; ++r) {
+        if (tid == 0) {
+            const int done = ld_relaxed(&ctrl->done);
+            const int cur = ld_relaxed(&ctrl->cur) & 1;
+            const int all = ld_relaxed(&ctrl->all_active);
+            const int n = all ? c.T : ld_relaxed(&ctrl->active_count[cur]);
+            st_go = !done && n > 0 && (all || n > c.engine_cap) &&
+                    ld_relaxed(&ctrl->rounds) < max_rounds && !ld_relaxed(&ctrl->internal_error);
+            st_cur = cur;
+            st_all = all;
+            st_n = n;
+        }
+        __syncthreads();
+        if (!st_go) break;
+        for (int e = tid; e < c.E; e += kThreads) pr[e] = c.prices[e];
+        __syncthreads();
+        const value_t eps = (value_t)ctrl->eps;
+        const int per_block = kThreads / G;
+        bid_range<M, G>(c, st_n, st_all != 0, c.active + (int64_t)st_cur * c.T, eps, pr,
+                        blockIdx.x * per_block + tid / G, gridDim.x * per_block, nullptr, nullptr);
+        target += gridDim.x;
+        if (!grid_barrier(c.bar, target, ctrl)) return;
+        const int novf = min(ld_relaxed(c.ovf_count), c.T);
+        for (int e = blockIdx.x; e < c.E; e += gridDim.x) update_expert<M>(c, e, st_cur ^ 1, novf, sm);
+        __threadfence();
+        __syncthreads();
+        if (tid == 0) last = atomicAdd(&ctrl->blocks_done, 1) == (int)gridDim.x - 1;
+        __syncthreads();
+        if (last && tid == 0) {
+            __threadfence();
+            ctrl->blocks_done = 0;
+            end_round(ctrl, c.T);
+        }
+        target += gridDim.x;
+        if (!grid_barrier(c.bar, target, ctrl)) return;
     }
 }
 
@@ -1233,34 +1333,6 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
     }
 }
 
-// Inserts key b (held in `slot`) if it belongs to the lowest K keys;
-// `complete` says every holder other than b is in the list.
-template <class M>
-__device__ inline void er_insert(ExpertRegs<M> &r, int K, uint64_t b, int slot, bool complete) {
-    const int lane = lane_id();
-    if (!complete && (r.cn == 0 || b > rl64(r.key, r.cn - 1))) return;   // stays outside
-    const int pos = __popcll(__ballot(lane < r.cn && r.key < b));
-    if (pos >= K) return;   // larger than a full list of keys
-    const uint64_t kprev = up1_u64(r.key);
-    const int sprev = up1_i32(r.slot);
-    const int nn = r.cn + 1 < K ? r.cn + 1 : K;
-    if (lane >= pos && lane < nn) {
-        r.key = lane == pos ? b : kprev;
-        r.slot = lane == pos ? slot : sprev;
-    }
-    r.cn = nn;
-}
-
-template <class M>
-__device__ inline void er_pop(ExpertRegs<M> &r) {
-    const int lane = lane_id();
-    const uint64_t knext = down1_u64(r.key);
-    const int snext = down1_i32(r.slot);
-    r.key = lane + 1 < r.cn ? knext : ~0ull;
-    r.slot = lane + 1 < r.cn ? snext : 0;
-    r.cn = r.cn > 0 ? r.cn - 1 : 0;
-}
-
 // Loads expert e's state into the wave's registers.
 template <class M>
 __device__ inline void er_load(const Eng<M> &s, int e, ExpertRegs<M> &r) {
@@ -1287,6 +1359,7 @@ __device__ inline void er_store(const Ctx<M> &c, const Eng<M> &s, int e, uint64_
         s.ck[e * K + lane] = r.key;
         s.cs[e * K + lane] = (uint16_t)r.slot;
     }
+    if (r.cnt == c.C) r.price = M::key_bid(rl64(r.key, 0));   // full: the lowest held bid
     if (lane == 0) {
         s.cn[e] = r.cn;
         s.cnt[e] = r.cnt;
@@ -1296,38 +1369,61 @@ __device__ inline void er_store(const Ctx<M> &c, const Eng<M> &s, int e, uint64_
 
 // Streams one bid key b into the expert held in r: a free slot takes it;
 // otherwise it replaces the lowest held key when larger. Returns the token
-// that leaves (the displaced holder or the bidder itself), or -1. A full
-// expert always leaves with a non-empty list (its head is the price), so the
-// list is refilled in one place, at the end.
+// that leaves (the displaced holder or the bidder itself), or -1.
+// The list update is one ballot (b's rank among the listed keys) and one
+// one-lane shift: up for an insertion, down for a replacement of the head
+// (the head leaves and b enters at its rank among the rest). A key above
+// every listed one enters only when the list holds every holder. A full
+// expert leaves with a non-empty list (refilled in one place, at the end);
+// its price is taken from the list head when the state is stored.
 template <class M>
 __device__ __attribute__((always_inline)) inline int er_bid(const Ctx<M> &c, uint64_t *hold,
                                                             int K, ExpertRegs<M> &r, uint64_t b,
                                                             uint64_t *scr_key, int *scr_slot) {
+    const int lane = lane_id();
     int out_tok = -1;
     if (r.cnt < c.C) {
         const int slot = r.cnt;
         const bool complete = r.cn == r.cnt;
         er_write<M>(c, hold, r, slot, b);
         r.cnt += 1;
-        er_insert<M>(r, K, b, slot, complete);
+        const int pos = __popcll(__ballot(lane < r.cn && r.key < b));
+        if ((pos < r.cn || complete) && pos < K) {
+            const uint64_t kprev = up1_u64(r.key);
+            const int sprev = up1_i32(r.slot);
+            const int nn = r.cn + 1 < K ? r.cn + 1 : K;
+            if (lane >= pos && lane < nn) {
+                r.key = lane == pos ? b : kprev;
+                r.slot = lane == pos ? slot : sprev;
+            }
+            r.cn = nn;
+        }
     } else {
         // (an empty list here only follows a flagged inconsistency: every
         // bid is then refused)
-        const uint64_t m = r.cn > 0 ? rl64(r.key, 0) : ~0ull;
-        if (b > m) {
+        const uint64_t head = r.cn > 0 ? rl64(r.key, 0) : ~0ull;
+        if (b > head) {
             const int slot = rl32(r.slot, 0);
-            out_tok = key_token(m);
-            er_pop<M>(r);
+            out_tok = key_token(head);
             er_write<M>(c, hold, r, slot, b);
-            er_insert<M>(r, K, b, slot, r.cn == r.cnt - 1);
+            const bool complete = r.cn == r.cnt;
+            const int pos = __popcll(__ballot(lane >= 1 && lane < r.cn && r.key < b)) ;
+            const bool keep = pos < r.cn - 1 || complete;
+            const uint64_t knext = down1_u64(r.key);
+            const int snext = down1_i32(r.slot);
+            if (lane < pos) {
+                r.key = knext;
+                r.slot = snext;
+            } else if (lane == pos) {
+                r.key = keep ? b : ~0ull;
+                r.slot = keep ? slot : 0;
+            }
+            if (!keep) r.cn -= 1;
         } else {
             out_tok = key_token(b);
         }
     }
-    if (r.cnt == c.C) {
-        if (r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
-        r.price = M::key_bid(rl64(r.key, 0));
-    }
+    if (r.cnt == c.C && r.cn == 0) er_refill<M>(c, hold, K, r, scr_key, scr_slot);
     return out_tok;
 }
 
@@ -1348,6 +1444,20 @@ __device__ __attribute__((always_inline)) void eng_update(const Ctx<M> &c, const
     int *scr_slot = s.scr_slot + (threadIdx.x >> 6) * 64;
     ExpertRegs<M> r;
     er_load<M>(s, e, r);
+    // Tokens that leave collect in lane order (lane k holds the k-th) and
+    // are appended to the next list 64 at a time.
+    int nout = 0, outv = 0;
+    auto flush_out = [&]() {
+        int base = 0;
+        if (lane == 0) base = atomicAdd(nnext, nout);
+        base = __builtin_amdgcn_readfirstlane(base);
+        if (lane < nout) {
+            const int at = base + lane;
+            if (at < kEngCap && outv >= 0 && outv < c.T) nxt[at] = outv;
+            else flag_internal(c.ctrl);
+        }
+        nout = 0;
+    };
     // Bids are read 64 at a time, one per lane, and taken in lane order.
     for (int j0 = 0; j0 < nb; j0 += 64) {
         const int j = j0 + lane;
@@ -1358,13 +1468,13 @@ __device__ __attribute__((always_inline)) void eng_update(const Ctx<M> &c, const
             const int src = __ffsll((long long)mask) - 1;
             mask &= mask - 1;
             const int out_tok = er_bid<M>(c, hold, s.K, r, rl64(mykey, src), scr_key, scr_slot);
-            if (out_tok >= 0 && lane == 0) {
-                const int at = atomicAdd(nnext, 1);
-                if (at < kEngCap && out_tok < c.T) nxt[at] = out_tok;
-                else flag_internal(c.ctrl);
+            if (out_tok >= 0) {
+                if (lane == nout) outv = out_tok;
+                if (++nout == 64) flush_out();
             }
         }
     }
+    if (nout > 0) flush_out();
     er_store<M>(c, s, e, hold, r);
 }
 
@@ -1922,8 +2032,10 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     const size_t pr_bytes = (size_t)c.E * sizeof(value_t);
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
     // Phase slots enqueued up front; the last one continues on its own if
-    // the epsilon schedule needs more phases than were enqueued.
-    int slots = 8;
+    // the epsilon schedule needs more phases than were enqueued. With the
+    // default schedule (first epsilon = range / 8, divisor 24) six slots
+    // cover score ranges up to 8 * 24^5 (about 6 * 10^7) times eps_final.
+    int slots = 6;
     if (p.eps_initial > 0.0) {
         double e = p.eps_initial;
         slots = 1;
@@ -1942,12 +2054,41 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
         if (sblocks > 4096) sblocks = 4096;
         hipLaunchKernelGGL((summary_kernel<M, G>), dim3(sblocks), dim3(kThreads), 0, s, c);
     }
+    // Cooperative round loop for phases that stay large: one block per
+    // compute unit when the device takes cooperative launches.
+    int coop_blocks = 0;
+    {
+        int dev = 0, coop = 0, cus = 0, per_cu = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
+            coop &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu, reinterpret_cast<const void *>(&wide_loop_kernel<M, G>), kThreads,
+                pr_bytes) == hipSuccess &&
+            per_cu > 0 && cus > 0)
+            coop_blocks = cus;
+        (void)hipGetLastError();
+    }
     for (int slot = 0; slot < slots; ++slot) {
         hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1), dim3(1024), 0, s, c, p);
         for (int r = 0; r < wide_rounds; ++r) {
             hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks), dim3(kThreads), pr_bytes,
                                s, c);
             hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks), dim3(kThreads), 0, s, c);
+        }
+        if (coop_blocks > 0) {
+            int max_wide = kWideLoopRounds;
+            int32_t max_rounds = p.max_rounds;
+            void *args[] = {&c, &max_wide, &max_rounds};
+            const hipError_t err = hipLaunchCooperativeKernel(
+                reinterpret_cast<const void *>(&wide_loop_kernel<M, G>), dim3(coop_blocks),
+                dim3(kThreads), args, (unsigned)pr_bytes, s);
+            if (err != hipSuccess) {
+                (void)hipGetLastError();
+                debug_note("cooperative round loop refused", err);
+                coop_blocks = 0;
+            }
         }
         if (engine) {
             hipLaunchKernelGGL(cache_build_kernel<M>, dim3(c.E), dim3(256), 0, s, c);

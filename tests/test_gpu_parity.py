@@ -7,6 +7,8 @@ bit for bit, the objective is at least the oracle optimum minus T * eps, the
 returned prices certify the same bound by LP duality, and the assignment is
 identical to the oracle's wherever the optimum is unique by more than T * eps
 (always in integer mode). Permute: bit-exact gather and scatter."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -234,6 +236,28 @@ def test_assign_user_epsilon_schedule():
     res = pb.assign(dev(S), eps_final=1e-3, eps_initial=0.5, eps_factor=4.0)
     assert res.stats.eps_final == pytest.approx(1e-3)
     check_assignment(S64, res, 1e-3, opt=(a_opt, obj_opt))
+
+
+@pytest.mark.parametrize("name,seed,div,factor", [("t32768-e128-d2048-mix8", 79, 2.0, 24.0),
+                                                  ("t65536-e256-d4096", None, 32.0, 8.0)])
+def test_assign_phases_that_stay_large(name, seed, div, factor):
+    """Epsilon schedules under which many tokens stay active after the fixed
+    wide rounds of a phase, so the cooperative round loop takes over before
+    the single-workgroup engine: the result still meets the epsilon bound
+    against the exact optimum."""
+    w = wl.WORKLOADS[name]
+    if seed is not None:
+        w = dataclasses.replace(w, seed=seed)
+    inp = wl.make_inputs(w)
+    H, W = inputs_on_device(inp)
+    S = pb.affinity(H, W)
+    torch.cuda.synchronize()
+    Sh = host(S)
+    rng = float(Sh.max() - Sh.min())
+    res = pb.assign(S, eps_initial=rng / div, eps_factor=factor)
+    S64 = Sh.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    check_assignment(S64, res, EPS_FINAL, opt=(a_opt, obj_opt))
 
 
 # ---------------------------------------------------------------- permute --
