@@ -28,6 +28,32 @@ import workloads as wl  # noqa: E402
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak, TFLOP/s
 UNPERMUTE_WORKLOADS = {"t65536-e256-d4096"}
+ENGINE_KERNEL = "engine_kernel"   # the solve's dominant kernel (rounds with few active tokens)
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def engine_source_digest() -> str:
+    """sha256 of the solver source: counters taken on another version of the
+    kernel do not describe this one."""
+    import hashlib
+    path = os.path.join(ROOT, "paper_2103_16716_amd", "csrc", "auction.hip")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per engine launch from the committed counter summary of this
+    workload (FETCH_SIZE and WRITE_SIZE per dispatch, each scaled by what the
+    counter reads for a plain copy of known size), or None when there is no
+    summary or it was taken on a different version of the solver source."""
+    path = os.path.join(PROFILES, f"engine_kernel_traffic_{workload}.json")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != engine_source_digest():
+        return None
+    return (rec["fetch_kib_per_dispatch"] * rec["fetch_factor"] +
+            rec["write_kib_per_dispatch"] * rec["write_factor"]) * 1024.0
 
 
 def parse():
@@ -141,12 +167,17 @@ def main():
     torch.cuda.synchronize()
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(args.steps)]
+    # The library brackets each engine launch with its own events on the same
+    # stream (base_timing_enable), so the dominant kernel is timed live.
+    pb.timing_enable(64 * args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
         step(events[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    eng_launches, eng_ms = pb.timing_read()
+    pb.timing_enable(0)
 
     names = ["affinity", "assign", "permute"] + (["unpermute"] if unpermute else [])
     per_call_ms = {n: float(np.mean([ev[i].elapsed_time(ev[i + 1]) for ev in events]))
@@ -182,8 +213,16 @@ def main():
     if unpermute:
         rl["unpermute"] = ("hbm", bytes_perm / (per_call_ms["unpermute"] * 1e-3) / 1e9,
                            HBM_PEAK_GBS, "GB/s", bytes_perm)
-    dominant = max(per_call_ms, key=per_call_ms.get)
-    bound, ach, peak, unit, algo_bytes = rl[dominant]
+    # The dominant kernel: the engine (most of the assign call). Its
+    # algorithmic bytes per launch are the bids it places times the bytes a
+    # bid needs (the token's score row, 4E bytes, plus a 16-byte key and
+    # expert), over the launches of one solve.
+    launches_per_solve = eng_launches / args.steps if eng_launches else 0.0
+    eng_avg_ms = eng_ms / eng_launches if eng_launches else float("nan")
+    eng_bytes = (st.engine_bids * (4 * E + 16) / launches_per_solve
+                 if launches_per_solve else 0.0)
+    eng_ach = eng_bytes / (eng_avg_ms * 1e-3) / 1e9 if eng_launches else 0.0
+    traffic = measured_traffic(w.name)
     out = {
         "metric": "tokens assigned/sec at T=32768,E=128,d=2048",
         "value": T * args.steps / wall,
@@ -199,9 +238,11 @@ def main():
         "data": "synthetic (seeded generator; no dataset or trained weights)",
         "config": {"workload": w.name, "T": T, "E": E, "C": T // E, "d": d, "dist": w.dist,
                    "inputs": w.dtype, "scores": "f32", "solver": "f32 auction, eps_final=1e-4"},
-        "roofline": {"kernel": dominant, "bound": bound, "achieved": ach, "peak": peak,
-                     "unit": unit, "frac": ach / peak, "traffic": None,
-                     "algorithmic_bytes": int(algo_bytes)},
+        "roofline": {"kernel": ENGINE_KERNEL, "bound": "hbm", "achieved": eng_ach,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": eng_ach / HBM_PEAK_GBS,
+                     "traffic": traffic, "algorithmic_bytes_per_launch": eng_bytes,
+                     "avg_launch_ms": eng_avg_ms, "launches_per_step": launches_per_solve,
+                     "share_of_step": eng_ms / args.steps / gpu_ms if gpu_ms > 0 else None},
         "per_call_ms": {k: round(v, 4) for k, v in per_call_ms.items()},
         "gpu_ms_per_step": gpu_ms,
         "per_call_roofline": {k: {"bound": v[0], "achieved": round(v[1], 2), "peak": v[2],
@@ -210,7 +251,8 @@ def main():
         "affinity_mfma": {"achieved_tflops": flops_aff / (per_call_ms["affinity"] * 1e-3) / 1e12,
                           "peak_tflops": MFMA_BF16_PEAK_TFLOPS},
         "assign_stats": {"phases": st.phases, "rounds": st.rounds, "bids": st.bids,
-                         "eps_final": st.eps_final, "converged": st.converged},
+                         "engine_bids": st.engine_bids, "eps_final": st.eps_final,
+                         "converged": st.converged},
         "balanced_solves": f"{balanced}/{checked}",
     }
     if not args.no_cpu_baseline:

@@ -156,6 +156,8 @@ typedef struct {
     double eps_final;    /* epsilon of the last phase, in score units */
     int32_t fell_back;   /* 1 if the greedy completion was used */
     int32_t converged;   /* 1 if every expert holds exactly T/E tokens */
+    int64_t engine_bids; /* the part of `bids` placed inside the single-workgroup
+                            engine (the rounds with few active tokens) */
 } base_assign_stats;
 
 /* Bytes of device workspace base_assign needs for T tokens and E experts
@@ -187,6 +189,26 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
  */
 int base_permute(const void *in, const int32_t *perm, void *out, int64_t T, int64_t d, int dtype,
                  int inverse, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Measurement support                                                       */
+/* ------------------------------------------------------------------------ */
+/*
+ * Not part of the path. While enabled, base_assign brackets every launch of
+ * its single-workgroup engine kernel (the rounds of a phase with few active
+ * tokens: most of a solve's time) with a pair of HIP events recorded on the
+ * call's stream, so a tool can time that kernel over a stretch of ordinary
+ * calls. At most `capacity` launches are recorded; later ones are not.
+ *
+ * base_timing_enable(capacity) creates 2 * capacity events on the current
+ * device and clears the record; capacity <= 0 destroys them and disables the
+ * timing. base_timing_read waits for the recorded launches, returns their
+ * number and summed duration (milliseconds), and clears the record. One
+ * process-wide record; not thread-safe.
+ * Errors: BASE_ERR_INVALID_ARG (null pointer), BASE_ERR_HIP.
+ */
+int base_timing_enable(int32_t capacity);
+int base_timing_read(int64_t *launches, double *total_ms);
 
 #ifdef __cplusplus
 }

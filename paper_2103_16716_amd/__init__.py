@@ -42,7 +42,7 @@ BASE_ASSIGN_CHECK_FINITE = 4
 
 # Every symbol include/base.h declares.
 EXPORTED = ("base_status_string", "base_affinity", "base_assign_workspace_size", "base_assign",
-            "base_permute")
+            "base_permute", "base_timing_enable", "base_timing_read")
 
 
 class AssignOpts(ctypes.Structure):
@@ -54,7 +54,7 @@ class AssignOpts(ctypes.Structure):
 class AssignStats(ctypes.Structure):
     _fields_ = [("phases", ctypes.c_int32), ("rounds", ctypes.c_int32), ("bids", ctypes.c_int64),
                 ("eps_final", ctypes.c_double), ("fell_back", ctypes.c_int32),
-                ("converged", ctypes.c_int32)]
+                ("converged", ctypes.c_int32), ("engine_bids", ctypes.c_int64)]
 
 
 class BaseError(RuntimeError):
@@ -87,6 +87,10 @@ def lib() -> ctypes.CDLL:
         L.base_assign.restype = i32
         L.base_permute.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
         L.base_permute.restype = i32
+        L.base_timing_enable.argtypes = [ctypes.c_int32]
+        L.base_timing_enable.restype = i32
+        L.base_timing_read.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
+        L.base_timing_read.restype = i32
         _lib = L
     return _lib
 
@@ -203,5 +207,21 @@ def permute(x, perm, inverse: bool = False, out=None, stream=None):
     return out
 
 
-__all__ = ["affinity", "assign", "permute", "assign_workspace_size", "AssignResult", "AssignOpts",
-           "AssignStats", "BaseError", "lib", "status_string", "EXPORTED"]
+def timing_enable(capacity: int) -> None:
+    """Start recording event timings of the engine kernel's launches
+    (base_timing_enable); capacity <= 0 stops and frees the record."""
+    _check(lib().base_timing_enable(int(capacity)), "base_timing_enable")
+
+
+def timing_read() -> tuple[int, float]:
+    """(recorded engine launches, their summed milliseconds); clears the
+    record (base_timing_read)."""
+    n = ctypes.c_int64()
+    ms = ctypes.c_double()
+    _check(lib().base_timing_read(ctypes.byref(n), ctypes.byref(ms)), "base_timing_read")
+    return int(n.value), float(ms.value)
+
+
+__all__ = ["affinity", "assign", "permute", "assign_workspace_size", "timing_enable",
+           "timing_read", "AssignResult", "AssignOpts", "AssignStats", "BaseError", "lib",
+           "status_string", "EXPORTED"]

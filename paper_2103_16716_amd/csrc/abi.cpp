@@ -139,6 +139,7 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
             stats->bids = (int64_t)c.bids;
             stats->eps_final = integer ? c.eps / (double)p.scale : c.eps;
             stats->fell_back = c.fell_back;
+            stats->engine_bids = (int64_t)c.engine_bids;
             stats->converged =
                 (E == 1) || (unconverged == 0 && (!c.not_converged || c.fell_back)) ? 1 : 0;
             if (E == 1) {
@@ -147,6 +148,7 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
                 stats->bids = 0;
                 stats->eps_final = 0.0;
                 stats->fell_back = 0;
+                stats->engine_bids = 0;
             }
         }
         if (E > 1) {
@@ -156,6 +158,15 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
         }
     }
     return BASE_OK;
+}
+
+int base_timing_enable(int32_t capacity) {
+    return hip_status(base::timing_enable(capacity));
+}
+
+int base_timing_read(int64_t *launches, double *total_ms) {
+    if (launches == nullptr || total_ms == nullptr) return BASE_ERR_INVALID_ARG;
+    return hip_status(base::timing_read(launches, total_ms));
 }
 
 int base_permute(const void *in, const int32_t *perm, void *out, int64_t T, int64_t d, int dtype,

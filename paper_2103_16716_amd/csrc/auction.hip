@@ -1847,6 +1847,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
     if (tid == 0) {
         ctrl->rounds += s_rounds;
         ctrl->bids += s_bids;
+        ctrl->engine_bids += s_bids;
         ctrl->active_count[s_cur] = s_n;
         ctrl->active_count[s_cur ^ 1] = 0;
         ctrl->pad0 = 0;
@@ -1991,6 +1992,30 @@ int lanes_per_token(int64_t E) {
     return g;
 }
 
+// ------------------------------------------------------------ timing --
+//
+// Measurement support: while enabled, every engine launch is bracketed by a
+// pair of pre-created events (one process-wide record, not thread-safe).
+
+struct EngineTiming {
+    int32_t capacity = 0;
+    int32_t used = 0;
+    int64_t dropped = 0;
+    hipEvent_t *ev = nullptr;   // 2 * capacity events
+};
+EngineTiming g_timing;
+
+void timing_pair(hipEvent_t *begin, hipEvent_t *end) {
+    if (g_timing.capacity == 0) return;
+    if (g_timing.used == g_timing.capacity) {
+        ++g_timing.dropped;
+        return;
+    }
+    *begin = g_timing.ev[2 * g_timing.used];
+    *end = g_timing.ev[2 * g_timing.used + 1];
+    ++g_timing.used;
+}
+
 template <class M, int G>
 hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     using value_t = typename M::value_t;
@@ -2095,8 +2120,12 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
             hipLaunchKernelGGL(summary_prefill_kernel, dim3(256), dim3(256), 0, s,
                                reinterpret_cast<const uint4 *>(c.sums), (int64_t)c.T * 4, c.ctrl,
                                kEngCap, reinterpret_cast<uint32_t *>(&c.ctrl->pad2));
+            hipEvent_t ev0 = nullptr, ev1 = nullptr;
+            timing_pair(&ev0, &ev1);
+            if (ev0 != nullptr) (void)hipEventRecord(ev0, s);
             hipLaunchKernelGGL((engine_kernel<M, G>), dim3(1), dim3(kEngThreads), eng_bytes, s, c,
                                p);
+            if (ev1 != nullptr) (void)hipEventRecord(ev1, s);
         }
         hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1), dim3(kThreads), tail_smem, s, c, p,
                            slot == slots - 1 ? 1 : 0);
@@ -2179,6 +2208,43 @@ hipError_t launch_assign(const void *S, const AssignParams &p, int32_t *assign, 
     }
     if (p.integer) return solve_mode<IntMode>(S, p, assign, perm, prices_out, workspace, stream);
     return solve_mode<FloatMode>(S, p, assign, perm, prices_out, workspace, stream);
+}
+
+hipError_t timing_enable(int32_t capacity) {
+    for (int32_t i = 0; i < 2 * g_timing.capacity; ++i) (void)hipEventDestroy(g_timing.ev[i]);
+    free(g_timing.ev);
+    g_timing = EngineTiming{};
+    if (capacity <= 0) return hipSuccess;
+    g_timing.ev = static_cast<hipEvent_t *>(calloc((size_t)2 * capacity, sizeof(hipEvent_t)));
+    if (g_timing.ev == nullptr) return hipErrorOutOfMemory;
+    for (int32_t i = 0; i < 2 * capacity; ++i) {
+        const hipError_t e = hipEventCreate(&g_timing.ev[i]);
+        if (e != hipSuccess) {
+            for (int32_t j = 0; j < i; ++j) (void)hipEventDestroy(g_timing.ev[j]);
+            free(g_timing.ev);
+            g_timing = EngineTiming{};
+            return e;
+        }
+    }
+    g_timing.capacity = capacity;
+    return hipSuccess;
+}
+
+hipError_t timing_read(int64_t *launches, double *total_ms) {
+    double sum = 0.0;
+    for (int32_t i = 0; i < g_timing.used; ++i) {
+        hipError_t e = hipEventSynchronize(g_timing.ev[2 * i + 1]);
+        if (e != hipSuccess) return e;
+        float ms = 0.0f;
+        e = hipEventElapsedTime(&ms, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]);
+        if (e != hipSuccess) return e;
+        sum += ms;
+    }
+    *launches = g_timing.used;
+    *total_ms = sum;
+    g_timing.used = 0;
+    g_timing.dropped = 0;
+    return hipSuccess;
 }
 
 hipError_t read_assign_stats(const void *workspace, int64_t /*T*/, int64_t /*E*/, SolveCtrl *out,

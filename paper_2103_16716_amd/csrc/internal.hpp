@@ -48,7 +48,8 @@ struct SolveCtrl {
     double eps_final_eff;
     int32_t internal_error; // a device-side consistency check failed
     int32_t pad2;
-    int64_t pad1[3];
+    unsigned long long engine_bids;   // bids placed inside the single-workgroup engine
+    int64_t pad1[2];
 };
 
 size_t assign_workspace_size(int64_t T, int64_t E);
@@ -60,6 +61,10 @@ hipError_t launch_assign(const void *S, const AssignParams &p, int32_t *assign, 
 // Reads the statistics back (synchronises the stream).
 hipError_t read_assign_stats(const void *workspace, int64_t T, int64_t E, SolveCtrl *out,
                              hipStream_t stream);
+
+// Event timing of the engine kernel's launches (measurement support).
+hipError_t timing_enable(int32_t capacity);
+hipError_t timing_read(int64_t *launches, double *total_ms);
 
 // Scans S for NaN/Inf (synchronous). *bad is set to 1 when one is found.
 hipError_t check_scores_finite(const float *S, int64_t n, void *workspace, int *bad,

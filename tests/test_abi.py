@@ -45,6 +45,13 @@ def test_library_exports_every_declared_symbol(L):
         assert re.search(rf"\bT {name}\b", out), name
 
 
+def test_timing_record_without_launches(L):
+    # Disabled or empty records need no device: nothing recorded, nothing summed.
+    pb.timing_enable(0)
+    assert pb.timing_read() == (0, 0.0)
+    assert L.base_timing_read(None, None) == pb.BASE_ERR_INVALID_ARG
+
+
 def test_status_strings(L):
     for code in range(0, -10, -1):
         s = pb.status_string(code)

@@ -260,6 +260,27 @@ def test_assign_phases_that_stay_large(name, seed, div, factor):
     check_assignment(S64, res, EPS_FINAL, opt=(a_opt, obj_opt))
 
 
+def test_engine_launch_timing():
+    """The measurement hook brackets each engine launch with events on the
+    call's stream: one record per phase slot, each within the whole call."""
+    S = wl.random_scores(8192, 64, seed=5)
+    Sd = dev(S)
+    ws = torch.empty(pb.assign_workspace_size(8192, 64), dtype=torch.uint8, device="cuda")
+    pb.assign(Sd, workspace=ws)
+    pb.timing_enable(64)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    pb.assign(Sd, workspace=ws, sync_stats=False)
+    e1.record()
+    torch.cuda.synchronize()
+    n, ms = pb.timing_read()
+    pb.timing_enable(0)
+    assert n >= 1
+    assert 0.0 < ms <= e0.elapsed_time(e1) * 1.01
+    res = pb.assign(Sd, workspace=ws)
+    assert 0 <= res.stats.engine_bids <= res.stats.bids
+
+
 # ---------------------------------------------------------------- permute --
 
 @pytest.mark.parametrize("dtype,d", [("bf16", 2048), ("bf16", 24), ("f32", 40), ("f32", 8)])
