@@ -119,7 +119,7 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
 
     if ((o.flags & BASE_ASSIGN_CHECK_FINITE) && !integer) {
         int bad = 0;
-        hipError_t e = base::check_scores_finite(static_cast<const float *>(S), T * E, workspace,
+        hipError_t e = base::check_scores_finite(static_cast<const float *>(S), T, E, workspace,
                                                  &bad, s);
         if (e != hipSuccess) return BASE_ERR_HIP;
         if (bad) return BASE_ERR_NONFINITE;

@@ -45,8 +45,9 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kCandLds = 4096;   // candidates of one expert staged in LDS when they fit
+constexpr int kRangeBlocks = 256;   // blocks of the score-range reduction
 constexpr int kCountTile = 256;  // tokens per block in the permutation build
-constexpr int kWideLoopRounds = 1024;  // rounds one cooperative launch may run
+constexpr int kWideLoopRounds = 1024;  // rounds one launch of the round loop may run
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -59,7 +60,7 @@ inline void debug_note(const char *what, hipError_t err) {
 
 struct Layout {
     size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
-        eck, ecs, ecn, sums, bar, total;
+        eck, ecs, ecn, sums, bar, rpart, total;
     int64_t cap, nblk;
 };
 
@@ -86,6 +87,7 @@ Layout make_layout(int64_t T, int64_t E) {
     L.ecn = off;     off += align_up((size_t)E * 4);
     L.sums = off;    off += align_up((size_t)T * 64);          // per-token score summaries
     L.bar = off;     off += align_up(512);                      // grid barrier words
+    L.rpart = off;   off += align_up((size_t)kRangeBlocks * 12);   // score-range partials
     L.total = off;
     return L;
 }
@@ -666,25 +668,86 @@ __global__ void init_kernel(SolveCtrl *ctrl, void *prices, int E, AssignParams p
 }
 
 // Score range (order-preserving images) and a non-finite count.
+// Score range (order-preserving images) and a non-finite flag: each block
+// reduces its share of S (16-byte loads) and writes one partial (max, min,
+// bad) to part[3 * block]; range_finish_kernel combines them. (One atomic
+// per wave on a single address took 99 us at T x E = 4M.)
+
 template <class M>
-__global__ void range_kernel(const typename M::score_t *S, int64_t n, SolveCtrl *ctrl) {
+__device__ inline void range_take(typename M::score_t x, uint32_t &mx, uint32_t &mn, int &bad) {
+    uint32_t o;
+    if constexpr (M::kInteger) {
+        o = (uint32_t)((int32_t)x) ^ 0x80000000u;
+    } else {
+        if (!isfinite(x)) {
+            bad = 1;
+            return;
+        }
+        o = f32_ord(x);
+    }
+    mx = o > mx ? o : mx;
+    mn = o < mn ? o : mn;
+}
+
+template <class M>
+__global__ __launch_bounds__(256) void range_kernel(const typename M::score_t *S, int64_t n,
+                                                    uint32_t *part) {
+    using score_t = typename M::score_t;
+    constexpr int kVec = 16 / sizeof(score_t);
+    __shared__ uint32_t smx[4], smn[4];
+    __shared__ int sbad[4];
     uint32_t mx = 0u, mn = 0xffffffffu;
     int bad = 0;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        uint32_t o;
-        if constexpr (M::kInteger) {
-            o = (uint32_t)((int32_t)S[i]) ^ 0x80000000u;
-        } else {
-            const float x = S[i];
-            if (!isfinite(x)) {
-                bad = 1;
-                continue;
-            }
-            o = f32_ord(x);
+    const int64_t nvec = n / kVec;   // S is 16-byte aligned
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nvec; i += stride) {
+        const uint4 v = reinterpret_cast<const uint4 *>(S)[i];
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int j = 0; j < kVec; ++j) {
+            score_t x;
+            if constexpr (sizeof(score_t) == 4) x = __uint_as_float(w[j]);
+            else x = (score_t)(int16_t)(uint16_t)(w[j >> 1] >> (16 * (j & 1)));
+            range_take<M>(x, mx, mn, bad);
         }
-        mx = o > mx ? o : mx;
-        mn = o < mn ? o : mn;
+    }
+    for (int64_t i = nvec * kVec + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        range_take<M>(S[i], mx, mn, bad);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t a = __shfl_xor(mx, off), b = __shfl_xor(mn, off);
+        mx = a > mx ? a : mx;
+        mn = b < mn ? b : mn;
+        bad |= __shfl_xor(bad, off);
+    }
+    const int wave = threadIdx.x >> 6;
+    if (lane_id() == 0) {
+        smx[wave] = mx;
+        smn[wave] = mn;
+        sbad[wave] = bad;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < (int)(blockDim.x >> 6); ++w) {
+            mx = smx[w] > mx ? smx[w] : mx;
+            mn = smn[w] < mn ? smn[w] : mn;
+            bad |= sbad[w];
+        }
+        part[3 * blockIdx.x] = mx;
+        part[3 * blockIdx.x + 1] = mn;
+        part[3 * blockIdx.x + 2] = (uint32_t)bad;
+    }
+}
+
+// Combines the range partials into the control block (one block).
+__global__ __launch_bounds__(256) void range_finish_kernel(SolveCtrl *ctrl, const uint32_t *part,
+                                                           int nparts) {
+    __shared__ uint32_t smx[4], smn[4], sbad[4];
+    uint32_t mx = 0u, mn = 0xffffffffu, bad = 0u;
+    for (int i = threadIdx.x; i < nparts; i += blockDim.x) {
+        mx = part[3 * i] > mx ? part[3 * i] : mx;
+        mn = part[3 * i + 1] < mn ? part[3 * i + 1] : mn;
+        bad |= part[3 * i + 2];
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -693,10 +756,22 @@ __global__ void range_kernel(const typename M::score_t *S, int64_t n, SolveCtrl 
         mn = b < mn ? b : mn;
         bad |= __shfl_xor(bad, off);
     }
+    const int wave = threadIdx.x >> 6;
     if (lane_id() == 0) {
-        atomicMax(&ctrl->smax_ord, mx);
-        atomicMin(&ctrl->smin_ord, mn);
-        if (bad) atomicOr(&ctrl->unconverged_experts, 1 << 30);
+        smx[wave] = mx;
+        smn[wave] = mn;
+        sbad[wave] = bad;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < (int)(blockDim.x >> 6); ++w) {
+            mx = smx[w] > mx ? smx[w] : mx;
+            mn = smn[w] < mn ? smn[w] : mn;
+            bad |= sbad[w];
+        }
+        ctrl->smax_ord = mx > ctrl->smax_ord ? mx : ctrl->smax_ord;
+        ctrl->smin_ord = mn < ctrl->smin_ord ? mn : ctrl->smin_ord;
+        if (bad) ctrl->unconverged_experts |= 1 << 30;
     }
 }
 
@@ -784,10 +859,16 @@ __global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c) {
 // ------------------------------------------------------ wide round loop --
 //
 // Rounds that still have more active tokens than the engine takes after
-// the fixed wide launches: all blocks of a cooperative launch (every block
-// resident) run them back to back with a grid barrier between the bids and
-// the updates and after the updates (the last block to finish closes the
-// round). All blocks read the same control words after a barrier and take
+// the fixed wide launches: one block per compute unit runs them back to
+// back with a grid barrier between the bids and the updates and after the
+// updates (the last block to finish closes the round). The launch follows
+// the stream's previous kernels, so on the idle device every block is
+// resident at once (each compute unit holds at least one; the host checks
+// the occupancy). A cooperative launch would guarantee that too, but costs
+// 20-40 us per launch here against about 2.5 us for a plain one, and this
+// kernel is launched once per phase slot. The barrier's wait is bounded,
+// so a block that never got scheduled ends the loop with an internal
+// error, not a hang. All blocks read the same control words after a barrier and take
 // the same exit. The launch returns at once when there is nothing to do.
 
 // Barrier k of a launch completes when bar[0] reaches k * gridDim.x. Every
@@ -2079,14 +2160,11 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
         if (sblocks > 4096) sblocks = 4096;
         hipLaunchKernelGGL((summary_kernel<M, G>), dim3(sblocks), dim3(kThreads), 0, s, c);
     }
-    // Cooperative round loop for phases that stay large: one block per
-    // compute unit when the device takes cooperative launches.
+    // Round loop for phases that stay large: one block per compute unit.
     int coop_blocks = 0;
     {
-        int dev = 0, coop = 0, cus = 0, per_cu = 0;
+        int dev = 0, cus = 0, per_cu = 0;
         if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess &&
-            coop &&
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
             hipOccupancyMaxActiveBlocksPerMultiprocessor(
                 &per_cu, reinterpret_cast<const void *>(&wide_loop_kernel<M, G>), kThreads,
@@ -2102,19 +2180,9 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
                                s, c);
             hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks), dim3(kThreads), 0, s, c);
         }
-        if (coop_blocks > 0) {
-            int max_wide = kWideLoopRounds;
-            int32_t max_rounds = p.max_rounds;
-            void *args[] = {&c, &max_wide, &max_rounds};
-            const hipError_t err = hipLaunchCooperativeKernel(
-                reinterpret_cast<const void *>(&wide_loop_kernel<M, G>), dim3(coop_blocks),
-                dim3(kThreads), args, (unsigned)pr_bytes, s);
-            if (err != hipSuccess) {
-                (void)hipGetLastError();
-                debug_note("cooperative round loop refused", err);
-                coop_blocks = 0;
-            }
-        }
+        if (coop_blocks > 0)
+            hipLaunchKernelGGL((wide_loop_kernel<M, G>), dim3(coop_blocks), dim3(kThreads), pr_bytes,
+                               s, c, kWideLoopRounds, p.max_rounds);
         if (engine) {
             hipLaunchKernelGGL(cache_build_kernel<M>, dim3(c.E), dim3(256), 0, s, c);
             hipLaunchKernelGGL(summary_prefill_kernel, dim3(256), dim3(256), 0, s,
@@ -2142,9 +2210,9 @@ hipError_t solve_mode(const void *S, const AssignParams &p, int32_t *assign, int
     Ctx<M> c = make_ctx<M>(S, p, ws);
     hipLaunchKernelGGL(init_kernel, dim3(1), dim3(256), 0, s, c.ctrl, (void *)c.prices, c.E, p);
     const int64_t n = p.T * p.E;
-    int rblocks = (int)((n + 255) / 256);
-    if (rblocks > 1024) rblocks = 1024;
-    hipLaunchKernelGGL(range_kernel<M>, dim3(rblocks), dim3(256), 0, s, c.S, n, c.ctrl);
+    uint32_t *rpart = reinterpret_cast<uint32_t *>(ws + L.rpart);
+    hipLaunchKernelGGL(range_kernel<M>, dim3(kRangeBlocks), dim3(256), 0, s, c.S, n, rpart);
+    hipLaunchKernelGGL(range_finish_kernel, dim3(1), dim3(256), 0, s, c.ctrl, rpart, kRangeBlocks);
     hipLaunchKernelGGL(eps_floor_kernel, dim3(1), dim3(1), 0, s, c.ctrl, p.integer ? 1 : 0);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
@@ -2255,14 +2323,17 @@ hipError_t read_assign_stats(const void *workspace, int64_t /*T*/, int64_t /*E*/
     return hipStreamSynchronize(stream);
 }
 
-hipError_t check_scores_finite(const float *S, int64_t n, void *workspace, int *bad,
+hipError_t check_scores_finite(const float *S, int64_t T, int64_t E, void *workspace, int *bad,
                                hipStream_t stream) {
     SolveCtrl *ctrl = static_cast<SolveCtrl *>(workspace);
+    uint32_t *rpart =
+        reinterpret_cast<uint32_t *>(static_cast<char *>(workspace) + make_layout(T, E).rpart);
     AssignParams p{};
     hipLaunchKernelGGL(init_kernel, dim3(1), dim3(256), 0, stream, ctrl, (void *)nullptr, 0, p);
-    int blocks = (int)((n + 255) / 256);
-    if (blocks > 1024) blocks = 1024;
-    hipLaunchKernelGGL(range_kernel<FloatMode>, dim3(blocks), dim3(256), 0, stream, S, n, ctrl);
+    hipLaunchKernelGGL(range_kernel<FloatMode>, dim3(kRangeBlocks), dim3(256), 0, stream, S, T * E,
+                       rpart);
+    hipLaunchKernelGGL(range_finish_kernel, dim3(1), dim3(256), 0, stream, ctrl, rpart,
+                       kRangeBlocks);
     SolveCtrl h{};
     hipError_t err = read_assign_stats(workspace, 0, 0, &h, stream);
     if (err != hipSuccess) return err;

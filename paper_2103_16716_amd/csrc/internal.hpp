@@ -67,7 +67,7 @@ hipError_t timing_enable(int32_t capacity);
 hipError_t timing_read(int64_t *launches, double *total_ms);
 
 // Scans S for NaN/Inf (synchronous). *bad is set to 1 when one is found.
-hipError_t check_scores_finite(const float *S, int64_t n, void *workspace, int *bad,
+hipError_t check_scores_finite(const float *S, int64_t T, int64_t E, void *workspace, int *bad,
                                hipStream_t stream);
 
 }  // namespace base
