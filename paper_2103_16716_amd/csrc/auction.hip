@@ -351,12 +351,208 @@ __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const type
     top2_reduce<M, G>(v1, e1, v2, s1);
 }
 
-// Bids of active tokens [i0, n) with stride `ngroups` groups. `touched`
-// (LDS, may be null) collects experts receiving their first bid this round.
+// ---------------------------------------------------------- score summaries --
+//
+// A token's summary is 64 bytes: its 8 highest scores (words 0..7, fp32 bits or
+// the raw int16 score), their experts (words 8..11, two uint16 per word), the
+// 9th highest score (word 12; the lowest value when E <= 8, where the 8 cover
+// every expert) and the number of entries (word 13). Scores never change
+// during a solve, so the summaries are built once. For prices p, every expert
+// outside a summary has S[t,e] - p[e] <= bound - min_e p[e]; a top-2 taken
+// over the summary is therefore the top-2 over all experts whenever its best
+// value exceeds that limit and its second value reaches it.
+
+constexpr int kSumWords = 16;
+
+template <class M>
+__device__ inline uint32_t score_bits(typename M::value_t v, int64_t scale) {
+    if constexpr (M::kInteger) return (uint32_t)(int32_t)(v / scale);
+    else return __float_as_uint(v);
+}
+template <class M>
+__device__ inline typename M::value_t bits_score(uint32_t w, int64_t scale) {
+    if constexpr (M::kInteger) return (typename M::value_t)(int32_t)w * scale;
+    else return __uint_as_float(w);
+}
+
+// One group of G lanes per token: 9 rounds of a group maximum (ties to the
+// lowest expert) over the lanes' 8 scores each.
+template <class M, int G>
+__global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c) {
+    using value_t = typename M::value_t;
+    const int lane = lane_id();
+    const int gl = lane & (G - 1);
+    const int per_block = kThreads / G;
+    const int n_round = ((c.T + per_block * (int)gridDim.x - 1) / (per_block * (int)gridDim.x)) *
+                        per_block * (int)gridDim.x;
+    const int e0 = 8 * gl;
+    const int take = c.E < 8 ? c.E : 8;
+    for (int t = blockIdx.x * per_block + threadIdx.x / G; t < n_round;
+         t += per_block * gridDim.x) {
+        const bool valid = t < c.T;
+        value_t sv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) sv[q] = M::lowest();
+        if (valid && e0 < c.E) load8<M>(c.S, (int64_t)t * c.E, e0, c.E, c.scale, sv);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            if (e0 + q >= c.E) sv[q] = M::lowest();
+        uint32_t *out = c.sums + (int64_t)(valid ? t : 0) * kSumWords;
+        uint32_t pairs[4] = {0, 0, 0, 0};
+        for (int r = 0; r <= take; ++r) {
+            // Lane-local best, then the group's best (lowest expert on ties).
+            value_t bv = M::lowest();
+            int be = 0x7fffffff;
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (e0 + q < c.E && sv[q] > bv) {
+                    bv = sv[q];
+                    be = e0 + q;
+                }
+#pragma unroll
+            for (int off = G / 2; off > 0; off >>= 1) {
+                const value_t ov = __shfl_xor(bv, off);
+                const int oe = __shfl_xor(be, off);
+                if (ov > bv || (ov == bv && oe < be)) {
+                    bv = ov;
+                    be = oe;
+                }
+            }
+            if (r < take) {
+                if (be >= e0 && be < e0 + 8) {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        if (e0 + q == be) sv[q] = M::lowest();
+                }
+                if (valid && gl == 0) out[r] = score_bits<M>(bv, c.scale);
+                pairs[r >> 1] |= (uint32_t)(be & 0xffff) << (16 * (r & 1));
+            } else if (valid && gl == 0) {
+                // the 9th score bounds every expert outside the summary
+                out[12] = (take < c.E) ? score_bits<M>(bv, c.scale)
+                                       : (M::kInteger ? 0x80000000u : __float_as_uint(-INFINITY));
+            }
+        }
+        if (valid && gl == 0) {
+            for (int q = 0; q < 4; ++q) out[8 + q] = pairs[q];
+            out[13] = (uint32_t)take;
+        }
+    }
+}
+
+// Reads the summary table from blocks spread over every XCD, so that the
+// L2 of whichever XCD runs the one-workgroup engine holds it. Consecutive
+// workgroups go to consecutive XCDs; with a multiple of 8 blocks, the blocks
+// of any one XCD cover the whole table whatever XCD block 0 lands on.
+__global__ __launch_bounds__(256) void summary_prefill_kernel(const uint4 *sums, int64_t n16,
+                                                              const SolveCtrl *ctrl, int cap,
+                                                              uint32_t *sink) {
+    if (ctrl->done || ctrl->all_active) return;
+    const int n = ld_relaxed(&ctrl->active_count[ctrl->cur]);
+    if (n <= 0 || n > cap) return;
+    const int per_xcd = gridDim.x / 8;
+    const int64_t chunk = (n16 + per_xcd - 1) / per_xcd;
+    const int64_t lo = (int64_t)(blockIdx.x / 8) * chunk;
+    const int64_t hi = lo + chunk < n16 ? lo + chunk : n16;
+    uint32_t acc = 0;
+    for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
+        const uint4 v = sums[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x9e3779b9u && threadIdx.x == 0) *sink = acc;   // keeps the loads
+}
+
+// Loads words of token t's summary into sw: lane gl of the group takes
+// entry gl % 8 (score, expert half-word), the bound and the entry count.
+__device__ inline void load_summary(const uint32_t *sums, int t, int gl, uint32_t (&sw)[4]) {
+    const uint32_t *sm = sums + (int64_t)t * kSumWords;
+    const int q = gl & 7;
+    sw[0] = sm[q];
+    sw[1] = sm[8 + (q >> 1)];
+    const uint2 bc = *reinterpret_cast<const uint2 *>(sm + 12);
+    sw[2] = bc.x;
+    sw[3] = bc.y;
+}
+
+// Top-2 of token t from its summary words (called by the whole wave; groups
+// with valid == false take part in the shuffles only). A token whose summary
+// cannot decide (or any token when G < 8) reads its full row instead.
+// pmin is a lower bound of every price.
+//
+// Exactness: every expert outside the summary has S[t,e] <= bound and
+// p[e] >= pmin, so its value S[t,e] - p[e] <= bound - pmin (also after fp32
+// rounding, which is monotone). A best value above that limit is therefore
+// the best over all experts (with the same lowest-index tie rule, as no
+// outside expert can tie it), and a second value reaching the limit is the
+// second best over all experts.
+template <class M, int G>
+__device__ inline void top2_summary(const Ctx<M> &c, const uint32_t (&sw)[4], int t, bool valid,
+                                    int gl, const typename M::value_t *pr,
+                                    typename M::value_t pmin, typename M::value_t &v1, int &e1,
+                                    typename M::value_t &v2, typename M::value_t &s1) {
+    using value_t = typename M::value_t;
+    const int cnt = (int)sw[3];
+    v1 = M::lowest();
+    v2 = M::lowest();
+    s1 = 0;
+    e1 = 0x7fffffff;
+    if (valid && gl < 8 && gl < cnt) {
+        const value_t sc = bits_score<M>(sw[0], c.scale);
+        int ex = (int)((sw[1] >> (16 * (gl & 1))) & 0xffff);
+        if (ex >= c.E) ex = 0;
+        v1 = sc - pr[ex];
+        e1 = ex;
+        s1 = sc;
+    }
+    top2_reduce<M, G>(v1, e1, v2, s1);
+    bool exact = cnt >= c.E;
+    if (!exact) {
+        const value_t lim = bits_score<M>(sw[2], c.scale) - pmin;
+        exact = v1 > lim && v2 >= lim;
+    }
+    if (G < 8) exact = false;   // a group narrower than 8 lanes cannot hold the 8 entries
+    const bool need = valid && !exact;
+    if (__ballot(need)) {
+        value_t w1, w2, ws1;
+        int we1;
+        top2_token<M, G>(c, t, need, pr, w1, we1, w2, ws1);
+        if (need) {
+            v1 = w1;
+            v2 = w2;
+            e1 = we1;
+            s1 = ws1;
+        }
+    }
+}
+
+// Lowest of the E prices in LDS, for the whole block (every thread calls).
+template <class M>
+__device__ inline typename M::value_t block_min_price(const typename M::value_t *pr, int E) {
+    using value_t = typename M::value_t;
+    __shared__ value_t part[16];
+    value_t m = pr[0];
+    for (int e = threadIdx.x; e < E; e += blockDim.x) m = pr[e] < m ? pr[e] : m;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const value_t o = __shfl_xor(m, off);
+        m = o < m ? o : m;
+    }
+    if (lane_id() == 0) part[threadIdx.x >> 6] = m;
+    __syncthreads();
+    m = part[0];
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) m = part[w] < m ? part[w] : m;
+    __syncthreads();
+    return m;
+}
+
+// Bids of active tokens [i0, n) with stride `ngroups` groups, from the
+// tokens' score summaries (rows only where a summary cannot decide; pmin is
+// the lowest price). `touched` (LDS, may be null) collects experts receiving
+// their first bid this round.
 template <class M, int G>
 __device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *list,
-                          typename M::value_t eps, const typename M::value_t *pr, int gid,
-                          int ngroups, int *touched, int *ntouched) {
+                          typename M::value_t eps, const typename M::value_t *pr,
+                          typename M::value_t pmin, int gid, int ngroups, int *touched,
+                          int *ntouched) {
     using value_t = typename M::value_t;
     const int gl = lane_id() & (G - 1);
     const int n_round = ((n + ngroups - 1) / ngroups) * ngroups;
@@ -369,7 +565,9 @@ __device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *li
         const bool valid = i < n && t >= 0;
         value_t v1, v2, s1;
         int e1;
-        top2_token<M, G>(c, t, valid, pr, v1, e1, v2, s1);
+        uint32_t sw[4] = {0, 0, 0, 0};
+        if (valid) load_summary(c.sums, t, gl, sw);
+        top2_summary<M, G>(c, sw, t, valid, gl, pr, pmin, v1, e1, v2, s1);
         if (valid && gl == 0) {
             if (e1 >= c.E) {   // every value non-finite: any expert, the bid overflows
                 e1 = 0;
@@ -398,6 +596,113 @@ __device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *li
             }
         }
     }
+}
+
+// Bids of the active tokens with list index in [i0, i1) (i1 - i0 <=
+// kBidTile), by one block (every thread calls): each group of G lanes bids
+// for tokens strided by the block's group count, four summaries in flight.
+// The bids collect in LDS with a per-expert rank (an LDS atomic); then one
+// global atomic per expert the block touched reserves the bucket slots, and
+// the keys are written. (One global atomic per bid serialised on the few
+// experts that most tokens prefer.)
+//   lcnt  LDS [E], zero on entry and on return
+//   lkey, lexp, lrank  LDS [kBidTile]
+constexpr int kBidTile = 128;
+constexpr int kBidRows = 4;
+
+template <class M, int G>
+__device__ void bid_block(const Ctx<M> &c, int i0, int i1, bool all_active, const int *list,
+                          typename M::value_t eps, const typename M::value_t *pr,
+                          typename M::value_t pmin, int *lcnt, uint64_t *lkey, int *lexp,
+                          int *lrank) {
+    using value_t = typename M::value_t;
+    const int tid = threadIdx.x;
+    const int gl = lane_id() & (G - 1);
+    const int per_block = (int)blockDim.x / G;
+    const int m = i1 - i0;
+    const int stride = per_block * kBidRows;
+    const int m_round = ((m + stride - 1) / stride) * stride;
+    for (int j0 = tid / G; j0 < m_round; j0 += stride) {
+        uint32_t sw[kBidRows][4];
+        int toks[kBidRows];
+#pragma unroll
+        for (int u = 0; u < kBidRows; ++u) {
+            const int j = j0 + u * per_block;
+            int t = 0;
+            if (j < m) {
+                t = all_active ? i0 + j : list[i0 + j];
+                if (t < 0 || t >= c.T) {
+                    if (gl == 0) flag_internal(c.ctrl);
+                    t = 0;
+                }
+            }
+            toks[u] = t;
+            sw[u][0] = sw[u][1] = sw[u][2] = sw[u][3] = 0;
+            if (j < m) load_summary(c.sums, t, gl, sw[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kBidRows; ++u) {
+            const int j = j0 + u * per_block;
+            const bool valid = j < m;
+            if (__ballot(valid) == 0) break;
+            const int t = toks[u];
+            value_t v1, v2, s1;
+            int e1;
+            top2_summary<M, G>(c, sw[u], t, valid, gl, pr, pmin, v1, e1, v2, s1);
+            if (valid && gl == 0) {
+                if (e1 >= c.E) {   // every value non-finite: any expert, the bid overflows
+                    e1 = 0;
+                    s1 = M::load(c.S, (int64_t)t * c.E, c.scale);
+                }
+                const value_t bid = (c.E > 1) ? (value_t)((s1 - v2) + eps) : (value_t)(s1 + eps);
+                int overflow = 0;
+                lkey[j] = M::make_key(bid, t, &overflow);
+                if (overflow) c.ctrl->overflow = 1;
+                lexp[j] = e1;
+                lrank[j] = atomicAdd(&lcnt[e1], 1);
+            }
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < c.E; e += blockDim.x) {
+        const int k = lcnt[e];
+        if (k > 0) lcnt[e] = atomicAdd(&c.bcount[e], k);   // now the base of the block's slots
+    }
+    __syncthreads();
+    for (int j = tid; j < m; j += blockDim.x) {
+        const int e = lexp[j];
+        const int pos = lcnt[e] + lrank[j];
+        if (pos < c.cap) {
+            c.bucket[(int64_t)e * c.cap + pos] = lkey[j];
+        } else {
+            const int q = atomicAdd(c.ovf_count, 1);
+            if (q < c.T) {
+                c.ovf_key[q] = lkey[j];
+                c.ovf_exp[q] = e;
+            } else {
+                flag_internal(c.ctrl);
+            }
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < c.E; e += blockDim.x) lcnt[e] = 0;
+    __syncthreads();
+}
+
+// Dynamic LDS of a kernel that bids with bid_block: prices, then lcnt [E],
+// then lkey / lexp / lrank [kBidTile].
+struct BidSmem {
+    size_t lcnt, lkey, lexp, lrank, total;
+};
+__host__ __device__ inline BidSmem bid_smem(int E, int value_bytes) {
+    BidSmem L{};
+    size_t off = ((size_t)E * value_bytes + 15) & ~size_t(15);
+    L.lcnt = off;  off = (off + (size_t)E * 4 + 15) & ~size_t(15);
+    L.lkey = off;  off += (size_t)kBidTile * 8;
+    L.lexp = off;  off += (size_t)kBidTile * 4;
+    L.lrank = off; off += (size_t)kBidTile * 4;
+    L.total = off;
+    return L;
 }
 
 // ----------------------------------------------------------------- update --
@@ -821,13 +1126,22 @@ __global__ __launch_bounds__(kThreads) void bid_wide_kernel(Ctx<M> c) {
     const int n = all ? c.T : ld_relaxed(&ctrl->active_count[cur]);
     if (n == 0) return;
     if (!all && n <= c.engine_cap) return;   // left to the tail engine
-    for (int e = threadIdx.x; e < c.E; e += blockDim.x) pr[e] = c.prices[e];
+    const int i0 = blockIdx.x * kBidTile;
+    if (i0 >= n) return;
+    const BidSmem B = bid_smem(c.E, (int)sizeof(value_t));
+    int *lcnt = reinterpret_cast<int *>(smem_raw + B.lcnt);
+    for (int e = threadIdx.x; e < c.E; e += blockDim.x) {
+        pr[e] = c.prices[e];
+        lcnt[e] = 0;
+    }
     __syncthreads();
     const value_t eps = (value_t)ctrl->eps;
-    const int per_block = kThreads / G;
-    const int gid = blockIdx.x * per_block + threadIdx.x / G;
-    bid_range<M, G>(c, n, all, c.active + (int64_t)cur * c.T, eps, pr, gid,
-                    gridDim.x * per_block, nullptr, nullptr);
+    const value_t pmin = block_min_price<M>(pr, c.E);
+    bid_block<M, G>(c, i0, i0 + kBidTile < n ? i0 + kBidTile : n, all,
+                    c.active + (int64_t)cur * c.T, eps, pr, pmin, lcnt,
+                    reinterpret_cast<uint64_t *>(smem_raw + B.lkey),
+                    reinterpret_cast<int *>(smem_raw + B.lexp),
+                    reinterpret_cast<int *>(smem_raw + B.lrank));
 }
 
 template <class M>
@@ -915,6 +1229,9 @@ __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c, int max_w
     __shared__ int st_go, st_cur, st_all, st_n, last;
     SolveCtrl *ctrl = c.ctrl;
     const int tid = threadIdx.x;
+    const BidSmem B = bid_smem(c.E, (int)sizeof(value_t));
+    int *lcnt = reinterpret_cast<int *>(smem_raw + B.lcnt);
+    for (int e = tid; e < c.E; e += kThreads) lcnt[e] = 0;
     uint64_t target = 0;
     for (int r = 0; r < max_wide; ++r) {
         if (tid == 0) {
@@ -933,9 +1250,13 @@ __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c, int max_w
         for (int e = tid; e < c.E; e += kThreads) pr[e] = c.prices[e];
         __syncthreads();
         const value_t eps = (value_t)ctrl->eps;
-        const int per_block = kThreads / G;
-        bid_range<M, G>(c, st_n, st_all != 0, c.active + (int64_t)st_cur * c.T, eps, pr,
-                        blockIdx.x * per_block + tid / G, gridDim.x * per_block, nullptr, nullptr);
+        const value_t pmin = block_min_price<M>(pr, c.E);
+        for (int i0 = blockIdx.x * kBidTile; i0 < st_n; i0 += gridDim.x * kBidTile)
+            bid_block<M, G>(c, i0, i0 + kBidTile < st_n ? i0 + kBidTile : st_n, st_all != 0,
+                            c.active + (int64_t)st_cur * c.T, eps, pr, pmin, lcnt,
+                            reinterpret_cast<uint64_t *>(smem_raw + B.lkey),
+                            reinterpret_cast<int *>(smem_raw + B.lexp),
+                            reinterpret_cast<int *>(smem_raw + B.lrank));
         target += gridDim.x;
         if (!grid_barrier(c.bar, target, ctrl)) return;
         const int novf = min(ld_relaxed(c.ovf_count), c.T);
@@ -1010,7 +1331,8 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
         for (int e = tid; e < c.E; e += blockDim.x) pr[e] = c.prices[e];
         __syncthreads();
         const value_t eps = (value_t)ctrl->eps;
-        bid_range<M, G>(c, st_n, st_all != 0, c.active + (int64_t)st_cur * c.T, eps, pr,
+        const value_t pmin = block_min_price<M>(pr, c.E);
+        bid_range<M, G>(c, st_n, st_all != 0, c.active + (int64_t)st_cur * c.T, eps, pr, pmin,
                         tid / G, kThreads / G, touched, &ntouched);
         __threadfence_block();
         __syncthreads();
@@ -1022,176 +1344,6 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p
         if (tid == 0) end_round(ctrl, c.T);
         __threadfence_block();
         __syncthreads();
-    }
-}
-
-// ---------------------------------------------------------- score summaries --
-//
-// A token's summary is 64 bytes: its 8 highest scores (words 0..7, fp32 bits or
-// the raw int16 score), their experts (words 8..11, two uint16 per word), the
-// 9th highest score (word 12; the lowest value when E <= 8, where the 8 cover
-// every expert) and the number of entries (word 13). Scores never change
-// during a solve, so the summaries are built once. For prices p, every expert
-// outside a summary has S[t,e] - p[e] <= bound - min_e p[e]; a top-2 taken
-// over the summary is therefore the top-2 over all experts whenever its best
-// value exceeds that limit and its second value reaches it.
-
-constexpr int kSumWords = 16;
-
-template <class M>
-__device__ inline uint32_t score_bits(typename M::value_t v, int64_t scale) {
-    if constexpr (M::kInteger) return (uint32_t)(int32_t)(v / scale);
-    else return __float_as_uint(v);
-}
-template <class M>
-__device__ inline typename M::value_t bits_score(uint32_t w, int64_t scale) {
-    if constexpr (M::kInteger) return (typename M::value_t)(int32_t)w * scale;
-    else return __uint_as_float(w);
-}
-
-// One group of G lanes per token: 9 rounds of a group maximum (ties to the
-// lowest expert) over the lanes' 8 scores each.
-template <class M, int G>
-__global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c) {
-    using value_t = typename M::value_t;
-    const int lane = lane_id();
-    const int gl = lane & (G - 1);
-    const int per_block = kThreads / G;
-    const int n_round = ((c.T + per_block * (int)gridDim.x - 1) / (per_block * (int)gridDim.x)) *
-                        per_block * (int)gridDim.x;
-    const int e0 = 8 * gl;
-    const int take = c.E < 8 ? c.E : 8;
-    for (int t = blockIdx.x * per_block + threadIdx.x / G; t < n_round;
-         t += per_block * gridDim.x) {
-        const bool valid = t < c.T;
-        value_t sv[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) sv[q] = M::lowest();
-        if (valid && e0 < c.E) load8<M>(c.S, (int64_t)t * c.E, e0, c.E, c.scale, sv);
-#pragma unroll
-        for (int q = 0; q < 8; ++q)
-            if (e0 + q >= c.E) sv[q] = M::lowest();
-        uint32_t *out = c.sums + (int64_t)(valid ? t : 0) * kSumWords;
-        uint32_t pairs[4] = {0, 0, 0, 0};
-        for (int r = 0; r <= take; ++r) {
-            // Lane-local best, then the group's best (lowest expert on ties).
-            value_t bv = M::lowest();
-            int be = 0x7fffffff;
-#pragma unroll
-            for (int q = 0; q < 8; ++q)
-                if (e0 + q < c.E && sv[q] > bv) {
-                    bv = sv[q];
-                    be = e0 + q;
-                }
-#pragma unroll
-            for (int off = G / 2; off > 0; off >>= 1) {
-                const value_t ov = __shfl_xor(bv, off);
-                const int oe = __shfl_xor(be, off);
-                if (ov > bv || (ov == bv && oe < be)) {
-                    bv = ov;
-                    be = oe;
-                }
-            }
-            if (r < take) {
-                if (be >= e0 && be < e0 + 8) {
-#pragma unroll
-                    for (int q = 0; q < 8; ++q)
-                        if (e0 + q == be) sv[q] = M::lowest();
-                }
-                if (valid && gl == 0) out[r] = score_bits<M>(bv, c.scale);
-                pairs[r >> 1] |= (uint32_t)(be & 0xffff) << (16 * (r & 1));
-            } else if (valid && gl == 0) {
-                // the 9th score bounds every expert outside the summary
-                out[12] = (take < c.E) ? score_bits<M>(bv, c.scale)
-                                       : (M::kInteger ? 0x80000000u : __float_as_uint(-INFINITY));
-            }
-        }
-        if (valid && gl == 0) {
-            for (int q = 0; q < 4; ++q) out[8 + q] = pairs[q];
-            out[13] = (uint32_t)take;
-        }
-    }
-}
-
-// Reads the summary table from blocks spread over every XCD, so that the
-// L2 of whichever XCD runs the one-workgroup engine holds it. Consecutive
-// workgroups go to consecutive XCDs; with a multiple of 8 blocks, the blocks
-// of any one XCD cover the whole table whatever XCD block 0 lands on.
-__global__ __launch_bounds__(256) void summary_prefill_kernel(const uint4 *sums, int64_t n16,
-                                                              const SolveCtrl *ctrl, int cap,
-                                                              uint32_t *sink) {
-    if (ctrl->done || ctrl->all_active) return;
-    const int n = ld_relaxed(&ctrl->active_count[ctrl->cur]);
-    if (n <= 0 || n > cap) return;
-    const int per_xcd = gridDim.x / 8;
-    const int64_t chunk = (n16 + per_xcd - 1) / per_xcd;
-    const int64_t lo = (int64_t)(blockIdx.x / 8) * chunk;
-    const int64_t hi = lo + chunk < n16 ? lo + chunk : n16;
-    uint32_t acc = 0;
-    for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
-        const uint4 v = sums[i];
-        acc ^= v.x ^ v.y ^ v.z ^ v.w;
-    }
-    if (acc == 0x9e3779b9u && threadIdx.x == 0) *sink = acc;   // keeps the loads
-}
-
-// Loads words of token t's summary into sw: lane gl of the group takes
-// entry gl % 8 (score, expert half-word), the bound and the entry count.
-__device__ inline void load_summary(const uint32_t *sums, int t, int gl, uint32_t (&sw)[4]) {
-    const uint32_t *sm = sums + (int64_t)t * kSumWords;
-    const int q = gl & 7;
-    sw[0] = sm[q];
-    sw[1] = sm[8 + (q >> 1)];
-    const uint2 bc = *reinterpret_cast<const uint2 *>(sm + 12);
-    sw[2] = bc.x;
-    sw[3] = bc.y;
-}
-
-// Top-2 of token t from its summary words (called by the whole wave; groups
-// with valid == false take part in the shuffles only). A token whose summary
-// cannot decide (or any token when G < 8) reads its full row instead.
-// pmin is a lower bound of every price.
-template <class M, int G>
-__device__ inline void top2_summary(const Ctx<M> &c, const uint32_t (&sw)[4], int t, bool valid,
-                                    int gl, const typename M::value_t *pr,
-                                    typename M::value_t pmin, typename M::value_t &v1, int &e1,
-                                    typename M::value_t &v2, typename M::value_t &s1) {
-    using value_t = typename M::value_t;
-    const int cnt = (int)sw[3];
-    v1 = M::lowest();
-    v2 = M::lowest();
-    s1 = 0;
-    e1 = 0x7fffffff;
-    if (valid && gl < 8 && gl < cnt) {
-        const value_t sc = bits_score<M>(sw[0], c.scale);
-        int ex = (int)((sw[1] >> (16 * (gl & 1))) & 0xffff);
-        if (ex >= c.E) ex = 0;
-        v1 = sc - pr[ex];
-        e1 = ex;
-        s1 = sc;
-    }
-    top2_reduce<M, G>(v1, e1, v2, s1);
-    bool exact = cnt >= c.E;
-    if (!exact) {
-        const value_t lim = bits_score<M>(sw[2], c.scale) - pmin;
-        exact = v1 > lim && v2 >= lim;
-    }
-    if (G < 8) exact = false;   // a group narrower than 8 lanes cannot hold the 8 entries
-    const bool need = valid && !exact;
-    if (__ballot(need)) {
-        value_t row[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) row[j] = 0;
-        if (need && 8 * gl < c.E) load8<M>(c.S, (int64_t)t * c.E, 8 * gl, c.E, c.scale, row);
-        value_t w1, w2, ws1;
-        int we1;
-        top2_row<M, G>(row, 8 * gl, c.E, need, pr, w1, we1, w2, ws1);
-        if (need) {
-            v1 = w1;
-            v2 = w2;
-            e1 = we1;
-            s1 = ws1;
-        }
     }
 }
 
@@ -2152,10 +2304,10 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     }
     const int wide_rounds = engine ? 3 : 2;
     const int per_block = kThreads / G;
-    int bid_blocks = (int)((c.T + per_block - 1) / per_block);
-    if (bid_blocks > 4096) bid_blocks = 4096;
+    const int bid_blocks = (int)((c.T + kBidTile - 1) / kBidTile);   // one tile of the list each
+    const size_t bid_bytes = bid_smem(c.E, (int)sizeof(value_t)).total;
     int upd_blocks = c.E < 2048 ? c.E : 2048;
-    if (engine) {
+    {
         int sblocks = (int)((c.T + per_block - 1) / per_block);
         if (sblocks > 4096) sblocks = 4096;
         hipLaunchKernelGGL((summary_kernel<M, G>), dim3(sblocks), dim3(kThreads), 0, s, c);
@@ -2168,7 +2320,7 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
             hipOccupancyMaxActiveBlocksPerMultiprocessor(
                 &per_cu, reinterpret_cast<const void *>(&wide_loop_kernel<M, G>), kThreads,
-                pr_bytes) == hipSuccess &&
+                bid_bytes) == hipSuccess &&
             per_cu > 0 && cus > 0)
             coop_blocks = cus;
         (void)hipGetLastError();
@@ -2176,12 +2328,12 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     for (int slot = 0; slot < slots; ++slot) {
         hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1), dim3(1024), 0, s, c, p);
         for (int r = 0; r < wide_rounds; ++r) {
-            hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks), dim3(kThreads), pr_bytes,
+            hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks), dim3(kThreads), bid_bytes,
                                s, c);
             hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks), dim3(kThreads), 0, s, c);
         }
         if (coop_blocks > 0)
-            hipLaunchKernelGGL((wide_loop_kernel<M, G>), dim3(coop_blocks), dim3(kThreads), pr_bytes,
+            hipLaunchKernelGGL((wide_loop_kernel<M, G>), dim3(coop_blocks), dim3(kThreads), bid_bytes,
                                s, c, kWideLoopRounds, p.max_rounds);
         if (engine) {
             hipLaunchKernelGGL(cache_build_kernel<M>, dim3(c.E), dim3(256), 0, s, c);
