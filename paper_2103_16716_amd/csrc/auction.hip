@@ -1475,10 +1475,19 @@ __device__ inline void er_flush(const Ctx<M> &c, uint64_t *hold, ExpertRegs<M> &
     r.np = 0;
 }
 
-// Records hold[slot] = key (stored by er_flush).
+// Records hold[slot] = key (stored by er_flush). A slot written again
+// before the flush keeps a single pending entry with the latest key: the
+// lanes of one store instruction reach memory in no defined order, so two
+// entries for one slot could leave the older key in the table (its token
+// then held twice, the newer one lost).
 template <class M>
 __device__ inline void er_write(const Ctx<M> &c, uint64_t *hold, ExpertRegs<M> &r, int slot,
                                 uint64_t key) {
+    const uint64_t same = __ballot(lane_id() < r.np && r.pslot == slot);
+    if (same != 0) {
+        if (lane_id() == __ffsll((long long)same) - 1) r.pkey = key;
+        return;
+    }
     if (r.np == 64) er_flush<M>(c, hold, r);
     if (lane_id() == r.np) {
         r.pslot = slot;

@@ -260,6 +260,26 @@ def test_assign_phases_that_stay_large(name, seed, div, factor):
     check_assignment(S64, res, EPS_FINAL, opt=(a_opt, obj_opt))
 
 
+@pytest.mark.parametrize("div", [8.0, 64.0, 512.0])
+def test_assign_single_phase_large_epsilon(div):
+    """One epsilon phase at a coarse epsilon (eps_initial = eps_final): bids
+    carry large margins, so within one round an expert's lowest holder is
+    often replaced, and the replacing key replaced again. Every token must be
+    held exactly once at the end (a lost holder-table store shows up as an
+    unbalanced assignment), within T * eps of the optimum."""
+    inp = wl.make_inputs("t8192-e64-d1024")
+    H, W = inputs_on_device(inp)
+    S = pb.affinity(H, W)
+    torch.cuda.synchronize()
+    Sh = host(S)
+    eps = float(Sh.max() - Sh.min()) / div
+    res = pb.assign(S, eps_initial=eps, eps_final=eps)
+    assert res.stats.phases == 1
+    S64 = Sh.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    check_assignment(S64, res, eps, opt=(a_opt, obj_opt))
+
+
 def test_engine_launch_timing():
     """The measurement hook brackets each engine launch with events on the
     call's stream: one record per phase slot, each within the whole call."""
