@@ -571,7 +571,7 @@ __device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *li
         if (valid && gl == 0) {
             if (e1 >= c.E) {   // every value non-finite: any expert, the bid overflows
                 e1 = 0;
-                s1 = M::load(c.S, (int64_t)t * c.E, c.scale);
+                s1 = 0;   // with v2 = -inf the bid is +inf: overflow is flagged
             }
             const value_t bid = (c.E > 1) ? (value_t)((s1 - v2) + eps) : (value_t)(s1 + eps);
             int overflow = 0;
@@ -652,7 +652,7 @@ __device__ void bid_block(const Ctx<M> &c, int i0, int i1, bool all_active, cons
             if (valid && gl == 0) {
                 if (e1 >= c.E) {   // every value non-finite: any expert, the bid overflows
                     e1 = 0;
-                    s1 = M::load(c.S, (int64_t)t * c.E, c.scale);
+                    s1 = 0;   // with v2 = -inf the bid is +inf: overflow is flagged
                 }
                 const value_t bid = (c.E > 1) ? (value_t)((s1 - v2) + eps) : (value_t)(s1 + eps);
                 int overflow = 0;
@@ -1580,10 +1580,14 @@ template <class M>
 __device__ inline void er_load(const Eng<M> &s, int e, ExpertRegs<M> &r) {
     const int lane = lane_id();
     const int K = s.K;
+    // The list words are read for every lane below K (no wait for cn) and
+    // masked afterwards.
+    const uint64_t kv = lane < K ? s.ck[e * K + lane] : ~0ull;
+    const int sv = lane < K ? (int)s.cs[e * K + lane] : 0;
     r.cn = s.cn[e];
     r.cnt = s.cnt[e];
-    r.key = lane < r.cn ? s.ck[e * K + lane] : ~0ull;
-    r.slot = lane < r.cn ? (int)s.cs[e * K + lane] : 0;
+    r.key = lane < r.cn ? kv : ~0ull;
+    r.slot = lane < r.cn ? sv : 0;
     r.price = s.pr[e];
     r.np = 0;
     r.pkey = 0;
@@ -1729,6 +1733,59 @@ __device__ inline void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// One bid b for expert e in the common case of the solo rounds: e is full
+// and its list holds at least two keys. The list words, count and length
+// are read in one LDS round trip; a refused bid changes nothing (the price
+// already is the lowest held bid); an accepted one replaces the head in the
+// list (one ballot and one DPP shift), stores b into the head's slot of the
+// holder table and sets the price from the new head. Returns the leaving
+// token, or -2 when the case does not apply (nothing changed then). The
+// holder-table store is left to the caller (*store_slot >= 0: store b
+// there), so that loads the caller issues first do not wait behind it.
+template <class M>
+__device__ __attribute__((always_inline)) inline int solo_replace_head(const Ctx<M> &c,
+                                                                       const Eng<M> &s, int e,
+                                                                       uint64_t b,
+                                                                       int *store_slot) {
+    *store_slot = -1;
+    const int lane = lane_id();
+    const int K = s.K;
+    const uint64_t kv = lane < K ? s.ck[e * K + lane] : ~0ull;
+    const int sv = lane < K ? (int)s.cs[e * K + lane] : 0;
+    const int cn = s.cn[e];
+    const int cnt = s.cnt[e];
+    if (cnt != c.C || cn < 2) return -2;
+    const uint64_t key = lane < cn ? kv : ~0ull;
+    const uint64_t head = rl64(key, 0);
+    if (b <= head) return key_token(b);
+    const int slot0 = rl32(sv, 0);
+    const bool complete = cn == cnt;
+    const int pos = __popcll(__ballot(lane >= 1 && lane < cn && key < b));
+    const bool keep = pos < cn - 1 || complete;
+    const uint64_t knext = down1_u64(key);
+    const int snext = down1_i32(sv);
+    uint64_t nk = key;
+    int ns = sv;
+    if (lane < pos) {
+        nk = knext;
+        ns = snext;
+    } else if (lane == pos) {
+        nk = keep ? b : ~0ull;
+        ns = keep ? slot0 : 0;
+    }
+    if (lane <= pos && lane < K) {
+        s.ck[e * K + lane] = nk;
+        s.cs[e * K + lane] = (uint16_t)ns;
+    }
+    const uint64_t nhead = rl64(nk, 0);
+    if (lane == 0) {
+        if (!keep) s.cn[e] = cn - 1;
+        s.pr[e] = M::key_bid(nhead);
+    }
+    *store_slot = slot0;
+    return key_token(head);
+}
+
 // Tokens one wave bids for at once: one group of G lanes each, at most 8.
 template <int G>
 constexpr int solo_tokens() { return (64 / G) < 8 ? (64 / G) : 8; }
@@ -1753,15 +1810,30 @@ __device__ __attribute__((always_inline)) void engine_solo(const Ctx<M> &c, cons
     unsigned long long bids = 0;
     int tokv = lane < n ? act[lane] : 0;   // lane k holds active token k
     int overflow = 0;
+    // Holder-table stores of the head replacements wait in a register queue
+    // (lane j: address and key of store j; one entry per address) and go out
+    // 64 at a time, before any update that reads the tables, and at the end:
+    // a store in the round's path would make the next round's first load
+    // wait for it.
+    uint64_t *q_addr = nullptr;
+    uint64_t q_key = 0;
+    int qn = 0;
+    auto q_flush = [&]() {
+        if (lane < qn) *q_addr = q_key;
+        qn = 0;
+    };
+    // Group g bids for token g; its summary for the coming round is loaded
+    // as soon as the token is known (for the next round: right after the
+    // update that makes it leave, ahead of that update's table stores).
+    int t = 0;
+    for (int k = 0; k < n; ++k) {
+        const int tk = rl32(tokv, k);
+        if (g == k) t = tk;
+    }
+    uint32_t sw[4] = {0, 0, 0, 0};
+    if (g < n) load_summary(c.sums, t, gl, sw);
     while (n > 0 && rounds < max_rounds_left) {
-        int t = 0;
-        for (int k = 0; k < n; ++k) {
-            const int tk = rl32(tokv, k);
-            if (g == k) t = tk;
-        }
         const bool valid = g < n;
-        uint32_t sw[4] = {0, 0, 0, 0};
-        if (valid) load_summary(c.sums, t, gl, sw);
         value_t v1, v2, s1;
         int e1;
         top2_summary<M, G>(c, sw, t, valid, gl, s.pr, pmin, v1, e1, v2, s1);
@@ -1770,32 +1842,66 @@ __device__ __attribute__((always_inline)) void engine_solo(const Ctx<M> &c, cons
         if (valid && gl == 0) {
             if (e1 >= c.E) {
                 e1 = 0;
-                s1 = M::load(c.S, (int64_t)t * c.E, c.scale);
+                s1 = 0;   // with v2 = -inf the bid is +inf: overflow is flagged
             }
             const value_t bid = (value_t)((s1 - v2) + eps);
             key = M::make_key(bid, t, &overflow);
             ex = e1;
         }
-        int nn = 0, nxt_tok = 0;
+        int nn = 0, nxt_tok = 0, t_next = 0;
+        uint32_t sw_next[4] = {0, 0, 0, 0};
         for (int k = 0; k < n; ++k) {
             const int e = rl32(ex, k * G);
-            uint64_t *hold = expert_holders<M>(c, s, e);
-            ExpertRegs<M> r;
-            er_load<M>(s, e, r);
-            const int out = er_bid<M>(c, hold, s.K, r, rl64(key, k * G), s.scr_key, s.scr_slot);
-            er_store<M>(c, s, e, hold, r);
-            wave_sync();
+            const uint64_t b = rl64(key, k * G);
+            int store_slot = -1;
+            int out = solo_replace_head<M>(c, s, e, b, &store_slot);
+            if (out == -2) {
+                q_flush();
+                uint64_t *hold = expert_holders<M>(c, s, e);
+                ExpertRegs<M> r;
+                er_load<M>(s, e, r);
+                out = er_bid<M>(c, hold, s.K, r, b, s.scr_key, s.scr_slot);
+                er_store<M>(c, s, e, hold, r);
+            }
+            if (out >= c.T) {
+                flag_internal(c.ctrl);
+                out = 0;
+            }
             if (out >= 0) {
-                if (out >= c.T) flag_internal(c.ctrl);
-                if (lane == nn) nxt_tok = out < c.T ? out : 0;
+                if (lane == nn) nxt_tok = out;
+                if (g == nn) {
+                    t_next = out;
+                    load_summary(c.sums, out, gl, sw_next);
+                }
                 ++nn;
             }
+            if (store_slot >= c.C) {
+                flag_internal(c.ctrl);
+            } else if (store_slot >= 0) {
+                uint64_t *addr = expert_holders<M>(c, s, e) + store_slot;
+                const uint64_t same = __ballot(lane < qn && q_addr == addr);
+                if (same != 0) {
+                    if (lane == __ffsll((long long)same) - 1) q_key = b;
+                } else {
+                    if (qn == 64) q_flush();
+                    if (lane == qn) {
+                        q_addr = addr;
+                        q_key = b;
+                    }
+                    ++qn;
+                }
+            }
+            wave_sync();
         }
         rounds += 1;
         bids += (unsigned long long)n;
         tokv = nxt_tok;
         n = nn;
+        t = t_next;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) sw[q] = sw_next[q];
     }
+    q_flush();
     if (lane < n) act[lane] = tokv;
     if (__ballot(overflow != 0) && lane == 0) c.ctrl->overflow = 1;
     if (lane == 0) {
@@ -2002,7 +2108,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
             if (valid && gl == 0) {
                 if (e1 >= c.E) {
                     e1 = 0;
-                    s1 = M::load(c.S, (int64_t)t * c.E, c.scale);
+                    s1 = 0;   // with v2 = -inf the bid is +inf: overflow is flagged
                 }
                 const value_t bid = (value_t)((s1 - v2) + eps);
                 int overflow = 0;
