@@ -169,6 +169,42 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
                 size_t workspace_bytes, base_assign_stats *stats, void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* base_assign_batched: many independent balanced assignments in one call   */
+/* ------------------------------------------------------------------------ */
+/*
+ * Sec. 3.2.1 (Sharding): the assignment over all workers is split into
+ * independent problems, one per worker, each of T tokens and E experts (the
+ * paper's runs: T = 2 x 1024, E = 128, Sec. 4.1). This call solves B such
+ * problems together on one device, every problem exactly as base_assign
+ * would (same algorithm, same options, bit-identical results); the
+ * single-workgroup parts of the solve run for all problems at once.
+ * Sec. 3.2.1 (Shuffling) routes tokens to workers at random before the
+ * solve: that is base_permute of the B * T rows with the caller's random
+ * permutation, before the affinity.
+ *
+ *   S          [device] B x T x E scores, problem after problem (T * E * sizeof
+ *              must be a multiple of 16 bytes when B > 1)
+ *   assign     [device] int32 [B][T]: expert of token t of problem b
+ *   perm       [device] int32 [B][T]: problem b's sort vector (token indices
+ *              within the problem)
+ *   prices     [device] may be NULL: [B][E] float32 (int64 in integer mode)
+ *   workspace  [device] base_assign_batched_workspace_size(B, T, E) bytes,
+ *              256-byte aligned
+ *   stats      [host] aggregate over the problems: phases and rounds the
+ *              largest, bids and engine_bids summed, eps_final the largest,
+ *              fell_back if any problem fell back, converged if all did
+ *   1 <= B <= 65535, B * T < 2^31; other arguments as for base_assign.
+ * Errors: as base_assign; a status from SYNC_STATS reports the first kind of
+ * failure found in any problem.
+ */
+size_t base_assign_batched_workspace_size(int64_t B, int64_t T, int64_t E);
+
+int base_assign_batched(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
+                        const base_assign_opts *opts, int32_t *assign, int32_t *perm,
+                        void *prices, void *workspace, size_t workspace_bytes,
+                        base_assign_stats *stats, void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* base_permute: route rows into expert-contiguous order, or back            */
 /* ------------------------------------------------------------------------ */
 /*

@@ -42,7 +42,8 @@ BASE_ASSIGN_CHECK_FINITE = 4
 
 # Every symbol include/base.h declares.
 EXPORTED = ("base_status_string", "base_affinity", "base_assign_workspace_size", "base_assign",
-            "base_permute", "base_timing_enable", "base_timing_read")
+            "base_assign_batched_workspace_size", "base_assign_batched", "base_permute",
+            "base_timing_enable", "base_timing_read")
 
 
 class AssignOpts(ctypes.Structure):
@@ -85,6 +86,12 @@ def lib() -> ctypes.CDLL:
         L.base_assign.argtypes = [vp, i32, i64, i64, ctypes.POINTER(AssignOpts), vp, vp, vp, vp,
                                   ctypes.c_size_t, ctypes.POINTER(AssignStats), vp]
         L.base_assign.restype = i32
+        L.base_assign_batched_workspace_size.argtypes = [i64, i64, i64]
+        L.base_assign_batched_workspace_size.restype = ctypes.c_size_t
+        L.base_assign_batched.argtypes = [vp, i32, i64, i64, i64, ctypes.POINTER(AssignOpts), vp,
+                                          vp, vp, vp, ctypes.c_size_t,
+                                          ctypes.POINTER(AssignStats), vp]
+        L.base_assign_batched.restype = i32
         L.base_permute.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
         L.base_permute.restype = i32
         L.base_timing_enable.argtypes = [ctypes.c_int32]
@@ -193,6 +200,43 @@ def assign(S, *, eps_final: float = 0.0, eps_initial: float = 0.0, eps_factor: f
     return AssignResult(out_assign, out_perm, out_prices, stats if sync_stats else None)
 
 
+def assign_batched_workspace_size(B: int, T: int, E: int) -> int:
+    return int(lib().base_assign_batched_workspace_size(B, T, E))
+
+
+def assign_batched(S, *, eps_final: float = 0.0, eps_initial: float = 0.0,
+                   eps_factor: float = 0.0, max_rounds: int = 0, flags: int = 0,
+                   sync_stats: bool = True, workspace=None, out_assign=None, out_perm=None,
+                   out_prices=None, stream=None) -> AssignResult:
+    """B independent balanced assignments of Eq. 2, S [B, T, E]
+    (base_assign_batched); outputs [B, T] and prices [B, E]. Statistics are
+    aggregated over the problems."""
+    torch = _torch()
+    _need_device(S)
+    B, T, E = S.shape
+    dev = S.device
+    integer = S.dtype == torch.int16
+    if out_assign is None:
+        out_assign = torch.empty((B, T), dtype=torch.int32, device=dev)
+    if out_perm is None:
+        out_perm = torch.empty((B, T), dtype=torch.int32, device=dev)
+    if out_prices is None:
+        out_prices = torch.empty((B, E), dtype=torch.int64 if integer else torch.float32,
+                                 device=dev)
+    ws_bytes = assign_batched_workspace_size(B, T, E)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    opts = AssignOpts(eps_final, eps_initial, eps_factor, max_rounds,
+                      flags | (BASE_ASSIGN_SYNC_STATS if sync_stats else 0))
+    stats = AssignStats()
+    _check(lib().base_assign_batched(S.data_ptr(), _dtype_code(S), B, T, E, ctypes.byref(opts),
+                                     out_assign.data_ptr(), out_perm.data_ptr(),
+                                     out_prices.data_ptr(), workspace.data_ptr(),
+                                     workspace.numel(), ctypes.byref(stats), _stream_ptr(stream)),
+           "base_assign_batched")
+    return AssignResult(out_assign, out_perm, out_prices, stats if sync_stats else None)
+
+
 def permute(x, perm, inverse: bool = False, out=None, stream=None):
     """Gather rows into expert order (out[k] = x[perm[k]]) or, with inverse,
     scatter them back (out[perm[k]] = x[k]) (base_permute)."""
@@ -222,6 +266,7 @@ def timing_read() -> tuple[int, float]:
     return int(n.value), float(ms.value)
 
 
-__all__ = ["affinity", "assign", "permute", "assign_workspace_size", "timing_enable",
+__all__ = ["affinity", "assign", "assign_batched", "permute", "assign_workspace_size",
+           "assign_batched_workspace_size", "timing_enable",
            "timing_read", "AssignResult", "AssignOpts", "AssignStats", "BaseError", "lib",
            "status_string", "EXPORTED"]

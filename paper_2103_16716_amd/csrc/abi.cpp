@@ -2,6 +2,7 @@
 // HIP launchers. Nothing is enqueued when validation fails.
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include "base.h"
 #include "internal.hpp"
@@ -19,6 +20,7 @@ constexpr int64_t kMaxExperts = 2048;                 // per-expert tables stage
 // fewer for ranges up to 8 * 24^4 * eps_final (about 265 at 1e-4).
 constexpr double kDefaultEpsFactor = 24.0;
 constexpr int64_t kMaxDim = (int64_t)1 << 30;
+constexpr int64_t kMaxBatch = 65535;   // problems per batched call (grid y dimension)
 
 bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
@@ -65,17 +67,26 @@ size_t base_assign_workspace_size(int64_t T, int64_t E) {
     return base::assign_workspace_size(T, E);
 }
 
-int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_assign_opts *opts,
-                int32_t *assign, int32_t *perm, void *prices, void *workspace,
-                size_t workspace_bytes, base_assign_stats *stats, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// base_assign and base_assign_batched: B independent problems, each a T x E
+// score matrix, solved by one sequence of launches (problem b in
+// blockIdx.y of every solver kernel).
+int assign_impl(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
+                const base_assign_opts *opts, int32_t *assign, int32_t *perm, void *prices,
+                void *workspace, size_t workspace_bytes, base_assign_stats *stats, void *stream) {
     if (S == nullptr || assign == nullptr || perm == nullptr) return BASE_ERR_INVALID_ARG;
-    if (T <= 0 || E <= 0) return BASE_ERR_INVALID_ARG;
+    if (T <= 0 || E <= 0 || B <= 0) return BASE_ERR_INVALID_ARG;
     if (s_dtype != BASE_F32 && s_dtype != BASE_I16) return BASE_ERR_UNSUPPORTED_DTYPE;
     if (T % E != 0) return BASE_ERR_NOT_DIVISIBLE;
     const bool integer = s_dtype == BASE_I16;
-    if (T >= kMaxTokens || E > kMaxExperts) return BASE_ERR_RANGE;
+    if (T >= kMaxTokens || E > kMaxExperts || B > kMaxBatch || B * T > INT32_MAX)
+        return BASE_ERR_RANGE;
     if (integer && T >= kMaxTokensInt) return BASE_ERR_RANGE;
     if (!aligned(S, 16) || !aligned(assign, 4) || !aligned(perm, 4)) return BASE_ERR_INVALID_ARG;
+    if (B > 1 && ((T * E * (integer ? 2 : 4)) % 16) != 0) return BASE_ERR_INVALID_ARG;
     if (prices != nullptr && !aligned(prices, integer ? 8 : 4)) return BASE_ERR_INVALID_ARG;
 
     base_assign_opts o{1e-4, 0.0, kDefaultEpsFactor, 4000000, 0u};
@@ -92,7 +103,7 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
         if (o.flags & ~known) return BASE_ERR_INVALID_ARG;
     }
 
-    const size_t need = base::assign_workspace_size(T, E);
+    const size_t need = base::assign_workspace_size(T, E) * (size_t)B;
     if (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 256))
         return BASE_ERR_WORKSPACE;
 
@@ -119,45 +130,79 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
 
     if ((o.flags & BASE_ASSIGN_CHECK_FINITE) && !integer) {
         int bad = 0;
-        hipError_t e = base::check_scores_finite(static_cast<const float *>(S), T, E, workspace,
-                                                 &bad, s);
+        hipError_t e = base::check_scores_finite(static_cast<const float *>(S), B * T * E, T, E,
+                                                 workspace, &bad, s);
         if (e != hipSuccess) return BASE_ERR_HIP;
         if (bad) return BASE_ERR_NONFINITE;
     }
 
-    hipError_t e = base::launch_assign(S, p, assign, perm, prices, workspace, s);
+    hipError_t e = base::launch_assign(S, p, B, assign, perm, prices, workspace, s);
     if (e != hipSuccess) return BASE_ERR_HIP;
 
     if (o.flags & BASE_ASSIGN_SYNC_STATS) {
-        base::SolveCtrl c{};
-        e = base::read_assign_stats(workspace, T, E, &c, s);
-        if (e != hipSuccess) return BASE_ERR_HIP;
-        const int unconverged = c.unconverged_experts & ~(1 << 30);
-        if (stats != nullptr) {
-            stats->phases = c.phase;
-            stats->rounds = c.rounds;
-            stats->bids = (int64_t)c.bids;
-            stats->eps_final = integer ? c.eps / (double)p.scale : c.eps;
-            stats->fell_back = c.fell_back;
-            stats->engine_bids = (int64_t)c.engine_bids;
-            stats->converged =
-                (E == 1) || (unconverged == 0 && (!c.not_converged || c.fell_back)) ? 1 : 0;
-            if (E == 1) {
-                stats->phases = 0;
-                stats->rounds = 0;
-                stats->bids = 0;
-                stats->eps_final = 0.0;
-                stats->fell_back = 0;
-                stats->engine_bids = 0;
-            }
+        base::SolveCtrl *cs = static_cast<base::SolveCtrl *>(calloc((size_t)B, sizeof(base::SolveCtrl)));
+        if (cs == nullptr) return BASE_ERR_HIP;
+        e = base::read_assign_stats(workspace, T, E, B, cs, s);
+        if (e != hipSuccess) {
+            free(cs);
+            return BASE_ERR_HIP;
         }
+        base_assign_stats agg{};
+        agg.converged = 1;
+        bool internal = false, overflow = false, not_converged = false;
+        for (int64_t b = 0; b < B; ++b) {
+            const base::SolveCtrl &c = cs[b];
+            const int unconverged = c.unconverged_experts & ~(1 << 30);
+            agg.phases = c.phase > agg.phases ? c.phase : agg.phases;
+            agg.rounds = c.rounds > agg.rounds ? c.rounds : agg.rounds;
+            agg.bids += (int64_t)c.bids;
+            agg.engine_bids += (int64_t)c.engine_bids;
+            const double eps = integer ? c.eps / (double)p.scale : c.eps;
+            agg.eps_final = eps > agg.eps_final ? eps : agg.eps_final;
+            agg.fell_back |= c.fell_back;
+            const bool conv = unconverged == 0 && (!c.not_converged || c.fell_back);
+            if (!conv) agg.converged = 0;
+            internal |= c.internal_error != 0;
+            overflow |= c.overflow != 0;
+            not_converged |= unconverged != 0 || (c.not_converged && !c.fell_back);
+        }
+        free(cs);
+        if (E == 1) {
+            agg = base_assign_stats{};
+            agg.converged = 1;
+        }
+        if (stats != nullptr) *stats = agg;
         if (E > 1) {
-            if (c.internal_error) return BASE_ERR_INTERNAL;
-            if (c.overflow) return BASE_ERR_RANGE;
-            if (unconverged != 0 || (c.not_converged && !c.fell_back)) return BASE_ERR_NOT_CONVERGED;
+            if (internal) return BASE_ERR_INTERNAL;
+            if (overflow) return BASE_ERR_RANGE;
+            if (not_converged) return BASE_ERR_NOT_CONVERGED;
         }
     }
     return BASE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_assign_opts *opts,
+                int32_t *assign, int32_t *perm, void *prices, void *workspace,
+                size_t workspace_bytes, base_assign_stats *stats, void *stream) {
+    return assign_impl(S, s_dtype, 1, T, E, opts, assign, perm, prices, workspace,
+                       workspace_bytes, stats, stream);
+}
+
+size_t base_assign_batched_workspace_size(int64_t B, int64_t T, int64_t E) {
+    if (B <= 0 || B > kMaxBatch) return 0;
+    return base_assign_workspace_size(T, E) * (size_t)B;
+}
+
+int base_assign_batched(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
+                        const base_assign_opts *opts, int32_t *assign, int32_t *perm,
+                        void *prices, void *workspace, size_t workspace_bytes,
+                        base_assign_stats *stats, void *stream) {
+    return assign_impl(S, s_dtype, B, T, E, opts, assign, perm, prices, workspace,
+                       workspace_bytes, stats, stream);
 }
 
 int base_timing_enable(int32_t capacity) {

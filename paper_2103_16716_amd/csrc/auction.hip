@@ -111,6 +111,38 @@ struct Ctx {
     int *eng_cn;
     uint32_t *sums;   // T x 16 words: each token's 8 best scores, their experts, a bound
     uint64_t *bar;    // grid barrier: arrivals at bar[0], release at bar[32] (own lines)
+    int64_t ws_stride;   // bytes between the workspaces of consecutive problems of a batch
+
+    // The view of problem b of a batch (blockIdx.y in every solver launch):
+    // the workspace pointers move by b workspace strides, the scores by b
+    // score matrices.
+    template <class P>
+    __host__ __device__ static P *shift(P *ptr, int64_t bytes) {
+        return reinterpret_cast<P *>(reinterpret_cast<uintptr_t>(ptr) + bytes);
+    }
+    __host__ __device__ Ctx at(int b) const {
+        Ctx r = *this;
+        if (b == 0) return r;
+        const int64_t w = (int64_t)b * ws_stride;
+        r.S = S + (int64_t)b * T * E;
+        r.ctrl = shift(ctrl, w);
+        r.prices = shift(prices, w);
+        r.hcount = shift(hcount, w);
+        r.hsel = shift(hsel, w);
+        r.bcount = shift(bcount, w);
+        r.holders = shift(holders, w);
+        r.bucket = shift(bucket, w);
+        r.ovf_key = shift(ovf_key, w);
+        r.ovf_exp = shift(ovf_exp, w);
+        r.active = shift(active, w);
+        r.ovf_count = shift(ovf_count, w);
+        r.eng_ck = shift(eng_ck, w);
+        r.eng_cs = shift(eng_cs, w);
+        r.eng_cn = shift(eng_cn, w);
+        r.sums = shift(sums, w);
+        r.bar = shift(bar, w);
+        return r;
+    }
 };
 
 template <class M>
@@ -141,6 +173,7 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.eng_cn = reinterpret_cast<int *>(ws + L.ecn);
     c.sums = reinterpret_cast<uint32_t *>(ws + L.sums);
     c.bar = reinterpret_cast<uint64_t *>(ws + L.bar);
+    c.ws_stride = (int64_t)L.total;
     return c;
 }
 
@@ -378,7 +411,8 @@ __device__ inline typename M::value_t bits_score(uint32_t w, int64_t scale) {
 // One group of G lanes per token: 9 rounds of a group maximum (ties to the
 // lowest expert) over the lanes' 8 scores each.
 template <class M, int G>
-__global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c) {
+__global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
+    const Ctx<M> c = c0.at(blockIdx.y);
     using value_t = typename M::value_t;
     const int lane = lane_id();
     const int gl = lane & (G - 1);
@@ -445,7 +479,11 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c) {
 // of any one XCD cover the whole table whatever XCD block 0 lands on.
 __global__ __launch_bounds__(256) void summary_prefill_kernel(const uint4 *sums, int64_t n16,
                                                               const SolveCtrl *ctrl, int cap,
-                                                              uint32_t *sink) {
+                                                              uint32_t *sink, int64_t ws_stride) {
+    const int64_t w = (int64_t)blockIdx.y * ws_stride;
+    sums = Ctx<FloatMode>::shift(sums, w);
+    ctrl = Ctx<FloatMode>::shift(ctrl, w);
+    sink = Ctx<FloatMode>::shift(sink, w);
     if (ctrl->done || ctrl->all_active) return;
     const int n = ld_relaxed(&ctrl->active_count[ctrl->cur]);
     if (n <= 0 || n > cap) return;
@@ -960,7 +998,10 @@ __device__ inline void begin_phase_scalar(SolveCtrl *ctrl, const AssignParams &p
 
 // ---------------------------------------------------------------- kernels --
 
-__global__ void init_kernel(SolveCtrl *ctrl, void *prices, int E, AssignParams p) {
+__global__ void init_kernel(SolveCtrl *ctrl, void *prices, int E, AssignParams p,
+                            int64_t ws_stride) {
+    ctrl = Ctx<FloatMode>::shift(ctrl, (int64_t)blockIdx.y * ws_stride);
+    if (prices != nullptr) prices = Ctx<FloatMode>::shift(prices, (int64_t)blockIdx.y * ws_stride);
     const int tid = threadIdx.x;
     if (tid == 0) {
         SolveCtrl z{};
@@ -996,7 +1037,9 @@ __device__ inline void range_take(typename M::score_t x, uint32_t &mx, uint32_t 
 
 template <class M>
 __global__ __launch_bounds__(256) void range_kernel(const typename M::score_t *S, int64_t n,
-                                                    uint32_t *part) {
+                                                    uint32_t *part, int64_t ws_stride) {
+    S += (int64_t)blockIdx.y * n;
+    part = Ctx<FloatMode>::shift(part, (int64_t)blockIdx.y * ws_stride);
     using score_t = typename M::score_t;
     constexpr int kVec = 16 / sizeof(score_t);
     __shared__ uint32_t smx[4], smn[4];
@@ -1046,7 +1089,9 @@ __global__ __launch_bounds__(256) void range_kernel(const typename M::score_t *S
 
 // Combines the range partials into the control block (one block).
 __global__ __launch_bounds__(256) void range_finish_kernel(SolveCtrl *ctrl, const uint32_t *part,
-                                                           int nparts) {
+                                                           int nparts, int64_t ws_stride) {
+    ctrl = Ctx<FloatMode>::shift(ctrl, (int64_t)blockIdx.y * ws_stride);
+    part = Ctx<FloatMode>::shift(part, (int64_t)blockIdx.y * ws_stride);
     __shared__ uint32_t smx[4], smn[4], sbad[4];
     uint32_t mx = 0u, mn = 0xffffffffu, bad = 0u;
     for (int i = threadIdx.x; i < nparts; i += blockDim.x) {
@@ -1082,7 +1127,8 @@ __global__ __launch_bounds__(256) void range_finish_kernel(SolveCtrl *ctrl, cons
 
 // Float mode: raise eps_final so that it stays far above fp32 rounding at the
 // magnitude prices and bids reach (scores plus a few score ranges).
-__global__ void eps_floor_kernel(SolveCtrl *ctrl, int integer) {
+__global__ void eps_floor_kernel(SolveCtrl *ctrl, int integer, int64_t ws_stride) {
+    ctrl = Ctx<FloatMode>::shift(ctrl, (int64_t)blockIdx.y * ws_stride);
     if (integer) {
         ctrl->eps_final_eff = 1.0;
         return;
@@ -1095,7 +1141,8 @@ __global__ void eps_floor_kernel(SolveCtrl *ctrl, int integer) {
 }
 
 template <class M>
-__global__ void phase_begin_kernel(Ctx<M> c, AssignParams p) {
+__global__ void phase_begin_kernel(Ctx<M> c0, AssignParams p) {
+    const Ctx<M> c = c0.at(blockIdx.y);
     __shared__ int skip;
     if (threadIdx.x == 0) {
         skip = c.ctrl->done;
@@ -1115,7 +1162,8 @@ __global__ void phase_begin_kernel(Ctx<M> c, AssignParams p) {
 }
 
 template <class M, int G>
-__global__ __launch_bounds__(kThreads) void bid_wide_kernel(Ctx<M> c) {
+__global__ __launch_bounds__(kThreads) void bid_wide_kernel(Ctx<M> c0) {
+    const Ctx<M> c = c0.at(blockIdx.y);
     using value_t = typename M::value_t;
     extern __shared__ __align__(16) unsigned char smem_raw[];
     value_t *pr = reinterpret_cast<value_t *>(smem_raw);
@@ -1145,7 +1193,8 @@ __global__ __launch_bounds__(kThreads) void bid_wide_kernel(Ctx<M> c) {
 }
 
 template <class M>
-__global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c) {
+__global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c0) {
+    const Ctx<M> c = c0.at(blockIdx.y);
     __shared__ UpdateSmem sm;
     __shared__ int last;
     SolveCtrl *ctrl = c.ctrl;
@@ -1220,8 +1269,9 @@ __device__ inline bool grid_barrier(uint64_t *bar, uint64_t target, SolveCtrl *c
 }
 
 template <class M, int G>
-__global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c, int max_wide,
+__global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c0, int max_wide,
                                                              int32_t max_rounds) {
+    const Ctx<M> c = c0.at(blockIdx.y);
     using value_t = typename M::value_t;
     extern __shared__ __align__(16) unsigned char smem_raw[];
     value_t *pr = reinterpret_cast<value_t *>(smem_raw);
@@ -1278,8 +1328,9 @@ __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c, int max_w
 // Remaining rounds of the current phase inside one workgroup. With
 // `continue_phases` the block also runs every later phase to the end.
 template <class M, int G>
-__global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c, AssignParams p,
+__global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c0, AssignParams p,
                                                         int continue_phases) {
+    const Ctx<M> c = c0.at(blockIdx.y);
     using value_t = typename M::value_t;
     __shared__ UpdateSmem sm;
     __shared__ int st_n, st_cur, st_all, st_stop, st_begin, ntouched;
@@ -1914,7 +1965,8 @@ __device__ __attribute__((always_inline)) void engine_solo(const Ctx<M> &c, cons
 // The engine's phase entry, one block per expert: sorts the expert's holder
 // table and stores its K lowest keys (with slots) for the engine to load.
 template <class M>
-__global__ __launch_bounds__(256) void cache_build_kernel(Ctx<M> c) {
+__global__ __launch_bounds__(256) void cache_build_kernel(Ctx<M> c0) {
+    const Ctx<M> c = c0.at(blockIdx.y);
     __shared__ uint64_t keys[kEngMaxC];
     __shared__ uint16_t slots[kEngMaxC];
     __shared__ int go;
@@ -1970,7 +2022,8 @@ __global__ __launch_bounds__(256) void cache_build_kernel(Ctx<M> c) {
 }
 
 template <class M, int G>
-__global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignParams p) {
+__global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignParams p) {
+    const Ctx<M> c = c0.at(blockIdx.y);
     using value_t = typename M::value_t;
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int K = c.eng_k;
@@ -2212,7 +2265,9 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c, AssignPar
 
 // assign[t] = e for every held token; counts experts that are not full.
 template <class M>
-__global__ void holders_to_assign_kernel(Ctx<M> c, int32_t *assign) {
+__global__ void holders_to_assign_kernel(Ctx<M> c0, int32_t *assign) {
+    const Ctx<M> c = c0.at(blockIdx.y);
+    assign += (int64_t)blockIdx.y * c.T;
     const int e = blockIdx.x;
     int h = c.hcount[e];
     if (h < 0 || h > c.C) {
@@ -2231,7 +2286,9 @@ __global__ void holders_to_assign_kernel(Ctx<M> c, int32_t *assign) {
 // Greedy completion after max_rounds (one block, sequential in token order):
 // every still-unassigned token takes its best expert among those with room.
 template <class M>
-__global__ void greedy_fill_kernel(Ctx<M> c, int32_t *assign, uint32_t flags) {
+__global__ void greedy_fill_kernel(Ctx<M> c0, int32_t *assign, uint32_t flags) {
+    const Ctx<M> c = c0.at(blockIdx.y);
+    assign += (int64_t)blockIdx.y * c.T;
     using value_t = typename M::value_t;
     SolveCtrl *ctrl = c.ctrl;
     if (!ctrl->not_converged || !(flags & BASE_ASSIGN_GREEDY_FALLBACK)) return;
@@ -2274,7 +2331,10 @@ __global__ void greedy_fill_kernel(Ctx<M> c, int32_t *assign, uint32_t flags) {
 
 // Per block of kCountTile tokens: how many go to each expert.
 __global__ __launch_bounds__(kCountTile) void block_count_kernel(const int32_t *assign, int T,
-                                                                 int E, int32_t *blk) {
+                                                                 int E, int32_t *blk,
+                                                                 int64_t ws_stride) {
+    assign += (int64_t)blockIdx.y * T;
+    blk = Ctx<FloatMode>::shift(blk, (int64_t)blockIdx.y * ws_stride);
     extern __shared__ int hist[];
     for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
     __syncthreads();
@@ -2287,15 +2347,35 @@ __global__ __launch_bounds__(kCountTile) void block_count_kernel(const int32_t *
     for (int e = threadIdx.x; e < E; e += blockDim.x) blk[(int64_t)blockIdx.x * E + e] = hist[e];
 }
 
-// Exclusive scan over blocks for each expert, offset by the expert's first row e*C.
-__global__ void block_scan_kernel(int32_t *blk, int nblk, int E, int C) {
-    const int e = blockIdx.x * blockDim.x + threadIdx.x;
-    if (e >= E) return;
-    int run = e * C;
-    for (int b = 0; b < nblk; ++b) {
-        const int v = blk[(int64_t)b * E + e];
-        blk[(int64_t)b * E + e] = run;
-        run += v;
+// Exclusive scan over the blocks' counts of one expert (one workgroup per
+// expert), offset by the expert's first row e*C.
+__global__ __launch_bounds__(256) void block_scan_kernel(int32_t *blk, int nblk, int E, int C,
+                                                         int64_t ws_stride) {
+    blk = Ctx<FloatMode>::shift(blk, (int64_t)blockIdx.y * ws_stride);
+    __shared__ int wsum[4];
+    __shared__ int carry;
+    const int e = blockIdx.x;
+    const int lane = lane_id();
+    const int wave = threadIdx.x >> 6;
+    if (threadIdx.x == 0) carry = e * C;
+    __syncthreads();
+    for (int b0 = 0; b0 < nblk; b0 += 256) {
+        const int b = b0 + threadIdx.x;
+        const int v = b < nblk ? blk[(int64_t)b * E + e] : 0;
+        int incl = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(incl, off);
+            if (lane >= off) incl += o;
+        }
+        if (lane == 63) wsum[wave] = incl;
+        __syncthreads();
+        int before = carry;
+        for (int w = 0; w < wave; ++w) before += wsum[w];
+        if (b < nblk) blk[(int64_t)b * E + e] = before + incl - v;
+        __syncthreads();
+        if (threadIdx.x == 0) carry += wsum[0] + wsum[1] + wsum[2] + wsum[3];
+        __syncthreads();
     }
 }
 
@@ -2303,7 +2383,10 @@ __global__ void block_scan_kernel(int32_t *blk, int nblk, int E, int C) {
 // a stable counting sort by expert.
 __global__ __launch_bounds__(kCountTile) void perm_scatter_kernel(const int32_t *assign, int T,
                                                                   int E, const int32_t *blk,
-                                                                  int32_t *perm) {
+                                                                  int32_t *perm, int64_t ws_stride) {
+    assign += (int64_t)blockIdx.y * T;
+    perm += (int64_t)blockIdx.y * T;
+    blk = Ctx<FloatMode>::shift(blk, (int64_t)blockIdx.y * ws_stride);
     __shared__ int loc[kCountTile];
     const int t = blockIdx.x * kCountTile + threadIdx.x;
     const int a = t < T ? assign[t] : -1;
@@ -2322,12 +2405,13 @@ __global__ void fill_kernel(int32_t *p, int64_t n, int32_t v) {
         p[i] = v;
 }
 
-// E == 1: every token goes to expert 0 and the sort vector is the identity.
-__global__ void single_expert_kernel(int32_t *assign, int32_t *perm, int64_t T) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < T;
+// E == 1: every token goes to expert 0 and the sort vector is the identity
+// (n = B * T entries, problem by problem).
+__global__ void single_expert_kernel(int32_t *assign, int32_t *perm, int64_t n, int64_t T) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {
         assign[i] = 0;
-        perm[i] = (int32_t)i;
+        perm[i] = (int32_t)(i % T);
     }
 }
 
@@ -2365,7 +2449,7 @@ void timing_pair(hipEvent_t *begin, hipEvent_t *end) {
 }
 
 template <class M, int G>
-hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
+hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t s) {
     using value_t = typename M::value_t;
     Ctx<M> c = c0;
     // The engine's LDS: the longest per-expert lists that fit the device's
@@ -2425,9 +2509,11 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
     {
         int sblocks = (int)((c.T + per_block - 1) / per_block);
         if (sblocks > 4096) sblocks = 4096;
-        hipLaunchKernelGGL((summary_kernel<M, G>), dim3(sblocks), dim3(kThreads), 0, s, c);
+        hipLaunchKernelGGL((summary_kernel<M, G>), dim3(sblocks, B), dim3(kThreads), 0, s, c);
     }
-    // Round loop for phases that stay large: one block per compute unit.
+    // Round loop for phases that stay large: one block per compute unit,
+    // shared out among the problems of a batch (every block of the grid must
+    // be resident at once; a batch larger than the device holds skips it).
     int coop_blocks = 0;
     {
         int dev = 0, cus = 0, per_cu = 0;
@@ -2436,83 +2522,91 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, hipStream_t s) {
             hipOccupancyMaxActiveBlocksPerMultiprocessor(
                 &per_cu, reinterpret_cast<const void *>(&wide_loop_kernel<M, G>), kThreads,
                 bid_bytes) == hipSuccess &&
-            per_cu > 0 && cus > 0)
-            coop_blocks = cus;
+            per_cu > 0 && cus > 0) {
+            coop_blocks = cus / B;
+            if (coop_blocks == 0 && B <= cus * per_cu) coop_blocks = 1;
+        }
         (void)hipGetLastError();
     }
     for (int slot = 0; slot < slots; ++slot) {
-        hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1), dim3(1024), 0, s, c, p);
+        hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1, B), dim3(1024), 0, s, c, p);
         for (int r = 0; r < wide_rounds; ++r) {
-            hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks), dim3(kThreads), bid_bytes,
-                               s, c);
-            hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks), dim3(kThreads), 0, s, c);
+            hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks, B), dim3(kThreads),
+                               bid_bytes, s, c);
+            hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks, B), dim3(kThreads), 0, s, c);
         }
         if (coop_blocks > 0)
-            hipLaunchKernelGGL((wide_loop_kernel<M, G>), dim3(coop_blocks), dim3(kThreads), bid_bytes,
-                               s, c, kWideLoopRounds, p.max_rounds);
+            hipLaunchKernelGGL((wide_loop_kernel<M, G>), dim3(coop_blocks, B), dim3(kThreads),
+                               bid_bytes, s, c, kWideLoopRounds, p.max_rounds);
         if (engine) {
-            hipLaunchKernelGGL(cache_build_kernel<M>, dim3(c.E), dim3(256), 0, s, c);
-            hipLaunchKernelGGL(summary_prefill_kernel, dim3(256), dim3(256), 0, s,
+            hipLaunchKernelGGL(cache_build_kernel<M>, dim3(c.E, B), dim3(256), 0, s, c);
+            // Multiples of 8 blocks per problem, 256 in all when one problem.
+            const int pf = B >= 32 ? 8 : 8 * (32 / B);
+            hipLaunchKernelGGL(summary_prefill_kernel, dim3(pf, B), dim3(256), 0, s,
                                reinterpret_cast<const uint4 *>(c.sums), (int64_t)c.T * 4, c.ctrl,
-                               kEngCap, reinterpret_cast<uint32_t *>(&c.ctrl->pad2));
+                               kEngCap, reinterpret_cast<uint32_t *>(&c.ctrl->pad2), c.ws_stride);
             hipEvent_t ev0 = nullptr, ev1 = nullptr;
             timing_pair(&ev0, &ev1);
             if (ev0 != nullptr) (void)hipEventRecord(ev0, s);
-            hipLaunchKernelGGL((engine_kernel<M, G>), dim3(1), dim3(kEngThreads), eng_bytes, s, c,
-                               p);
+            hipLaunchKernelGGL((engine_kernel<M, G>), dim3(1, B), dim3(kEngThreads), eng_bytes, s,
+                               c, p);
             if (ev1 != nullptr) (void)hipEventRecord(ev1, s);
         }
-        hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1), dim3(kThreads), tail_smem, s, c, p,
+        hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1, B), dim3(kThreads), tail_smem, s, c, p,
                            slot == slots - 1 ? 1 : 0);
     }
     return hipGetLastError();
 }
 
 template <class M>
-hipError_t solve_mode(const void *S, const AssignParams &p, int32_t *assign, int32_t *perm,
+hipError_t solve_mode(const void *S, const AssignParams &p, int B, int32_t *assign, int32_t *perm,
                       void *prices_out, void *workspace, hipStream_t s) {
     using value_t = typename M::value_t;
     char *ws = static_cast<char *>(workspace);
     const Layout L = make_layout(p.T, p.E);
     Ctx<M> c = make_ctx<M>(S, p, ws);
-    hipLaunchKernelGGL(init_kernel, dim3(1), dim3(256), 0, s, c.ctrl, (void *)c.prices, c.E, p);
+    const int64_t wst = c.ws_stride;
+    hipLaunchKernelGGL(init_kernel, dim3(1, B), dim3(256), 0, s, c.ctrl, (void *)c.prices, c.E, p,
+                       wst);
     const int64_t n = p.T * p.E;
     uint32_t *rpart = reinterpret_cast<uint32_t *>(ws + L.rpart);
-    hipLaunchKernelGGL(range_kernel<M>, dim3(kRangeBlocks), dim3(256), 0, s, c.S, n, rpart);
-    hipLaunchKernelGGL(range_finish_kernel, dim3(1), dim3(256), 0, s, c.ctrl, rpart, kRangeBlocks);
-    hipLaunchKernelGGL(eps_floor_kernel, dim3(1), dim3(1), 0, s, c.ctrl, p.integer ? 1 : 0);
+    hipLaunchKernelGGL(range_kernel<M>, dim3(kRangeBlocks, B), dim3(256), 0, s, c.S, n, rpart, wst);
+    hipLaunchKernelGGL(range_finish_kernel, dim3(1, B), dim3(256), 0, s, c.ctrl, rpart,
+                       kRangeBlocks, wst);
+    hipLaunchKernelGGL(eps_floor_kernel, dim3(1, B), dim3(1), 0, s, c.ctrl, p.integer ? 1 : 0, wst);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
 
     switch (lanes_per_token(p.E)) {
-        case 1: err = run_solve<M, 1>(c, p, s); break;
-        case 2: err = run_solve<M, 2>(c, p, s); break;
-        case 4: err = run_solve<M, 4>(c, p, s); break;
-        case 8: err = run_solve<M, 8>(c, p, s); break;
-        case 16: err = run_solve<M, 16>(c, p, s); break;
-        case 32: err = run_solve<M, 32>(c, p, s); break;
-        default: err = run_solve<M, 64>(c, p, s); break;
+        case 1: err = run_solve<M, 1>(c, p, B, s); break;
+        case 2: err = run_solve<M, 2>(c, p, B, s); break;
+        case 4: err = run_solve<M, 4>(c, p, B, s); break;
+        case 8: err = run_solve<M, 8>(c, p, B, s); break;
+        case 16: err = run_solve<M, 16>(c, p, B, s); break;
+        case 32: err = run_solve<M, 32>(c, p, B, s); break;
+        default: err = run_solve<M, 64>(c, p, B, s); break;
     }
     if (err != hipSuccess) {
         debug_note("solver launches", err);
         return err;
     }
 
-    int fblocks = (int)((p.T + 255) / 256);
+    int fblocks = (int)((p.T * B + 255) / 256);
     if (fblocks > 2048) fblocks = 2048;
-    hipLaunchKernelGGL(fill_kernel, dim3(fblocks), dim3(256), 0, s, assign, p.T, -1);
-    hipLaunchKernelGGL(holders_to_assign_kernel<M>, dim3(c.E), dim3(256), 0, s, c, assign);
-    hipLaunchKernelGGL(greedy_fill_kernel<M>, dim3(1), dim3(64), 0, s, c, assign, p.flags);
+    hipLaunchKernelGGL(fill_kernel, dim3(fblocks), dim3(256), 0, s, assign, p.T * B, -1);
+    hipLaunchKernelGGL(holders_to_assign_kernel<M>, dim3(c.E, B), dim3(256), 0, s, c, assign);
+    hipLaunchKernelGGL(greedy_fill_kernel<M>, dim3(1, B), dim3(64), 0, s, c, assign, p.flags);
     int32_t *blk = reinterpret_cast<int32_t *>(ws + L.blk);
-    hipLaunchKernelGGL(block_count_kernel, dim3((unsigned)L.nblk), dim3(kCountTile),
-                       (size_t)p.E * sizeof(int), s, assign, c.T, c.E, blk);
-    hipLaunchKernelGGL(block_scan_kernel, dim3((unsigned)((p.E + 255) / 256)), dim3(256), 0, s,
-                       blk, (int)L.nblk, c.E, c.C);
-    hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)L.nblk), dim3(kCountTile), 0, s,
-                       assign, c.T, c.E, blk, perm);
+    hipLaunchKernelGGL(block_count_kernel, dim3((unsigned)L.nblk, B), dim3(kCountTile),
+                       (size_t)p.E * sizeof(int), s, assign, c.T, c.E, blk, wst);
+    hipLaunchKernelGGL(block_scan_kernel, dim3((unsigned)p.E, B), dim3(256), 0, s, blk,
+                       (int)L.nblk, c.E, c.C, wst);
+    hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)L.nblk, B), dim3(kCountTile), 0, s,
+                       assign, c.T, c.E, blk, perm, wst);
     if (prices_out != nullptr) {
-        err = hipMemcpyAsync(prices_out, c.prices, (size_t)p.E * sizeof(value_t),
-                             hipMemcpyDeviceToDevice, s);
+        const size_t row = (size_t)p.E * sizeof(value_t);
+        err = hipMemcpy2DAsync(prices_out, row, c.prices, (size_t)wst, row, (size_t)B,
+                               hipMemcpyDeviceToDevice, s);
         if (err != hipSuccess) return err;
     }
     return hipGetLastError();
@@ -2525,24 +2619,28 @@ size_t assign_workspace_size(int64_t T, int64_t E) {
     return make_layout(T, E).total;
 }
 
-hipError_t launch_assign(const void *S, const AssignParams &p, int32_t *assign, int32_t *perm,
-                         void *prices_out, void *workspace, hipStream_t stream) {
+hipError_t launch_assign(const void *S, const AssignParams &p, int64_t B, int32_t *assign,
+                         int32_t *perm, void *prices_out, void *workspace, hipStream_t stream) {
     if (p.E == 1) {
-        SolveCtrl *ctrl = static_cast<SolveCtrl *>(workspace);
-        hipError_t err = hipMemsetAsync(ctrl, 0, sizeof(SolveCtrl), stream);
-        if (err != hipSuccess) return err;
-        int blocks = (int)((p.T + 255) / 256);
+        const size_t wst = make_layout(p.T, p.E).total;
+        for (int64_t b = 0; b < B; ++b) {
+            hipError_t err = hipMemsetAsync(static_cast<char *>(workspace) + b * wst, 0,
+                                            sizeof(SolveCtrl), stream);
+            if (err != hipSuccess) return err;
+        }
+        int blocks = (int)((p.T * B + 255) / 256);
         if (blocks > 2048) blocks = 2048;
         hipLaunchKernelGGL(single_expert_kernel, dim3(blocks), dim3(256), 0, stream, assign, perm,
-                           p.T);
+                           p.T * B, p.T);
         if (prices_out != nullptr) {
-            err = hipMemsetAsync(prices_out, 0, p.integer ? 8 : 4, stream);
+            hipError_t err = hipMemsetAsync(prices_out, 0, (size_t)B * (p.integer ? 8 : 4), stream);
             if (err != hipSuccess) return err;
         }
         return hipGetLastError();
     }
-    if (p.integer) return solve_mode<IntMode>(S, p, assign, perm, prices_out, workspace, stream);
-    return solve_mode<FloatMode>(S, p, assign, perm, prices_out, workspace, stream);
+    if (p.integer)
+        return solve_mode<IntMode>(S, p, (int)B, assign, perm, prices_out, workspace, stream);
+    return solve_mode<FloatMode>(S, p, (int)B, assign, perm, prices_out, workspace, stream);
 }
 
 hipError_t timing_enable(int32_t capacity) {
@@ -2582,27 +2680,29 @@ hipError_t timing_read(int64_t *launches, double *total_ms) {
     return hipSuccess;
 }
 
-hipError_t read_assign_stats(const void *workspace, int64_t /*T*/, int64_t /*E*/, SolveCtrl *out,
-                             hipStream_t stream) {
-    hipError_t err = hipMemcpyAsync(out, workspace, sizeof(SolveCtrl), hipMemcpyDeviceToHost,
-                                    stream);
+hipError_t read_assign_stats(const void *workspace, int64_t T, int64_t E, int64_t B,
+                             SolveCtrl *out, hipStream_t stream) {
+    const size_t wst = make_layout(T, E).total;
+    hipError_t err = hipMemcpy2DAsync(out, sizeof(SolveCtrl), workspace, wst, sizeof(SolveCtrl),
+                                      (size_t)B, hipMemcpyDeviceToHost, stream);
     if (err != hipSuccess) return err;
     return hipStreamSynchronize(stream);
 }
 
-hipError_t check_scores_finite(const float *S, int64_t T, int64_t E, void *workspace, int *bad,
-                               hipStream_t stream) {
+hipError_t check_scores_finite(const float *S, int64_t n, int64_t T, int64_t E, void *workspace,
+                               int *bad, hipStream_t stream) {
     SolveCtrl *ctrl = static_cast<SolveCtrl *>(workspace);
     uint32_t *rpart =
         reinterpret_cast<uint32_t *>(static_cast<char *>(workspace) + make_layout(T, E).rpart);
     AssignParams p{};
-    hipLaunchKernelGGL(init_kernel, dim3(1), dim3(256), 0, stream, ctrl, (void *)nullptr, 0, p);
-    hipLaunchKernelGGL(range_kernel<FloatMode>, dim3(kRangeBlocks), dim3(256), 0, stream, S, T * E,
-                       rpart);
+    hipLaunchKernelGGL(init_kernel, dim3(1), dim3(256), 0, stream, ctrl, (void *)nullptr, 0, p,
+                       (int64_t)0);
+    hipLaunchKernelGGL(range_kernel<FloatMode>, dim3(kRangeBlocks), dim3(256), 0, stream, S, n,
+                       rpart, (int64_t)0);
     hipLaunchKernelGGL(range_finish_kernel, dim3(1), dim3(256), 0, stream, ctrl, rpart,
-                       kRangeBlocks);
+                       kRangeBlocks, (int64_t)0);
     SolveCtrl h{};
-    hipError_t err = read_assign_stats(workspace, 0, 0, &h, stream);
+    hipError_t err = read_assign_stats(workspace, T, E, 1, &h, stream);
     if (err != hipSuccess) return err;
     *bad = (h.unconverged_experts & (1 << 30)) ? 1 : 0;
     return hipSuccess;

@@ -55,19 +55,24 @@ struct SolveCtrl {
 size_t assign_workspace_size(int64_t T, int64_t E);
 
 // Enqueues the whole solve; returns the first HIP error of the launches.
-hipError_t launch_assign(const void *S, const AssignParams &p, int32_t *assign, int32_t *perm,
-                         void *prices_out, void *workspace, hipStream_t stream);
+// Enqueues the whole solve of B independent problems of T x E scores
+// (scores, outputs and workspaces laid out problem after problem).
+hipError_t launch_assign(const void *S, const AssignParams &p, int64_t B, int32_t *assign,
+                         int32_t *perm, void *prices_out, void *workspace, hipStream_t stream);
 
 // Reads the statistics back (synchronises the stream).
-hipError_t read_assign_stats(const void *workspace, int64_t T, int64_t E, SolveCtrl *out,
-                             hipStream_t stream);
+// Reads the B control blocks back (synchronises the stream).
+hipError_t read_assign_stats(const void *workspace, int64_t T, int64_t E, int64_t B,
+                             SolveCtrl *out, hipStream_t stream);
 
 // Event timing of the engine kernel's launches (measurement support).
 hipError_t timing_enable(int32_t capacity);
 hipError_t timing_read(int64_t *launches, double *total_ms);
 
 // Scans S for NaN/Inf (synchronous). *bad is set to 1 when one is found.
-hipError_t check_scores_finite(const float *S, int64_t T, int64_t E, void *workspace, int *bad,
-                               hipStream_t stream);
+// Scans n scores for NaN/Inf (synchronous), using the workspace of one
+// T x E problem. *bad is set to 1 when one is found.
+hipError_t check_scores_finite(const float *S, int64_t n, int64_t T, int64_t E, void *workspace,
+                               int *bad, hipStream_t stream);
 
 }  // namespace base

@@ -45,6 +45,23 @@ def test_library_exports_every_declared_symbol(L):
         assert re.search(rf"\bT {name}\b", out), name
 
 
+def test_batched_arguments_checked_before_launch(L):
+    import ctypes
+    assert pb.assign_batched_workspace_size(4, 2048, 128) == 4 * pb.assign_workspace_size(2048, 128)
+    assert pb.assign_batched_workspace_size(0, 2048, 128) == 0
+    assert pb.assign_batched_workspace_size(1 << 16, 64, 8) == 0
+    st = pb.AssignStats()
+    buf = ctypes.create_string_buffer(1 << 12)
+    p16 = (ctypes.addressof(buf) + 255) & ~255
+    # bad batch count, then a score block that breaks 16-byte alignment per problem
+    assert L.base_assign_batched(p16, pb.BASE_F32, 0, 8, 4, None, p16, p16, None, p16, 0,
+                                 ctypes.byref(st), None) == pb.BASE_ERR_INVALID_ARG
+    assert L.base_assign_batched(p16, pb.BASE_F32, 2, 3, 1, None, p16, p16, None, p16, 0,
+                                 ctypes.byref(st), None) == pb.BASE_ERR_INVALID_ARG
+    assert L.base_assign_batched(p16, pb.BASE_F32, 2, 8, 4, None, p16, p16, None, p16, 0,
+                                 ctypes.byref(st), None) == pb.BASE_ERR_WORKSPACE
+
+
 def test_timing_record_without_launches(L):
     # Disabled or empty records need no device: nothing recorded, nothing summed.
     pb.timing_enable(0)

@@ -280,6 +280,64 @@ def test_assign_single_phase_large_epsilon(div):
     check_assignment(S64, res, eps, opt=(a_opt, obj_opt))
 
 
+def _worker_batch(B, seed0):
+    """B independent problems of the paper's per-worker shape (T=2048, E=128,
+    d=2048), each drawn with its own seed, as fp32 scores [B, T, E]."""
+    base = wl.WORKLOADS["t2048-e128-d2048-worker"]
+    Ss = []
+    for b in range(B):
+        inp = wl.make_inputs(dataclasses.replace(base, seed=seed0 + b))
+        H, W = inputs_on_device(inp)
+        Ss.append(pb.affinity(H, W))
+    return torch.stack(Ss).contiguous()
+
+
+def test_assign_batched_identical_to_single_solves():
+    """Sec. 3.2.1 (Sharding): B independent worker problems in one call give,
+    problem by problem, exactly what base_assign gives for each alone, and
+    each meets the oracle's bound."""
+    B = 6
+    S = _worker_batch(B, 900)
+    res = pb.assign_batched(S)
+    assert res.stats.converged == 1
+    T, E = S.shape[1], S.shape[2]
+    bids = 0
+    for b in range(B):
+        one = pb.assign(S[b].contiguous())
+        bids += one.stats.bids
+        assert torch.equal(res.assign[b], one.assign)
+        assert torch.equal(res.perm[b], one.perm)
+        assert torch.equal(res.prices[b], one.prices)
+    assert res.stats.bids == bids
+    for b in (0, B - 1):
+        S64 = host(S[b]).astype(np.float64)
+        a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+        one = pb.AssignResult(res.assign[b], res.perm[b], res.prices[b], res.stats)
+        check_assignment(S64, one, EPS_FINAL, opt=(a_opt, obj_opt))
+
+
+def test_assign_batched_integer_mode_and_single_expert():
+    B, T, E = 3, 512, 8
+    rng = np.random.Generator(np.random.PCG64(77))
+    Si = rng.integers(-300, 300, size=(B, T, E), dtype=np.int16)
+    res = pb.assign_batched(dev(Si))
+    for b in range(B):
+        one = pb.assign(dev(Si[b].copy()))
+        assert torch.equal(res.assign[b], one.assign)
+        assert torch.equal(res.prices[b], one.prices)
+        S64 = Si[b].astype(np.float64)
+        a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+        a = host(res.assign[b])
+        assert oracle.balanced_counts_ok(a, E)
+        assert oracle.objective(S64, a) == obj_opt      # integer mode: exact optimum
+        if oracle.optimum_gap(S64, a_opt) > 0:
+            np.testing.assert_array_equal(a, a_opt)
+    S1 = torch.randn((4, 96, 1), device="cuda")
+    r1 = pb.assign_batched(S1)
+    assert torch.all(r1.assign == 0)
+    assert torch.equal(r1.perm, torch.arange(96, dtype=torch.int32, device="cuda").repeat(4, 1))
+
+
 def test_engine_launch_timing():
     """The measurement hook brackets each engine launch with events on the
     call's stream: one record per phase slot, each within the whole call."""
