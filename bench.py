@@ -6,7 +6,12 @@ H into expert-contiguous rows (plus the inverse permute on the workload that
 includes it). Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                    [--no-cpu-baseline]
+                    [--no-cpu-baseline] [--batch B]
+
+With --batch B > 1 it measures B independent problems of the paper's
+per-worker shape (Sec. 3.2.1 Sharding; T=2048, E=128, d=2048): one affinity
+GEMM over the B * T tokens against the shared expert embeddings, one
+base_assign_batched call, and each problem's permute.
 """
 from __future__ import annotations
 
@@ -63,7 +68,76 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=wl.HEADLINE, choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--batch", type=int, default=1)
     return ap.parse_args()
+
+
+def bench_batched(args) -> None:
+    """B independent worker-shape problems per step (see the module note)."""
+    import dataclasses
+
+    import torch
+
+    import paper_2103_16716_amd as pb
+
+    torch.cuda.set_device(0)
+    B = args.batch
+    base = wl.WORKLOADS["t2048-e128-d2048-worker"]
+    T, E, d = base.T, base.E, base.d
+    hs = []
+    W = None
+    for b in range(B):
+        inp = wl.make_inputs(dataclasses.replace(base, seed=base.seed + 1000 * b))
+        hs.append(inp.H_store)
+        if W is None:
+            W = torch.from_numpy(inp.W_store.view(np.int16)).cuda().view(torch.bfloat16)
+    H = torch.from_numpy(np.concatenate(hs).view(np.int16)).cuda().view(torch.bfloat16)
+    S = torch.empty((B * T, E), dtype=torch.float32, device="cuda")
+    a = torch.empty((B, T), dtype=torch.int32, device="cuda")
+    perm = torch.empty((B, T), dtype=torch.int32, device="cuda")
+    prices = torch.empty((B, E), dtype=torch.float32, device="cuda")
+    ws = torch.empty(pb.assign_batched_workspace_size(B, T, E), dtype=torch.uint8, device="cuda")
+    X = torch.empty((B * T, d), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        pb.affinity(H, W, out=S, stream=stream)
+        pb.assign_batched(S.view(B, T, E), sync_stats=False, workspace=ws, out_assign=a,
+                          out_perm=perm, out_prices=prices, stream=stream)
+        for b in range(B):
+            pb.permute(H[b * T:(b + 1) * T], perm[b], out=X[b * T:(b + 1) * T], stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    res = pb.assign_batched(S.view(B, T, E), workspace=ws, out_assign=a, out_perm=perm,
+                            out_prices=prices)
+    counts_ok = bool(torch.all(torch.stack([torch.bincount(a[b].long(), minlength=E)
+                                            for b in range(B)]) == T // E))
+    out = {
+        "metric": f"tokens assigned/sec, {B} independent problems of T=2048,E=128,d=2048",
+        "value": B * T * args.steps / wall,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded generator; no dataset or trained weights)",
+        "config": {"workload": f"t2048-e128-d2048-worker x {B}", "B": B, "T": T, "E": E, "d": d},
+        "assign_stats": {"phases": res.stats.phases, "rounds_max": res.stats.rounds,
+                         "bids": res.stats.bids, "converged": res.stats.converged},
+        "balanced_problems": counts_ok,
+    }
+    print(json.dumps(out), flush=True)
 
 
 def cpu_baseline(inp: wl.Inputs, budget_s: float = 20.0) -> dict:
@@ -113,6 +187,10 @@ def main():
         print("bench.py measures one GPU: the assignment path has no multi-GPU mode "
               "(each GPU solves its own batch independently). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if args.batch > 1:
+        bench_batched(args)
+        return
 
     import torch
 
