@@ -15,6 +15,9 @@ What it computes, each function citing the passage it follows:
   optimum_gap       second-best gap / uniqueness of an optimum
   stable_perm       sort vector grouping tokens by expert        (Fig. 2 caption)
   gather / scatter  routing into expert-contiguous rows and back (Fig. 2, Sec. 3)
+  expert_offsets    row ranges of a (possibly unbalanced) routed order (Sec. 3.2.2)
+  gate_combine      gated residual y = sigmoid(h.w_a) f + h          (Sec. 3.1, Eq. 1)
+  gate_backward     gradients of Eq. 1's gate and residual           (Sec. 3.1, Eq. 1)
 """
 from .affinity import affinity
 from .assign import (
@@ -27,10 +30,14 @@ from .assign import (
     solve_hungarian,
     solve_ssp,
 )
+from .gate import expert_offsets, gate_backward, gate_combine
 from .permute import gather, scatter, stable_perm
 
 __all__ = [
     "affinity",
+    "expert_offsets",
+    "gate_backward",
+    "gate_combine",
     "balanced_counts_ok",
     "dual_bound",
     "gather",
