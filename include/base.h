@@ -227,6 +227,58 @@ int base_permute(const void *in, const int32_t *perm, void *out, int64_t T, int6
                  int inverse, void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Test-time routing and the gated residual                                  */
+/* ------------------------------------------------------------------------ */
+/*
+ * base_greedy_assign - Sec. 3.2.2: at test time every token takes its
+ * highest-scoring expert (lowest index on ties; a row of NaN/-inf takes
+ * expert 0). No balance: expert loads are whatever the scores give.
+ *   S         [device] T x E float32 scores, row-major, 16-byte aligned
+ *   assign    [device] int32 [T] out
+ *   perm      [device] int32 [T] out: the stable sort of assign (experts
+ *             ascending, tokens ascending within an expert)
+ *   offsets   [device] int32 [E + 1] out: expert e's rows of the routed order
+ *             are [offsets[e], offsets[e + 1])
+ *   workspace [device] base_greedy_workspace_size(T, E) bytes, 256-aligned
+ *   0 < T < 2^31, 0 < E <= 2048.
+ * Errors: BASE_ERR_INVALID_ARG, BASE_ERR_RANGE, BASE_ERR_WORKSPACE, BASE_ERR_HIP.
+ *
+ * base_gate_combine - Sec. 3.1, Eq. 1, fused into the return to token order:
+ *     out[t] = sigmoid(S[t, a_t]) * F[k] + H[t]   for t = perm[k],
+ * where F [T x d] is the experts' output in routed order (row k belongs to
+ * token perm[k]) and S[t, a_t] = h_t . w_{a_t} the affinity already computed.
+ * fp32 arithmetic; BASE_BF16 rows are widened exactly and the result rounded
+ * to nearest even. F, H, out: [device] T x d of dtype (BASE_BF16 or BASE_F32),
+ * 16-byte aligned, out must not overlap F or H; d % 8 == 0. perm must be a
+ * permutation of [0, T) and assign[t] in [0, E) (not checked; an entry out
+ * of range is treated as expert 0 / the row skipped, never read out of bounds).
+ *
+ * base_gate_backward - the gradient of Eq. 1's gate and residual with the
+ * expert output held fixed (its own backward belongs to the expert network),
+ * for an upstream gradient dY of the layer output:
+ *     dS[t]  = g_t (1 - g_t) (dY[t] . f_t),   g_t = sigmoid(S[t, a_t])
+ *     dH[t]  = dY[t] + dS[t] W[a_t]
+ *     dF[k]  = g_t dY[t]                      (routed order, t = perm[k])
+ *     dW[e]  = sum over t with a_t = e of dS[t] H[t]
+ * dY, F, H, dH, dF: T x d of dtype; W: E x d of dtype; dW: E x d float32;
+ * dS: float32 [T]. offsets [E + 1]: expert row ranges of the routed order
+ * (e * T/E for a balanced assignment; base_greedy_assign's for a greedy one).
+ * Accumulation in fp32 in a fixed order (deterministic).
+ * Errors: BASE_ERR_INVALID_ARG, BASE_ERR_UNSUPPORTED_DTYPE, BASE_ERR_RANGE,
+ * BASE_ERR_HIP.
+ */
+size_t base_greedy_workspace_size(int64_t T, int64_t E);
+int base_greedy_assign(const float *S, int64_t T, int64_t E, int32_t *assign, int32_t *perm,
+                       int32_t *offsets, void *workspace, size_t workspace_bytes, void *stream);
+int base_gate_combine(const void *F, const void *H, const float *S, const int32_t *assign,
+                      const int32_t *perm, void *out, int64_t T, int64_t E, int64_t d, int dtype,
+                      void *stream);
+int base_gate_backward(const void *dY, const void *F, const void *H, const void *W,
+                       const float *S, const int32_t *assign, const int32_t *perm,
+                       const int32_t *offsets, void *dH, void *dF, float *dW, float *dS,
+                       int64_t T, int64_t E, int64_t d, int dtype, void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Measurement support                                                       */
 /* ------------------------------------------------------------------------ */
 /*

@@ -43,7 +43,8 @@ BASE_ASSIGN_CHECK_FINITE = 4
 # Every symbol include/base.h declares.
 EXPORTED = ("base_status_string", "base_affinity", "base_assign_workspace_size", "base_assign",
             "base_assign_batched_workspace_size", "base_assign_batched", "base_permute",
-            "base_timing_enable", "base_timing_read")
+            "base_greedy_workspace_size", "base_greedy_assign", "base_gate_combine",
+            "base_gate_backward", "base_timing_enable", "base_timing_read")
 
 
 class AssignOpts(ctypes.Structure):
@@ -94,6 +95,15 @@ def lib() -> ctypes.CDLL:
         L.base_assign_batched.restype = i32
         L.base_permute.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
         L.base_permute.restype = i32
+        L.base_greedy_workspace_size.argtypes = [i64, i64]
+        L.base_greedy_workspace_size.restype = ctypes.c_size_t
+        L.base_greedy_assign.argtypes = [vp, i64, i64, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.base_greedy_assign.restype = i32
+        L.base_gate_combine.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i32, vp]
+        L.base_gate_combine.restype = i32
+        L.base_gate_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64,
+                                         i64, i32, vp]
+        L.base_gate_backward.restype = i32
         L.base_timing_enable.argtypes = [ctypes.c_int32]
         L.base_timing_enable.restype = i32
         L.base_timing_read.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(ctypes.c_double)]
@@ -251,6 +261,67 @@ def permute(x, perm, inverse: bool = False, out=None, stream=None):
     return out
 
 
+def greedy_assign(S, workspace=None, stream=None):
+    """Test-time routing (base_greedy_assign): (assign [T], perm [T],
+    offsets [E + 1]) with every token at its best expert."""
+    torch = _torch()
+    _need_device(S)
+    T, E = S.shape
+    dev = S.device
+    a = torch.empty(T, dtype=torch.int32, device=dev)
+    perm = torch.empty(T, dtype=torch.int32, device=dev)
+    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    n = int(lib().base_greedy_workspace_size(T, E))
+    if workspace is None:
+        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+    _check(lib().base_greedy_assign(S.data_ptr(), T, E, a.data_ptr(), perm.data_ptr(),
+                                    offsets.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                    _stream_ptr(stream)), "base_greedy_assign")
+    return a, perm, offsets
+
+
+def gate_combine(F, H, S, assign, perm, out=None, stream=None):
+    """Eq. 1 fused into the return to token order (base_gate_combine):
+    out[t] = sigmoid(S[t, assign[t]]) * F[k] + H[t] for t = perm[k]."""
+    torch = _torch()
+    _need_device(F, H, S, assign, perm)
+    T, d = H.shape
+    E = S.shape[1]
+    if out is None:
+        out = torch.empty_like(H)
+    _check(lib().base_gate_combine(F.data_ptr(), H.data_ptr(), S.data_ptr(), assign.data_ptr(),
+                                   perm.data_ptr(), out.data_ptr(), T, E, d, _dtype_code(H),
+                                   _stream_ptr(stream)), "base_gate_combine")
+    return out
+
+
+def balanced_offsets(T: int, E: int, device):
+    """Routed-order row ranges of a balanced assignment: offsets[e] = e * T/E."""
+    torch = _torch()
+    return torch.arange(E + 1, dtype=torch.int32).mul_(T // E).to(device)
+
+
+def gate_backward(dY, F, H, W, S, assign, perm, offsets=None, stream=None):
+    """Gradient of Eq. 1's gate and residual (base_gate_backward): returns
+    (dH, dF in routed order, dW float32, dS float32)."""
+    torch = _torch()
+    _need_device(dY, F, H, W, S, assign, perm)
+    T, d = H.shape
+    E = W.shape[0]
+    if offsets is None:
+        offsets = balanced_offsets(T, E, H.device)
+    dH = torch.empty_like(H)
+    dF = torch.empty_like(F)
+    dW = torch.empty((E, d), dtype=torch.float32, device=H.device)
+    dS = torch.empty(T, dtype=torch.float32, device=H.device)
+    _check(lib().base_gate_backward(dY.data_ptr(), F.data_ptr(), H.data_ptr(), W.data_ptr(),
+                                    S.data_ptr(), assign.data_ptr(), perm.data_ptr(),
+                                    offsets.data_ptr(), dH.data_ptr(), dF.data_ptr(),
+                                    dW.data_ptr(), dS.data_ptr(), T, E, d, _dtype_code(H),
+                                    _stream_ptr(stream)), "base_gate_backward")
+    return dH, dF, dW, dS
+
+
 def timing_enable(capacity: int) -> None:
     """Start recording event timings of the engine kernel's launches
     (base_timing_enable); capacity <= 0 stops and frees the record."""
@@ -266,7 +337,8 @@ def timing_read() -> tuple[int, float]:
     return int(n.value), float(ms.value)
 
 
-__all__ = ["affinity", "assign", "assign_batched", "permute", "assign_workspace_size",
+__all__ = ["affinity", "assign", "assign_batched", "permute", "greedy_assign", "gate_combine",
+           "gate_backward", "balanced_offsets", "assign_workspace_size",
            "assign_batched_workspace_size", "timing_enable",
            "timing_read", "AssignResult", "AssignOpts", "AssignStats", "BaseError", "lib",
            "status_string", "EXPORTED"]

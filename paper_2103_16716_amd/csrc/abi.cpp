@@ -205,6 +205,63 @@ int base_assign_batched(const void *S, int s_dtype, int64_t B, int64_t T, int64_
                        workspace_bytes, stats, stream);
 }
 
+size_t base_greedy_workspace_size(int64_t T, int64_t E) {
+    if (T <= 0 || E <= 0 || T > INT32_MAX || E > kMaxExperts) return 0;
+    return base::greedy_workspace_size(T, E);
+}
+
+int base_greedy_assign(const float *S, int64_t T, int64_t E, int32_t *assign, int32_t *perm,
+                       int32_t *offsets, void *workspace, size_t workspace_bytes, void *stream) {
+    if (S == nullptr || assign == nullptr || perm == nullptr || offsets == nullptr)
+        return BASE_ERR_INVALID_ARG;
+    if (T <= 0 || E <= 0) return BASE_ERR_INVALID_ARG;
+    if (T > INT32_MAX || E > kMaxExperts) return BASE_ERR_RANGE;
+    if (!aligned(S, 16) || !aligned(assign, 4) || !aligned(perm, 4) || !aligned(offsets, 4))
+        return BASE_ERR_INVALID_ARG;
+    if (workspace == nullptr || workspace_bytes < base::greedy_workspace_size(T, E) ||
+        !aligned(workspace, 256))
+        return BASE_ERR_WORKSPACE;
+    return hip_status(base::launch_greedy(S, T, E, assign, perm, offsets, workspace,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+int base_gate_combine(const void *F, const void *H, const float *S, const int32_t *assign,
+                      const int32_t *perm, void *out, int64_t T, int64_t E, int64_t d, int dtype,
+                      void *stream) {
+    if (F == nullptr || H == nullptr || S == nullptr || assign == nullptr || perm == nullptr ||
+        out == nullptr)
+        return BASE_ERR_INVALID_ARG;
+    if (T <= 0 || E <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
+    if (dtype != BASE_BF16 && dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
+    if (T > INT32_MAX || E > INT32_MAX || d > kMaxDim) return BASE_ERR_RANGE;
+    if (!aligned(F, 16) || !aligned(H, 16) || !aligned(out, 16) || !aligned(S, 4) ||
+        !aligned(assign, 4) || !aligned(perm, 4))
+        return BASE_ERR_INVALID_ARG;
+    return hip_status(base::launch_gate_combine(F, H, S, assign, perm, out, T, E, d,
+                                                dtype == BASE_BF16 ? 1 : 0,
+                                                static_cast<hipStream_t>(stream)));
+}
+
+int base_gate_backward(const void *dY, const void *F, const void *H, const void *W,
+                       const float *S, const int32_t *assign, const int32_t *perm,
+                       const int32_t *offsets, void *dH, void *dF, float *dW, float *dS,
+                       int64_t T, int64_t E, int64_t d, int dtype, void *stream) {
+    if (dY == nullptr || F == nullptr || H == nullptr || W == nullptr || S == nullptr ||
+        assign == nullptr || perm == nullptr || offsets == nullptr || dH == nullptr ||
+        dF == nullptr || dW == nullptr || dS == nullptr)
+        return BASE_ERR_INVALID_ARG;
+    if (T <= 0 || E <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
+    if (dtype != BASE_BF16 && dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
+    if (T > INT32_MAX || E > 65535 || d > kMaxDim) return BASE_ERR_RANGE;
+    if (!aligned(dY, 16) || !aligned(F, 16) || !aligned(H, 16) || !aligned(W, 16) ||
+        !aligned(dH, 16) || !aligned(dF, 16) || !aligned(dW, 4) || !aligned(dS, 4) ||
+        !aligned(S, 4) || !aligned(assign, 4) || !aligned(perm, 4) || !aligned(offsets, 4))
+        return BASE_ERR_INVALID_ARG;
+    return hip_status(base::launch_gate_backward(dY, F, H, W, S, assign, perm, offsets, dH, dF, dW,
+                                                 dS, T, E, d, dtype == BASE_BF16 ? 1 : 0,
+                                                 static_cast<hipStream_t>(stream)));
+}
+
 int base_timing_enable(int32_t capacity) {
     return hip_status(base::timing_enable(capacity));
 }

@@ -1,0 +1,381 @@
+// Test-time routing and the gated residual of a BASE layer.
+//
+// Sec. 3.2.2: at test time every token goes to its highest-scoring expert
+// (no balance). Sec. 3.1, Eq. 1: the layer returns
+//     y_t = sigmoid(h_t . w_{a_t}) f_{a_t}(h_t) + h_t,
+// where the expert output f arrives in routed (expert-contiguous) order:
+// row k belongs to token perm[k] (Fig. 2 caption; Sec. 3, the output returns
+// to the token's position). The gate score h_t . w_{a_t} is the affinity
+// S[t, a_t] already computed for the routing.
+//
+// Kernels:
+//   greedy_count_kernel    argmax per token (16 lanes per token, 8 experts
+//                          per lane per chunk of 128) + per-block expert counts
+//   greedy_scan_kernel     per-expert exclusive scan over the blocks
+//   greedy_offsets_kernel  exclusive scan of the expert totals -> offsets
+//   greedy_scatter_kernel  stable counting sort -> perm
+//   gate_combine_kernel    y = g * F[k] + H[t] for t = perm[k] (16-byte chunks)
+//   gate_rows_kernel       backward per routed row: dS, dF, dH
+//   gate_dw_kernel         dW[e] = sum over expert e's rows of dS_t h_t
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "base.h"
+#include "internal.hpp"
+
+namespace base {
+namespace {
+
+constexpr int kGreedyTile = 256;   // tokens per block of the greedy count
+constexpr int kGroup = 16;         // lanes per token in the argmax
+
+__device__ inline int lane_of() { return threadIdx.x & 63; }
+
+__device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN kept quiet).
+__device__ inline uint32_t f32_to_bf16_bits(float x) {
+    uint32_t u = __float_as_uint(x);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ inline float gate_of(float s) { return 1.0f / (1.0f + expf(-s)); }
+
+// ---------------------------------------------------------------- greedy --
+
+__global__ __launch_bounds__(256) void greedy_count_kernel(const float *S, int T, int E,
+                                                           int32_t *assign, int32_t *blk) {
+    extern __shared__ int hist[];
+    for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
+    __syncthreads();
+    const int gl = lane_of() & (kGroup - 1);
+    const int per_pass = blockDim.x / kGroup;
+    const int t0 = blockIdx.x * kGreedyTile;
+    for (int j = threadIdx.x / kGroup; j < kGreedyTile; j += per_pass) {
+        const int t = t0 + j;
+        const bool valid = t < T;
+        float best = -INFINITY;
+        int be = 0x7fffffff;
+        if (valid) {
+            const float *row = S + (int64_t)t * E;
+            for (int base = 0; base < E; base += 8 * kGroup) {
+                const int e0 = base + 8 * gl;
+                if (e0 >= E) break;
+                float v[8];
+                if (e0 + 8 <= E && (E & 3) == 0) {   // 16-byte aligned rows
+                    const float4 x = *reinterpret_cast<const float4 *>(row + e0);
+                    const float4 y = *reinterpret_cast<const float4 *>(row + e0 + 4);
+                    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+                    v[4] = y.x; v[5] = y.y; v[6] = y.z; v[7] = y.w;
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) v[q] = e0 + q < E ? row[e0 + q] : -INFINITY;
+                }
+#pragma unroll
+                for (int q = 0; q < 8; ++q)
+                    if (e0 + q < E && v[q] > best) {   // ascending scan: ties keep the lower expert
+                        best = v[q];
+                        be = e0 + q;
+                    }
+            }
+        }
+#pragma unroll
+        for (int off = kGroup / 2; off > 0; off >>= 1) {
+            const float ob = __shfl_xor(best, off);
+            const int oe = __shfl_xor(be, off);
+            if (ob > best || (ob == best && oe < be)) {
+                best = ob;
+                be = oe;
+            }
+        }
+        if (valid && gl == 0) {
+            const int a = (be >= 0 && be < E) ? be : 0;   // a row of NaN/-inf goes to expert 0
+            assign[t] = a;
+            atomicAdd(&hist[a], 1);
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += blockDim.x) blk[(int64_t)blockIdx.x * E + e] = hist[e];
+}
+
+// Expert e's block counts -> exclusive running sums (in place); the total goes
+// to offsets[e + 1].
+__global__ __launch_bounds__(256) void greedy_scan_kernel(int32_t *blk, int nblk, int E,
+                                                          int32_t *offsets) {
+    __shared__ int wsum[4];
+    __shared__ int carry;
+    const int e = blockIdx.x;
+    const int lane = lane_of();
+    const int wave = threadIdx.x >> 6;
+    if (threadIdx.x == 0) carry = 0;
+    __syncthreads();
+    for (int b0 = 0; b0 < nblk; b0 += 256) {
+        const int b = b0 + threadIdx.x;
+        const int v = b < nblk ? blk[(int64_t)b * E + e] : 0;
+        int incl = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(incl, off);
+            if (lane >= off) incl += o;
+        }
+        if (lane == 63) wsum[wave] = incl;
+        __syncthreads();
+        int before = carry;
+        for (int w = 0; w < wave; ++w) before += wsum[w];
+        if (b < nblk) blk[(int64_t)b * E + e] = before + incl - v;
+        __syncthreads();
+        if (threadIdx.x == 0) carry += wsum[0] + wsum[1] + wsum[2] + wsum[3];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) offsets[e + 1] = carry;
+}
+
+// offsets[1..E] hold the totals; turn them into the exclusive scan (one block).
+__global__ __launch_bounds__(1024) void greedy_offsets_kernel(int32_t *offsets, int E) {
+    __shared__ int wsum[16];
+    __shared__ int carry;
+    const int lane = lane_of();
+    const int wave = threadIdx.x >> 6;
+    if (threadIdx.x == 0) {
+        carry = 0;
+        offsets[0] = 0;
+    }
+    __syncthreads();
+    for (int e0 = 0; e0 < E; e0 += 1024) {
+        const int e = e0 + threadIdx.x;
+        const int v = e < E ? offsets[e + 1] : 0;
+        int incl = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(incl, off);
+            if (lane >= off) incl += o;
+        }
+        if (lane == 63) wsum[wave] = incl;
+        __syncthreads();
+        int before = carry;
+        for (int w = 0; w < wave; ++w) before += wsum[w];
+        __syncthreads();
+        if (e < E) offsets[e + 1] = before + incl;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int tot = 0;
+            for (int w = 0; w < 16; ++w) tot += wsum[w];
+            carry += tot;
+        }
+        __syncthreads();
+    }
+}
+
+// perm[offsets[a] + blk[block][a] + rank of t among the block's tokens of a] = t.
+__global__ __launch_bounds__(kGreedyTile) void greedy_scatter_kernel(const int32_t *assign, int T,
+                                                                     int E, const int32_t *blk,
+                                                                     const int32_t *offsets,
+                                                                     int32_t *perm) {
+    __shared__ int loc[kGreedyTile];
+    const int t = blockIdx.x * kGreedyTile + threadIdx.x;
+    const int a = t < T ? assign[t] : -1;
+    loc[threadIdx.x] = a;
+    __syncthreads();
+    if (a < 0 || a >= E) return;
+    int rank = 0;
+    for (int j = 0; j < (int)threadIdx.x; ++j) rank += (loc[j] == a);
+    const int pos = offsets[a] + blk[(int64_t)blockIdx.x * E + a] + rank;
+    if (pos >= 0 && pos < T) perm[pos] = t;
+}
+
+// ---------------------------------------------------------- gated residual --
+
+// One 16-byte chunk of a row: 8 bf16 or 4 fp32 values, widened to fp32.
+template <bool BF16>
+struct Chunk {
+    static constexpr int kN = BF16 ? 8 : 4;
+    __device__ static void load(const void *base, int64_t chunk, float (&v)[8]) {
+        const uint4 x = reinterpret_cast<const uint4 *>(base)[chunk];
+        const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+        if (BF16) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) v[i] = bf16_bits_to_f32((w[i >> 1] >> (16 * (i & 1))) & 0xffffu);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[i] = __uint_as_float(w[i]);
+        }
+    }
+    __device__ static void store(void *base, int64_t chunk, const float (&v)[8]) {
+        uint32_t w[4];
+        if (BF16) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                w[i] = f32_to_bf16_bits(v[2 * i]) | (f32_to_bf16_bits(v[2 * i + 1]) << 16);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(v[i]);
+        }
+        reinterpret_cast<uint4 *>(base)[chunk] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+};
+
+// y[t] = g_t F[k] + H[t] for t = perm[k], g_t = sigmoid(S[t, assign[t]]).
+// Each thread takes 16-byte chunks; a row is ncs chunks.
+template <bool BF16>
+__global__ __launch_bounds__(256) void gate_combine_kernel(const void *F, const void *H,
+                                                           const float *S,
+                                                           const int32_t *assign,
+                                                           const int32_t *perm, void *Y, int T,
+                                                           int E, int ncs) {
+    using Ck = Chunk<BF16>;
+    const int64_t total = (int64_t)T * ncs;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int k = (int)(i / ncs);
+        const int j = (int)(i - (int64_t)k * ncs);
+        const int t = perm[k];
+        if (t < 0 || t >= T) continue;   // not a permutation: undefined, but in bounds
+        int a = assign[t];
+        a = (a >= 0 && a < E) ? a : 0;
+        const float g = gate_of(S[(int64_t)t * E + a]);
+        float f[8], h[8], y[8];
+        Ck::load(F, (int64_t)k * ncs + j, f);
+        Ck::load(H, (int64_t)t * ncs + j, h);
+#pragma unroll
+        for (int q = 0; q < Ck::kN; ++q) y[q] = fmaf(g, f[q], h[q]);
+        Ck::store(Y, (int64_t)t * ncs + j, y);
+    }
+}
+
+// Backward per routed row k (one block per row, grid-stride): with t =
+// perm[k], a = assign[t], g = sigmoid(S[t, a]):
+//   dS[t] = g (1 - g) (dY[t] . F[k]);  dF[k] = g dY[t];  dH[t] = dY[t] + dS[t] W[a].
+template <bool BF16>
+__global__ __launch_bounds__(256) void gate_rows_kernel(const void *dY, const void *F,
+                                                        const void *W, const float *S,
+                                                        const int32_t *assign,
+                                                        const int32_t *perm, void *dH, void *dF,
+                                                        float *dS, int T, int E, int ncs) {
+    using Ck = Chunk<BF16>;
+    __shared__ float part[4];
+    for (int k = blockIdx.x; k < T; k += gridDim.x) {
+        const int t = perm[k];
+        const bool ok = t >= 0 && t < T;
+        const int tt = ok ? t : 0;
+        int a = assign[tt];
+        a = (a >= 0 && a < E) ? a : 0;
+        const float g = gate_of(S[(int64_t)tt * E + a]);
+        float dot = 0.0f;
+        for (int j = threadIdx.x; j < ncs; j += blockDim.x) {
+            float y[8], f[8];
+            Ck::load(dY, (int64_t)tt * ncs + j, y);
+            Ck::load(F, (int64_t)k * ncs + j, f);
+#pragma unroll
+            for (int q = 0; q < Ck::kN; ++q) dot = fmaf(y[q], f[q], dot);
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
+        if (lane_of() == 0) part[threadIdx.x >> 6] = dot;
+        __syncthreads();
+        dot = 0.0f;
+        for (int w = 0; w < (int)(blockDim.x >> 6); ++w) dot += part[w];
+        __syncthreads();
+        const float ds = g * (1.0f - g) * dot;
+        if (!ok) continue;
+        if (threadIdx.x == 0) dS[t] = ds;
+        for (int j = threadIdx.x; j < ncs; j += blockDim.x) {
+            float y[8], w[8], o[8];
+            Ck::load(dY, (int64_t)t * ncs + j, y);
+#pragma unroll
+            for (int q = 0; q < Ck::kN; ++q) o[q] = g * y[q];
+            Ck::store(dF, (int64_t)k * ncs + j, o);
+            Ck::load(W, (int64_t)a * ncs + j, w);
+#pragma unroll
+            for (int q = 0; q < Ck::kN; ++q) o[q] = fmaf(ds, w[q], y[q]);
+            Ck::store(dH, (int64_t)t * ncs + j, o);
+        }
+    }
+}
+
+// dW[e][c] = sum over routed rows k in [offsets[e], offsets[e + 1]) of
+// dS[t] H[t][c], t = perm[k]. One block per (expert, 256 columns).
+template <bool BF16>
+__global__ __launch_bounds__(256) void gate_dw_kernel(const void *H, const float *dS,
+                                                      const int32_t *perm,
+                                                      const int32_t *offsets, float *dW, int T,
+                                                      int E, int d) {
+    const int e = blockIdx.x;
+    const int c = blockIdx.y * blockDim.x + threadIdx.x;
+    if (e >= E || c >= d) return;
+    int k0 = offsets[e], k1 = offsets[e + 1];
+    k0 = k0 < 0 ? 0 : (k0 > T ? T : k0);
+    k1 = k1 < k0 ? k0 : (k1 > T ? T : k1);
+    float acc = 0.0f;
+    for (int k = k0; k < k1; ++k) {
+        const int t = perm[k];
+        if (t < 0 || t >= T) continue;
+        float h;
+        if (BF16) h = bf16_bits_to_f32(reinterpret_cast<const uint16_t *>(H)[(int64_t)t * d + c]);
+        else h = reinterpret_cast<const float *>(H)[(int64_t)t * d + c];
+        acc = fmaf(dS[t], h, acc);
+    }
+    dW[(int64_t)e * d + c] = acc;
+}
+
+}  // namespace
+
+size_t greedy_workspace_size(int64_t T, int64_t E) {
+    const int64_t nblk = (T + kGreedyTile - 1) / kGreedyTile;
+    return (size_t)(nblk * E * 4 + 255) & ~size_t(255);
+}
+
+hipError_t launch_greedy(const float *S, int64_t T, int64_t E, int32_t *assign, int32_t *perm,
+                         int32_t *offsets, void *workspace, hipStream_t s) {
+    const int nblk = (int)((T + kGreedyTile - 1) / kGreedyTile);
+    int32_t *blk = static_cast<int32_t *>(workspace);
+    hipLaunchKernelGGL(greedy_count_kernel, dim3(nblk), dim3(256), (size_t)E * sizeof(int), s, S,
+                       (int)T, (int)E, assign, blk);
+    hipLaunchKernelGGL(greedy_scan_kernel, dim3((unsigned)E), dim3(256), 0, s, blk, nblk, (int)E,
+                       offsets);
+    hipLaunchKernelGGL(greedy_offsets_kernel, dim3(1), dim3(1024), 0, s, offsets, (int)E);
+    hipLaunchKernelGGL(greedy_scatter_kernel, dim3(nblk), dim3(kGreedyTile), 0, s, assign, (int)T,
+                       (int)E, blk, offsets, perm);
+    return hipGetLastError();
+}
+
+hipError_t launch_gate_combine(const void *F, const void *H, const float *S,
+                               const int32_t *assign, const int32_t *perm, void *Y, int64_t T,
+                               int64_t E, int64_t d, int bf16, hipStream_t s) {
+    const int ncs = (int)(d / (bf16 ? 8 : 4));
+    int64_t total = T * ncs;
+    int blocks = (int)((total + 255) / 256);
+    if (blocks > 8192) blocks = 8192;
+    if (bf16)
+        hipLaunchKernelGGL(gate_combine_kernel<true>, dim3(blocks), dim3(256), 0, s, F, H, S,
+                           assign, perm, Y, (int)T, (int)E, ncs);
+    else
+        hipLaunchKernelGGL(gate_combine_kernel<false>, dim3(blocks), dim3(256), 0, s, F, H, S,
+                           assign, perm, Y, (int)T, (int)E, ncs);
+    return hipGetLastError();
+}
+
+hipError_t launch_gate_backward(const void *dY, const void *F, const void *H, const void *W,
+                                const float *S, const int32_t *assign, const int32_t *perm,
+                                const int32_t *offsets, void *dH, void *dF, float *dW, float *dS,
+                                int64_t T, int64_t E, int64_t d, int bf16, hipStream_t s) {
+    const int ncs = (int)(d / (bf16 ? 8 : 4));
+    const int rows = (int)(T < 65536 ? T : 65536);
+    const dim3 dwg((unsigned)E, (unsigned)((d + 255) / 256));
+    if (bf16) {
+        hipLaunchKernelGGL(gate_rows_kernel<true>, dim3(rows), dim3(256), 0, s, dY, F, W, S, assign,
+                           perm, dH, dF, dS, (int)T, (int)E, ncs);
+        hipLaunchKernelGGL(gate_dw_kernel<true>, dwg, dim3(256), 0, s, H, dS, perm, offsets, dW,
+                           (int)T, (int)E, (int)d);
+    } else {
+        hipLaunchKernelGGL(gate_rows_kernel<false>, dim3(rows), dim3(256), 0, s, dY, F, W, S,
+                           assign, perm, dH, dF, dS, (int)T, (int)E, ncs);
+        hipLaunchKernelGGL(gate_dw_kernel<false>, dwg, dim3(256), 0, s, H, dS, perm, offsets, dW,
+                           (int)T, (int)E, (int)d);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace base

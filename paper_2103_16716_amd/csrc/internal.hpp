@@ -65,6 +65,19 @@ hipError_t launch_assign(const void *S, const AssignParams &p, int64_t B, int32_
 hipError_t read_assign_stats(const void *workspace, int64_t T, int64_t E, int64_t B,
                              SolveCtrl *out, hipStream_t stream);
 
+// Test-time routing (argmax per token, stable counting sort) and the gated
+// residual of Eq. 1 with its gradient (gate.hip).
+size_t greedy_workspace_size(int64_t T, int64_t E);
+hipError_t launch_greedy(const float *S, int64_t T, int64_t E, int32_t *assign, int32_t *perm,
+                         int32_t *offsets, void *workspace, hipStream_t s);
+hipError_t launch_gate_combine(const void *F, const void *H, const float *S,
+                               const int32_t *assign, const int32_t *perm, void *Y, int64_t T,
+                               int64_t E, int64_t d, int bf16, hipStream_t s);
+hipError_t launch_gate_backward(const void *dY, const void *F, const void *H, const void *W,
+                                const float *S, const int32_t *assign, const int32_t *perm,
+                                const int32_t *offsets, void *dH, void *dF, float *dW, float *dS,
+                                int64_t T, int64_t E, int64_t d, int bf16, hipStream_t s);
+
 // Event timing of the engine kernel's launches (measurement support).
 hipError_t timing_enable(int32_t capacity);
 hipError_t timing_read(int64_t *launches, double *total_ms);
