@@ -135,7 +135,11 @@ enum {
                                         the epsilon bound void; stats.fell_back = 1) */
     BASE_ASSIGN_SYNC_STATS = 2,      /* wait for the solve, fill *stats, report
                                         NOT_CONVERGED / RANGE */
-    BASE_ASSIGN_CHECK_FINITE = 4     /* scan S first (synchronous); NaN/Inf -> BASE_ERR_NONFINITE */
+    BASE_ASSIGN_CHECK_FINITE = 4,    /* scan S first (synchronous); NaN/Inf -> BASE_ERR_NONFINITE */
+    BASE_ASSIGN_WARM_PRICES = 8      /* start from the prices in `prices` (then overwritten
+                                        with the result) instead of 0, e.g. the prices of
+                                        the previous batch; must be finite (float mode) or
+                                        in scaled units (integer mode) */
 };
 
 typedef struct {
@@ -158,6 +162,10 @@ typedef struct {
     int32_t converged;   /* 1 if every expert holds exactly T/E tokens */
     int64_t engine_bids; /* the part of `bids` placed inside the single-workgroup
                             engine (the rounds with few active tokens) */
+    double dual_gap;     /* D(p) - sum_t S[t, a_t] for the returned prices, in score
+                            units: an upper bound of optimum - objective for a balanced
+                            result (the certificate of the bound above; after the greedy
+                            fallback it measures what the fallback gave up) */
 } base_assign_stats;
 
 /* Bytes of device workspace base_assign needs for T tokens and E experts

@@ -39,6 +39,7 @@ BASE_I16 = 2
 BASE_ASSIGN_GREEDY_FALLBACK = 1
 BASE_ASSIGN_SYNC_STATS = 2
 BASE_ASSIGN_CHECK_FINITE = 4
+BASE_ASSIGN_WARM_PRICES = 8
 
 # Every symbol include/base.h declares.
 EXPORTED = ("base_status_string", "base_affinity", "base_assign_workspace_size", "base_assign",
@@ -56,7 +57,8 @@ class AssignOpts(ctypes.Structure):
 class AssignStats(ctypes.Structure):
     _fields_ = [("phases", ctypes.c_int32), ("rounds", ctypes.c_int32), ("bids", ctypes.c_int64),
                 ("eps_final", ctypes.c_double), ("fell_back", ctypes.c_int32),
-                ("converged", ctypes.c_int32), ("engine_bids", ctypes.c_int64)]
+                ("converged", ctypes.c_int32), ("engine_bids", ctypes.c_int64),
+                ("dual_gap", ctypes.c_double)]
 
 
 class BaseError(RuntimeError):
@@ -182,10 +184,17 @@ class AssignResult:
 
 def assign(S, *, eps_final: float = 0.0, eps_initial: float = 0.0, eps_factor: float = 0.0,
            max_rounds: int = 0, flags: int = 0, sync_stats: bool = True, workspace=None,
-           out_assign=None, out_perm=None, out_prices=None, stream=None) -> AssignResult:
+           out_assign=None, out_perm=None, out_prices=None, warm_start: bool = False,
+           stream=None) -> AssignResult:
     """Balanced assignment of Eq. 2 (base_assign). Zero-valued options take
     the library defaults. With sync_stats (the default) the call waits for the
-    solve and returns its statistics; pass False to keep it asynchronous."""
+    solve and returns its statistics; pass False to keep it asynchronous.
+    With warm_start the solve starts from the prices in out_prices (required;
+    overwritten with the result)."""
+    if warm_start:
+        if out_prices is None:
+            raise ValueError("warm_start needs out_prices holding the starting prices")
+        flags |= BASE_ASSIGN_WARM_PRICES
     torch = _torch()
     _need_device(S)
     T, E = S.shape

@@ -98,9 +98,10 @@ int assign_impl(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
         if (!(o.eps_final > 0.0)) o.eps_final = 1e-4;
         if (!(o.eps_factor > 1.0)) o.eps_factor = kDefaultEpsFactor;
         if (o.max_rounds <= 0) o.max_rounds = 4000000;
-        const uint32_t known =
-            BASE_ASSIGN_GREEDY_FALLBACK | BASE_ASSIGN_SYNC_STATS | BASE_ASSIGN_CHECK_FINITE;
+        const uint32_t known = BASE_ASSIGN_GREEDY_FALLBACK | BASE_ASSIGN_SYNC_STATS |
+                               BASE_ASSIGN_CHECK_FINITE | BASE_ASSIGN_WARM_PRICES;
         if (o.flags & ~known) return BASE_ERR_INVALID_ARG;
+        if ((o.flags & BASE_ASSIGN_WARM_PRICES) && prices == nullptr) return BASE_ERR_INVALID_ARG;
     }
 
     const size_t need = base::assign_workspace_size(T, E) * (size_t)B;
@@ -127,6 +128,7 @@ int assign_impl(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
     p.eps_factor = o.eps_factor;
     p.max_rounds = o.max_rounds;
     p.flags = o.flags;
+    p.warm_prices = (o.flags & BASE_ASSIGN_WARM_PRICES) ? prices : nullptr;
 
     if ((o.flags & BASE_ASSIGN_CHECK_FINITE) && !integer) {
         int bad = 0;
@@ -157,6 +159,7 @@ int assign_impl(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
             agg.rounds = c.rounds > agg.rounds ? c.rounds : agg.rounds;
             agg.bids += (int64_t)c.bids;
             agg.engine_bids += (int64_t)c.engine_bids;
+            agg.dual_gap += integer ? c.dual_gap / (double)p.scale : c.dual_gap;
             const double eps = integer ? c.eps / (double)p.scale : c.eps;
             agg.eps_final = eps > agg.eps_final ? eps : agg.eps_final;
             agg.fell_back |= c.fell_back;

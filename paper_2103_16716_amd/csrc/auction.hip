@@ -1010,7 +1010,21 @@ __global__ void init_kernel(SolveCtrl *ctrl, void *prices, int E, AssignParams p
         z.eps_final_eff = p.eps_final;
         *ctrl = z;
     }
-    for (int e = tid; e < E; e += blockDim.x) reinterpret_cast<int64_t *>(prices)[e] = 0;
+    if (prices == nullptr) return;
+    // Prices start at 0, or at the caller's (warm start: prices only rise
+    // from any starting point, which keeps every bid's complementary
+    // slackness argument intact).
+    for (int e = tid; e < E; e += blockDim.x) {
+        if (p.warm_prices == nullptr) {
+            reinterpret_cast<int64_t *>(prices)[e] = 0;
+        } else if (p.integer) {
+            reinterpret_cast<int64_t *>(prices)[e] =
+                reinterpret_cast<const int64_t *>(p.warm_prices)[(int64_t)blockIdx.y * E + e];
+        } else {
+            reinterpret_cast<float *>(prices)[e] =
+                reinterpret_cast<const float *>(p.warm_prices)[(int64_t)blockIdx.y * E + e];
+        }
+    }
 }
 
 // Score range (order-preserving images) and a non-finite count.
@@ -2283,6 +2297,72 @@ __global__ void holders_to_assign_kernel(Ctx<M> c0, int32_t *assign) {
     if (threadIdx.x == 0 && h != c.C) atomicAdd(&c.ctrl->unconverged_experts, 1);
 }
 
+int lanes_per_token(int64_t E);
+
+// The duality gap of the result (statistics only): D(p) - objective =
+//     sum_t [max_e (S[t,e] - p[e]) - S[t, a_t]] + C sum_e p[e],
+// per-token values in the solve's arithmetic, the sum in double. For a
+// balanced assignment it bounds the distance to the optimum from above.
+template <class M, int G>
+__global__ __launch_bounds__(kThreads) void dual_gap_kernel(Ctx<M> c0, const int32_t *assign) {
+    using value_t = typename M::value_t;
+    const Ctx<M> c = c0.at(blockIdx.y);
+    assign += (int64_t)blockIdx.y * c.T;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
+    __shared__ double part[kThreads / 64];
+    for (int e = threadIdx.x; e < c.E; e += kThreads) pr[e] = c.prices[e];
+    __syncthreads();
+    const int gl = lane_id() & (G - 1);
+    const int per_block = kThreads / G;
+    const int ngroups = per_block * gridDim.x;
+    const int n_round = ((c.T + ngroups - 1) / ngroups) * ngroups;
+    double acc = 0.0;
+    for (int t = blockIdx.x * per_block + threadIdx.x / G; t < n_round; t += ngroups) {
+        const bool valid = t < c.T;
+        value_t v1, v2, s1;
+        int e1;
+        top2_token<M, G>(c, valid ? t : 0, valid, pr, v1, e1, v2, s1);
+        if (valid && gl == 0) {
+            int a = assign[t];
+            a = (a >= 0 && a < c.E) ? a : 0;
+            acc += (double)v1 - (double)M::load(c.S, (int64_t)t * c.E + a, c.scale);
+        }
+    }
+    if (blockIdx.x == 0 && threadIdx.x < 64) {
+        double sp = 0.0;
+        for (int e = threadIdx.x; e < c.E; e += 64) sp += (double)pr[e];
+        acc += (double)c.C * sp;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    if (lane_id() == 0) part[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double sum = 0.0;
+        for (int w = 0; w < kThreads / 64; ++w) sum += part[w];
+        atomicAdd(&c.ctrl->dual_gap, sum);
+    }
+}
+
+template <class M>
+hipError_t launch_dual_gap(const Ctx<M> &c, int B, const int32_t *assign, hipStream_t s) {
+    const size_t pr_bytes = (size_t)c.E * sizeof(typename M::value_t);
+    int blocks = (int)((c.T + 255) / 256);
+    if (blocks > 1024) blocks = 1024;
+    const dim3 grid(blocks, B);
+    switch (lanes_per_token(c.E)) {
+        case 1: hipLaunchKernelGGL((dual_gap_kernel<M, 1>), grid, dim3(kThreads), pr_bytes, s, c, assign); break;
+        case 2: hipLaunchKernelGGL((dual_gap_kernel<M, 2>), grid, dim3(kThreads), pr_bytes, s, c, assign); break;
+        case 4: hipLaunchKernelGGL((dual_gap_kernel<M, 4>), grid, dim3(kThreads), pr_bytes, s, c, assign); break;
+        case 8: hipLaunchKernelGGL((dual_gap_kernel<M, 8>), grid, dim3(kThreads), pr_bytes, s, c, assign); break;
+        case 16: hipLaunchKernelGGL((dual_gap_kernel<M, 16>), grid, dim3(kThreads), pr_bytes, s, c, assign); break;
+        case 32: hipLaunchKernelGGL((dual_gap_kernel<M, 32>), grid, dim3(kThreads), pr_bytes, s, c, assign); break;
+        default: hipLaunchKernelGGL((dual_gap_kernel<M, 64>), grid, dim3(kThreads), pr_bytes, s, c, assign); break;
+    }
+    return hipGetLastError();
+}
+
 // Greedy completion after max_rounds (one block, sequential in token order):
 // every still-unassigned token takes its best expert among those with room.
 template <class M>
@@ -2603,6 +2683,10 @@ hipError_t solve_mode(const void *S, const AssignParams &p, int B, int32_t *assi
                        (int)L.nblk, c.E, c.C, wst);
     hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)L.nblk, B), dim3(kCountTile), 0, s,
                        assign, c.T, c.E, blk, perm, wst);
+    if (p.flags & BASE_ASSIGN_SYNC_STATS) {
+        err = launch_dual_gap<M>(c, B, assign, s);
+        if (err != hipSuccess) return err;
+    }
     if (prices_out != nullptr) {
         const size_t row = (size_t)p.E * sizeof(value_t);
         err = hipMemcpy2DAsync(prices_out, row, c.prices, (size_t)wst, row, (size_t)B,

@@ -25,6 +25,7 @@ struct AssignParams {
     double eps_factor;
     int32_t max_rounds;
     uint32_t flags;
+    const void *warm_prices;   // non-null: initial prices ([B][E], the prices output layout)
 };
 
 // Device-side solver state and statistics, at the head of the workspace.
@@ -49,7 +50,8 @@ struct SolveCtrl {
     int32_t internal_error; // a device-side consistency check failed
     int32_t pad2;
     unsigned long long engine_bids;   // bids placed inside the single-workgroup engine
-    int64_t pad1[2];
+    double dual_gap;        // D(p) - objective after the solve (when statistics are asked for)
+    int64_t pad1[1];
 };
 
 size_t assign_workspace_size(int64_t T, int64_t E);

@@ -338,6 +338,55 @@ def test_assign_batched_integer_mode_and_single_expert():
     assert torch.equal(r1.perm, torch.arange(96, dtype=torch.int32, device="cuda").repeat(4, 1))
 
 
+def test_dual_gap_statistic_matches_oracle():
+    inp = wl.make_inputs("t8192-e64-d1024")
+    S = pb.affinity(*inputs_on_device(inp))
+    res = pb.assign(S)
+    S64 = host(S).astype(np.float64)
+    p = host(res.prices).astype(np.float64)
+    gap = oracle.dual_bound(S64, p) - oracle.objective(S64, host(res.assign))
+    T = S64.shape[0]
+    assert abs(res.stats.dual_gap - gap) <= rounding_slack(T, S64, p)
+    assert res.stats.dual_gap <= T * res.stats.eps_final + rounding_slack(T, S64, p)
+
+
+def test_fallback_dual_gap_certifies_the_loss():
+    """Bounded-latency mode: a round budget far below what the solve needs,
+    with the balance-keeping greedy completion; the reported gap still bounds
+    the distance to the optimum from above."""
+    inp = wl.make_inputs("t8192-e64-d1024")
+    S = pb.affinity(*inputs_on_device(inp))
+    res = pb.assign(S, max_rounds=20, flags=pb.BASE_ASSIGN_GREEDY_FALLBACK)
+    assert res.stats.fell_back == 1
+    S64 = host(S).astype(np.float64)
+    a = host(res.assign)
+    assert oracle.balanced_counts_ok(a, S64.shape[1])
+    _, obj_opt, _ = oracle.solve_ssp(S64)
+    loss = obj_opt - oracle.objective(S64, a)
+    p = host(res.prices).astype(np.float64)
+    assert loss >= -1e-6
+    assert res.stats.dual_gap >= loss - rounding_slack(S64.shape[0], S64, p)
+
+
+def test_warm_start_prices():
+    """Prices of a previous, similar batch as the starting point: the result
+    meets the same bound, typically in fewer rounds."""
+    inp = wl.make_inputs("t8192-e64-d1024")
+    S = pb.affinity(*inputs_on_device(inp))
+    first = pb.assign(S)
+    rng = np.random.Generator(np.random.PCG64(3))
+    noise = torch.from_numpy(rng.standard_normal(tuple(S.shape), dtype=np.float32)).cuda()
+    S2 = (S + 0.01 * noise).contiguous()
+    cold = pb.assign(S2)
+    prices = first.prices.clone()
+    warm = pb.assign(S2, out_prices=prices, warm_start=True)
+    S64 = host(S2).astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    check_assignment(S64, warm, EPS_FINAL, opt=(a_opt, obj_opt))
+    check_assignment(S64, cold, EPS_FINAL, opt=(a_opt, obj_opt))
+    print("rounds cold", cold.stats.rounds, "warm", warm.stats.rounds)
+
+
 def test_engine_launch_timing():
     """The measurement hook brackets each engine launch with events on the
     call's stream: one record per phase slot, each within the whole call."""
