@@ -120,7 +120,7 @@ struct Ctx {
     __host__ __device__ static P *shift(P *ptr, int64_t bytes) {
         return reinterpret_cast<P *>(reinterpret_cast<uintptr_t>(ptr) + bytes);
     }
-    __host__ __device__ Ctx at(int b) const {
+    __host__ __device__ __attribute__((always_inline)) Ctx at(int b) const {
         Ctx r = *this;
         if (b == 0) return r;
         const int64_t w = (int64_t)b * ws_stride;
