@@ -1436,7 +1436,7 @@ __device__ inline void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-constexpr int kEngThreads = 512;
+constexpr int kEngThreads = 1024;
 constexpr int kEngWaves = kEngThreads / 64;
 constexpr int kEngCap = 1024;
 constexpr int kEngDirect = 64;   // rounds with at most this many bids skip the grouping
