@@ -6,12 +6,15 @@ H into expert-contiguous rows (plus the inverse permute on the workload that
 includes it). Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                    [--no-cpu-baseline] [--batch B]
+                    [--no-cpu-baseline] [--batch B] [--no-shuffle]
 
 With --batch B > 1 it measures B independent problems of the paper's
-per-worker shape (Sec. 3.2.1 Sharding; T=2048, E=128, d=2048): one affinity
-GEMM over the B * T tokens against the shared expert embeddings, one
-base_assign_batched call, and each problem's permute.
+per-worker shape (Sec. 3.2.1 Sharding; T=2048, E=128, d=2048) with the
+random shuffle of tokens to workers (Sec. 3.2.1 Shuffling; a seeded
+permutation of the B * T tokens, an input): one affinity GEMM over the
+shuffled rows against the shared expert embeddings (base_affinity_gather),
+one base_assign_batched call, and one permute of all problems' rows
+(base_permute_batched), both reading H through the shuffle index.
 """
 from __future__ import annotations
 
@@ -69,6 +72,7 @@ def parse():
     ap.add_argument("--workload", default=wl.HEADLINE, choices=sorted(wl.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--no-shuffle", action="store_true")
     return ap.parse_args()
 
 
@@ -98,14 +102,15 @@ def bench_batched(args) -> None:
     prices = torch.empty((B, E), dtype=torch.float32, device="cuda")
     ws = torch.empty(pb.assign_batched_workspace_size(B, T, E), dtype=torch.uint8, device="cuda")
     X = torch.empty((B * T, d), dtype=torch.bfloat16, device="cuda")
+    shuffle = None if args.no_shuffle else \
+        torch.from_numpy(wl.shuffle_permutation(B * T, 2103)).cuda()
     stream = torch.cuda.current_stream()
 
     def step():
-        pb.affinity(H, W, out=S, stream=stream)
+        pb.affinity(H, W, out=S, rows=shuffle, stream=stream)
         pb.assign_batched(S.view(B, T, E), sync_stats=False, workspace=ws, out_assign=a,
                           out_perm=perm, out_prices=prices, stream=stream)
-        for b in range(B):
-            pb.permute(H[b * T:(b + 1) * T], perm[b], out=X[b * T:(b + 1) * T], stream=stream)
+        pb.permute_batched(H, perm, shuffle=shuffle, out=X, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -132,7 +137,8 @@ def bench_batched(args) -> None:
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded generator; no dataset or trained weights)",
-        "config": {"workload": f"t2048-e128-d2048-worker x {B}", "B": B, "T": T, "E": E, "d": d},
+        "config": {"workload": f"t2048-e128-d2048-worker x {B}", "B": B, "T": T, "E": E, "d": d,
+                   "shuffle": shuffle is not None},
         "assign_stats": {"phases": res.stats.phases, "rounds_max": res.stats.rounds,
                          "bids": res.stats.bids, "converged": res.stats.converged},
         "balanced_problems": counts_ok,

@@ -83,6 +83,26 @@ const char *base_status_string(int status);
 int base_affinity(const void *H, const void *W, float *S, int64_t T, int64_t E, int64_t d,
                   int in_dtype, void *stream);
 
+/*
+ * base_affinity_gather - the same product with the rows of H taken through an
+ * index: S[i, e] = H[rows[i], :] . W[e, :] for i in [0, N). Sec. 3.2.1
+ * (Shuffling): before the assignment, tokens are sent to workers at random;
+ * with rows = a random permutation of the B * T tokens, rows
+ * [b T, (b + 1) T) of S are worker b's problem. The shuffled copy of H is
+ * never materialised: the GEMM reads H through the index, and
+ * base_permute_batched / base_gate_combine_batched take the same index.
+ *
+ *   H       [device] h_rows x d, in_dtype, row-major
+ *   rows    [device] int32 [N], entries in [0, h_rows) (an entry outside
+ *           that range gives a zero row of S; never read out of bounds)
+ *   S       [device] N x E float32, row-major, written entirely
+ *   N, h_rows <= 2^31 - 1; other arguments and arithmetic as base_affinity
+ *   (bit-identical to base_affinity of the gathered rows).
+ * Errors: as base_affinity; rows == NULL is BASE_ERR_INVALID_ARG.
+ */
+int base_affinity_gather(const void *H, int64_t h_rows, const int32_t *rows, const void *W,
+                         float *S, int64_t N, int64_t E, int64_t d, int in_dtype, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* base_assign: balanced assignment of Eq. 2                                  */
 /* ------------------------------------------------------------------------ */
@@ -187,8 +207,9 @@ int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_ass
  * would (same algorithm, same options, bit-identical results); the
  * single-workgroup parts of the solve run for all problems at once.
  * Sec. 3.2.1 (Shuffling) routes tokens to workers at random before the
- * solve: that is base_permute of the B * T rows with the caller's random
- * permutation, before the affinity.
+ * solve: base_affinity_gather computes the scores of the shuffled rows, and
+ * base_permute_batched / base_gate_combine_batched route them, all reading
+ * the unshuffled H through the caller's random permutation.
  *
  *   S          [device] B x T x E scores, problem after problem (T * E * sizeof
  *              must be a multiple of 16 bytes when B > 1)
@@ -226,13 +247,37 @@ int base_assign_batched(const void *S, int s_dtype, int64_t B, int64_t T, int64_
  *            1: out[perm[k], :] = in[k, :]   (scatter back to token order)
  *   T > 0, d > 0, d % 8 == 0
  *
- * Rows are copied bit for bit. perm is not checked on the device: an entry
- * outside [0, T) is undefined behaviour, a repeated entry leaves rows of out
+ * Rows are copied bit for bit. An entry of perm outside [0, T) skips its row
+ * (never read or written out of bounds); a repeated entry leaves rows of out
  * unwritten (gather) or written twice (scatter).
- * Errors: BASE_ERR_INVALID_ARG, BASE_ERR_UNSUPPORTED_DTYPE, BASE_ERR_RANGE, BASE_ERR_HIP.
+ * Errors: BASE_ERR_INVALID_ARG (also when in and out overlap),
+ * BASE_ERR_UNSUPPORTED_DTYPE, BASE_ERR_RANGE, BASE_ERR_HIP.
  */
 int base_permute(const void *in, const int32_t *perm, void *out, int64_t T, int64_t d, int dtype,
                  int inverse, void *stream);
+
+/*
+ * base_permute_batched - the permute of B independent problems of T tokens
+ * (base_assign_batched's sort vectors) in one pass, optionally through the
+ * shuffle index of base_affinity_gather (Sec. 3.2.1, Shuffling). Routed row
+ * k = b T + j (problem b, position j) has the source row
+ *     src(k) = shuffle[b T + perm[k]]   (shuffle given)
+ *     src(k) = b T + perm[k]            (shuffle NULL)
+ * and inverse 0: out[k] = in[src(k)];  inverse 1: out[src(k)] = in[k].
+ * With the shuffle, inverse 0 reads the unshuffled H directly into each
+ * worker's expert order, and inverse 1 returns expert rows straight to the
+ * unshuffled token order.
+ *
+ *   in, out  [device] B T x d rows of dtype, must not overlap
+ *   perm     [device] int32 [B][T], each row a permutation of [0, T)
+ *   shuffle  [device] int32 [B T] or NULL, a permutation of [0, B T)
+ *   1 <= B, T; B T <= 2^31 - 1; d % 8 == 0
+ * Entries out of range skip their row, as in base_permute. B = 1 with no
+ * shuffle is base_permute.
+ * Errors: as base_permute.
+ */
+int base_permute_batched(const void *in, const int32_t *perm, const int32_t *shuffle, void *out,
+                         int64_t B, int64_t T, int64_t d, int dtype, int inverse, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Test-time routing and the gated residual                                  */
@@ -257,9 +302,20 @@ int base_permute(const void *in, const int32_t *perm, void *out, int64_t T, int6
  * token perm[k]) and S[t, a_t] = h_t . w_{a_t} the affinity already computed.
  * fp32 arithmetic; BASE_BF16 rows are widened exactly and the result rounded
  * to nearest even. F, H, out: [device] T x d of dtype (BASE_BF16 or BASE_F32),
- * 16-byte aligned, out must not overlap F or H; d % 8 == 0. perm must be a
- * permutation of [0, T) and assign[t] in [0, E) (not checked; an entry out
- * of range is treated as expert 0 / the row skipped, never read out of bounds).
+ * 16-byte aligned, out must not overlap F or H (BASE_ERR_INVALID_ARG);
+ * d % 8 == 0. perm must be a permutation of [0, T) and assign[t] in [0, E)
+ * (not checked; an entry out of range is treated as expert 0 / the row
+ * skipped, never read out of bounds).
+ *
+ * base_gate_combine_batched - the same over B problems of T tokens routed
+ * with base_assign_batched, optionally shuffled (base_affinity_gather): S
+ * [B T x E], assign and perm [B][T] are in worker order, F [B T x d] in
+ * routed order, H and out [B T x d] in the unshuffled token order. Routed
+ * row k = b T + j belongs to worker token w = b T + perm[k] and to token
+ * t = shuffle[w] (t = w if shuffle is NULL):
+ *     out[t] = sigmoid(S[w, assign[w]]) * F[k] + H[t].
+ * B T <= 2^31 - 1; shuffle a permutation of [0, B T) (entries out of range
+ * skip their row). B = 1 with no shuffle is base_gate_combine.
  *
  * base_gate_backward - the gradient of Eq. 1's gate and residual with the
  * expert output held fixed (its own backward belongs to the expert network),
@@ -281,6 +337,10 @@ int base_greedy_assign(const float *S, int64_t T, int64_t E, int32_t *assign, in
 int base_gate_combine(const void *F, const void *H, const float *S, const int32_t *assign,
                       const int32_t *perm, void *out, int64_t T, int64_t E, int64_t d, int dtype,
                       void *stream);
+int base_gate_combine_batched(const void *F, const void *H, const float *S,
+                              const int32_t *assign, const int32_t *perm, const int32_t *shuffle,
+                              void *out, int64_t B, int64_t T, int64_t E, int64_t d, int dtype,
+                              void *stream);
 int base_gate_backward(const void *dY, const void *F, const void *H, const void *W,
                        const float *S, const int32_t *assign, const int32_t *perm,
                        const int32_t *offsets, void *dH, void *dF, float *dW, float *dS,

@@ -18,6 +18,9 @@ What it computes, each function citing the passage it follows:
   expert_offsets    row ranges of a (possibly unbalanced) routed order (Sec. 3.2.2)
   gate_combine      gated residual y = sigmoid(h.w_a) f + h          (Sec. 3.1, Eq. 1)
   gate_backward     gradients of Eq. 1's gate and residual           (Sec. 3.1, Eq. 1)
+  route_shuffled    shuffle to workers, per-worker solve and route   (Sec. 3.2.1)
+  unroute_shuffled  expert rows back to the original token order     (Sec. 3.2.1, Sec. 3)
+  gate_combine_shuffled  Eq. 1 over shuffled workers, token order    (Sec. 3.1, 3.2.1)
 """
 from .affinity import affinity
 from .assign import (
@@ -32,12 +35,16 @@ from .assign import (
 )
 from .gate import expert_offsets, gate_backward, gate_combine
 from .permute import gather, scatter, stable_perm
+from .shuffle import gate_combine_shuffled, route_shuffled, unroute_shuffled
 
 __all__ = [
     "affinity",
     "expert_offsets",
     "gate_backward",
     "gate_combine",
+    "gate_combine_shuffled",
+    "route_shuffled",
+    "unroute_shuffled",
     "balanced_counts_ok",
     "dual_bound",
     "gather",

@@ -42,10 +42,12 @@ BASE_ASSIGN_CHECK_FINITE = 4
 BASE_ASSIGN_WARM_PRICES = 8
 
 # Every symbol include/base.h declares.
-EXPORTED = ("base_status_string", "base_affinity", "base_assign_workspace_size", "base_assign",
-            "base_assign_batched_workspace_size", "base_assign_batched", "base_permute",
+EXPORTED = ("base_status_string", "base_affinity", "base_affinity_gather",
+            "base_assign_workspace_size", "base_assign", "base_assign_batched_workspace_size",
+            "base_assign_batched", "base_permute", "base_permute_batched",
             "base_greedy_workspace_size", "base_greedy_assign", "base_gate_combine",
-            "base_gate_backward", "base_timing_enable", "base_timing_read")
+            "base_gate_combine_batched", "base_gate_backward", "base_timing_enable",
+            "base_timing_read")
 
 
 class AssignOpts(ctypes.Structure):
@@ -84,6 +86,8 @@ def lib() -> ctypes.CDLL:
         L.base_status_string.restype = ctypes.c_char_p
         L.base_affinity.argtypes = [vp, vp, vp, i64, i64, i64, i32, vp]
         L.base_affinity.restype = i32
+        L.base_affinity_gather.argtypes = [vp, i64, vp, vp, vp, i64, i64, i64, i32, vp]
+        L.base_affinity_gather.restype = i32
         L.base_assign_workspace_size.argtypes = [i64, i64]
         L.base_assign_workspace_size.restype = ctypes.c_size_t
         L.base_assign.argtypes = [vp, i32, i64, i64, ctypes.POINTER(AssignOpts), vp, vp, vp, vp,
@@ -97,12 +101,17 @@ def lib() -> ctypes.CDLL:
         L.base_assign_batched.restype = i32
         L.base_permute.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
         L.base_permute.restype = i32
+        L.base_permute_batched.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, i32, vp]
+        L.base_permute_batched.restype = i32
         L.base_greedy_workspace_size.argtypes = [i64, i64]
         L.base_greedy_workspace_size.restype = ctypes.c_size_t
         L.base_greedy_assign.argtypes = [vp, i64, i64, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.base_greedy_assign.restype = i32
         L.base_gate_combine.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i32, vp]
         L.base_gate_combine.restype = i32
+        L.base_gate_combine_batched.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64,
+                                                i32, vp]
+        L.base_gate_combine_batched.restype = i32
         L.base_gate_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64,
                                          i64, i32, vp]
         L.base_gate_backward.restype = i32
@@ -154,19 +163,30 @@ def _need_device(*ts) -> None:
             raise ValueError("tensors must be contiguous")
 
 
-def affinity(H, W, out=None, stream=None):
-    """S = H . W^T as float32 [T, E] (base_affinity)."""
+def affinity(H, W, out=None, rows=None, stream=None):
+    """S = H . W^T as float32 [T, E] (base_affinity). With `rows` (int32 [N]),
+    S[i] = H[rows[i]] . W^T, N rows (base_affinity_gather: the shuffle of
+    tokens to workers read through the index)."""
     torch = _torch()
     _need_device(H, W)
     T, d = H.shape
     E, d2 = W.shape
     if d != d2 or H.dtype != W.dtype:
         raise ValueError("H [T, d] and W [E, d] must share d and dtype")
+    N = T if rows is None else rows.numel()
     if out is None:
-        out = torch.empty((T, E), dtype=torch.float32, device=H.device)
+        out = torch.empty((N, E), dtype=torch.float32, device=H.device)
     _need_device(out)
-    _check(lib().base_affinity(H.data_ptr(), W.data_ptr(), out.data_ptr(), T, E, d,
-                               _dtype_code(H), _stream_ptr(stream)), "base_affinity")
+    if rows is None:
+        _check(lib().base_affinity(H.data_ptr(), W.data_ptr(), out.data_ptr(), T, E, d,
+                                   _dtype_code(H), _stream_ptr(stream)), "base_affinity")
+    else:
+        _need_device(rows)
+        if rows.dtype != torch.int32:
+            raise TypeError("rows must be int32")
+        _check(lib().base_affinity_gather(H.data_ptr(), T, rows.data_ptr(), W.data_ptr(),
+                                          out.data_ptr(), N, E, d, _dtype_code(H),
+                                          _stream_ptr(stream)), "base_affinity_gather")
     return out
 
 
@@ -270,6 +290,32 @@ def permute(x, perm, inverse: bool = False, out=None, stream=None):
     return out
 
 
+def permute_batched(x, perm, shuffle=None, inverse: bool = False, out=None, stream=None):
+    """Permute of B problems in one pass (base_permute_batched): x [B*T, d],
+    perm [B, T]; routed row k = b*T + j has source src = shuffle[b*T +
+    perm[b, j]] (or b*T + perm[b, j]); out[k] = x[src], or with inverse
+    out[src] = x[k]."""
+    torch = _torch()
+    _need_device(x, perm)
+    B, T = perm.shape
+    N, d = x.shape
+    if N != B * T:
+        raise ValueError("x must have B*T rows")
+    if out is None:
+        out = torch.empty_like(x)
+    _need_device(out)
+    sp = 0
+    if shuffle is not None:
+        _need_device(shuffle)
+        if shuffle.numel() != N or shuffle.dtype != torch.int32:
+            raise ValueError("shuffle must be int32 [B*T]")
+        sp = shuffle.data_ptr()
+    _check(lib().base_permute_batched(x.data_ptr(), perm.data_ptr(), sp or None, out.data_ptr(),
+                                      B, T, d, _dtype_code(x), 1 if inverse else 0,
+                                      _stream_ptr(stream)), "base_permute_batched")
+    return out
+
+
 def greedy_assign(S, workspace=None, stream=None):
     """Test-time routing (base_greedy_assign): (assign [T], perm [T],
     offsets [E + 1]) with every token at its best expert."""
@@ -301,6 +347,32 @@ def gate_combine(F, H, S, assign, perm, out=None, stream=None):
     _check(lib().base_gate_combine(F.data_ptr(), H.data_ptr(), S.data_ptr(), assign.data_ptr(),
                                    perm.data_ptr(), out.data_ptr(), T, E, d, _dtype_code(H),
                                    _stream_ptr(stream)), "base_gate_combine")
+    return out
+
+
+def gate_combine_batched(F, H, S, assign, perm, shuffle=None, out=None, stream=None):
+    """Eq. 1 over B problems (base_gate_combine_batched): S [B*T, E], assign
+    and perm [B, T] in worker order, F [B*T, d] in routed order, H and the
+    result [B*T, d] in the unshuffled token order."""
+    torch = _torch()
+    _need_device(F, H, S, assign, perm)
+    B, T = perm.shape
+    N, d = H.shape
+    E = S.shape[-1]
+    if N != B * T or S.numel() != N * E or F.shape != H.shape:
+        raise ValueError("shapes: F, H [B*T, d], S [B*T, E], assign and perm [B, T]")
+    if out is None:
+        out = torch.empty_like(H)
+    sp = 0
+    if shuffle is not None:
+        _need_device(shuffle)
+        if shuffle.numel() != N or shuffle.dtype != torch.int32:
+            raise ValueError("shuffle must be int32 [B*T]")
+        sp = shuffle.data_ptr()
+    _check(lib().base_gate_combine_batched(F.data_ptr(), H.data_ptr(), S.data_ptr(),
+                                           assign.data_ptr(), perm.data_ptr(), sp or None,
+                                           out.data_ptr(), B, T, E, d, _dtype_code(H),
+                                           _stream_ptr(stream)), "base_gate_combine_batched")
     return out
 
 
@@ -346,7 +418,8 @@ def timing_read() -> tuple[int, float]:
     return int(n.value), float(ms.value)
 
 
-__all__ = ["affinity", "assign", "assign_batched", "permute", "greedy_assign", "gate_combine",
+__all__ = ["affinity", "assign", "assign_batched", "permute", "permute_batched", "greedy_assign",
+           "gate_combine", "gate_combine_batched",
            "gate_backward", "balanced_offsets", "assign_workspace_size",
            "assign_batched_workspace_size", "timing_enable",
            "timing_read", "AssignResult", "AssignOpts", "AssignStats", "BaseError", "lib",

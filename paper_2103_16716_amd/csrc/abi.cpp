@@ -26,6 +26,67 @@ bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0;
 
 int hip_status(hipError_t e) { return e == hipSuccess ? BASE_OK : BASE_ERR_HIP; }
 
+// [a, a + an) and [b, b + bn) share a byte.
+bool overlap(const void *a, int64_t an, const void *b, int64_t bn) {
+    const char *pa = static_cast<const char *>(a);
+    const char *pb = static_cast<const char *>(b);
+    return pa < pb + bn && pb < pa + an;
+}
+
+int affinity_impl(const void *H, int64_t h_rows, const int32_t *rows, const void *W, float *S,
+                  int64_t T, int64_t E, int64_t d, int in_dtype, void *stream) {
+    if (H == nullptr || W == nullptr || S == nullptr) return BASE_ERR_INVALID_ARG;
+    if (T <= 0 || E <= 0 || d <= 0 || d % 8 != 0 || h_rows <= 0) return BASE_ERR_INVALID_ARG;
+    if (!aligned(H, 16) || !aligned(W, 16) || !aligned(S, 16) || !aligned(rows, 4))
+        return BASE_ERR_INVALID_ARG;
+    if (in_dtype != BASE_BF16 && in_dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
+    if (T > INT32_MAX || h_rows > INT32_MAX || E > 65535 * 128 || d > kMaxDim)
+        return BASE_ERR_RANGE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (in_dtype == BASE_BF16)
+        return hip_status(base::launch_affinity_bf16(static_cast<const uint16_t *>(H), rows, h_rows,
+                                                     static_cast<const uint16_t *>(W), S, T, E, d,
+                                                     s));
+    return hip_status(base::launch_affinity_f32(static_cast<const float *>(H), rows, h_rows,
+                                                static_cast<const float *>(W), S, T, E, d, s));
+}
+
+int permute_impl(const void *in, const int32_t *perm, const int32_t *shuffle, void *out,
+                 int64_t B, int64_t T, int64_t d, int dtype, int inverse, void *stream) {
+    if (in == nullptr || perm == nullptr || out == nullptr) return BASE_ERR_INVALID_ARG;
+    if (B <= 0 || T <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
+    if (inverse != 0 && inverse != 1) return BASE_ERR_INVALID_ARG;
+    if (!aligned(in, 16) || !aligned(out, 16) || !aligned(perm, 4) || !aligned(shuffle, 4))
+        return BASE_ERR_INVALID_ARG;
+    if (dtype != BASE_BF16 && dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
+    if (B > INT32_MAX || T > INT32_MAX || B * T > INT32_MAX || d > kMaxDim) return BASE_ERR_RANGE;
+    const int64_t row_bytes = d * (dtype == BASE_BF16 ? 2 : 4);
+    const int64_t bytes = B * T * row_bytes;
+    if (overlap(in, bytes, out, bytes)) return BASE_ERR_INVALID_ARG;
+    return hip_status(base::launch_permute(in, perm, shuffle, out, B, T, row_bytes, inverse,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int gate_combine_impl(const void *F, const void *H, const float *S, const int32_t *assign,
+                      const int32_t *perm, const int32_t *shuffle, void *out, int64_t B,
+                      int64_t T, int64_t E, int64_t d, int dtype, void *stream) {
+    if (F == nullptr || H == nullptr || S == nullptr || assign == nullptr || perm == nullptr ||
+        out == nullptr)
+        return BASE_ERR_INVALID_ARG;
+    if (B <= 0 || T <= 0 || E <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
+    if (dtype != BASE_BF16 && dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
+    if (B > INT32_MAX || T > INT32_MAX || B * T > INT32_MAX || E > INT32_MAX || d > kMaxDim)
+        return BASE_ERR_RANGE;
+    if (!aligned(F, 16) || !aligned(H, 16) || !aligned(out, 16) || !aligned(S, 4) ||
+        !aligned(assign, 4) || !aligned(perm, 4) || !aligned(shuffle, 4))
+        return BASE_ERR_INVALID_ARG;
+    const int64_t bytes = B * T * d * (dtype == BASE_BF16 ? 2 : 4);
+    if (overlap(out, bytes, F, bytes) || overlap(out, bytes, H, bytes)) return BASE_ERR_INVALID_ARG;
+    return hip_status(base::launch_gate_combine(F, H, S, assign, perm, shuffle, out, B, T, E, d,
+                                                dtype == BASE_BF16 ? 1 : 0,
+                                                static_cast<hipStream_t>(stream)));
+}
+
 }  // namespace
 
 extern "C" {
@@ -48,18 +109,13 @@ const char *base_status_string(int status) {
 
 int base_affinity(const void *H, const void *W, float *S, int64_t T, int64_t E, int64_t d,
                   int in_dtype, void *stream) {
-    if (H == nullptr || W == nullptr || S == nullptr) return BASE_ERR_INVALID_ARG;
-    if (T <= 0 || E <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
-    if (!aligned(H, 16) || !aligned(W, 16) || !aligned(S, 16)) return BASE_ERR_INVALID_ARG;
-    if (in_dtype != BASE_BF16 && in_dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
-    if (T > INT32_MAX || E > 65535 * 128 || d > kMaxDim) return BASE_ERR_RANGE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    if (in_dtype == BASE_BF16)
-        return hip_status(base::launch_affinity_bf16(static_cast<const uint16_t *>(H),
-                                                     static_cast<const uint16_t *>(W), S, T, E, d,
-                                                     s));
-    return hip_status(base::launch_affinity_f32(static_cast<const float *>(H),
-                                                static_cast<const float *>(W), S, T, E, d, s));
+    return affinity_impl(H, T, nullptr, W, S, T, E, d, in_dtype, stream);
+}
+
+int base_affinity_gather(const void *H, int64_t h_rows, const int32_t *rows, const void *W,
+                         float *S, int64_t N, int64_t E, int64_t d, int in_dtype, void *stream) {
+    if (rows == nullptr) return BASE_ERR_INVALID_ARG;
+    return affinity_impl(H, h_rows, rows, W, S, N, E, d, in_dtype, stream);
 }
 
 size_t base_assign_workspace_size(int64_t T, int64_t E) {
@@ -231,18 +287,14 @@ int base_greedy_assign(const float *S, int64_t T, int64_t E, int32_t *assign, in
 int base_gate_combine(const void *F, const void *H, const float *S, const int32_t *assign,
                       const int32_t *perm, void *out, int64_t T, int64_t E, int64_t d, int dtype,
                       void *stream) {
-    if (F == nullptr || H == nullptr || S == nullptr || assign == nullptr || perm == nullptr ||
-        out == nullptr)
-        return BASE_ERR_INVALID_ARG;
-    if (T <= 0 || E <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
-    if (dtype != BASE_BF16 && dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
-    if (T > INT32_MAX || E > INT32_MAX || d > kMaxDim) return BASE_ERR_RANGE;
-    if (!aligned(F, 16) || !aligned(H, 16) || !aligned(out, 16) || !aligned(S, 4) ||
-        !aligned(assign, 4) || !aligned(perm, 4))
-        return BASE_ERR_INVALID_ARG;
-    return hip_status(base::launch_gate_combine(F, H, S, assign, perm, out, T, E, d,
-                                                dtype == BASE_BF16 ? 1 : 0,
-                                                static_cast<hipStream_t>(stream)));
+    return gate_combine_impl(F, H, S, assign, perm, nullptr, out, 1, T, E, d, dtype, stream);
+}
+
+int base_gate_combine_batched(const void *F, const void *H, const float *S,
+                              const int32_t *assign, const int32_t *perm, const int32_t *shuffle,
+                              void *out, int64_t B, int64_t T, int64_t E, int64_t d, int dtype,
+                              void *stream) {
+    return gate_combine_impl(F, H, S, assign, perm, shuffle, out, B, T, E, d, dtype, stream);
 }
 
 int base_gate_backward(const void *dY, const void *F, const void *H, const void *W,
@@ -276,19 +328,12 @@ int base_timing_read(int64_t *launches, double *total_ms) {
 
 int base_permute(const void *in, const int32_t *perm, void *out, int64_t T, int64_t d, int dtype,
                  int inverse, void *stream) {
-    if (in == nullptr || perm == nullptr || out == nullptr) return BASE_ERR_INVALID_ARG;
-    if (T <= 0 || d <= 0 || d % 8 != 0) return BASE_ERR_INVALID_ARG;
-    if (inverse != 0 && inverse != 1) return BASE_ERR_INVALID_ARG;
-    if (!aligned(in, 16) || !aligned(out, 16) || !aligned(perm, 4)) return BASE_ERR_INVALID_ARG;
-    if (dtype != BASE_BF16 && dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
-    if (T > INT32_MAX || d > kMaxDim) return BASE_ERR_RANGE;
-    const int64_t row_bytes = d * (dtype == BASE_BF16 ? 2 : 4);
-    const char *ib = static_cast<const char *>(in);
-    const char *ob = static_cast<const char *>(out);
-    const int64_t bytes = T * row_bytes;
-    if (ib < ob + bytes && ob < ib + bytes) return BASE_ERR_INVALID_ARG;   // overlap
-    return hip_status(
-        base::launch_permute(in, perm, out, T, row_bytes, inverse, static_cast<hipStream_t>(stream)));
+    return permute_impl(in, perm, nullptr, out, 1, T, d, dtype, inverse, stream);
+}
+
+int base_permute_batched(const void *in, const int32_t *perm, const int32_t *shuffle, void *out,
+                         int64_t B, int64_t T, int64_t d, int dtype, int inverse, void *stream) {
+    return permute_impl(in, perm, shuffle, out, B, T, d, dtype, inverse, stream);
 }
 
 }  // extern "C"

@@ -13,6 +13,12 @@
 //
 // fp32 path: a plain LDS-tiled FMA kernel (fp32 products and sums, no
 // reduced-precision matrix instructions).
+//
+// Both kernels can read H through a row index (`rows`, null for the identity):
+// output row i is then h_{rows[i]} . W^T. This is the random shuffle of tokens
+// to workers (Sec. 3.2.1, Shuffling) folded into the GEMM's loads, so the
+// shuffled copy of H is never written. An index outside [0, h_rows) gives a
+// zero row (memory-safe; not a valid shuffle).
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -27,7 +33,15 @@ constexpr int kBN = 128;            // experts per block
 constexpr int kBK = 64;             // bf16 elements of d per chunk
 constexpr int kLdsRow = kBK + 8;    // padded LDS row (elements): 144 B, shifts 4 banks per row
 
+__device__ inline int64_t source_row(const int32_t *rows, int64_t h_rows, int i) {
+    if (rows == nullptr) return i;
+    const int64_t r = rows[i];
+    return (r >= 0 && r < h_rows) ? r : -1;
+}
+
 __global__ __launch_bounds__(256) void affinity_bf16_kernel(const uint16_t *__restrict__ H,
+                                                            const int32_t *__restrict__ rows,
+                                                            int64_t h_rows,
                                                             const uint16_t *__restrict__ W,
                                                             float *__restrict__ S, int T, int E,
                                                             int d) {
@@ -40,17 +54,24 @@ __global__ __launch_bounds__(256) void affinity_bf16_kernel(const uint16_t *__re
     const int m0 = blockIdx.x * kBM;
     const int n0 = blockIdx.y * kBN;
 
+    // Source rows of H for this thread's two staging chunks (fixed over k).
+    int64_t hrow[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int r = (tid + 256 * i) >> 3;
+        hrow[i] = m0 + r < T ? source_row(rows, h_rows, m0 + r) : -1;
+    }
+
     // Global -> register staging: chunk c covers row c/8, elements (c%8)*8 .. +8.
     uint4 ra[2], rb[4];
     auto gload = [&](int k0) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int c = tid + 256 * i;
-            const int r = c >> 3;
             const int k = k0 + (c & 7) * 8;
             ra[i] = make_uint4(0, 0, 0, 0);
-            if (m0 + r < T && k < d)
-                ra[i] = *reinterpret_cast<const uint4 *>(H + (int64_t)(m0 + r) * d + k);
+            if (hrow[i] >= 0 && k < d)
+                ra[i] = *reinterpret_cast<const uint4 *>(H + hrow[i] * d + k);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -125,6 +146,8 @@ constexpr int kFT = 64;
 constexpr int kFK = 16;
 
 __global__ __launch_bounds__(256) void affinity_f32_kernel(const float *__restrict__ H,
+                                                           const int32_t *__restrict__ rows,
+                                                           int64_t h_rows,
                                                            const float *__restrict__ W,
                                                            float *__restrict__ S, int T, int E,
                                                            int d) {
@@ -135,11 +158,12 @@ __global__ __launch_bounds__(256) void affinity_f32_kernel(const float *__restri
     const int m0 = blockIdx.x * kFT, n0 = blockIdx.y * kFT;
     // Loader: thread covers row tid/4, elements (tid%4)*4 .. +4 of the chunk.
     const int lr = tid >> 2, lk = (tid & 3) * 4;
+    const int64_t hrow = m0 + lr < T ? source_row(rows, h_rows, m0 + lr) : -1;
     float acc[4][4] = {};
     for (int k0 = 0; k0 < d; k0 += kFK) {
         float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
-        if (m0 + lr < T && k0 + lk < d)
-            a = *reinterpret_cast<const float4 *>(H + (int64_t)(m0 + lr) * d + k0 + lk);
+        if (hrow >= 0 && k0 + lk < d)
+            a = *reinterpret_cast<const float4 *>(H + hrow * d + k0 + lk);
         if (n0 + lr < E && k0 + lk < d)
             b = *reinterpret_cast<const float4 *>(W + (int64_t)(n0 + lr) * d + k0 + lk);
         __syncthreads();
@@ -173,19 +197,21 @@ __global__ __launch_bounds__(256) void affinity_f32_kernel(const float *__restri
 
 }  // namespace
 
-hipError_t launch_affinity_bf16(const uint16_t *H, const uint16_t *W, float *S, int64_t T,
-                                int64_t E, int64_t d, hipStream_t stream) {
+hipError_t launch_affinity_bf16(const uint16_t *H, const int32_t *rows, int64_t h_rows,
+                                const uint16_t *W, float *S, int64_t T, int64_t E, int64_t d,
+                                hipStream_t stream) {
     dim3 grid((unsigned)((T + kBM - 1) / kBM), (unsigned)((E + kBN - 1) / kBN));
-    hipLaunchKernelGGL(affinity_bf16_kernel, grid, dim3(256), 0, stream, H, W, S, (int)T, (int)E,
-                       (int)d);
+    hipLaunchKernelGGL(affinity_bf16_kernel, grid, dim3(256), 0, stream, H, rows, h_rows, W, S,
+                       (int)T, (int)E, (int)d);
     return hipGetLastError();
 }
 
-hipError_t launch_affinity_f32(const float *H, const float *W, float *S, int64_t T, int64_t E,
-                               int64_t d, hipStream_t stream) {
+hipError_t launch_affinity_f32(const float *H, const int32_t *rows, int64_t h_rows,
+                               const float *W, float *S, int64_t T, int64_t E, int64_t d,
+                               hipStream_t stream) {
     dim3 grid((unsigned)((T + kFT - 1) / kFT), (unsigned)((E + kFT - 1) / kFT));
-    hipLaunchKernelGGL(affinity_f32_kernel, grid, dim3(256), 0, stream, H, W, S, (int)T, (int)E,
-                       (int)d);
+    hipLaunchKernelGGL(affinity_f32_kernel, grid, dim3(256), 0, stream, H, rows, h_rows, W, S,
+                       (int)T, (int)E, (int)d);
     return hipGetLastError();
 }
 

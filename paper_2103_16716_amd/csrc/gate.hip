@@ -14,7 +14,9 @@
 //   greedy_scan_kernel     per-expert exclusive scan over the blocks
 //   greedy_offsets_kernel  exclusive scan of the expert totals -> offsets
 //   greedy_scatter_kernel  stable counting sort -> perm
-//   gate_combine_kernel    y = g * F[k] + H[t] for t = perm[k] (16-byte chunks)
+//   gate_combine_kernel    y = g * F[k] + H[t] for t = perm[k] (16-byte chunks);
+//                          also over B problems of T tokens with a shuffle
+//                          index (Sec. 3.2.1, Shuffling), see below
 //   gate_rows_kernel       backward per routed row: dS, dF, dH
 //   gate_dw_kernel         dW[e] = sum over expert e's rows of dS_t h_t
 #include <hip/hip_runtime.h>
@@ -217,25 +219,32 @@ struct Chunk {
     }
 };
 
-// y[t] = g_t F[k] + H[t] for t = perm[k], g_t = sigmoid(S[t, assign[t]]).
-// Each thread takes 16-byte chunks; a row is ncs chunks.
+// N = B T routed rows. Row k of problem b = k / T holds worker token
+// w = b T + perm[k], whose gate is g = sigmoid(S[w, assign[w]]) (S and
+// assign in worker order); its original token is t = shuffle[w] (t = w
+// without a shuffle). y[t] = g F[k] + H[t]. Each thread takes 16-byte
+// chunks; a row is ncs chunks.
 template <bool BF16>
 __global__ __launch_bounds__(256) void gate_combine_kernel(const void *F, const void *H,
                                                            const float *S,
                                                            const int32_t *assign,
-                                                           const int32_t *perm, void *Y, int T,
-                                                           int E, int ncs) {
+                                                           const int32_t *perm,
+                                                           const int32_t *shuffle, void *Y,
+                                                           int N, int T, int E, int ncs) {
     using Ck = Chunk<BF16>;
-    const int64_t total = (int64_t)T * ncs;
+    const int64_t total = (int64_t)N * ncs;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (int64_t)gridDim.x * blockDim.x) {
         const int k = (int)(i / ncs);
         const int j = (int)(i - (int64_t)k * ncs);
-        const int t = perm[k];
-        if (t < 0 || t >= T) continue;   // not a permutation: undefined, but in bounds
-        int a = assign[t];
+        const int p = perm[k];
+        if (p < 0 || p >= T) continue;   // not a permutation: undefined, but in bounds
+        const int w = (N == T ? 0 : (k / T) * T) + p;
+        const int t = shuffle == nullptr ? w : shuffle[w];
+        if (t < 0 || t >= N) continue;
+        int a = assign[w];
         a = (a >= 0 && a < E) ? a : 0;
-        const float g = gate_of(S[(int64_t)t * E + a]);
+        const float g = gate_of(S[(int64_t)w * E + a]);
         float f[8], h[8], y[8];
         Ck::load(F, (int64_t)k * ncs + j, f);
         Ck::load(H, (int64_t)t * ncs + j, h);
@@ -342,18 +351,20 @@ hipError_t launch_greedy(const float *S, int64_t T, int64_t E, int32_t *assign, 
 }
 
 hipError_t launch_gate_combine(const void *F, const void *H, const float *S,
-                               const int32_t *assign, const int32_t *perm, void *Y, int64_t T,
-                               int64_t E, int64_t d, int bf16, hipStream_t s) {
+                               const int32_t *assign, const int32_t *perm,
+                               const int32_t *shuffle, void *Y, int64_t B, int64_t T, int64_t E,
+                               int64_t d, int bf16, hipStream_t s) {
     const int ncs = (int)(d / (bf16 ? 8 : 4));
-    int64_t total = T * ncs;
+    const int64_t N = B * T;
+    int64_t total = N * ncs;
     int blocks = (int)((total + 255) / 256);
     if (blocks > 8192) blocks = 8192;
     if (bf16)
         hipLaunchKernelGGL(gate_combine_kernel<true>, dim3(blocks), dim3(256), 0, s, F, H, S,
-                           assign, perm, Y, (int)T, (int)E, ncs);
+                           assign, perm, shuffle, Y, (int)N, (int)T, (int)E, ncs);
     else
         hipLaunchKernelGGL(gate_combine_kernel<false>, dim3(blocks), dim3(256), 0, s, F, H, S,
-                           assign, perm, Y, (int)T, (int)E, ncs);
+                           assign, perm, shuffle, Y, (int)N, (int)T, (int)E, ncs);
     return hipGetLastError();
 }
 

@@ -8,13 +8,18 @@
 
 namespace base {
 
-hipError_t launch_affinity_bf16(const uint16_t *H, const uint16_t *W, float *S, int64_t T,
-                                int64_t E, int64_t d, hipStream_t stream);
-hipError_t launch_affinity_f32(const float *H, const float *W, float *S, int64_t T, int64_t E,
-                               int64_t d, hipStream_t stream);
+// rows: null, or output row i reads row rows[i] of H (h_rows rows).
+hipError_t launch_affinity_bf16(const uint16_t *H, const int32_t *rows, int64_t h_rows,
+                                const uint16_t *W, float *S, int64_t T, int64_t E, int64_t d,
+                                hipStream_t stream);
+hipError_t launch_affinity_f32(const float *H, const int32_t *rows, int64_t h_rows,
+                               const float *W, float *S, int64_t T, int64_t E, int64_t d,
+                               hipStream_t stream);
 
-hipError_t launch_permute(const void *in, const int32_t *perm, void *out, int64_t T,
-                          int64_t row_bytes, int inverse, hipStream_t stream);
+// B problems of T rows; shuffle: null or the [B*T] index composed after perm.
+hipError_t launch_permute(const void *in, const int32_t *perm, const int32_t *shuffle,
+                          void *out, int64_t B, int64_t T, int64_t row_bytes, int inverse,
+                          hipStream_t stream);
 
 struct AssignParams {
     int64_t T, E, C;
@@ -72,9 +77,11 @@ hipError_t read_assign_stats(const void *workspace, int64_t T, int64_t E, int64_
 size_t greedy_workspace_size(int64_t T, int64_t E);
 hipError_t launch_greedy(const float *S, int64_t T, int64_t E, int32_t *assign, int32_t *perm,
                          int32_t *offsets, void *workspace, hipStream_t s);
+// B problems of T tokens; shuffle: null or the [B*T] worker -> token index.
 hipError_t launch_gate_combine(const void *F, const void *H, const float *S,
-                               const int32_t *assign, const int32_t *perm, void *Y, int64_t T,
-                               int64_t E, int64_t d, int bf16, hipStream_t s);
+                               const int32_t *assign, const int32_t *perm,
+                               const int32_t *shuffle, void *Y, int64_t B, int64_t T, int64_t E,
+                               int64_t d, int bf16, hipStream_t s);
 hipError_t launch_gate_backward(const void *dY, const void *F, const void *H, const void *W,
                                 const float *S, const int32_t *assign, const int32_t *perm,
                                 const int32_t *offsets, void *dH, void *dF, float *dW, float *dS,

@@ -151,6 +151,32 @@ def test_permute_validation(L):
     assert f(FAKE, FAKE, FAKE + 16, 4, 8, pb.BASE_BF16, 0, None) == pb.BASE_ERR_INVALID_ARG
 
 
+def test_shuffled_routing_validation(L):
+    g = L.base_affinity_gather
+    # rows missing, h_rows <= 0, misaligned rows, d % 8
+    assert g(FAKE, 4, None, FAKE, FAKE, 4, 2, 8, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    assert g(FAKE, 0, FAKE, FAKE, FAKE, 4, 2, 8, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    assert g(FAKE, 4, FAKE + 2, FAKE, FAKE, 4, 2, 8, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    assert g(FAKE, 4, FAKE, FAKE, FAKE, 4, 2, 6, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    assert g(FAKE, 1 << 31, FAKE, FAKE, FAKE, 4, 2, 8, pb.BASE_BF16, None) == pb.BASE_ERR_RANGE
+    p = L.base_permute_batched
+    out = FAKE + (1 << 20)
+    assert p(FAKE, FAKE, None, out, 0, 4, 8, pb.BASE_BF16, 0, None) == pb.BASE_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, FAKE + 1, out, 2, 4, 8, pb.BASE_BF16, 0, None) == pb.BASE_ERR_INVALID_ARG
+    assert p(FAKE, FAKE, None, out, 1 << 16, 1 << 16, 8, pb.BASE_BF16, 0, None) == pb.BASE_ERR_RANGE
+    # B * T rows of in overlap out
+    assert p(FAKE, FAKE, None, FAKE + 2 * 4 * 16, 3, 4, 8, pb.BASE_BF16, 0, None) == \
+        pb.BASE_ERR_INVALID_ARG
+    c = L.base_gate_combine_batched
+    assert c(FAKE, FAKE + (1 << 20), FAKE, FAKE, FAKE, None, FAKE + (2 << 20), 0, 4, 2, 8,
+             pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    # out overlaps F
+    assert c(FAKE, FAKE + (1 << 20), FAKE, FAKE, FAKE, None, FAKE + 16, 2, 4, 2, 8,
+             pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+    assert L.base_gate_combine(FAKE, FAKE + (1 << 20), FAKE, FAKE, FAKE, FAKE + (1 << 20) + 16,
+                               4, 2, 8, pb.BASE_BF16, None) == pb.BASE_ERR_INVALID_ARG
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(pb, "_lib", None)
     monkeypatch.setattr(pb, "LIB_PATH", str(tmp_path / "missing.so"))

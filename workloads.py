@@ -148,3 +148,11 @@ def quantize_scores_int16(S: np.ndarray) -> tuple[np.ndarray, int]:
     s = int(np.floor(np.log2(32767.0 / m))) if m > 0 else 0
     q = np.clip(np.rint(S * (2.0 ** s)), -32768, 32767).astype(np.int16)
     return q, s
+
+
+def shuffle_permutation(n: int, seed: int) -> np.ndarray:
+    """The random routing of tokens to workers before the solve (Sec. 3.2.1,
+    Shuffling), drawn here and passed to both sides as an input: worker
+    token i is original token shuffle[i]. int32 [n], a permutation of [0, n)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.permutation(n).astype(np.int32)
