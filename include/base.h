@@ -324,9 +324,10 @@ int base_permute_batched(const void *in, const int32_t *perm, const int32_t *shu
  *     dH[t]  = dY[t] + dS[t] W[a_t]
  *     dF[k]  = g_t dY[t]                      (routed order, t = perm[k])
  *     dW[e]  = sum over t with a_t = e of dS[t] H[t]
- * dY, F, H, dH, dF: T x d of dtype; W: E x d of dtype; dW: E x d float32;
- * dS: float32 [T]. offsets [E + 1]: expert row ranges of the routed order
- * (e * T/E for a balanced assignment; base_greedy_assign's for a greedy one).
+ * dY, F, H, dH, dF: T x d of dtype; W: E x d of dtype (all 16-byte aligned);
+ * dW: E x d float32, 16-byte aligned; dS: float32 [T]. offsets [E + 1]:
+ * expert row ranges of the routed order (e * T/E for a balanced assignment;
+ * base_greedy_assign's for a greedy one).
  * Accumulation in fp32 in a fixed order (deterministic).
  * Errors: BASE_ERR_INVALID_ARG, BASE_ERR_UNSUPPORTED_DTYPE, BASE_ERR_RANGE,
  * BASE_ERR_HIP.

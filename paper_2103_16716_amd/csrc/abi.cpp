@@ -309,7 +309,7 @@ int base_gate_backward(const void *dY, const void *F, const void *H, const void 
     if (dtype != BASE_BF16 && dtype != BASE_F32) return BASE_ERR_UNSUPPORTED_DTYPE;
     if (T > INT32_MAX || E > 65535 || d > kMaxDim) return BASE_ERR_RANGE;
     if (!aligned(dY, 16) || !aligned(F, 16) || !aligned(H, 16) || !aligned(W, 16) ||
-        !aligned(dH, 16) || !aligned(dF, 16) || !aligned(dW, 4) || !aligned(dS, 4) ||
+        !aligned(dH, 16) || !aligned(dF, 16) || !aligned(dW, 16) || !aligned(dS, 4) ||
         !aligned(S, 4) || !aligned(assign, 4) || !aligned(perm, 4) || !aligned(offsets, 4))
         return BASE_ERR_INVALID_ARG;
     return hip_status(base::launch_gate_backward(dY, F, H, W, S, assign, perm, offsets, dH, dF, dW,

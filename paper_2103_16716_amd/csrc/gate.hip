@@ -305,28 +305,73 @@ __global__ __launch_bounds__(256) void gate_rows_kernel(const void *dY, const vo
 }
 
 // dW[e][c] = sum over routed rows k in [offsets[e], offsets[e + 1]) of
-// dS[t] H[t][c], t = perm[k]. One block per (expert, 256 columns).
+// dS[t] H[t][c], t = perm[k]: per expert, a weighted sum of its tokens' rows,
+// bound by reading each row of H once. Block = (expert, slab of 64 16-byte
+// chunks of a row); lane l owns chunk l of the slab. The block's kDwWaves
+// waves split the expert's rows (wave w takes k0 + w, k0 + w + kDwWaves, ...
+// in ascending order, kDwRows rows in flight), then the wave partials are
+// added in wave order: a fixed summation order, so the result is
+// deterministic.
+constexpr int kDwWaves = 8;
+constexpr int kDwRows = 4;
+
 template <bool BF16>
-__global__ __launch_bounds__(256) void gate_dw_kernel(const void *H, const float *dS,
-                                                      const int32_t *perm,
-                                                      const int32_t *offsets, float *dW, int T,
-                                                      int E, int d) {
+__global__ __launch_bounds__(64 * kDwWaves) void gate_dw_kernel(const void *H, const float *dS,
+                                                                const int32_t *perm,
+                                                                const int32_t *offsets,
+                                                                float *dW, int T, int E,
+                                                                int ncs) {
+    using Ck = Chunk<BF16>;
+    __shared__ float part[kDwWaves][64][Ck::kN];
     const int e = blockIdx.x;
-    const int c = blockIdx.y * blockDim.x + threadIdx.x;
-    if (e >= E || c >= d) return;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int j = blockIdx.y * 64 + lane;
     int k0 = offsets[e], k1 = offsets[e + 1];
     k0 = k0 < 0 ? 0 : (k0 > T ? T : k0);
     k1 = k1 < k0 ? k0 : (k1 > T ? T : k1);
-    float acc = 0.0f;
-    for (int k = k0; k < k1; ++k) {
-        const int t = perm[k];
-        if (t < 0 || t >= T) continue;
-        float h;
-        if (BF16) h = bf16_bits_to_f32(reinterpret_cast<const uint16_t *>(H)[(int64_t)t * d + c]);
-        else h = reinterpret_cast<const float *>(H)[(int64_t)t * d + c];
-        acc = fmaf(dS[t], h, acc);
+    float acc[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    if (j < ncs) {
+        for (int k = k0 + wave; k < k1; k += kDwWaves * kDwRows) {
+            int t[kDwRows];
+            float w[kDwRows], h[kDwRows][8];
+#pragma unroll
+            for (int u = 0; u < kDwRows; ++u) {
+                const int kk = k + u * kDwWaves;
+                t[u] = kk < k1 ? perm[kk] : -1;
+                if (t[u] >= T) t[u] = -1;
+            }
+#pragma unroll
+            for (int u = 0; u < kDwRows; ++u) {
+                w[u] = 0.0f;
+                if (t[u] >= 0) {
+                    w[u] = dS[t[u]];
+                    Ck::load(H, (int64_t)t[u] * ncs + j, h[u]);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kDwRows; ++u)
+                if (t[u] >= 0) {
+#pragma unroll
+                    for (int q = 0; q < Ck::kN; ++q) acc[q] = fmaf(w[u], h[u][q], acc[q]);
+                }
+        }
     }
-    dW[(int64_t)e * d + c] = acc;
+#pragma unroll
+    for (int q = 0; q < Ck::kN; ++q) part[wave][lane][q] = acc[q];
+    __syncthreads();
+    if (wave == 0 && j < ncs) {
+        float o[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int q = 0; q < Ck::kN; ++q) {
+            float v = part[0][lane][q];
+            for (int w = 1; w < kDwWaves; ++w) v += part[w][lane][q];
+            o[q] = v;
+        }
+        float4 *dst = reinterpret_cast<float4 *>(dW + ((int64_t)e * ncs + j) * Ck::kN);
+        dst[0] = make_float4(o[0], o[1], o[2], o[3]);
+        if (BF16) dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+    }
 }
 
 }  // namespace
@@ -357,14 +402,14 @@ hipError_t launch_gate_combine(const void *F, const void *H, const float *S,
     const int ncs = (int)(d / (bf16 ? 8 : 4));
     const int64_t N = B * T;
     int64_t total = N * ncs;
-    int blocks = (int)((total + 255) / 256);
+    int64_t blocks = (total + 255) / 256;
     if (blocks > 8192) blocks = 8192;
     if (bf16)
-        hipLaunchKernelGGL(gate_combine_kernel<true>, dim3(blocks), dim3(256), 0, s, F, H, S,
-                           assign, perm, shuffle, Y, (int)N, (int)T, (int)E, ncs);
+        hipLaunchKernelGGL(gate_combine_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, s, F,
+                           H, S, assign, perm, shuffle, Y, (int)N, (int)T, (int)E, ncs);
     else
-        hipLaunchKernelGGL(gate_combine_kernel<false>, dim3(blocks), dim3(256), 0, s, F, H, S,
-                           assign, perm, shuffle, Y, (int)N, (int)T, (int)E, ncs);
+        hipLaunchKernelGGL(gate_combine_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, s, F,
+                           H, S, assign, perm, shuffle, Y, (int)N, (int)T, (int)E, ncs);
     return hipGetLastError();
 }
 
@@ -374,17 +419,17 @@ hipError_t launch_gate_backward(const void *dY, const void *F, const void *H, co
                                 int64_t T, int64_t E, int64_t d, int bf16, hipStream_t s) {
     const int ncs = (int)(d / (bf16 ? 8 : 4));
     const int rows = (int)(T < 65536 ? T : 65536);
-    const dim3 dwg((unsigned)E, (unsigned)((d + 255) / 256));
+    const dim3 dwg((unsigned)E, (unsigned)((ncs + 63) / 64));
     if (bf16) {
         hipLaunchKernelGGL(gate_rows_kernel<true>, dim3(rows), dim3(256), 0, s, dY, F, W, S, assign,
                            perm, dH, dF, dS, (int)T, (int)E, ncs);
-        hipLaunchKernelGGL(gate_dw_kernel<true>, dwg, dim3(256), 0, s, H, dS, perm, offsets, dW,
-                           (int)T, (int)E, (int)d);
+        hipLaunchKernelGGL(gate_dw_kernel<true>, dwg, dim3(64 * kDwWaves), 0, s, H, dS, perm,
+                           offsets, dW, (int)T, (int)E, ncs);
     } else {
         hipLaunchKernelGGL(gate_rows_kernel<false>, dim3(rows), dim3(256), 0, s, dY, F, W, S,
                            assign, perm, dH, dF, dS, (int)T, (int)E, ncs);
-        hipLaunchKernelGGL(gate_dw_kernel<false>, dwg, dim3(256), 0, s, H, dS, perm, offsets, dW,
-                           (int)T, (int)E, (int)d);
+        hipLaunchKernelGGL(gate_dw_kernel<false>, dwg, dim3(64 * kDwWaves), 0, s, H, dS, perm,
+                           offsets, dW, (int)T, (int)E, ncs);
     }
     return hipGetLastError();
 }
