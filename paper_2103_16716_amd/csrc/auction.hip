@@ -1027,7 +1027,6 @@ __global__ void init_kernel(SolveCtrl *ctrl, void *prices, int E, AssignParams p
     }
 }
 
-// Score range (order-preserving images) and a non-finite count.
 // Score range (order-preserving images) and a non-finite flag: each block
 // reduces its share of S (16-byte loads) and writes one partial (max, min,
 // bad) to part[3 * block]; range_finish_kernel combines them. (One atomic
