@@ -115,12 +115,19 @@ int base_affinity_gather(const void *H, int64_t h_rows, const int32_t *rows, con
  * bids for its best expert (top-2 over the values S[t,e] - p[e]); each expert
  * keeps its C highest bids (ties: lower token index wins), evicts the rest,
  * and once full sets its price to its lowest held bid. A phase ends when
- * every expert holds C tokens; epsilon then shrinks by eps_factor until
- * eps_final. The result satisfies epsilon-complementary slackness with the
- * returned prices, so
+ * every expert holds C tokens; epsilon then shrinks by eps_factor (or
+ * less, below) until eps_final. With the returned prices p the result satisfies
  *     sum_t max_e (S[t,e] - p[e]) + C * sum_e p[e] - sum_t S[t, a_t] <= T * eps_final
  * (up to fp32 rounding in float mode), i.e. the assignment is within
- * T * eps_final of the optimum.
+ * T * eps_final of the optimum: the left side is the duality gap, an upper
+ * bound of optimum - objective. The last phase (epsilon = eps_final)
+ * guarantees it by epsilon-complementary slackness. After every earlier
+ * phase the device also measures the gap directly; when it already meets
+ * the bound (with an allowance for fp32 rounding), the solve stops there
+ * (stats.certified). When it misses by less than eps_factor, the next
+ * epsilon shrinks only enough for the gap, taken as proportional to
+ * epsilon, to reach half the bound. BASE_ASSIGN_FULL_SCHEDULE runs every
+ * phase with the plain eps_factor steps instead.
  *
  * Integer mode (s_dtype == BASE_I16): scores are int16; the solve runs in
  * int64 on the scores scaled by K = 2^ceil(log2(T + 1)) with eps_final = 1
@@ -156,10 +163,12 @@ enum {
     BASE_ASSIGN_SYNC_STATS = 2,      /* wait for the solve, fill *stats, report
                                         NOT_CONVERGED / RANGE */
     BASE_ASSIGN_CHECK_FINITE = 4,    /* scan S first (synchronous); NaN/Inf -> BASE_ERR_NONFINITE */
-    BASE_ASSIGN_WARM_PRICES = 8      /* start from the prices in `prices` (then overwritten
+    BASE_ASSIGN_WARM_PRICES = 8,     /* start from the prices in `prices` (then overwritten
                                         with the result) instead of 0, e.g. the prices of
                                         the previous batch; must be finite (float mode) or
                                         in scaled units (integer mode) */
+    BASE_ASSIGN_FULL_SCHEDULE = 16   /* run every epsilon phase down to eps_final, without
+                                        the duality check that may stop the solve earlier */
 };
 
 typedef struct {
@@ -168,7 +177,9 @@ typedef struct {
     double eps_initial;  /* first-phase epsilon in score units (also in integer mode,
                             where it is scaled by K); <= 0 -> (max S - min S) / 8
                             computed on the device */
-    double eps_factor;   /* epsilon divisor between phases; <= 1 -> 24 */
+    double eps_factor;   /* epsilon divisor between phases; <= 1 -> 32. After a duality
+                            check that misses the bound, the step is smaller when the
+                            measured gap asks for less (see above) */
     int32_t max_rounds;  /* bound on bidding rounds over all phases; <= 0 -> 4,000,000 */
     uint32_t flags;      /* BASE_ASSIGN_* */
 } base_assign_opts;
@@ -177,7 +188,9 @@ typedef struct {
     int32_t phases;      /* epsilon phases run */
     int32_t rounds;      /* bidding rounds over all phases */
     int64_t bids;        /* bids placed over all phases */
-    double eps_final;    /* epsilon of the last phase, in score units */
+    double eps_final;    /* the bound per token, in score units: the assignment is within
+                            T * eps_final of the optimum (eps_final as raised for fp32
+                            resolution) */
     int32_t fell_back;   /* 1 if the greedy completion was used */
     int32_t converged;   /* 1 if every expert holds exactly T/E tokens */
     int64_t engine_bids; /* the part of `bids` placed inside the single-workgroup
@@ -186,6 +199,11 @@ typedef struct {
                             units: an upper bound of optimum - objective for a balanced
                             result (the certificate of the bound above; after the greedy
                             fallback it measures what the fallback gave up) */
+    double eps_last;     /* epsilon of the last phase run, in score units (above eps_final
+                            when the solve stopped on the duality check) */
+    int32_t certified;   /* problems whose solve stopped after an earlier phase because
+                            the measured duality gap met T * eps_final */
+    int32_t reserved;
 } base_assign_stats;
 
 /* Bytes of device workspace base_assign needs for T tokens and E experts

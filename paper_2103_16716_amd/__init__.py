@@ -40,6 +40,7 @@ BASE_ASSIGN_GREEDY_FALLBACK = 1
 BASE_ASSIGN_SYNC_STATS = 2
 BASE_ASSIGN_CHECK_FINITE = 4
 BASE_ASSIGN_WARM_PRICES = 8
+BASE_ASSIGN_FULL_SCHEDULE = 16
 
 # Every symbol include/base.h declares.
 EXPORTED = ("base_status_string", "base_affinity", "base_affinity_gather",
@@ -60,7 +61,8 @@ class AssignStats(ctypes.Structure):
     _fields_ = [("phases", ctypes.c_int32), ("rounds", ctypes.c_int32), ("bids", ctypes.c_int64),
                 ("eps_final", ctypes.c_double), ("fell_back", ctypes.c_int32),
                 ("converged", ctypes.c_int32), ("engine_bids", ctypes.c_int64),
-                ("dual_gap", ctypes.c_double)]
+                ("dual_gap", ctypes.c_double), ("eps_last", ctypes.c_double),
+                ("certified", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class BaseError(RuntimeError):

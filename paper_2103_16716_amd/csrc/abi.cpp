@@ -13,12 +13,14 @@ constexpr int64_t kMaxTokens = (int64_t)1 << 24;      // token index field of a 
 constexpr int64_t kMaxTokensInt = (int64_t)1 << 21;   // integer mode: scaled scores stay < 2^37
 constexpr int64_t kMaxExperts = 2048;                 // per-expert tables staged in LDS
 // Epsilon divisor between phases. Chosen from a sweep of the first-phase
-// epsilon and the divisor over eight synthetic workloads (T from 2048 to
-// 65536, E from 64 to 256, normal and clustered scores): 24 gave the lowest
-// geometric-mean solve time. With the default first epsilon (score range
-// / 8) a solve runs 1 + ceil(log_24(range / (8 eps_final))) phases: 5 or
-// fewer for ranges up to 8 * 24^4 * eps_final (about 265 at 1e-4).
-constexpr double kDefaultEpsFactor = 24.0;
+// epsilon (score range / 4 ... / 16) and the divisor (16 ... 96) over twelve
+// synthetic workloads (T from 2048 to 65536, E from 64 to 256, normal and
+// clustered scores), with the duality check that ends a solve once its
+// measured gap meets the bound and the gap-guided step after a check that
+// misses it: range / 8 and 32 gave the lowest geometric-mean solve time.
+// Without the check a solve runs 1 + ceil(log_32(range / (8 eps_final)))
+// phases: 5 or fewer for ranges up to 8 * 32^4 * eps_final (about 840 at 1e-4).
+constexpr double kDefaultEpsFactor = 32.0;
 constexpr int64_t kMaxDim = (int64_t)1 << 30;
 constexpr int64_t kMaxBatch = 65535;   // problems per batched call (grid y dimension)
 
@@ -155,7 +157,8 @@ int assign_impl(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
         if (!(o.eps_factor > 1.0)) o.eps_factor = kDefaultEpsFactor;
         if (o.max_rounds <= 0) o.max_rounds = 4000000;
         const uint32_t known = BASE_ASSIGN_GREEDY_FALLBACK | BASE_ASSIGN_SYNC_STATS |
-                               BASE_ASSIGN_CHECK_FINITE | BASE_ASSIGN_WARM_PRICES;
+                               BASE_ASSIGN_CHECK_FINITE | BASE_ASSIGN_WARM_PRICES |
+                               BASE_ASSIGN_FULL_SCHEDULE;
         if (o.flags & ~known) return BASE_ERR_INVALID_ARG;
         if ((o.flags & BASE_ASSIGN_WARM_PRICES) && prices == nullptr) return BASE_ERR_INVALID_ARG;
     }
@@ -217,7 +220,11 @@ int assign_impl(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
             agg.engine_bids += (int64_t)c.engine_bids;
             agg.dual_gap += integer ? c.dual_gap / (double)p.scale : c.dual_gap;
             const double eps = integer ? c.eps / (double)p.scale : c.eps;
-            agg.eps_final = eps > agg.eps_final ? eps : agg.eps_final;
+            agg.eps_last = eps > agg.eps_last ? eps : agg.eps_last;
+            const double bound =
+                integer ? c.eps_final_eff / (double)p.scale : c.eps_final_eff;
+            agg.eps_final = bound > agg.eps_final ? bound : agg.eps_final;
+            agg.certified += c.certified != 0 ? 1 : 0;
             agg.fell_back |= c.fell_back;
             const bool conv = unconverged == 0 && (!c.not_converged || c.fell_back);
             if (!conv) agg.converged = 0;

@@ -48,6 +48,7 @@ constexpr int kCandLds = 4096;   // candidates of one expert staged in LDS when 
 constexpr int kRangeBlocks = 256;   // blocks of the score-range reduction
 constexpr int kCountTile = 256;  // tokens per block in the permutation build
 constexpr int kWideLoopRounds = 1024;  // rounds one launch of the round loop may run
+constexpr int kCheckBlocks = 4096;     // largest grid of the phase check
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -60,7 +61,7 @@ inline void debug_note(const char *what, hipError_t err) {
 
 struct Layout {
     size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
-        eck, ecs, ecn, sums, bar, rpart, total;
+        eck, ecs, ecn, sums, bar, rpart, gpart, total;
     int64_t cap, nblk;
 };
 
@@ -88,6 +89,7 @@ Layout make_layout(int64_t T, int64_t E) {
     L.sums = off;    off += align_up((size_t)T * 64);          // per-token score summaries
     L.bar = off;     off += align_up(512);                      // grid barrier words
     L.rpart = off;   off += align_up((size_t)kRangeBlocks * 12);   // score-range partials
+    L.gpart = off;   off += align_up((size_t)kCheckBlocks * 8);    // phase-check partials
     L.total = off;
     return L;
 }
@@ -111,6 +113,7 @@ struct Ctx {
     int *eng_cn;
     uint32_t *sums;   // T x 16 words: each token's 8 best scores, their experts, a bound
     uint64_t *bar;    // grid barrier: arrivals at bar[0], release at bar[32] (own lines)
+    double *gpart;    // per-block partial sums of the phase check
     int64_t ws_stride;   // bytes between the workspaces of consecutive problems of a batch
 
     // The view of problem b of a batch (blockIdx.y in every solver launch):
@@ -141,6 +144,7 @@ struct Ctx {
         r.eng_cn = shift(eng_cn, w);
         r.sums = shift(sums, w);
         r.bar = shift(bar, w);
+        r.gpart = shift(gpart, w);
         return r;
     }
 };
@@ -173,6 +177,7 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.eng_cn = reinterpret_cast<int *>(ws + L.ecn);
     c.sums = reinterpret_cast<uint32_t *>(ws + L.sums);
     c.bar = reinterpret_cast<uint64_t *>(ws + L.bar);
+    c.gpart = reinterpret_cast<double *>(ws + L.gpart);
     c.ws_stride = (int64_t)L.total;
     return c;
 }
@@ -984,7 +989,17 @@ __device__ inline void begin_phase_scalar(SolveCtrl *ctrl, const AssignParams &p
         }
     } else {
         eps = ctrl->eps / p.eps_factor;
+        // A gap measured after the previous phase that misses T eps_final by
+        // less than the divisor asks for a smaller step: epsilon shrinks just
+        // enough for the gap, taken as proportional to epsilon, to fall to
+        // half the bound.
+        const double gap = ctrl->check_gap;
+        if (gap > 0.0) {
+            const double guided = ctrl->eps * 0.5 * (double)T * ctrl->eps_final_eff / gap;
+            if (guided > eps) eps = guided;
+        }
     }
+    ctrl->check_gap = 0.0;
     if (p.integer) eps = floor(eps);
     if (!(eps > ctrl->eps_final_eff)) eps = ctrl->eps_final_eff;
     ctrl->eps = eps;
@@ -2298,6 +2313,145 @@ __global__ void holders_to_assign_kernel(Ctx<M> c0, int32_t *assign) {
 
 int lanes_per_token(int64_t E);
 
+// ------------------------------------------------------------ phase check --
+//
+// The duality certificate after a phase that is not the last. With every
+// expert holding C tokens, D(p) - objective equals
+//     sum over held tokens t of [max_e (S[t,e] - p[e]) - (S[t,a_t] - p[a_t])],
+// a sum of nonnegative per-token slacks (no cancellation between two large
+// sums). By weak duality it bounds optimum - objective. When it is at most
+// T eps_final, less an allowance for the rounding of the per-token maxima
+// in the solve's arithmetic, the assignment already meets the bound the
+// last phase would guarantee, and the solve stops here. Groups of G lanes
+// take holder slots in expert order and read each token's maximum from its
+// score summary (its row when the summary cannot decide); each block writes
+// one partial sum, and phase_check_finish_kernel decides.
+template <class M, int G>
+__global__ __launch_bounds__(kThreads) void phase_check_kernel(Ctx<M> c0) {
+    using value_t = typename M::value_t;
+    const Ctx<M> c = c0.at(blockIdx.y);
+    SolveCtrl *ctrl = c.ctrl;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
+    __shared__ double part[kThreads / 64];
+    __shared__ int go;
+    if (threadIdx.x == 0) {
+        go = !ctrl->done && !ctrl->last_phase && ctrl->phase > 0 && !ctrl->all_active &&
+             ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
+    }
+    __syncthreads();
+    if (!go) return;
+    // The holder-table selectors, as the previous kernels left them.
+    int *sel = reinterpret_cast<int *>(smem_raw + (((size_t)c.E * sizeof(value_t) + 15) & ~size_t(15)));
+    for (int e = threadIdx.x; e < c.E; e += kThreads) {
+        pr[e] = c.prices[e];
+        sel[e] = c.hsel[e] & 1;
+    }
+    __syncthreads();
+    const value_t pmin = block_min_price<M>(pr, c.E);
+    const int gl = lane_id() & (G - 1);
+    const int per_block = kThreads / G;
+    const int ngroups = per_block * gridDim.x;
+    const int n_round = ((c.T + ngroups - 1) / ngroups) * ngroups;
+    double acc = 0.0;
+    for (int i = blockIdx.x * per_block + threadIdx.x / G; i < n_round; i += ngroups) {
+        bool valid = i < c.T;
+        const int e = valid ? i / c.C : 0;
+        int t = 0;
+        if (valid) {
+            const uint64_t *hold = c.holders + (int64_t)sel[e] * c.T + (int64_t)e * c.C;
+            t = key_token(hold[i - e * c.C]);
+            if (t < 0 || t >= c.T) {
+                if (gl == 0) flag_internal(ctrl);
+                valid = false;
+                t = 0;
+            }
+        }
+        uint32_t sw[4] = {0, 0, 0, 0};
+        if (valid) load_summary(c.sums, t, gl, sw);
+        value_t v1, v2, s1;
+        int e1;
+        top2_summary<M, G>(c, sw, t, valid, gl, pr, pmin, v1, e1, v2, s1);
+        if (valid && gl == 0)
+            acc += (double)v1 -
+                   ((double)M::load(c.S, (int64_t)t * c.E + e, c.scale) - (double)pr[e]);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    if (lane_id() == 0) part[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double sum = 0.0;
+        for (int w = 0; w < kThreads / 64; ++w) sum += part[w];
+        c.gpart[blockIdx.x] = sum;
+    }
+}
+
+// The decision, one block per problem: the partials added in a fixed order
+// (thread i takes blocks i, i + kThreads, ...; then the waves' shuffle trees
+// and the waves in order), so it does not depend on scheduling. (A
+// last-block counter in the check kernel instead cost about 70 us: a
+// thousand device-scope atomics on one address.)
+template <class M>
+__global__ __launch_bounds__(kThreads) void phase_check_finish_kernel(Ctx<M> c0, int nparts) {
+    const Ctx<M> c = c0.at(blockIdx.y);
+    SolveCtrl *ctrl = c.ctrl;
+    __shared__ double part[kThreads / 64], pbig[kThreads / 64];
+    __shared__ int go;
+    if (threadIdx.x == 0) {
+        go = !ctrl->done && !ctrl->last_phase && ctrl->phase > 0 && !ctrl->all_active &&
+             ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
+    }
+    __syncthreads();
+    if (!go) return;
+    double g = 0.0, pm = 0.0;
+    for (int b = threadIdx.x; b < nparts; b += kThreads) g += c.gpart[b];
+    for (int e = threadIdx.x; e < c.E; e += kThreads) pm = fmax(pm, fabs((double)c.prices[e]));
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        g += __shfl_xor(g, off);
+        pm = fmax(pm, __shfl_xor(pm, off));
+    }
+    if (lane_id() == 0) {
+        part[threadIdx.x >> 6] = g;
+        pbig[threadIdx.x >> 6] = pm;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    double gap = 0.0, pmax = 0.0;
+    for (int w = 0; w < kThreads / 64; ++w) {
+        gap += part[w];
+        pmax = fmax(pmax, pbig[w]);
+    }
+    double allowance = 0.0;
+    if (!M::kInteger) {
+        // Each maximum is one fp32 subtraction of values below max|S| + max|p|:
+        // at most half an ulp, 2^-24 of that magnitude; four times that per token.
+        const double smax = fmax(fabs((double)f32_unord(ctrl->smax_ord)),
+                                 fabs((double)f32_unord(ctrl->smin_ord)));
+        allowance = (double)c.T * ldexp(smax + pmax, -22);
+    }
+    if (gap + allowance <= (double)c.T * ctrl->eps_final_eff) {
+        ctrl->certified = 1;
+        ctrl->done = 1;
+    } else {
+        ctrl->check_gap = gap + allowance;
+    }
+}
+
+template <class M, int G>
+hipError_t launch_phase_check(const Ctx<M> &c, int B, hipStream_t s) {
+    const size_t pr_bytes = (((size_t)c.E * sizeof(typename M::value_t) + 15) & ~size_t(15)) +
+                            (size_t)c.E * sizeof(int);
+    const int per_block = kThreads / G;
+    int blocks = (c.T + 2 * per_block - 1) / (2 * per_block);
+    if (blocks > kCheckBlocks) blocks = kCheckBlocks;
+    hipLaunchKernelGGL((phase_check_kernel<M, G>), dim3(blocks, B), dim3(kThreads), pr_bytes, s,
+                       c);
+    hipLaunchKernelGGL(phase_check_finish_kernel<M>, dim3(1, B), dim3(kThreads), 0, s, c, blocks);
+    return hipGetLastError();
+}
+
 // The duality gap of the result (statistics only): D(p) - objective =
 //     sum_t [max_e (S[t,e] - p[e]) - S[t, a_t]] + C sum_e p[e],
 // per-token values in the solve's arithmetic, the sum in double. For a
@@ -2633,6 +2787,10 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
         }
         hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1, B), dim3(kThreads), tail_smem, s, c, p,
                            slot == slots - 1 ? 1 : 0);
+        if (slot < slots - 1 && !(p.flags & BASE_ASSIGN_FULL_SCHEDULE)) {
+            const hipError_t err = launch_phase_check<M, G>(c, B, s);
+            if (err != hipSuccess) return err;
+        }
     }
     return hipGetLastError();
 }

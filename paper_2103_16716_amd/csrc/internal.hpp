@@ -56,18 +56,18 @@ struct SolveCtrl {
     int32_t pad2;
     unsigned long long engine_bids;   // bids placed inside the single-workgroup engine
     double dual_gap;        // D(p) - objective after the solve (when statistics are asked for)
-    int64_t pad1[1];
+    int32_t certified;      // 1: stopped after a phase whose duality gap met T eps_final
+    int32_t pad3;
+    double check_gap;       // duality gap measured after the last phase (0: not measured)
 };
 
 size_t assign_workspace_size(int64_t T, int64_t E);
 
-// Enqueues the whole solve; returns the first HIP error of the launches.
 // Enqueues the whole solve of B independent problems of T x E scores
 // (scores, outputs and workspaces laid out problem after problem).
 hipError_t launch_assign(const void *S, const AssignParams &p, int64_t B, int32_t *assign,
                          int32_t *perm, void *prices_out, void *workspace, hipStream_t stream);
 
-// Reads the statistics back (synchronises the stream).
 // Reads the B control blocks back (synchronises the stream).
 hipError_t read_assign_stats(const void *workspace, int64_t T, int64_t E, int64_t B,
                              SolveCtrl *out, hipStream_t stream);

@@ -387,6 +387,67 @@ def test_warm_start_prices():
     print("rounds cold", cold.stats.rounds, "warm", warm.stats.rounds)
 
 
+def test_duality_check_stops_early_within_the_bound():
+    """After each phase but the last the device measures the duality gap and
+    stops once it meets T eps_final: the result is then certified by weak
+    duality, not by eps_final-complementary slackness. Against the exact
+    optimum both the early result and the full schedule meet the bound; the
+    full schedule runs more phases and certifies nothing."""
+    inp = wl.make_inputs("t32768-e128-d2048-mix8")
+    S = pb.affinity(*inputs_on_device(inp))
+    early = pb.assign(S)
+    full = pb.assign(S, flags=pb.BASE_ASSIGN_FULL_SCHEDULE)
+    S64 = host(S).astype(np.float64)
+    T = S64.shape[0]
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    check_assignment(S64, early, EPS_FINAL, opt=(a_opt, obj_opt))
+    check_assignment(S64, full, EPS_FINAL, opt=(a_opt, obj_opt))
+    assert early.stats.certified == 1 and full.stats.certified == 0
+    assert early.stats.phases < full.stats.phases
+    assert early.stats.eps_last > early.stats.eps_final
+    assert full.stats.eps_last == pytest.approx(full.stats.eps_final)
+    # The device's gap agrees with the oracle's dual bound at the returned prices.
+    gap = oracle.dual_bound(S64, host(early.prices).astype(np.float64)) - \
+        oracle.objective(S64, host(early.assign))
+    assert abs(early.stats.dual_gap - gap) <= 1e-6 * T
+    assert gap <= T * early.stats.eps_final
+
+
+def test_duality_check_missed_then_guided():
+    """A bound tight enough that the first checks miss it: the next phases
+    take the gap-guided steps and the solve still ends within the bound (or
+    at the last phase)."""
+    inp = wl.make_inputs("t8192-e64-d1024")
+    S = pb.affinity(*inputs_on_device(inp))
+    S64 = host(S).astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    for eps in (2e-5, 1e-3, 3e-2):
+        res = pb.assign(S, eps_final=eps)
+        check_assignment(S64, res, eps, opt=(a_opt, obj_opt))
+        if eps <= 1e-3:
+            assert res.stats.phases >= 2
+
+
+def test_duality_check_batched_and_integer():
+    """The check runs per problem of a batch (each stops on its own), and in
+    integer mode a certified stop is still the exact optimum."""
+    B = 4
+    S = _worker_batch(B, 4200)
+    res = pb.assign_batched(S)
+    for b in range(B):
+        one = pb.assign(S[b].contiguous())
+        assert torch.equal(res.assign[b], one.assign)
+        assert torch.equal(res.prices[b], one.prices)
+    T, E = 2048, 16
+    rng = np.random.Generator(np.random.PCG64(91))
+    Si = rng.integers(-2000, 2000, size=(T, E), dtype=np.int16)
+    r = pb.assign(dev(Si))
+    S64 = Si.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    assert oracle.objective(S64, host(r.assign)) == obj_opt
+    print("integer phases", r.stats.phases, "certified", r.stats.certified)
+
+
 def test_engine_launch_timing():
     """The measurement hook brackets each engine launch with events on the
     call's stream: one record per phase slot, each within the whole call."""
