@@ -478,27 +478,20 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
     }
 }
 
-// Reads the summary table from blocks spread over every XCD, so that the
-// L2 of whichever XCD runs the one-workgroup engine holds it. Consecutive
-// workgroups go to consecutive XCDs; with a multiple of 8 blocks, the blocks
-// of any one XCD cover the whole table whatever XCD block 0 lands on.
-__global__ __launch_bounds__(256) void summary_prefill_kernel(const uint4 *sums, int64_t n16,
-                                                              const SolveCtrl *ctrl, int cap,
-                                                              uint32_t *sink, int64_t ws_stride) {
-    const int64_t w = (int64_t)blockIdx.y * ws_stride;
-    sums = Ctx<FloatMode>::shift(sums, w);
-    ctrl = Ctx<FloatMode>::shift(ctrl, w);
-    sink = Ctx<FloatMode>::shift(sink, w);
-    if (ctrl->done || ctrl->all_active) return;
-    const int n = ld_relaxed(&ctrl->active_count[ctrl->cur]);
-    if (n <= 0 || n > cap) return;
-    const int per_xcd = gridDim.x / 8;
+// Reads the summary table from `pf` blocks (a multiple of 8) spread over
+// every XCD, so that the L2 of whichever XCD runs the one-workgroup engine
+// holds it. Consecutive workgroups go to consecutive XCDs; block i of the
+// pf covers chunk i / 8, so the blocks on any one XCD cover the whole table
+// whatever XCD the first lands on.
+__device__ inline void summary_prefill(const uint4 *sums, int64_t n16, int i, int pf,
+                                       uint32_t *sink) {
+    const int per_xcd = pf / 8;
     const int64_t chunk = (n16 + per_xcd - 1) / per_xcd;
-    const int64_t lo = (int64_t)(blockIdx.x / 8) * chunk;
+    const int64_t lo = (int64_t)(i / 8) * chunk;
     const int64_t hi = lo + chunk < n16 ? lo + chunk : n16;
     uint32_t acc = 0;
-    for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
-        const uint4 v = sums[i];
+    for (int64_t k = lo + threadIdx.x; k < hi; k += blockDim.x) {
+        const uint4 v = sums[k];
         acc ^= v.x ^ v.y ^ v.z ^ v.w;
     }
     if (acc == 0x9e3779b9u && threadIdx.x == 0) *sink = acc;   // keeps the loads
@@ -1168,20 +1161,175 @@ __global__ void eps_floor_kernel(SolveCtrl *ctrl, int integer, int64_t ws_stride
     if (ctrl->eps_final_eff < floor_eps) ctrl->eps_final_eff = floor_eps;
 }
 
-template <class M>
-__global__ void phase_begin_kernel(Ctx<M> c0, AssignParams p) {
+// ------------------------------------------------------------ phase check --
+//
+// The duality certificate after a phase that is not the last. With every
+// expert holding C tokens, D(p) - objective equals
+//     sum over held tokens t of [max_e (S[t,e] - p[e]) - (S[t,a_t] - p[a_t])],
+// a sum of nonnegative per-token slacks (no cancellation between two large
+// sums). By weak duality it bounds optimum - objective. When it is at most
+// T eps_final, less an allowance for the rounding of the per-token maxima
+// in the solve's arithmetic, the assignment already meets the bound the
+// last phase would guarantee, and the solve stops here. Groups of G lanes
+// take holder slots in expert order and read each token's maximum from its
+// score summary (its row when the summary cannot decide); each block writes
+// one partial sum, and the next slot's phase_begin_kernel decides.
+template <class M, int G>
+__global__ __launch_bounds__(kThreads) void phase_check_kernel(Ctx<M> c0) {
+    using value_t = typename M::value_t;
     const Ctx<M> c = c0.at(blockIdx.y);
-    __shared__ int skip;
+    SolveCtrl *ctrl = c.ctrl;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
+    __shared__ double part[kThreads / 64];
+    __shared__ int go;
     if (threadIdx.x == 0) {
-        skip = c.ctrl->done;
-        if (!skip) begin_phase_scalar(c.ctrl, p, c.T);
+        go = !ctrl->done && !ctrl->last_phase && ctrl->phase > 0 && !ctrl->all_active &&
+             ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
     }
+    __syncthreads();
+    if (!go) return;
+    // The holder-table selectors, as the previous kernels left them.
+    int *sel = reinterpret_cast<int *>(smem_raw + (((size_t)c.E * sizeof(value_t) + 15) & ~size_t(15)));
+    for (int e = threadIdx.x; e < c.E; e += kThreads) {
+        pr[e] = c.prices[e];
+        sel[e] = c.hsel[e] & 1;
+    }
+    __syncthreads();
+    const value_t pmin = block_min_price<M>(pr, c.E);
+    const int gl = lane_id() & (G - 1);
+    const int per_block = kThreads / G;
+    const int ngroups = per_block * gridDim.x;
+    const int n_round = ((c.T + ngroups - 1) / ngroups) * ngroups;
+    double acc = 0.0;
+    for (int i = blockIdx.x * per_block + threadIdx.x / G; i < n_round; i += ngroups) {
+        bool valid = i < c.T;
+        const int e = valid ? i / c.C : 0;
+        int t = 0;
+        if (valid) {
+            const uint64_t *hold = c.holders + (int64_t)sel[e] * c.T + (int64_t)e * c.C;
+            t = key_token(hold[i - e * c.C]);
+            if (t < 0 || t >= c.T) {
+                if (gl == 0) flag_internal(ctrl);
+                valid = false;
+                t = 0;
+            }
+        }
+        uint32_t sw[4] = {0, 0, 0, 0};
+        if (valid) load_summary(c.sums, t, gl, sw);
+        value_t v1, v2, s1;
+        int e1;
+        top2_summary<M, G>(c, sw, t, valid, gl, pr, pmin, v1, e1, v2, s1);
+        if (valid && gl == 0)
+            acc += (double)v1 -
+                   ((double)M::load(c.S, (int64_t)t * c.E + e, c.scale) - (double)pr[e]);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    if (lane_id() == 0) part[threadIdx.x >> 6] = acc;
+    __syncthreads();
     if (threadIdx.x == 0) {
+        double sum = 0.0;
+        for (int w = 0; w < kThreads / 64; ++w) sum += part[w];
+        c.gpart[blockIdx.x] = sum;
+    }
+}
+
+// The decision on the gap phase_check_kernel measured, by one block: the
+// partials added in a fixed order (thread i takes blocks i, i + blockDim,
+// ...; then the waves' shuffle trees and the waves in order), so it does not
+// depend on scheduling. (A last-block counter in the check kernel instead
+// cost about 70 us: a thousand device-scope atomics on one address.)
+template <class M>
+__device__ void phase_check_decide(const Ctx<M> &c, int nparts) {
+    SolveCtrl *ctrl = c.ctrl;
+    __shared__ double part[16], pbig[16];
+    double g = 0.0, pm = 0.0;
+    for (int b = threadIdx.x; b < nparts; b += blockDim.x) g += c.gpart[b];
+    for (int e = threadIdx.x; e < c.E; e += blockDim.x) pm = fmax(pm, fabs((double)c.prices[e]));
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        g += __shfl_xor(g, off);
+        pm = fmax(pm, __shfl_xor(pm, off));
+    }
+    if (lane_id() == 0) {
+        part[threadIdx.x >> 6] = g;
+        pbig[threadIdx.x >> 6] = pm;
+    }
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    double gap = 0.0, pmax = 0.0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+        gap += part[w];
+        pmax = fmax(pmax, pbig[w]);
+    }
+    double allowance = 0.0;
+    if (!M::kInteger) {
+        // Each maximum is one fp32 subtraction of values below max|S| + max|p|:
+        // at most half an ulp, 2^-24 of that magnitude; four times that per token.
+        const double smax = fmax(fabs((double)f32_unord(ctrl->smax_ord)),
+                                 fabs((double)f32_unord(ctrl->smin_ord)));
+        allowance = (double)c.T * ldexp(smax + pmax, -22);
+    }
+    if (gap + allowance <= (double)c.T * ctrl->eps_final_eff) {
+        ctrl->certified = 1;
+        ctrl->done = 1;
+    } else {
+        ctrl->check_gap = gap + allowance;
+    }
+}
+
+// Blocks of phase_check_kernel for T tokens (the partials the next slot's
+// phase_begin_kernel adds).
+inline int phase_check_blocks(int T, int G) {
+    const int per_block = kThreads / G;
+    const int blocks = (T + 2 * per_block - 1) / (2 * per_block);
+    return blocks < kCheckBlocks ? blocks : kCheckBlocks;
+}
+
+template <class M, int G>
+hipError_t launch_phase_check(const Ctx<M> &c, int B, hipStream_t s) {
+    const size_t pr_bytes = (((size_t)c.E * sizeof(typename M::value_t) + 15) & ~size_t(15)) +
+                            (size_t)c.E * sizeof(int);
+    const int blocks = phase_check_blocks(c.T, G);
+    hipLaunchKernelGGL((phase_check_kernel<M, G>), dim3(blocks, B), dim3(kThreads), pr_bytes, s,
+                       c);
+    return hipGetLastError();
+}
+
+// Starts a phase slot (one block per problem): first the decision on the
+// duality gap the previous slot measured (nparts partials; 0 when no check
+// ran), then the next epsilon phase, unless the solve is done or the
+// current phase still has active tokens (its rounds then go on in this slot).
+template <class M>
+__global__ void phase_begin_kernel(Ctx<M> c0, AssignParams p, int nparts) {
+    const Ctx<M> c = c0.at(blockIdx.y);
+    SolveCtrl *ctrl = c.ctrl;
+    __shared__ int check, begin;
+    if (threadIdx.x == 0) {
+        const bool finished = ctrl->phase > 0 && !ctrl->all_active &&
+                              ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
+        check = nparts > 0 && !ctrl->done && !ctrl->last_phase && finished;
         c.bar[0] = 0;    // the round loop's barrier counts from zero in every launch
         c.bar[32] = 0;
     }
     __syncthreads();
-    if (skip) return;
+    if (check) phase_check_decide<M>(c, nparts);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        begin = 0;
+        if (!ctrl->done) {
+            const bool in_progress =
+                ctrl->phase > 0 &&
+                (ctrl->all_active || ld_relaxed(&ctrl->active_count[ctrl->cur]) > 0);
+            if (!in_progress) {
+                begin_phase_scalar(ctrl, p, c.T);
+                begin = 1;
+            }
+        }
+    }
+    __syncthreads();
+    if (!begin) return;
     for (int e = threadIdx.x; e < c.E; e += blockDim.x) {
         c.hcount[e] = 0;
         c.hsel[e] = 0;
@@ -1990,10 +2138,11 @@ __device__ __attribute__((always_inline)) void engine_solo(const Ctx<M> &c, cons
     }
 }
 
-// The engine's phase entry, one block per expert: sorts the expert's holder
-// table and stores its K lowest keys (with slots) for the engine to load.
+// The engine's phase entry, one launch: blocks [0, E) sort expert e's
+// holder table and store its K lowest keys (with slots) for the engine to
+// load; the `pf` blocks after them pull the score summaries into every L2.
 template <class M>
-__global__ __launch_bounds__(256) void cache_build_kernel(Ctx<M> c0) {
+__global__ __launch_bounds__(256) void engine_entry_kernel(Ctx<M> c0, int pf) {
     const Ctx<M> c = c0.at(blockIdx.y);
     __shared__ uint64_t keys[kEngMaxC];
     __shared__ uint16_t slots[kEngMaxC];
@@ -2008,6 +2157,11 @@ __global__ __launch_bounds__(256) void cache_build_kernel(Ctx<M> c0) {
     }
     __syncthreads();
     if (!go) return;
+    if ((int)blockIdx.x >= c.E) {
+        summary_prefill(reinterpret_cast<const uint4 *>(c.sums), (int64_t)c.T * 4,
+                        (int)blockIdx.x - c.E, pf, reinterpret_cast<uint32_t *>(&ctrl->pad2));
+        return;
+    }
     const int e = blockIdx.x;
     int cnt = ld_relaxed(&c.hcount[e]);
     if (cnt < 0 || cnt > c.C) {
@@ -2313,145 +2467,6 @@ __global__ void holders_to_assign_kernel(Ctx<M> c0, int32_t *assign) {
 
 int lanes_per_token(int64_t E);
 
-// ------------------------------------------------------------ phase check --
-//
-// The duality certificate after a phase that is not the last. With every
-// expert holding C tokens, D(p) - objective equals
-//     sum over held tokens t of [max_e (S[t,e] - p[e]) - (S[t,a_t] - p[a_t])],
-// a sum of nonnegative per-token slacks (no cancellation between two large
-// sums). By weak duality it bounds optimum - objective. When it is at most
-// T eps_final, less an allowance for the rounding of the per-token maxima
-// in the solve's arithmetic, the assignment already meets the bound the
-// last phase would guarantee, and the solve stops here. Groups of G lanes
-// take holder slots in expert order and read each token's maximum from its
-// score summary (its row when the summary cannot decide); each block writes
-// one partial sum, and phase_check_finish_kernel decides.
-template <class M, int G>
-__global__ __launch_bounds__(kThreads) void phase_check_kernel(Ctx<M> c0) {
-    using value_t = typename M::value_t;
-    const Ctx<M> c = c0.at(blockIdx.y);
-    SolveCtrl *ctrl = c.ctrl;
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
-    __shared__ double part[kThreads / 64];
-    __shared__ int go;
-    if (threadIdx.x == 0) {
-        go = !ctrl->done && !ctrl->last_phase && ctrl->phase > 0 && !ctrl->all_active &&
-             ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
-    }
-    __syncthreads();
-    if (!go) return;
-    // The holder-table selectors, as the previous kernels left them.
-    int *sel = reinterpret_cast<int *>(smem_raw + (((size_t)c.E * sizeof(value_t) + 15) & ~size_t(15)));
-    for (int e = threadIdx.x; e < c.E; e += kThreads) {
-        pr[e] = c.prices[e];
-        sel[e] = c.hsel[e] & 1;
-    }
-    __syncthreads();
-    const value_t pmin = block_min_price<M>(pr, c.E);
-    const int gl = lane_id() & (G - 1);
-    const int per_block = kThreads / G;
-    const int ngroups = per_block * gridDim.x;
-    const int n_round = ((c.T + ngroups - 1) / ngroups) * ngroups;
-    double acc = 0.0;
-    for (int i = blockIdx.x * per_block + threadIdx.x / G; i < n_round; i += ngroups) {
-        bool valid = i < c.T;
-        const int e = valid ? i / c.C : 0;
-        int t = 0;
-        if (valid) {
-            const uint64_t *hold = c.holders + (int64_t)sel[e] * c.T + (int64_t)e * c.C;
-            t = key_token(hold[i - e * c.C]);
-            if (t < 0 || t >= c.T) {
-                if (gl == 0) flag_internal(ctrl);
-                valid = false;
-                t = 0;
-            }
-        }
-        uint32_t sw[4] = {0, 0, 0, 0};
-        if (valid) load_summary(c.sums, t, gl, sw);
-        value_t v1, v2, s1;
-        int e1;
-        top2_summary<M, G>(c, sw, t, valid, gl, pr, pmin, v1, e1, v2, s1);
-        if (valid && gl == 0)
-            acc += (double)v1 -
-                   ((double)M::load(c.S, (int64_t)t * c.E + e, c.scale) - (double)pr[e]);
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-    if (lane_id() == 0) part[threadIdx.x >> 6] = acc;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        double sum = 0.0;
-        for (int w = 0; w < kThreads / 64; ++w) sum += part[w];
-        c.gpart[blockIdx.x] = sum;
-    }
-}
-
-// The decision, one block per problem: the partials added in a fixed order
-// (thread i takes blocks i, i + kThreads, ...; then the waves' shuffle trees
-// and the waves in order), so it does not depend on scheduling. (A
-// last-block counter in the check kernel instead cost about 70 us: a
-// thousand device-scope atomics on one address.)
-template <class M>
-__global__ __launch_bounds__(kThreads) void phase_check_finish_kernel(Ctx<M> c0, int nparts) {
-    const Ctx<M> c = c0.at(blockIdx.y);
-    SolveCtrl *ctrl = c.ctrl;
-    __shared__ double part[kThreads / 64], pbig[kThreads / 64];
-    __shared__ int go;
-    if (threadIdx.x == 0) {
-        go = !ctrl->done && !ctrl->last_phase && ctrl->phase > 0 && !ctrl->all_active &&
-             ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
-    }
-    __syncthreads();
-    if (!go) return;
-    double g = 0.0, pm = 0.0;
-    for (int b = threadIdx.x; b < nparts; b += kThreads) g += c.gpart[b];
-    for (int e = threadIdx.x; e < c.E; e += kThreads) pm = fmax(pm, fabs((double)c.prices[e]));
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        g += __shfl_xor(g, off);
-        pm = fmax(pm, __shfl_xor(pm, off));
-    }
-    if (lane_id() == 0) {
-        part[threadIdx.x >> 6] = g;
-        pbig[threadIdx.x >> 6] = pm;
-    }
-    __syncthreads();
-    if (threadIdx.x != 0) return;
-    double gap = 0.0, pmax = 0.0;
-    for (int w = 0; w < kThreads / 64; ++w) {
-        gap += part[w];
-        pmax = fmax(pmax, pbig[w]);
-    }
-    double allowance = 0.0;
-    if (!M::kInteger) {
-        // Each maximum is one fp32 subtraction of values below max|S| + max|p|:
-        // at most half an ulp, 2^-24 of that magnitude; four times that per token.
-        const double smax = fmax(fabs((double)f32_unord(ctrl->smax_ord)),
-                                 fabs((double)f32_unord(ctrl->smin_ord)));
-        allowance = (double)c.T * ldexp(smax + pmax, -22);
-    }
-    if (gap + allowance <= (double)c.T * ctrl->eps_final_eff) {
-        ctrl->certified = 1;
-        ctrl->done = 1;
-    } else {
-        ctrl->check_gap = gap + allowance;
-    }
-}
-
-template <class M, int G>
-hipError_t launch_phase_check(const Ctx<M> &c, int B, hipStream_t s) {
-    const size_t pr_bytes = (((size_t)c.E * sizeof(typename M::value_t) + 15) & ~size_t(15)) +
-                            (size_t)c.E * sizeof(int);
-    const int per_block = kThreads / G;
-    int blocks = (c.T + 2 * per_block - 1) / (2 * per_block);
-    if (blocks > kCheckBlocks) blocks = kCheckBlocks;
-    hipLaunchKernelGGL((phase_check_kernel<M, G>), dim3(blocks, B), dim3(kThreads), pr_bytes, s,
-                       c);
-    hipLaunchKernelGGL(phase_check_finish_kernel<M>, dim3(1, B), dim3(kThreads), 0, s, c, blocks);
-    return hipGetLastError();
-}
-
 // The duality gap of the result (statistics only): D(p) - objective =
 //     sum_t [max_e (S[t,e] - p[e]) - S[t, a_t]] + C sum_e p[e],
 // per-token values in the solve's arithmetic, the sum in double. For a
@@ -2723,8 +2738,8 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
     // Phase slots enqueued up front; the last one continues on its own if
     // the epsilon schedule needs more phases than were enqueued. With the
-    // default schedule (first epsilon = range / 8, divisor 24) six slots
-    // cover score ranges up to 8 * 24^5 (about 6 * 10^7) times eps_final.
+    // default schedule (first epsilon = range / 8, divisor 32) six slots
+    // cover score ranges up to 8 * 32^5 (about 3 * 10^8) times eps_final.
     int slots = 6;
     if (p.eps_initial > 0.0) {
         double e = p.eps_initial;
@@ -2761,8 +2776,15 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
         }
         (void)hipGetLastError();
     }
+    // Each slot: the phase start (with the decision on the previous slot's
+    // duality check), the wide rounds, the round loop, the engine, the
+    // one-workgroup tail (with the engine only in the last slot: a phase the
+    // engine leaves unfinished goes on in the next slot), and the check.
+    const bool checks = !(p.flags & BASE_ASSIGN_FULL_SCHEDULE);
+    const int check_parts = phase_check_blocks(c.T, G);
     for (int slot = 0; slot < slots; ++slot) {
-        hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1, B), dim3(1024), 0, s, c, p);
+        hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1, B), dim3(1024), 0, s, c, p,
+                           checks && slot > 0 ? check_parts : 0);
         for (int r = 0; r < wide_rounds; ++r) {
             hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks, B), dim3(kThreads),
                                bid_bytes, s, c);
@@ -2772,12 +2794,10 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
             hipLaunchKernelGGL((wide_loop_kernel<M, G>), dim3(coop_blocks, B), dim3(kThreads),
                                bid_bytes, s, c, kWideLoopRounds, p.max_rounds);
         if (engine) {
-            hipLaunchKernelGGL(cache_build_kernel<M>, dim3(c.E, B), dim3(256), 0, s, c);
-            // Multiples of 8 blocks per problem, 256 in all when one problem.
+            // Summary readers: multiples of 8 blocks per problem, 256 in all
+            // when one problem.
             const int pf = B >= 32 ? 8 : 8 * (32 / B);
-            hipLaunchKernelGGL(summary_prefill_kernel, dim3(pf, B), dim3(256), 0, s,
-                               reinterpret_cast<const uint4 *>(c.sums), (int64_t)c.T * 4, c.ctrl,
-                               kEngCap, reinterpret_cast<uint32_t *>(&c.ctrl->pad2), c.ws_stride);
+            hipLaunchKernelGGL(engine_entry_kernel<M>, dim3(c.E + pf, B), dim3(256), 0, s, c, pf);
             hipEvent_t ev0 = nullptr, ev1 = nullptr;
             timing_pair(&ev0, &ev1);
             if (ev0 != nullptr) (void)hipEventRecord(ev0, s);
@@ -2785,9 +2805,10 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
                                c, p);
             if (ev1 != nullptr) (void)hipEventRecord(ev1, s);
         }
-        hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1, B), dim3(kThreads), tail_smem, s, c, p,
-                           slot == slots - 1 ? 1 : 0);
-        if (slot < slots - 1 && !(p.flags & BASE_ASSIGN_FULL_SCHEDULE)) {
+        if (!engine || slot == slots - 1)
+            hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1, B), dim3(kThreads), tail_smem, s, c,
+                               p, slot == slots - 1 ? 1 : 0);
+        if (checks && slot < slots - 1) {
             const hipError_t err = launch_phase_check<M, G>(c, B, s);
             if (err != hipSuccess) return err;
         }
