@@ -36,6 +36,7 @@ import workloads as wl  # noqa: E402
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak, TFLOP/s
 UNPERMUTE_WORKLOADS = {"t65536-e256-d4096"}
+COLD_STEPS = 5                 # steps timed after evicting the caches
 ENGINE_KERNEL = "engine_kernel"   # the solve's dominant kernel (rounds with few active tokens)
 PROFILES = os.path.join(ROOT, "profiles")
 
@@ -266,18 +267,37 @@ def main():
     names = ["affinity", "assign", "permute"] + (["unpermute"] if unpermute else [])
     per_call_ms = {n: float(np.mean([ev[i].elapsed_time(ev[i + 1]) for ev in events]))
                    for i, n in enumerate(names)}
-    gpu_ms = float(np.mean([ev[0].elapsed_time(ev[-1]) for ev in events]))
+    step_ms = np.array([ev[0].elapsed_time(ev[-1]) for ev in events])
+    gpu_ms = float(np.mean(step_ms))
     ms_per_step = wall * 1e3 / args.steps
 
-    # One more solve with statistics, and balance checks on a few more steps.
+    # Cold caches: a 512 MiB write before each of a few more steps evicts the
+    # inputs from L2 and the last-level cache (they stay resident in HBM).
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cold = []
+    for k in range(COLD_STEPS):
+        scratch.fill_(k & 0xff)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_ev)]
+        step(ev)
+        torch.cuda.synchronize()
+        cold.append(ev[0].elapsed_time(ev[-1]))
+    del scratch
+
+    # Solves with statistics and balance checks on a few more steps: the solve
+    # is deterministic, so every repetition must give the same rounds, bids
+    # and assignment.
     checked, balanced = 0, 0
+    runs = []
     for _ in range(3):
         step()
-        torch.cuda.synchronize()
+        res = pb.assign(S, workspace=ws, out_assign=a, out_perm=perm, out_prices=prices)
         counts = torch.bincount(a.long(), minlength=E)
         balanced += int(bool(torch.all(counts == T // E)))
         checked += 1
-    res = pb.assign(S, workspace=ws, out_assign=a, out_perm=perm, out_prices=prices)
+        runs.append((res.stats.rounds, res.stats.bids, a.clone()))
+    deterministic = all(r[0] == runs[0][0] and r[1] == runs[0][1] and torch.equal(r[2], runs[0][2])
+                        for r in runs)
+    assert deterministic, "repeated solves differ"
     st = res.stats
 
     # Algorithmic traffic per call (bytes), and flops for the GEMM.
@@ -329,15 +349,22 @@ def main():
                      "share_of_step": eng_ms / args.steps / gpu_ms if gpu_ms > 0 else None},
         "per_call_ms": {k: round(v, 4) for k, v in per_call_ms.items()},
         "gpu_ms_per_step": gpu_ms,
+        "step_ms_quantiles": {"p10": float(np.percentile(step_ms, 10)),
+                              "median": float(np.median(step_ms)),
+                              "p90": float(np.percentile(step_ms, 90))},
+        "cold_step_ms_median": float(np.median(cold)),
         "per_call_roofline": {k: {"bound": v[0], "achieved": round(v[1], 2), "peak": v[2],
                                   "unit": v[3], "frac": round(v[1] / v[2], 4)}
                               for k, v in rl.items()},
         "affinity_mfma": {"achieved_tflops": flops_aff / (per_call_ms["affinity"] * 1e-3) / 1e12,
                           "peak_tflops": MFMA_BF16_PEAK_TFLOPS},
         "assign_stats": {"phases": st.phases, "rounds": st.rounds, "bids": st.bids,
-                         "engine_bids": st.engine_bids, "eps_final": st.eps_final,
-                         "converged": st.converged},
+                         "bids_per_token": st.bids / T, "engine_bids": st.engine_bids,
+                         "eps_final": st.eps_final, "eps_last": st.eps_last,
+                         "certified": st.certified, "dual_gap": st.dual_gap,
+                         "gap_bound": T * st.eps_final, "converged": st.converged},
         "balanced_solves": f"{balanced}/{checked}",
+        "deterministic": deterministic,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inp)
