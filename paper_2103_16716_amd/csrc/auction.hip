@@ -746,8 +746,8 @@ __host__ __device__ inline BidSmem bid_smem(int E, int value_bytes) {
 struct UpdateSmem {
     uint64_t cand[kCandLds];
     uint32_t hist[256];
-    uint64_t minkey;
-    int sel_digit, need, kept, pos;
+    uint64_t minkey, kmin, kmax;
+    int sel_digit, sel_count, need, kept, pos;
 };
 
 // Calls fn(key) for every candidate of expert e (holders, bucket, overflow)
@@ -800,6 +800,7 @@ __device__ inline void pick_digit(UpdateSmem &sm, int need) {
             for (int j = 0; j < 4; ++j) {
                 if ((int)(cum + h[j]) >= need) {
                     sm.sel_digit = 255 - 4 * l - j;
+                    sm.sel_count = (int)h[j];
                     sm.need = need - (int)cum;
                     break;
                 }
@@ -873,12 +874,41 @@ __device__ void update_expert(const Ctx<M> &c, int e, int next, int novf, Update
     }
 
     // More candidates than slots: find the C-th largest key by MSD radix
-    // select (8 bits per pass), keep keys >= it, evict the rest.
+    // select (8 bits per pass), keep keys >= it, evict the rest. The passes
+    // start below the leading bytes every candidate shares (from their
+    // smallest and largest key) and stop once the chosen digit's keys are
+    // exactly the ones still needed: the C-th largest is then their minimum.
     const bool staged = total <= kCandLds;
+    if (tid == 0) {
+        sm.pos = 0;
+        sm.kmin = ~0ull;
+        sm.kmax = 0;
+    }
+    __syncthreads();
+    // Smallest and largest candidate: per thread, then per wave, then one
+    // LDS atomic per wave (one per candidate would serialise on two words).
+    uint64_t tmin = ~0ull, tmax = 0;
+    auto range = [&](uint64_t k, bool v) {
+        if (v) {
+            tmin = k < tmin ? k : tmin;
+            tmax = k > tmax ? k : tmax;
+        }
+    };
+    auto range_done = [&]() {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const uint64_t a = __shfl_xor(tmin, off), b = __shfl_xor(tmax, off);
+            tmin = a < tmin ? a : tmin;
+            tmax = b > tmax ? b : tmax;
+        }
+        if (lane_id() == 0) {
+            atomicMin(reinterpret_cast<unsigned long long *>(&sm.kmin), (unsigned long long)tmin);
+            atomicMax(reinterpret_cast<unsigned long long *>(&sm.kmax), (unsigned long long)tmax);
+        }
+    };
     if (staged) {
-        if (tid == 0) sm.pos = 0;
-        __syncthreads();
         for_each_candidate<M>(c, e, hold, h, nb, novf_e, [&](uint64_t k, bool v) {
+            range(k, v);
             const uint64_t m = __ballot(v);
             if (m == 0) return;
             const int leader = __ffsll((long long)m) - 1;
@@ -888,11 +918,18 @@ __device__ void update_expert(const Ctx<M> &c, int e, int next, int novf, Update
             const int at = base + __popcll(m & lanemask_lt());
             if (v && at < kCandLds) sm.cand[at] = k;
         });
-        __syncthreads();
+    } else {
+        for_each_candidate<M>(c, e, hold, h, nb, novf_e, range);
     }
-    uint64_t prefix = 0, pmask = 0;
+    range_done();
+    __syncthreads();
+    const uint64_t kdiff = sm.kmin ^ sm.kmax;   // non-zero: more than C distinct keys
+    const int first = kdiff ? ((63 - __clzll((long long)kdiff)) / 8) * 8 : 0;
+    uint64_t pmask = first >= 56 ? 0ull : ~0ull << (first + 8);
+    uint64_t prefix = sm.kmin & pmask;
     int need = c.C;
-    for (int shift = 56; shift >= 0; shift -= 8) {
+    bool at_min = false;
+    for (int shift = first; shift >= 0; shift -= 8) {
         for (int i = tid; i < 256; i += blockDim.x) sm.hist[i] = 0;
         __syncthreads();
         auto count = [&](uint64_t k, bool v) {
@@ -909,9 +946,28 @@ __device__ void update_expert(const Ctx<M> &c, int e, int next, int novf, Update
         prefix |= (uint64_t)sm.sel_digit << shift;
         pmask |= 255ull << shift;
         need = sm.need;
+        const bool whole = sm.sel_count == need;
+        __syncthreads();
+        if (whole && shift > 0) {
+            at_min = true;
+            break;
+        }
+    }
+    if (at_min) {
+        if (tid == 0) sm.kmin = ~0ull;
+        __syncthreads();
+        tmin = ~0ull;
+        tmax = 0;
+        auto low = [&](uint64_t k, bool v) { range(k, v && (k & pmask) == prefix); };
+        if (staged) {
+            for (int i = tid; i < total; i += blockDim.x) low(sm.cand[i], true);
+        } else {
+            for_each_candidate<M>(c, e, hold, h, nb, novf_e, low);
+        }
+        range_done();
         __syncthreads();
     }
-    const uint64_t kstar = prefix;   // keys are unique, so this is a key
+    const uint64_t kstar = at_min ? sm.kmin : prefix;   // keys are unique: a key
 
     uint64_t *alt = c.holders + (int64_t)(sel ^ 1) * c.T + (int64_t)e * c.C;
     if (tid == 0) sm.kept = 0;
