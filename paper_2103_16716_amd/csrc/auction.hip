@@ -2792,11 +2792,15 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
     if (engine) c.engine_cap = kEngCap;
     const size_t pr_bytes = (size_t)c.E * sizeof(value_t);
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
-    // Phase slots enqueued up front; the last one continues on its own if
-    // the epsilon schedule needs more phases than were enqueued. With the
-    // default schedule (first epsilon = range / 8, divisor 32) six slots
-    // cover score ranges up to 8 * 32^5 (about 3 * 10^8) times eps_final.
-    int slots = 6;
+    // Phase slots enqueued up front; the last one continues on its own (in
+    // one workgroup, slowly) if the epsilon schedule needs more phases than
+    // were enqueued. A slot the solve no longer needs still costs about
+    // 45 us of empty launches. With the default schedule (first epsilon =
+    // range / 8, divisor 32) five slots cover score ranges up to 8 * 32^4
+    // (about 8 * 10^6) times eps_final even without a certified early stop,
+    // which typically comes one or two phases sooner; the full schedule
+    // gets six (up to 8 * 32^5, about 3 * 10^8).
+    int slots = (p.flags & BASE_ASSIGN_FULL_SCHEDULE) ? 6 : 5;
     if (p.eps_initial > 0.0) {
         double e = p.eps_initial;
         slots = 1;
