@@ -1779,6 +1779,14 @@ __device__ inline void er_write(const Ctx<M> &c, uint64_t *hold, ExpertRegs<M> &
     r.np += 1;
 }
 
+// Rank of this lane's key among the keys of lanes [0, n) (keys distinct):
+// n readlane steps, no LDS round trip.
+__device__ inline int wave_rank(uint64_t key, int n) {
+    int r = 0;
+    for (int j = 0; j < n; ++j) r += rl64(key, j) < key ? 1 : 0;
+    return r;
+}
+
 // The K lowest keys of the expert's holder table, sorted, into the lanes.
 // The table is read from global memory and patched with the pending stores;
 // the K-th smallest key is found by a bitwise search on ballot counts, the
@@ -1809,9 +1817,71 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
     r.slot = 0;
     if (take == 0) return;
     // thr: the largest value with fewer than `take` keys below it, i.e. the
-    // take-th smallest key (keys are distinct).
-    uint64_t thr = 0;
-    for (int bit = 63; bit >= 0; --bit) {
+    // take-th smallest key (keys are distinct). The bits above the highest
+    // one where the smallest and largest key differ are common to every key
+    // (and to thr): the search starts below them.
+    uint64_t kmin = ~0ull, kmax = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        if (kk[q] != ~0ull) {
+            kmin = kk[q] < kmin ? kk[q] : kmin;
+            kmax = kk[q] > kmax ? kk[q] : kmax;
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint64_t a = __shfl_xor(kmin, off), b = __shfl_xor(kmax, off);
+        kmin = a < kmin ? a : kmin;
+        kmax = b > kmax ? b : kmax;
+    }
+    const uint64_t kdiff = kmin ^ kmax;
+    const int top = kdiff ? 63 - __clzll((long long)kdiff) : 0;
+    uint64_t thr = top >= 63 ? 0ull : kmin & (~0ull << (top + 1));
+    // Bit by bit over the top 12 differing bits; then, when at most 64 keys
+    // share the prefix found, the take-th smallest is among them (the keys
+    // below the prefix are fewer than take, those up to its end at least
+    // take): ranking them finishes the search. Otherwise the bits go on.
+    const int lo = top >= 12 ? top - 11 : 0;
+    int bit = top;
+    for (; bit >= lo; --bit) {
+        const uint64_t trial = thr | (1ull << bit);
+        int below = 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) below += __popcll(__ballot(kk[q] < trial));
+        if (below < take) thr = trial;
+    }
+    if (lo > 0) {
+        const uint64_t hi = thr >> lo;
+        int below = 0, inb = 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            below += __popcll(__ballot((kk[q] >> lo) < hi));
+            inb += __popcll(__ballot((kk[q] >> lo) == hi));
+        }
+        if (inb <= 64) {
+            int at = 0;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const bool in = (kk[q] >> lo) == hi;
+                const uint64_t m = __ballot(in);
+                if (in) scr_key[at + __popcll(m & lanemask_lt())] = kk[q];
+                at += __popcll(m);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const uint64_t bk = lane < inb ? scr_key[lane] : ~0ull;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const int need = take - below;   // in [1, inb]
+            const uint64_t hit = __ballot(lane < inb && wave_rank(bk, inb) == need - 1);
+            if (hit != 0) thr = rl64(bk, __ffsll((long long)hit) - 1);
+            else flag_internal(c.ctrl);
+            bit = -1;
+        }
+    }
+    for (; bit >= 0; --bit) {
         const uint64_t trial = thr | (1ull << bit);
         int below = 0;
 #pragma unroll
@@ -1835,6 +1905,20 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // The take selected keys in ascending order: each goes to its rank.
+    const uint64_t sk = lane < take ? scr_key[lane] : ~0ull;
+    const int ss = lane < take ? scr_slot[lane] : 0;
+    const int rk = wave_rank(sk, take);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane < take && rk < 64) {
+        scr_key[rk] = sk;
+        scr_slot[rk] = ss;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (lane < take) {
         r.key = scr_key[lane];
         r.slot = scr_slot[lane];
@@ -1842,20 +1926,6 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-    for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            const uint64_t pk = __shfl_xor(r.key, j);
-            const int ps = __shfl_xor(r.slot, j);
-            const bool ascending = (lane & k) == 0;
-            const bool keep_min = ((lane & j) == 0) == ascending;
-            if (keep_min ? pk < r.key : pk > r.key) {
-                r.key = pk;
-                r.slot = ps;
-            }
-        }
-    }
 }
 
 // Loads expert e's state into the wave's registers.
