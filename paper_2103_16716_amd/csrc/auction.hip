@@ -1779,11 +1779,13 @@ __device__ inline void er_write(const Ctx<M> &c, uint64_t *hold, ExpertRegs<M> &
     r.np += 1;
 }
 
-// Rank of this lane's key among the keys of lanes [0, n) (keys distinct):
-// n readlane steps, no LDS round trip.
-__device__ inline int wave_rank(uint64_t key, int n) {
+// Rank of `key` among keys[0, n) in the wave's LDS scratch (keys
+// distinct): every lane reads the same word at a time (broadcast loads,
+// several in flight).
+__device__ inline int lds_rank(const uint64_t *keys, int n, uint64_t key) {
     int r = 0;
-    for (int j = 0; j < n; ++j) r += rl64(key, j) < key ? 1 : 0;
+#pragma unroll 8
+    for (int j = 0; j < n; ++j) r += keys[j] < key ? 1 : 0;
     return r;
 }
 
@@ -1871,11 +1873,11 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
             const uint64_t bk = lane < inb ? scr_key[lane] : ~0ull;
+            const int need = take - below;   // in [1, inb]
+            const uint64_t hit = __ballot(lane < inb && lds_rank(scr_key, inb, bk) == need - 1);
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            const int need = take - below;   // in [1, inb]
-            const uint64_t hit = __ballot(lane < inb && wave_rank(bk, inb) == need - 1);
             if (hit != 0) thr = rl64(bk, __ffsll((long long)hit) - 1);
             else flag_internal(c.ctrl);
             bit = -1;
@@ -1908,7 +1910,7 @@ __device__ void er_refill(const Ctx<M> &c, const uint64_t *hold, int K, ExpertRe
     // The take selected keys in ascending order: each goes to its rank.
     const uint64_t sk = lane < take ? scr_key[lane] : ~0ull;
     const int ss = lane < take ? scr_slot[lane] : 0;
-    const int rk = wave_rank(sk, take);
+    const int rk = lds_rank(scr_key, take, sk);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
