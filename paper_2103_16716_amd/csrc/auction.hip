@@ -401,6 +401,7 @@ __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const type
 // value exceeds that limit and its second value reaches it.
 
 constexpr int kSumWords = 16;
+constexpr int kSumChunks = 4;   // chunks of 8 G experts per row: E <= 4 * 8 * 64 = 2048
 
 template <class M>
 __device__ inline uint32_t score_bits(typename M::value_t v, int64_t scale) {
@@ -424,18 +425,23 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
     const int per_block = kThreads / G;
     const int n_round = ((c.T + per_block * (int)gridDim.x - 1) / (per_block * (int)gridDim.x)) *
                         per_block * (int)gridDim.x;
-    const int e0 = 8 * gl;
+    // Lane gl holds experts 8 gl .. 8 gl + 7 of each chunk of 8 G experts
+    // (several chunks when E > 8 G, which happens only at G = 64).
     const int take = c.E < 8 ? c.E : 8;
     for (int t = blockIdx.x * per_block + threadIdx.x / G; t < n_round;
          t += per_block * gridDim.x) {
         const bool valid = t < c.T;
-        value_t sv[8];
+        value_t sv[kSumChunks][8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) sv[q] = M::lowest();
-        if (valid && e0 < c.E) load8<M>(c.S, (int64_t)t * c.E, e0, c.E, c.scale, sv);
+        for (int ch = 0; ch < kSumChunks; ++ch) {
+            const int e0 = ch * 8 * G + 8 * gl;
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-            if (e0 + q >= c.E) sv[q] = M::lowest();
+            for (int q = 0; q < 8; ++q) sv[ch][q] = M::lowest();
+            if (valid && e0 < c.E) load8<M>(c.S, (int64_t)t * c.E, e0, c.E, c.scale, sv[ch]);
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                if (e0 + q >= c.E) sv[ch][q] = M::lowest();
+        }
         uint32_t *out = c.sums + (int64_t)(valid ? t : 0) * kSumWords;
         uint32_t pairs[4] = {0, 0, 0, 0};
         for (int r = 0; r <= take; ++r) {
@@ -443,10 +449,14 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
             value_t bv = M::lowest();
             int be = 0x7fffffff;
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
-                if (e0 + q < c.E && sv[q] > bv) {
-                    bv = sv[q];
-                    be = e0 + q;
+            for (int ch = 0; ch < kSumChunks; ++ch)
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const int e = ch * 8 * G + 8 * gl + q;
+                    if (e < c.E && sv[ch][q] > bv) {
+                        bv = sv[ch][q];
+                        be = e;
+                    }
                 }
 #pragma unroll
             for (int off = G / 2; off > 0; off >>= 1) {
@@ -458,11 +468,11 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
                 }
             }
             if (r < take) {
-                if (be >= e0 && be < e0 + 8) {
+#pragma unroll
+                for (int ch = 0; ch < kSumChunks; ++ch)
 #pragma unroll
                     for (int q = 0; q < 8; ++q)
-                        if (e0 + q == be) sv[q] = M::lowest();
-                }
+                        if (ch * 8 * G + 8 * gl + q == be) sv[ch][q] = M::lowest();
                 if (valid && gl == 0) out[r] = score_bits<M>(bv, c.scale);
                 pairs[r >> 1] |= (uint32_t)(be & 0xffff) << (16 * (r & 1));
             } else if (valid && gl == 0) {

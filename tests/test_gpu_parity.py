@@ -143,6 +143,32 @@ def test_assign_ragged_shapes_against_ssp(T, E):
                      unique_gap=oracle.optimum_gap(S64, a_opt))
 
 
+@pytest.mark.parametrize("T,E", [(3000, 600), (8192, 1024), (4096, 2048), (2048, 2)])
+@pytest.mark.parametrize("full", [False, True])
+def test_assign_without_the_engine(T, E, full):
+    """Shapes the single-workgroup engine does not serve (E > 512 or
+    C = T/E > 512): the wide rounds, the round loop and the one-workgroup
+    tail solve every phase, with and without the duality check."""
+    S = wl.random_scores(T, E, seed=T + E)
+    S64 = S.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    res = pb.assign(dev(S), flags=pb.BASE_ASSIGN_FULL_SCHEDULE if full else 0)
+    check_assignment(S64, res, EPS_FINAL, opt=(a_opt, obj_opt),
+                     unique_gap=oracle.optimum_gap(S64, a_opt) if E <= 64 else None)
+    if full:
+        assert res.stats.certified == 0
+
+
+def test_assign_batched_without_the_engine():
+    B, T, E = 3, 3000, 600
+    S = np.stack([wl.random_scores(T, E, seed=77 + b) for b in range(B)])
+    res = pb.assign_batched(dev(S))
+    for b in range(B):
+        one = pb.assign(dev(S[b].copy()))
+        assert torch.equal(res.assign[b], one.assign)
+        assert torch.equal(res.prices[b], one.prices)
+
+
 @pytest.mark.parametrize("name", ["t512-e8-d128-f32", "t4096-e16-d512", "t8192-e64-d1024",
                                   "t2048-e128-d2048-worker"])
 def test_assign_workloads_against_ssp(name):
