@@ -159,6 +159,29 @@ def test_assign_without_the_engine(T, E, full):
         assert res.stats.certified == 0
 
 
+def test_assign_without_the_engine_integer_and_fallback():
+    """The tail path in integer mode (an exact optimum) and under a round
+    bound with the greedy completion (balanced, the loss certified)."""
+    T, E = 1800, 600
+    rng = np.random.Generator(np.random.PCG64(31))
+    Si = rng.integers(-500, 500, size=(T, E), dtype=np.int16)
+    S64 = Si.astype(np.float64)
+    a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+    r = pb.assign(dev(Si))
+    assert r.stats.converged == 1
+    assert oracle.balanced_counts_ok(host(r.assign), E)
+    assert oracle.objective(S64, host(r.assign)) == obj_opt
+    S = wl.random_scores(T, E, seed=32)
+    Sf = S.astype(np.float64)
+    _, obj_f, _ = oracle.solve_ssp(Sf)
+    res = pb.assign(dev(S), max_rounds=3, flags=pb.BASE_ASSIGN_GREEDY_FALLBACK)
+    a = host(res.assign)
+    assert res.stats.fell_back == 1 and res.stats.converged == 1
+    assert oracle.balanced_counts_ok(a, E)
+    np.testing.assert_array_equal(host(res.perm), oracle.stable_perm(a, E))
+    assert obj_f - oracle.objective(Sf, a) <= res.stats.dual_gap + 1e-6 * T
+
+
 def test_assign_batched_without_the_engine():
     B, T, E = 3, 3000, 600
     S = np.stack([wl.random_scores(T, E, seed=77 + b) for b in range(B)])
