@@ -182,6 +182,24 @@ def test_assign_without_the_engine_integer_and_fallback():
     assert obj_f - oracle.objective(Sf, a) <= res.stats.dual_gap + 1e-6 * T
 
 
+def test_assign_batched_more_problems_than_compute_units():
+    """300 problems: more than the 256 compute units, so the batch runs
+    without the round loop (its blocks could not all be resident); each
+    problem still equals its own solve."""
+    B, T, E = 300, 256, 8
+    rng = np.random.Generator(np.random.PCG64(301))
+    S = rng.standard_normal((B, T, E), dtype=np.float32)
+    res = pb.assign_batched(dev(S))
+    assert res.stats.converged == 1
+    for b in (0, 137, B - 1):
+        one = pb.assign(dev(S[b].copy()))
+        assert torch.equal(res.assign[b], one.assign)
+        assert torch.equal(res.prices[b], one.prices)
+        S64 = S[b].astype(np.float64)
+        a_opt, obj_opt, _ = oracle.solve_ssp(S64)
+        check_assignment(S64, one, EPS_FINAL, opt=(a_opt, obj_opt))
+
+
 def test_assign_batched_without_the_engine():
     B, T, E = 3, 3000, 600
     S = np.stack([wl.random_scores(T, E, seed=77 + b) for b in range(B)])

@@ -88,6 +88,17 @@ def test_permute_batched_bit_exact(dtype, shuffled):
     np.testing.assert_array_equal(back, x)
 
 
+def test_permute_batched_many_tiny_problems():
+    B, T, d = 1000, 8, 16
+    rng = np.random.Generator(np.random.PCG64(45))
+    x = rand_rows(rng, B * T, d, "bf16")
+    perm = _row_perms(rng, B, T)
+    sh = wl.shuffle_permutation(B * T, 46)
+    src = sh[(np.arange(B)[:, None] * T + perm).ravel()]
+    out = host(pb.permute_batched(dev(x), dev(perm), shuffle=dev(sh)))
+    np.testing.assert_array_equal(out, x[src])
+
+
 def test_permute_batched_single_problem_is_base_permute():
     rng = np.random.Generator(np.random.PCG64(44))
     T, d = 300, 64
