@@ -2046,29 +2046,38 @@ __device__ inline uint64_t *expert_holders(const Ctx<M> &c, const Eng<M> &s, int
 // One wave: streams expert e's bids of this round into its holders. Bids are
 // bids[0..nb), or, with `exps`, the entries of bids[0..nb) whose expert is e
 // (picked out by a ballot, 64 entries per step).
+// Tokens that leave, collected by one wave in lane order (lane k holds
+// the k-th) over the experts it updates in a round, and appended to the
+// next active list 64 at a time (one LDS atomic per append).
+struct OutQueue {
+    int n = 0;
+    int tok = 0;
+};
+
+template <class M>
+__device__ inline void flush_outs(const Ctx<M> &c, OutQueue &q, int *nxt, int *nnext) {
+    const int lane = lane_id();
+    if (q.n == 0) return;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(nnext, q.n);
+    base = __builtin_amdgcn_readfirstlane(base);
+    if (lane < q.n) {
+        const int at = base + lane;
+        if (at < kEngCap && q.tok >= 0 && q.tok < c.T) nxt[at] = q.tok;
+        else flag_internal(c.ctrl);
+    }
+    q.n = 0;
+}
+
 template <class M>
 __device__ __attribute__((always_inline)) void eng_update(const Ctx<M> &c, const Eng<M> &s, int e, const uint64_t *bids,
-                           const int *exps, int nb, int *nxt, int *nnext) {
+                           const int *exps, int nb, int *nxt, int *nnext, OutQueue &q) {
     const int lane = lane_id();
     uint64_t *hold = expert_holders<M>(c, s, e);
     uint64_t *scr_key = s.scr_key + (threadIdx.x >> 6) * 64;
     int *scr_slot = s.scr_slot + (threadIdx.x >> 6) * 64;
     ExpertRegs<M> r;
     er_load<M>(s, e, r);
-    // Tokens that leave collect in lane order (lane k holds the k-th) and
-    // are appended to the next list 64 at a time.
-    int nout = 0, outv = 0;
-    auto flush_out = [&]() {
-        int base = 0;
-        if (lane == 0) base = atomicAdd(nnext, nout);
-        base = __builtin_amdgcn_readfirstlane(base);
-        if (lane < nout) {
-            const int at = base + lane;
-            if (at < kEngCap && outv >= 0 && outv < c.T) nxt[at] = outv;
-            else flag_internal(c.ctrl);
-        }
-        nout = 0;
-    };
     // Bids are read 64 at a time, one per lane, and taken in lane order.
     for (int j0 = 0; j0 < nb; j0 += 64) {
         const int j = j0 + lane;
@@ -2080,12 +2089,11 @@ __device__ __attribute__((always_inline)) void eng_update(const Ctx<M> &c, const
             mask &= mask - 1;
             const int out_tok = er_bid<M>(c, hold, s.K, r, rl64(mykey, src), scr_key, scr_slot);
             if (out_tok >= 0) {
-                if (lane == nout) outv = out_tok;
-                if (++nout == 64) flush_out();
+                if (lane == q.n) q.tok = out_tok;
+                if (++q.n == 64) flush_outs<M>(c, q, nxt, nnext);
             }
         }
     }
-    if (nout > 0) flush_out();
     er_store<M>(c, s, e, hold, r);
 }
 
@@ -2500,8 +2508,10 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
         const int nt = s_ntouched < c.E ? s_ntouched : c.E;
         if (n <= kEngDirect) {
             // Few bids: every wave reads them all and keeps its experts' ones.
+            OutQueue q;
             for (int j = wave; j < nt; j += kEngWaves)
-                eng_update<M>(c, s, s.tch[j], s.bkey, s.bexp, n, nxt, &s_nnext);
+                eng_update<M>(c, s, s.tch[j], s.bkey, s.bexp, n, nxt, &s_nnext, q);
+            flush_outs<M>(c, q, nxt, &s_nnext);
         } else {
             if (wave == 0) {
                 int base = 0;
@@ -2526,6 +2536,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
                 else flag_internal(ctrl);
             }
             lds_barrier();
+            OutQueue q;
             for (int j = wave; j < nt; j += kEngWaves) {
                 const int e = s.tch[j];
                 int nb = s.bcnt[e];
@@ -2534,8 +2545,9 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
                     if (lane == 0) flag_internal(ctrl);
                     nb = kEngCap - off;
                 }
-                eng_update<M>(c, s, e, s.bsort + off, nullptr, nb, nxt, &s_nnext);
+                eng_update<M>(c, s, e, s.bsort + off, nullptr, nb, nxt, &s_nnext, q);
             }
+            flush_outs<M>(c, q, nxt, &s_nnext);
         }
         lds_barrier();
         for (int j = tid; j < nt; j += kEngThreads) {
