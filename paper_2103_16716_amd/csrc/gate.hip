@@ -29,7 +29,7 @@
 namespace base {
 namespace {
 
-constexpr int kGreedyTile = 256;   // tokens per block of the greedy count
+constexpr int kGreedyTile = 64;    // tokens per block of the greedy count
 constexpr int kGroup = 16;         // lanes per token in the argmax
 
 __device__ inline int lane_of() { return threadIdx.x & 63; }
