@@ -309,7 +309,7 @@ def test_assign_user_epsilon_schedule():
                                                   ("t65536-e256-d4096", None, 32.0, 8.0)])
 def test_assign_phases_that_stay_large(name, seed, div, factor):
     """Epsilon schedules under which many tokens stay active after the fixed
-    wide rounds of a phase, so the cooperative round loop takes over before
+    wide rounds of a phase, so the grid-barrier round loop takes over before
     the single-workgroup engine: the result still meets the epsilon bound
     against the exact optimum."""
     w = wl.WORKLOADS[name]
