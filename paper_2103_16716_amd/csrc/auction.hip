@@ -1687,10 +1687,10 @@ __host__ __device__ inline EngLayout eng_layout(int E, int value_bytes, int K) {
     L.cnt = off;   off = eng_align(off + (size_t)E * 4);
     L.cn = off;    off = eng_align(off + (size_t)E * 4);
     L.sel = off;   off = eng_align(off + (size_t)E * 4);
-    L.bcnt = off;  off = eng_align(off + (size_t)E * 4);
+    L.bcnt = off;  off = eng_align(off + (size_t)2 * E * 4);   // two rounds' worth
     L.boff = off;  off = eng_align(off + (size_t)E * 4);
     L.bfill = off; off = eng_align(off + (size_t)E * 4);
-    L.tch = off;   off = eng_align(off + (size_t)E * 4);
+    L.tch = off;   off = eng_align(off + (size_t)2 * E * 4);
     L.ck = off;    off = eng_align(off + (size_t)E * K * 8);
     L.cs = off;    off = eng_align(off + (size_t)E * K * 2);
     L.bkey = off;  off = eng_align(off + (size_t)kEngCap * 8);
@@ -1707,7 +1707,8 @@ __host__ __device__ inline EngLayout eng_layout(int E, int value_bytes, int K) {
 template <class M>
 struct Eng {
     typename M::value_t *pr;
-    int *cnt, *cn, *sel, *bcnt, *boff, *bfill, *tch;
+    int *cnt, *cn, *sel, *boff, *bfill;
+    int *bcnt, *tch;   // [2][E]: consecutive rounds alternate halves
     uint64_t *ck;
     uint16_t *cs;
     uint64_t *bkey, *bsort;
@@ -2172,14 +2173,12 @@ constexpr int solo_tokens() { return (64 / G) < 8 ? (64 / G) : 8; }
 // caller's next barrier.
 template <class M, int G>
 __device__ __attribute__((always_inline)) void engine_solo(const Ctx<M> &c, const Eng<M> &s, int *act, typename M::value_t eps,
-                            typename M::value_t pmin, int max_rounds_left, int *s_n,
-                            int *s_rounds, unsigned long long *s_bids) {
+                            typename M::value_t pmin, int max_rounds_left, int n, int rounds,
+                            int *s_n, int *s_rounds, unsigned long long *s_bids) {
     using value_t = typename M::value_t;
     const int lane = lane_id();
     const int gl = lane & (G - 1);
     const int g = lane / G;
-    int n = *s_n;
-    int rounds = *s_rounds;
     unsigned long long bids = 0;
     int tokv = lane < n ? act[lane] : 0;   // lane k holds active token k
     int overflow = 0;
@@ -2375,7 +2374,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
     s.scr_slot = reinterpret_cast<int *>(smem_raw + L.sslot);
     int *act = reinterpret_cast<int *>(smem_raw + L.actA);
     int *nxt = reinterpret_cast<int *>(smem_raw + L.actB);
-    __shared__ int s_go, s_cur, s_n, s_nnext, s_ntouched, s_rounds, s_stop;
+    __shared__ int s_go, s_cur, s_n, s_nnext[2], s_ntouched[2], s_rounds, s_stop;
     __shared__ unsigned long long s_bids;
 
     SolveCtrl *ctrl = c.ctrl;
@@ -2392,8 +2391,8 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
                 s_n = n;
             }
         }
-        s_nnext = 0;
-        s_ntouched = 0;
+        s_nnext[0] = s_nnext[1] = 0;
+        s_ntouched[0] = s_ntouched[1] = 0;
         s_rounds = 0;
         s_stop = 0;
         s_bids = 0;
@@ -2415,6 +2414,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
         s.cn[e] = cn;
         s.sel[e] = ld_relaxed(&c.hsel[e]) & 1;
         s.bcnt[e] = 0;
+        s.bcnt[c.E + e] = 0;
         s.bfill[e] = 0;
     }
     for (int i = tid; i < c.E * K; i += kEngThreads) {
@@ -2446,18 +2446,45 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
     const int per_pass = kEngThreads / G;
     const int gid = tid / G;
     const int gl = lane & (G - 1);
+    // Round bookkeeping: every thread keeps the active count and the round
+    // number in registers. The per-expert bid counts, the touched-expert
+    // list and the two LDS counters alternate halves between consecutive
+    // rounds (parity h): a round clears what the round before used while it
+    // bids, so a round needs two workgroup barriers (three with grouping)
+    // and no separate clearing step.
+    int n = s_n;
+    int rounds = 0;
+    int h = 0;
+    int nt_prev = 0;
     for (;;) {
-        const int n = s_n;
         if (n == 0) break;
-        if (s_rounds >= max_rounds_left) {
+        if (rounds >= max_rounds_left) {
             if (tid == 0) s_stop = 1;
             break;
         }
         if (n <= solo_tokens<G>()) {
+            // Runs the rest of the phase (see engine_solo): the loop ends next.
             if (wave == 0)
-                engine_solo<M, G>(c, s, act, eps, pmin, max_rounds_left, &s_n, &s_rounds, &s_bids);
+                engine_solo<M, G>(c, s, act, eps, pmin, max_rounds_left, n, rounds, &s_n,
+                                  &s_rounds, &s_bids);
             __syncthreads();
+            n = s_n;
+            rounds = s_rounds;
             continue;
+        }
+        int *const bcnt = s.bcnt + h * c.E;
+        int *const tch = s.tch + h * c.E;
+        {
+            // The previous round's counts and fill counters back to zero
+            // (read last before the barrier that ended it).
+            const int *tch_prev = s.tch + (h ^ 1) * c.E;
+            int *bcnt_prev = s.bcnt + (h ^ 1) * c.E;
+            for (int j = tid; j < nt_prev; j += kEngThreads) {
+                const int e = tch_prev[j];
+                bcnt_prev[e] = 0;
+                s.bfill[e] = 0;
+            }
+            if (tid == 0) s_ntouched[h ^ 1] = 0;
         }
         // Bids against the prices at the start of the round.
         // Each group keeps kEngRows score rows in flight: all loads first,
@@ -2497,34 +2524,36 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
                 if (overflow) ctrl->overflow = 1;
                 s.bkey[i] = key;
                 s.bexp[i] = e1;
-                if (atomicAdd(&s.bcnt[e1], 1) == 0) {
-                    const int at = atomicAdd(&s_ntouched, 1);
-                    if (at < c.E) s.tch[at] = e1;
+                if (atomicAdd(&bcnt[e1], 1) == 0) {
+                    const int at = atomicAdd(&s_ntouched[h], 1);
+                    if (at < c.E) tch[at] = e1;
                 }
             }
           }
         }
         __syncthreads();   // also completes the previous round's holder-table stores
-        const int nt = s_ntouched < c.E ? s_ntouched : c.E;
+        const int nt = s_ntouched[h] < c.E ? s_ntouched[h] : c.E;
+        int *const nnext = &s_nnext[h];
+        if (tid == 0) s_nnext[h ^ 1] = 0;   // read last right after the previous round
         if (n <= kEngDirect) {
             // Few bids: every wave reads them all and keeps its experts' ones.
             OutQueue q;
             for (int j = wave; j < nt; j += kEngWaves)
-                eng_update<M>(c, s, s.tch[j], s.bkey, s.bexp, n, nxt, &s_nnext, q);
-            flush_outs<M>(c, q, nxt, &s_nnext);
+                eng_update<M>(c, s, tch[j], s.bkey, s.bexp, n, nxt, nnext, q);
+            flush_outs<M>(c, q, nxt, nnext);
         } else {
             if (wave == 0) {
                 int base = 0;
                 for (int j0 = 0; j0 < nt; j0 += 64) {
                     const int j = j0 + lane;
-                    const int cj = j < nt ? s.bcnt[s.tch[j]] : 0;
+                    const int cj = j < nt ? bcnt[tch[j]] : 0;
                     int incl = cj;
 #pragma unroll
                     for (int off = 1; off < 64; off <<= 1) {
                         const int o = __shfl_up(incl, off);
                         if (lane >= off) incl += o;
                     }
-                    if (j < nt) s.boff[s.tch[j]] = base + incl - cj;
+                    if (j < nt) s.boff[tch[j]] = base + incl - cj;
                     base += __shfl(incl, 63);
                 }
             }
@@ -2538,34 +2567,26 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
             lds_barrier();
             OutQueue q;
             for (int j = wave; j < nt; j += kEngWaves) {
-                const int e = s.tch[j];
-                int nb = s.bcnt[e];
+                const int e = tch[j];
+                int nb = bcnt[e];
                 const int off = s.boff[e];
                 if (off + nb > kEngCap) {
                     if (lane == 0) flag_internal(ctrl);
                     nb = kEngCap - off;
                 }
-                eng_update<M>(c, s, e, s.bsort + off, nullptr, nb, nxt, &s_nnext, q);
+                eng_update<M>(c, s, e, s.bsort + off, nullptr, nb, nxt, nnext, q);
             }
-            flush_outs<M>(c, q, nxt, &s_nnext);
+            flush_outs<M>(c, q, nxt, nnext);
         }
         lds_barrier();
-        for (int j = tid; j < nt; j += kEngThreads) {
-            const int e = s.tch[j];
-            s.bcnt[e] = 0;
-            s.bfill[e] = 0;
-        }
-        if (tid == 0) {
-            s_rounds += 1;
-            s_bids += (unsigned long long)n;
-            s_n = s_nnext < kEngCap ? s_nnext : kEngCap;
-            s_nnext = 0;
-            s_ntouched = 0;
-        }
+        rounds += 1;
+        if (tid == 0) s_bids += (unsigned long long)n;
+        n = *nnext < kEngCap ? *nnext : kEngCap;
+        nt_prev = nt;
+        h ^= 1;
         int *tmp = act;
         act = nxt;
         nxt = tmp;
-        lds_barrier();
     }
 
     // Hand the state back.
@@ -2574,20 +2595,20 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
         c.hcount[e] = s.cnt[e];
         c.bcount[e] = 0;
     }
-    for (int i = tid; i < s_n; i += kEngThreads) c.active[(int64_t)s_cur * c.T + i] = act[i];
+    for (int i = tid; i < n; i += kEngThreads) c.active[(int64_t)s_cur * c.T + i] = act[i];
     __threadfence();
     __syncthreads();
     if (tid == 0) {
-        ctrl->rounds += s_rounds;
+        ctrl->rounds += rounds;
         ctrl->bids += s_bids;
         ctrl->engine_bids += s_bids;
-        ctrl->active_count[s_cur] = s_n;
+        ctrl->active_count[s_cur] = n;
         ctrl->active_count[s_cur ^ 1] = 0;
         ctrl->pad0 = 0;
         if (s_stop) {
             ctrl->not_converged = 1;
             ctrl->done = 1;
-        } else if (s_n == 0 && ctrl->last_phase) {
+        } else if (n == 0 && ctrl->last_phase) {
             ctrl->done = 1;
         }
     }
