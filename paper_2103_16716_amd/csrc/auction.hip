@@ -301,14 +301,14 @@ __device__ inline void top2_step(typename M::value_t &v1, int &e1, typename M::v
     const int oe1 = grp_partner<OFF>(e1);
     const value_t ov2 = grp_partner<OFF>(v2);
     const value_t os1 = grp_partner<OFF>(s1);
-    if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
-        v2 = v1 > ov2 ? v1 : ov2;
-        v1 = ov1;
-        e1 = oe1;
-        s1 = os1;
-    } else {
-        v2 = v2 > ov1 ? v2 : ov1;
-    }
+    // Selects only (no branches: every lane takes the same instructions).
+    const bool take = (ov1 > v1) | ((ov1 == v1) & (oe1 < e1));
+    const value_t keep2 = v2 > ov1 ? v2 : ov1;
+    const value_t take2 = v1 > ov2 ? v1 : ov2;
+    v2 = take ? take2 : keep2;
+    v1 = take ? ov1 : v1;
+    e1 = take ? oe1 : e1;
+    s1 = take ? os1 : s1;
 }
 
 // Top-2 over a group of G lanes; every lane of the group ends with the result.
@@ -321,6 +321,21 @@ __device__ inline void top2_reduce(typename M::value_t &v1, int &e1, typename M:
     if constexpr (G > 8) top2_step<8, M>(v1, e1, v2, s1);
     if constexpr (G > 16) top2_step<16, M>(v1, e1, v2, s1);
     if constexpr (G > 32) top2_step<32, M>(v1, e1, v2, s1);
+}
+
+// Adds value v (expert e, score sc) to a lane's running top-2, with selects
+// only. The first of equal values keeps the best place (experts arrive in
+// ascending order).
+template <class M>
+__device__ __attribute__((always_inline)) inline void top2_push(
+    typename M::value_t v, int e, typename M::value_t sc, typename M::value_t &v1, int &e1,
+    typename M::value_t &v2, typename M::value_t &s1) {
+    const bool gt1 = v > v1;
+    const bool gt2 = v > v2;
+    v2 = gt1 ? v1 : (gt2 ? v : v2);
+    v1 = gt1 ? v : v1;
+    e1 = gt1 ? e : e1;
+    s1 = gt1 ? sc : s1;
 }
 
 // Top-2 of one token whose lane-local scores sv (experts e0 .. e0 + 7) are
@@ -338,16 +353,9 @@ __device__ inline void top2_row(const typename M::value_t (&sv)[8], int e0, int 
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int e = e0 + j;
-            if (e >= E) break;
-            const value_t v = sv[j] - pr[e];
-            if (v > v1) {
-                v2 = v1;
-                v1 = v;
-                e1 = e;
-                s1 = sv[j];
-            } else if (v > v2) {
-                v2 = v;
-            }
+            const bool in = e < E;
+            const value_t v = in ? sv[j] - pr[in ? e : 0] : M::lowest();
+            top2_push<M>(v, e, sv[j], v1, e1, v2, s1);
         }
     }
     top2_reduce<M, G>(v1, e1, v2, s1);
@@ -373,16 +381,9 @@ __device__ inline void top2_token(const Ctx<M> &c, int t, bool valid, const type
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const int e = e0 + j;
-                if (e >= c.E) break;
-                const value_t v = sv[j] - pr[e];
-                if (v > v1) {
-                    v2 = v1;
-                    v1 = v;
-                    e1 = e;
-                    s1 = sv[j];
-                } else if (v > v2) {
-                    v2 = v;
-                }
+                const bool in = e < c.E;
+                const value_t v = in ? sv[j] - pr[in ? e : 0] : M::lowest();
+                top2_push<M>(v, e, sv[j], v1, e1, v2, s1);
             }
         }
     }
