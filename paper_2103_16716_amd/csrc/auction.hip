@@ -2958,10 +2958,15 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
     // engine leaves unfinished goes on in the next slot), and the check.
     const bool checks = !(p.flags & BASE_ASSIGN_FULL_SCHEDULE);
     const int check_parts = phase_check_blocks(c.T, G);
+    // From the third slot on, the round loop takes the phase's first rounds
+    // as well: those slots often come after the solve has stopped (then
+    // every launch returns at once, and fewer launches cost less), and when
+    // one runs, its first rounds cost little more in the loop.
     for (int slot = 0; slot < slots; ++slot) {
         hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1, B), dim3(1024), 0, s, c, p,
                            checks && slot > 0 ? check_parts : 0);
-        for (int r = 0; r < wide_rounds; ++r) {
+        const int wr = (slot >= 2 && coop_blocks > 0) ? 0 : wide_rounds;
+        for (int r = 0; r < wr; ++r) {
             hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks, B), dim3(kThreads),
                                bid_bytes, s, c);
             hipLaunchKernelGGL(update_wide_kernel<M>, dim3(upd_blocks, B), dim3(kThreads), 0, s, c);
