@@ -2375,7 +2375,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
     s.scr_slot = reinterpret_cast<int *>(smem_raw + L.sslot);
     int *act = reinterpret_cast<int *>(smem_raw + L.actA);
     int *nxt = reinterpret_cast<int *>(smem_raw + L.actB);
-    __shared__ int s_go, s_cur, s_n, s_nnext[2], s_ntouched[2], s_rounds, s_stop;
+    __shared__ int s_go, s_cur, s_n, s_nnext[2], s_ntouched[2], s_grab[2], s_rounds, s_stop;
     __shared__ unsigned long long s_bids;
 
     SolveCtrl *ctrl = c.ctrl;
@@ -2394,6 +2394,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
         }
         s_nnext[0] = s_nnext[1] = 0;
         s_ntouched[0] = s_ntouched[1] = 0;
+        s_grab[0] = s_grab[1] = 0;
         s_rounds = 0;
         s_stop = 0;
         s_bids = 0;
@@ -2485,7 +2486,10 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
                 bcnt_prev[e] = 0;
                 s.bfill[e] = 0;
             }
-            if (tid == 0) s_ntouched[h ^ 1] = 0;
+            if (tid == 0) {
+                s_ntouched[h ^ 1] = 0;
+                s_grab[h ^ 1] = 0;
+            }
         }
         // Bids against the prices at the start of the round.
         // Each group keeps kEngRows score rows in flight: all loads first,
@@ -2566,8 +2570,14 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
                 else flag_internal(ctrl);
             }
             lds_barrier();
+            // Waves take the touched experts one at a time from a shared
+            // counter (their bid counts differ widely).
             OutQueue q;
-            for (int j = wave; j < nt; j += kEngWaves) {
+            for (;;) {
+                int j = 0;
+                if (lane == 0) j = atomicAdd(&s_grab[h], 1);
+                j = __builtin_amdgcn_readfirstlane(j);
+                if (j >= nt) break;
                 const int e = tch[j];
                 int nb = bcnt[e];
                 const int off = s.boff[e];
