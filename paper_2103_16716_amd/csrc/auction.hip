@@ -654,7 +654,7 @@ __device__ void bid_range(const Ctx<M> &c, int n, bool all_active, const int *li
 // experts that most tokens prefer.)
 //   lcnt  LDS [E], zero on entry and on return
 //   lkey, lexp, lrank  LDS [kBidTile]
-constexpr int kBidTile = 128;
+constexpr int kBidTile = 64;
 constexpr int kBidRows = 4;
 
 template <class M, int G>
