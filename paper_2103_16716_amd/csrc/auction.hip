@@ -415,6 +415,26 @@ __device__ inline typename M::value_t bits_score(uint32_t w, int64_t scale) {
     else return __uint_as_float(w);
 }
 
+// Group maximum of (value, expert), ties to the lower expert, with selects
+// only; every lane of the group ends with the result.
+template <int OFF, class M>
+__device__ __attribute__((always_inline)) inline void max_step(typename M::value_t &bv, int &be) {
+    const typename M::value_t ov = grp_partner<OFF>(bv);
+    const int oe = grp_partner<OFF>(be);
+    const bool take = (ov > bv) | ((ov == bv) & (oe < be));
+    bv = take ? ov : bv;
+    be = take ? oe : be;
+}
+template <class M, int G>
+__device__ __attribute__((always_inline)) inline void group_max(typename M::value_t &bv, int &be) {
+    if constexpr (G > 1) max_step<1, M>(bv, be);
+    if constexpr (G > 2) max_step<2, M>(bv, be);
+    if constexpr (G > 4) max_step<4, M>(bv, be);
+    if constexpr (G > 8) max_step<8, M>(bv, be);
+    if constexpr (G > 16) max_step<16, M>(bv, be);
+    if constexpr (G > 32) max_step<32, M>(bv, be);
+}
+
 // One group of G lanes per token: 9 rounds of a group maximum (ties to the
 // lowest expert) over the lanes' 8 scores each.
 template <class M, int G>
@@ -450,30 +470,25 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
             value_t bv = M::lowest();
             int be = 0x7fffffff;
 #pragma unroll
-            for (int ch = 0; ch < kSumChunks; ++ch)
+            for (int ch = 0; ch < kSumChunks; ++ch) {
+                if (ch * 8 * G >= c.E) break;   // (uniform: chunks past the row)
 #pragma unroll
                 for (int q = 0; q < 8; ++q) {
                     const int e = ch * 8 * G + 8 * gl + q;
-                    if (e < c.E && sv[ch][q] > bv) {
-                        bv = sv[ch][q];
-                        be = e;
-                    }
-                }
-#pragma unroll
-            for (int off = G / 2; off > 0; off >>= 1) {
-                const value_t ov = __shfl_xor(bv, off);
-                const int oe = __shfl_xor(be, off);
-                if (ov > bv || (ov == bv && oe < be)) {
-                    bv = ov;
-                    be = oe;
+                    const bool better = (e < c.E) & (sv[ch][q] > bv);
+                    bv = better ? sv[ch][q] : bv;
+                    be = better ? e : be;
                 }
             }
+            group_max<M, G>(bv, be);
             if (r < take) {
 #pragma unroll
-                for (int ch = 0; ch < kSumChunks; ++ch)
+                for (int ch = 0; ch < kSumChunks; ++ch) {
+                    if (ch * 8 * G >= c.E) break;
 #pragma unroll
                     for (int q = 0; q < 8; ++q)
-                        if (ch * 8 * G + 8 * gl + q == be) sv[ch][q] = M::lowest();
+                        sv[ch][q] = ch * 8 * G + 8 * gl + q == be ? M::lowest() : sv[ch][q];
+                }
                 if (valid && gl == 0) out[r] = score_bits<M>(bv, c.scale);
                 pairs[r >> 1] |= (uint32_t)(be & 0xffff) << (16 * (r & 1));
             } else if (valid && gl == 0) {

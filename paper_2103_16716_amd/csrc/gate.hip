@@ -77,21 +77,21 @@ __global__ __launch_bounds__(256) void greedy_count_kernel(const float *S, int T
                     for (int q = 0; q < 8; ++q) v[q] = e0 + q < E ? row[e0 + q] : -INFINITY;
                 }
 #pragma unroll
-                for (int q = 0; q < 8; ++q)
-                    if (e0 + q < E && v[q] > best) {   // ascending scan: ties keep the lower expert
-                        best = v[q];
-                        be = e0 + q;
-                    }
+                for (int q = 0; q < 8; ++q) {   // ascending scan: ties keep the lower expert
+                    const bool better = (e0 + q < E) & (v[q] > best);
+                    best = better ? v[q] : best;
+                    be = better ? e0 + q : be;
+                }
             }
         }
 #pragma unroll
         for (int off = kGroup / 2; off > 0; off >>= 1) {
+            // (selects, not branches: the lanes of a wave disagree here)
             const float ob = __shfl_xor(best, off);
             const int oe = __shfl_xor(be, off);
-            if (ob > best || (ob == best && oe < be)) {
-                best = ob;
-                be = oe;
-            }
+            const bool take = (ob > best) | ((ob == best) & (oe < be));
+            best = take ? ob : best;
+            be = take ? oe : be;
         }
         if (valid && gl == 0) {
             const int a = (be >= 0 && be < E) ? be : 0;   // a row of NaN/-inf goes to expert 0
