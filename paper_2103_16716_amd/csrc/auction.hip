@@ -2935,8 +2935,8 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
     // Phase slots enqueued up front; the last one continues on its own (in
     // one workgroup, slowly) if the epsilon schedule needs more phases than
-    // were enqueued. A slot the solve no longer needs still costs about
-    // 45 us of empty launches. With the default schedule (first epsilon =
+    // were enqueued. A slot the solve no longer needs still costs its empty
+    // launches (a few microseconds each). With the default schedule (first epsilon =
     // range / 8, divisor 32) five slots cover score ranges up to 8 * 32^4
     // (about 8 * 10^6) times eps_final even without a certified early stop,
     // which typically comes one or two phases sooner; the full schedule
