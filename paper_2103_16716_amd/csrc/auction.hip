@@ -2465,10 +2465,11 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
     const int gl = lane & (G - 1);
     // Round bookkeeping: every thread keeps the active count and the round
     // number in registers. The per-expert bid counts, the touched-expert
-    // list and the two LDS counters alternate halves between consecutive
-    // rounds (parity h): a round clears what the round before used while it
-    // bids, so a round needs two workgroup barriers (three with grouping)
-    // and no separate clearing step.
+    // list and the LDS counters (next list length, touched experts, experts
+    // taken) alternate halves between consecutive rounds (parity h): a round
+    // clears what the round before used while it bids, so a round needs two
+    // workgroup barriers (four when it groups its bids) and no separate
+    // clearing step.
     int n = s_n;
     int rounds = 0;
     int h = 0;
