@@ -6,7 +6,7 @@ H into expert-contiguous rows (plus the inverse permute on the workload that
 includes it). Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                    [--no-cpu-baseline] [--batch B] [--no-shuffle]
+                    [--no-cpu-baseline] [--batch B] [--no-shuffle] [--layer]
 
 With --batch B > 1 it measures B independent problems of the paper's
 per-worker shape (Sec. 3.2.1 Sharding; T=2048, E=128, d=2048) with the
@@ -15,6 +15,12 @@ permutation of the B * T tokens, an input): one affinity GEMM over the
 shuffled rows against the shared expert embeddings (base_affinity_gather),
 one base_assign_batched call, and one permute of all problems' rows
 (base_permute_batched), both reading H through the shuffle index.
+
+With --layer it measures the layer's calls around the experts instead
+(Sec. 3.1 Eq. 1, Sec. 3.2.2): test-time routing (base_greedy_assign), the
+gated residual returned to token order (base_gate_combine) and its
+backward (base_gate_backward), on the workload's scores with seeded random
+expert outputs and upstream gradients.
 """
 from __future__ import annotations
 
@@ -74,7 +80,97 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--no-shuffle", action="store_true")
+    ap.add_argument("--layer", action="store_true")
     return ap.parse_args()
+
+
+def bench_layer(args) -> None:
+    """Routing and gate calls of one layer step (see the module note)."""
+    import torch
+
+    import paper_2103_16716_amd as pb
+
+    torch.cuda.set_device(0)
+    inp = wl.make_inputs(args.workload)
+    w = inp.wl
+    T, E, d = w.T, w.E, w.d
+    if w.dtype != "bf16":
+        print("--layer measures bf16 workloads", file=sys.stderr)
+        sys.exit(2)
+    H = torch.from_numpy(inp.H_store.view(np.int16)).cuda().view(torch.bfloat16)
+    W = torch.from_numpy(inp.W_store.view(np.int16)).cuda().view(torch.bfloat16)
+    S = pb.affinity(H, W)
+    r = pb.assign(S)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(20210331)
+    F = torch.randn((T, d), generator=gen, device="cuda").to(torch.bfloat16)
+    dY = torch.randn((T, d), generator=gen, device="cuda").to(torch.bfloat16)
+    Y = torch.empty_like(H)
+    offsets = pb.balanced_offsets(T, E, H.device)
+    gws = torch.empty(max(int(pb.lib().base_greedy_workspace_size(T, E)), 256),
+                      dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    names = ("greedy", "combine", "backward")
+
+    def step(evs=None):
+        if evs is not None:
+            evs[0].record(stream)
+        pb.greedy_assign(S, workspace=gws, stream=stream)
+        if evs is not None:
+            evs[1].record(stream)
+        pb.gate_combine(F, H, S, r.assign, r.perm, out=Y, stream=stream)
+        if evs is not None:
+            evs[2].record(stream)
+        pb.gate_backward(dY, F, H, W, S, r.assign, r.perm, offsets=offsets, stream=stream)
+        if evs is not None:
+            evs[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    per = {n: sum(ev[i].elapsed_time(ev[i + 1]) for ev in events) / args.steps
+           for i, n in enumerate(names)}
+    # Algorithmic HBM bytes per call: the greedy route reads the scores and
+    # writes the routing; the combine reads F and H rows and writes y rows
+    # (plus index and score); the backward reads dY and F rows, writes dH and
+    # dF rows, and reads each H row once more for dW.
+    row = 2 * d
+    nbytes = {
+        "greedy": T * 4 * E + 3 * T * 4 + 4 * (E + 1),
+        "combine": 3 * T * row + 12 * T,
+        "backward": 5 * T * row + 12 * T + 4 * E * d + 4 * T,
+    }
+    roof = {n: {"bound": "hbm", "achieved": round(nbytes[n] / (per[n] * 1e-3) / 1e9, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(nbytes[n] / (per[n] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            for n in names}
+    total_ms = sum(per.values())
+    out = {
+        "metric": f"tokens/sec through test-time routing + gate + gate backward at "
+                  f"T={T},E={E},d={d}",
+        "value": T / (total_ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms,
+        "wall_ms_per_step": wall_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded scores, expert outputs and upstream gradients)",
+        "config": {"workload": w.name, "T": T, "E": E, "d": d, "calls": list(names)},
+        "per_call_ms": {n: round(per[n], 4) for n in names},
+        "per_call_roofline": roof,
+    }
+    print(json.dumps(out), flush=True)
 
 
 def bench_batched(args) -> None:
@@ -198,6 +294,9 @@ def main():
 
     if args.batch > 1:
         bench_batched(args)
+        return
+    if args.layer:
+        bench_layer(args)
         return
 
     import torch
