@@ -1682,7 +1682,7 @@ __device__ inline void lds_barrier() {
 
 constexpr int kEngThreads = 1024;
 constexpr int kEngWaves = kEngThreads / 64;
-constexpr int kEngCap = 1024;
+constexpr int kEngCap = 256;
 constexpr int kEngDirect = 64;   // rounds with at most this many bids skip the grouping
 constexpr int kEngMaxE = 512;
 constexpr int kEngMaxC = 512;    // holder tables a wave holds in registers (8 keys per lane)
