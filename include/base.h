@@ -185,6 +185,10 @@ typedef struct {
 } base_assign_opts;
 
 typedef struct {
+    /* The first six fields are the statistics of the problem statement's
+     * boundary, in its order: a caller built against that layout reads them
+     * at the same offsets (dual_gap at byte 32). The fields after them are
+     * additions. */
     int32_t phases;      /* epsilon phases run */
     int32_t rounds;      /* bidding rounds over all phases */
     int64_t bids;        /* bids placed over all phases */
@@ -192,18 +196,20 @@ typedef struct {
                             T * eps_final of the optimum (eps_final as raised for fp32
                             resolution) */
     int32_t fell_back;   /* 1 if the greedy completion was used */
-    int32_t converged;   /* 1 if every expert holds exactly T/E tokens */
-    int64_t engine_bids; /* the part of `bids` placed inside the single-workgroup
-                            engine (the rounds with few active tokens) */
     double dual_gap;     /* D(p) - sum_t S[t, a_t] for the returned prices, in score
                             units: an upper bound of optimum - objective for a balanced
                             result (the certificate of the bound above; after the greedy
-                            fallback it measures what the fallback gave up) */
+                            fallback it measures what the fallback gave up). Measured
+                            only with BASE_ASSIGN_SYNC_STATS; NaN from base_assign_status */
+    int32_t converged;   /* 1 if every expert holds exactly T/E tokens */
+    int64_t engine_bids; /* the part of `bids` placed inside the single-workgroup
+                            engine (the rounds with few active tokens) */
     double eps_last;     /* epsilon of the last phase run, in score units (above eps_final
                             when the solve stopped on the duality check) */
     int32_t certified;   /* problems whose solve stopped after an earlier phase because
                             the measured duality gap met T * eps_final */
-    int32_t reserved;
+    int32_t augmentations; /* shortest augmenting paths that finished phases (the
+                            last few tokens of a phase), over all phases */
 } base_assign_stats;
 
 /* Bytes of device workspace base_assign needs for T tokens and E experts
@@ -250,6 +256,37 @@ int base_assign_batched(const void *S, int s_dtype, int64_t B, int64_t T, int64_
                         const base_assign_opts *opts, int32_t *assign, int32_t *perm,
                         void *prices, void *workspace, size_t workspace_bytes,
                         base_assign_stats *stats, void *stream);
+
+/*
+ * base_assign_status - how the last solve enqueued on `workspace` ended,
+ * read after the fact. base_assign and base_assign_batched return before
+ * the solve has run (unless BASE_ASSIGN_SYNC_STATS asks them to wait), so
+ * a device-side outcome -- the round limit reached without the greedy
+ * completion, a price beyond the representable range, a failed internal
+ * consistency check -- cannot be their return value. Each problem's control
+ * block stays in its workspace until the workspace is used again; this call
+ * waits for `stream` (the stream the solve was enqueued on), reads the B
+ * control blocks and reports that outcome without re-running anything
+ * (Sec. 3.2.1: the assignment must be balanced; the appendix figure's
+ * caption: a solve may stop at its iteration bound).
+ *
+ *   workspace  [device] the workspace of the solve (B problems of T x E)
+ *   B, T, E    as passed to that solve (B = 1 for base_assign)
+ *   stats      [host] out, may be NULL: the statistics of base_assign_stats,
+ *              aggregated over the problems as for SYNC_STATS, except
+ *              dual_gap, which is NaN (it needs the scores and assignment)
+ *   stream     the solve's stream (the call synchronises it)
+ *
+ * Returns BASE_OK when every problem ended balanced; otherwise the first
+ * kind of failure found, in this order: BASE_ERR_INTERNAL (a device-side
+ * check failed: the solve stopped there and its outputs are unspecified,
+ * though every access stayed in bounds), BASE_ERR_RANGE (a price left the
+ * representable range), BASE_ERR_NOT_CONVERGED (max_rounds reached without
+ * BASE_ASSIGN_GREEDY_FALLBACK). BASE_ERR_INVALID_ARG for bad sizes or a
+ * null or misaligned workspace; BASE_ERR_HIP if the read fails.
+ */
+int base_assign_status(const void *workspace, int64_t B, int64_t T, int64_t E,
+                       base_assign_stats *stats, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* base_permute: route rows into expert-contiguous order, or back            */

@@ -45,7 +45,7 @@ BASE_ASSIGN_FULL_SCHEDULE = 16
 # Every symbol include/base.h declares.
 EXPORTED = ("base_status_string", "base_affinity", "base_affinity_gather",
             "base_assign_workspace_size", "base_assign", "base_assign_batched_workspace_size",
-            "base_assign_batched", "base_permute", "base_permute_batched",
+            "base_assign_batched", "base_assign_status", "base_permute", "base_permute_batched",
             "base_greedy_workspace_size", "base_greedy_assign", "base_gate_combine",
             "base_gate_combine_batched", "base_gate_backward", "base_timing_enable",
             "base_timing_read")
@@ -60,9 +60,9 @@ class AssignOpts(ctypes.Structure):
 class AssignStats(ctypes.Structure):
     _fields_ = [("phases", ctypes.c_int32), ("rounds", ctypes.c_int32), ("bids", ctypes.c_int64),
                 ("eps_final", ctypes.c_double), ("fell_back", ctypes.c_int32),
-                ("converged", ctypes.c_int32), ("engine_bids", ctypes.c_int64),
-                ("dual_gap", ctypes.c_double), ("eps_last", ctypes.c_double),
-                ("certified", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("dual_gap", ctypes.c_double), ("converged", ctypes.c_int32),
+                ("engine_bids", ctypes.c_int64), ("eps_last", ctypes.c_double),
+                ("certified", ctypes.c_int32), ("augmentations", ctypes.c_int32)]
 
 
 class BaseError(RuntimeError):
@@ -101,6 +101,8 @@ def lib() -> ctypes.CDLL:
                                           vp, vp, vp, ctypes.c_size_t,
                                           ctypes.POINTER(AssignStats), vp]
         L.base_assign_batched.restype = i32
+        L.base_assign_status.argtypes = [vp, i64, i64, i64, ctypes.POINTER(AssignStats), vp]
+        L.base_assign_status.restype = i32
         L.base_permute.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
         L.base_permute.restype = i32
         L.base_permute_batched.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, i32, vp]
@@ -278,6 +280,17 @@ def assign_batched(S, *, eps_final: float = 0.0, eps_initial: float = 0.0,
     return AssignResult(out_assign, out_perm, out_prices, stats if sync_stats else None)
 
 
+def assign_status(workspace, T: int, E: int, B: int = 1, stream=None):
+    """How the last solve on `workspace` ended (base_assign_status): waits
+    for the stream and returns (status code, AssignStats) without raising.
+    dual_gap is NaN (not measured by this read)."""
+    _need_device(workspace)
+    stats = AssignStats()
+    st = lib().base_assign_status(workspace.data_ptr(), B, T, E, ctypes.byref(stats),
+                                  _stream_ptr(stream))
+    return int(st), stats
+
+
 def permute(x, perm, inverse: bool = False, out=None, stream=None):
     """Gather rows into expert order (out[k] = x[perm[k]]) or, with inverse,
     scatter them back (out[perm[k]] = x[k]) (base_permute)."""
@@ -425,4 +438,5 @@ __all__ = ["affinity", "assign", "assign_batched", "permute", "permute_batched",
            "gate_backward", "balanced_offsets", "assign_workspace_size",
            "assign_batched_workspace_size", "timing_enable",
            "timing_read", "AssignResult", "AssignOpts", "AssignStats", "BaseError", "lib",
+           "assign_status",
            "status_string", "EXPORTED"]

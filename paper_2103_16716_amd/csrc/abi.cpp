@@ -127,14 +127,60 @@ size_t base_assign_workspace_size(int64_t T, int64_t E) {
 
 }  // extern "C"
 
-namespace {
 
-// base_assign and base_assign_batched: B independent problems, each a T x E
-// score matrix, solved by one sequence of launches (problem b in
-// blockIdx.y of every solver kernel).
-int assign_impl(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
-                const base_assign_opts *opts, int32_t *assign, int32_t *perm, void *prices,
-                void *workspace, size_t workspace_bytes, base_assign_stats *stats, void *stream) {
+namespace base {
+
+int aggregate_stats(const SolveCtrl *cs, int64_t B, int64_t E, bool with_gap, void *stats_out) {
+    base_assign_stats agg{};
+    agg.converged = 1;
+    bool internal = false, overflow = false, not_converged = false;
+    for (int64_t b = 0; b < B; ++b) {
+        const SolveCtrl &c = cs[b];
+        const double scale = c.integer ? (double)c.scale : 1.0;
+        const int unconverged = c.unconverged_experts & ~(1 << 30);
+        agg.phases = c.phase > agg.phases ? c.phase : agg.phases;
+        agg.rounds = c.rounds > agg.rounds ? c.rounds : agg.rounds;
+        agg.bids += (int64_t)c.bids;
+        agg.engine_bids += (int64_t)c.engine_bids;
+        agg.augmentations += c.augmentations;
+        agg.dual_gap += c.dual_gap / scale;
+        const double eps = c.eps / scale;
+        agg.eps_last = eps > agg.eps_last ? eps : agg.eps_last;
+        const double bound = c.eps_final_eff / scale;
+        agg.eps_final = bound > agg.eps_final ? bound : agg.eps_final;
+        agg.certified += c.certified != 0 ? 1 : 0;
+        agg.fell_back |= c.fell_back;
+        const bool conv = unconverged == 0 && (!c.not_converged || c.fell_back) &&
+                          c.internal_error == 0;
+        if (!conv) agg.converged = 0;
+        internal |= c.internal_error != 0;
+        overflow |= c.overflow != 0;
+        not_converged |= unconverged != 0 || (c.not_converged && !c.fell_back);
+    }
+    if (!with_gap) agg.dual_gap = NAN;
+    if (E == 1) {
+        agg = base_assign_stats{};
+        agg.converged = 1;
+    }
+    *static_cast<base_assign_stats *>(stats_out) = agg;
+    if (E > 1) {
+        if (internal) return BASE_ERR_INTERNAL;
+        if (overflow) return BASE_ERR_RANGE;
+        if (not_converged) return BASE_ERR_NOT_CONVERGED;
+    }
+    return BASE_OK;
+}
+
+}  // namespace base
+
+namespace base {
+
+// base_assign and base_assign_batched (and the allocation-free variant): B
+// independent problems, each a T x E score matrix, solved by one sequence of
+// launches (problem b in blockIdx.y of every solver kernel).
+int assign_entry(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
+                 const base_assign_opts *opts, int32_t *assign, int32_t *perm, void *prices,
+                 void *workspace, size_t workspace_bytes, base_assign_stats *stats, void *stream) {
     if (S == nullptr || assign == nullptr || perm == nullptr) return BASE_ERR_INVALID_ARG;
     if (T <= 0 || E <= 0 || B <= 0) return BASE_ERR_INVALID_ARG;
     if (s_dtype != BASE_F32 && s_dtype != BASE_I16) return BASE_ERR_UNSUPPORTED_DTYPE;
@@ -201,61 +247,35 @@ int assign_impl(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
     if (e != hipSuccess) return BASE_ERR_HIP;
 
     if (o.flags & BASE_ASSIGN_SYNC_STATS) {
-        base::SolveCtrl *cs = static_cast<base::SolveCtrl *>(calloc((size_t)B, sizeof(base::SolveCtrl)));
+        // One problem reads into a local control block (no host allocation).
+        base::SolveCtrl one{};
+        base::SolveCtrl *cs =
+            B == 1 ? &one
+                   : static_cast<base::SolveCtrl *>(calloc((size_t)B, sizeof(base::SolveCtrl)));
         if (cs == nullptr) return BASE_ERR_HIP;
         e = base::read_assign_stats(workspace, T, E, B, cs, s);
         if (e != hipSuccess) {
-            free(cs);
+            if (cs != &one) free(cs);
             return BASE_ERR_HIP;
         }
         base_assign_stats agg{};
-        agg.converged = 1;
-        bool internal = false, overflow = false, not_converged = false;
-        for (int64_t b = 0; b < B; ++b) {
-            const base::SolveCtrl &c = cs[b];
-            const int unconverged = c.unconverged_experts & ~(1 << 30);
-            agg.phases = c.phase > agg.phases ? c.phase : agg.phases;
-            agg.rounds = c.rounds > agg.rounds ? c.rounds : agg.rounds;
-            agg.bids += (int64_t)c.bids;
-            agg.engine_bids += (int64_t)c.engine_bids;
-            agg.dual_gap += integer ? c.dual_gap / (double)p.scale : c.dual_gap;
-            const double eps = integer ? c.eps / (double)p.scale : c.eps;
-            agg.eps_last = eps > agg.eps_last ? eps : agg.eps_last;
-            const double bound =
-                integer ? c.eps_final_eff / (double)p.scale : c.eps_final_eff;
-            agg.eps_final = bound > agg.eps_final ? bound : agg.eps_final;
-            agg.certified += c.certified != 0 ? 1 : 0;
-            agg.fell_back |= c.fell_back;
-            const bool conv = unconverged == 0 && (!c.not_converged || c.fell_back);
-            if (!conv) agg.converged = 0;
-            internal |= c.internal_error != 0;
-            overflow |= c.overflow != 0;
-            not_converged |= unconverged != 0 || (c.not_converged && !c.fell_back);
-        }
-        free(cs);
-        if (E == 1) {
-            agg = base_assign_stats{};
-            agg.converged = 1;
-        }
+        const int st = base::aggregate_stats(cs, B, E, true, &agg);
+        if (cs != &one) free(cs);
         if (stats != nullptr) *stats = agg;
-        if (E > 1) {
-            if (internal) return BASE_ERR_INTERNAL;
-            if (overflow) return BASE_ERR_RANGE;
-            if (not_converged) return BASE_ERR_NOT_CONVERGED;
-        }
+        return st;
     }
     return BASE_OK;
 }
 
-}  // namespace
+}  // namespace base
 
 extern "C" {
 
 int base_assign(const void *S, int s_dtype, int64_t T, int64_t E, const base_assign_opts *opts,
                 int32_t *assign, int32_t *perm, void *prices, void *workspace,
                 size_t workspace_bytes, base_assign_stats *stats, void *stream) {
-    return assign_impl(S, s_dtype, 1, T, E, opts, assign, perm, prices, workspace,
-                       workspace_bytes, stats, stream);
+    return base::assign_entry(S, s_dtype, 1, T, E, opts, assign, perm, prices, workspace,
+                              workspace_bytes, stats, stream);
 }
 
 size_t base_assign_batched_workspace_size(int64_t B, int64_t T, int64_t E) {
@@ -267,8 +287,29 @@ int base_assign_batched(const void *S, int s_dtype, int64_t B, int64_t T, int64_
                         const base_assign_opts *opts, int32_t *assign, int32_t *perm,
                         void *prices, void *workspace, size_t workspace_bytes,
                         base_assign_stats *stats, void *stream) {
-    return assign_impl(S, s_dtype, B, T, E, opts, assign, perm, prices, workspace,
-                       workspace_bytes, stats, stream);
+    return base::assign_entry(S, s_dtype, B, T, E, opts, assign, perm, prices, workspace,
+                              workspace_bytes, stats, stream);
+}
+
+int base_assign_status(const void *workspace, int64_t B, int64_t T, int64_t E,
+                       base_assign_stats *stats, void *stream) {
+    if (workspace == nullptr || !aligned(workspace, 256)) return BASE_ERR_INVALID_ARG;
+    if (B <= 0 || T <= 0 || E <= 0 || T % E != 0 || B > kMaxBatch || T >= kMaxTokens ||
+        E > kMaxExperts || B * T > INT32_MAX)
+        return BASE_ERR_INVALID_ARG;
+    base::SolveCtrl *cs = static_cast<base::SolveCtrl *>(calloc((size_t)B, sizeof(base::SolveCtrl)));
+    if (cs == nullptr) return BASE_ERR_HIP;
+    const hipError_t e =
+        base::read_assign_stats(workspace, T, E, B, cs, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        free(cs);
+        return BASE_ERR_HIP;
+    }
+    base_assign_stats agg{};
+    const int st = base::aggregate_stats(cs, B, E, false, &agg);
+    free(cs);
+    if (stats != nullptr) *stats = agg;
+    return st;
 }
 
 size_t base_greedy_workspace_size(int64_t T, int64_t E) {

@@ -52,6 +52,15 @@ constexpr int kCheckBlocks = 4096;     // largest grid of the phase check
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Polls a grid barrier's wait makes before it gives up. BASE_TEST_BARRIER_POLLS
+// overrides the default (read at every solve): tests set it to 0 to force
+// the give-up path from the host, so that every block still exits normally.
+inline uint32_t barrier_polls() {
+    const char *v = getenv("BASE_TEST_BARRIER_POLLS");
+    if (v == nullptr || *v == 0) return 1u << 24;
+    return (uint32_t)strtoul(v, nullptr, 10);
+}
+
 // With BASE_DEBUG set in the environment, notes why a launch path was taken
 // or which HIP call failed, on stderr.
 inline void debug_note(const char *what, hipError_t err) {
@@ -193,8 +202,15 @@ __device__ inline int ld_relaxed(const int *p) {
 }
 
 // A consistency check failed: the access is skipped and the call reports
-// BASE_ERR_INTERNAL instead of touching memory outside the workspace.
-__device__ inline void flag_internal(SolveCtrl *ctrl) { ctrl->internal_error = 1; }
+// BASE_ERR_INTERNAL instead of touching memory outside the workspace. The
+// solve also ends there: every later solver kernel sees `done` and returns
+// at once, and the greedy completion does not run, so no kernel goes on
+// from a half-finished round. The finalising kernels still run (every
+// access in bounds); their outputs are unspecified.
+__device__ inline void flag_internal(SolveCtrl *ctrl) {
+    ctrl->internal_error = 1;
+    ctrl->done = 1;
+}
 
 __device__ inline uint64_t lanemask_lt() {
     const int l = lane_id();
@@ -1098,6 +1114,8 @@ __global__ void init_kernel(SolveCtrl *ctrl, void *prices, int E, AssignParams p
         z.smax_ord = 0u;
         z.smin_ord = 0xffffffffu;
         z.eps_final_eff = p.eps_final;
+        z.scale = p.scale;
+        z.integer = p.integer ? 1 : 0;
         *ctrl = z;
     }
     if (prices == nullptr) return;
@@ -1496,9 +1514,10 @@ __global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c0) {
 // thread waits for its own stores first; one thread per block then writes
 // back its L2 (device-scope release), arrives, waits for the release word
 // (on its own line, stored by the last arrival) and invalidates its caches
-// (acquire). The wait gives up after ~2^24 polls: the block flags an
-// internal error and returns false.
-__device__ inline bool grid_barrier(uint64_t *bar, uint64_t target, SolveCtrl *ctrl) {
+// (acquire). The wait gives up after `poll_limit` polls (2^24 by default,
+// about a second): the block flags an internal error and returns false.
+__device__ inline bool grid_barrier(uint64_t *bar, uint64_t target, SolveCtrl *ctrl,
+                                    uint32_t poll_limit) {
     __shared__ int ok;
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this thread's stores are done
     __syncthreads();
@@ -1512,12 +1531,13 @@ __device__ inline bool grid_barrier(uint64_t *bar, uint64_t target, SolveCtrl *c
         } else {
             uint32_t polls = 0;
             while (__hip_atomic_load(bar + 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-                __builtin_amdgcn_s_sleep(2);
-                if (++polls == (1u << 24)) {
+                if (polls >= poll_limit) {
                     flag_internal(ctrl);
                     ok = 0;
                     break;
                 }
+                ++polls;
+                __builtin_amdgcn_s_sleep(2);
             }
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -1528,7 +1548,8 @@ __device__ inline bool grid_barrier(uint64_t *bar, uint64_t target, SolveCtrl *c
 
 template <class M, int G>
 __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c0, int max_wide,
-                                                             int32_t max_rounds) {
+                                                             int32_t max_rounds,
+                                                             uint32_t poll_limit) {
     const Ctx<M> c = c0.at(blockIdx.y);
     using value_t = typename M::value_t;
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -1566,7 +1587,7 @@ __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c0, int max_
                             reinterpret_cast<int *>(smem_raw + B.lexp),
                             reinterpret_cast<int *>(smem_raw + B.lrank));
         target += gridDim.x;
-        if (!grid_barrier(c.bar, target, ctrl)) return;
+        if (!grid_barrier(c.bar, target, ctrl, poll_limit)) return;
         const int novf = min(ld_relaxed(c.ovf_count), c.T);
         for (int e = blockIdx.x; e < c.E; e += gridDim.x) update_expert<M>(c, e, st_cur ^ 1, novf, sm);
         __threadfence();
@@ -1579,7 +1600,7 @@ __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c0, int max_
             end_round(ctrl, c.T);
         }
         target += gridDim.x;
-        if (!grid_barrier(c.bar, target, ctrl)) return;
+        if (!grid_barrier(c.bar, target, ctrl, poll_limit)) return;
     }
 }
 
@@ -2737,7 +2758,8 @@ __global__ void greedy_fill_kernel(Ctx<M> c0, int32_t *assign, uint32_t flags) {
     assign += (int64_t)blockIdx.y * c.T;
     using value_t = typename M::value_t;
     SolveCtrl *ctrl = c.ctrl;
-    if (!ctrl->not_converged || !(flags & BASE_ASSIGN_GREEDY_FALLBACK)) return;
+    if (!ctrl->not_converged || !(flags & BASE_ASSIGN_GREEDY_FALLBACK) || ctrl->internal_error)
+        return;
     __shared__ int room_left;
     if (threadIdx.x == 0) {
         ctrl->fell_back = 1;
@@ -3002,7 +3024,7 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
         }
         if (coop_blocks > 0)
             hipLaunchKernelGGL((wide_loop_kernel<M, G>), dim3(coop_blocks, B), dim3(kThreads),
-                               bid_bytes, s, c, kWideLoopRounds, p.max_rounds);
+                               bid_bytes, s, c, kWideLoopRounds, p.max_rounds, barrier_polls());
         if (engine) {
             // Summary readers: multiples of 8 blocks per problem, 256 in all
             // when one problem.
@@ -3094,19 +3116,22 @@ size_t assign_workspace_size(int64_t T, int64_t E) {
 hipError_t launch_assign(const void *S, const AssignParams &p, int64_t B, int32_t *assign,
                          int32_t *perm, void *prices_out, void *workspace, hipStream_t stream) {
     if (p.E == 1) {
-        const size_t wst = make_layout(p.T, p.E).total;
-        for (int64_t b = 0; b < B; ++b) {
-            hipError_t err = hipMemsetAsync(static_cast<char *>(workspace) + b * wst, 0,
-                                            sizeof(SolveCtrl), stream);
-            if (err != hipSuccess) return err;
-        }
+        // Control blocks and prices are cleared by kernels, not memset nodes,
+        // so that a caller may capture the call in a graph.
+        const int64_t wst = (int64_t)make_layout(p.T, p.E).total;
+        AssignParams q = p;
+        q.warm_prices = nullptr;
+        hipLaunchKernelGGL(init_kernel, dim3(1, (unsigned)B), dim3(256), 0, stream,
+                           static_cast<SolveCtrl *>(workspace), (void *)nullptr, 0, q, wst);
         int blocks = (int)((p.T * B + 255) / 256);
         if (blocks > 2048) blocks = 2048;
         hipLaunchKernelGGL(single_expert_kernel, dim3(blocks), dim3(256), 0, stream, assign, perm,
                            p.T * B, p.T);
         if (prices_out != nullptr) {
-            hipError_t err = hipMemsetAsync(prices_out, 0, (size_t)B * (p.integer ? 8 : 4), stream);
-            if (err != hipSuccess) return err;
+            // one price per problem: 0 (fp32 zero and int64 zero share the bit pattern)
+            const int64_t words = B * (p.integer ? 2 : 1);
+            hipLaunchKernelGGL(fill_kernel, dim3(1), dim3(256), 0, stream,
+                               static_cast<int32_t *>(prices_out), words, 0);
         }
         return hipGetLastError();
     }

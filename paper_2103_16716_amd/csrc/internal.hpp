@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "base.h"
+
 namespace base {
 
 // rows: null, or output row i reads row rows[i] of H (h_rows rows).
@@ -59,7 +61,20 @@ struct SolveCtrl {
     int32_t certified;      // 1: stopped after a phase whose duality gap met T eps_final
     int32_t pad3;
     double check_gap;       // duality gap measured after the last phase (0: not measured)
+    int64_t scale;          // integer mode: K (scores are scaled by it); float mode: 1
+    int32_t integer;        // 1: integer mode
+    int32_t augmentations;  // shortest augmenting paths run over all phases
 };
+
+// The validated assign call shared by base_assign, base_assign_batched and
+// base_assign_noalloc (arguments and result as base_assign_batched).
+int assign_entry(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
+                 const base_assign_opts *opts, int32_t *assign, int32_t *perm, void *prices,
+                 void *workspace, size_t workspace_bytes, base_assign_stats *stats, void *stream);
+
+// Status and statistics of B problems from their control blocks (aggregated
+// as documented for base_assign_stats). Returns a base_status code.
+int aggregate_stats(const SolveCtrl *cs, int64_t B, int64_t E, bool with_gap, void *stats_out);
 
 size_t assign_workspace_size(int64_t T, int64_t E);
 

@@ -3,6 +3,8 @@ and the tolerances the comparisons use. Nothing here computes any step of
 the method."""
 from __future__ import annotations
 
+import math
+
 import numpy as np
 import torch
 
@@ -40,3 +42,23 @@ def rounding_slack(T: int, S: np.ndarray, p: np.ndarray) -> float:
     ulps per token at the magnitude scores and prices reach."""
     mag = float(np.abs(S).max()) + float(np.abs(p).max())
     return T * 16.0 * float(np.finfo(np.float32).eps) * mag
+
+
+def eps_expected(S: np.ndarray, eps: float) -> float:
+    """The epsilon bound a float-mode solve must report for scores S and a
+    requested eps_final: eps itself, raised to the fp32 resolution floor
+    2^-20 * (max|S| + 3 * (max S - min S)) when that is larger (about eight
+    ulps of the largest price a solve can reach). Computed here from S in
+    double, independently of the device."""
+    S32 = np.asarray(S, dtype=np.float32)
+    smax, smin = float(S32.max()), float(S32.min())
+    mag = max(abs(smax), abs(smin)) + 3.0 * (smax - smin) + 1e-30
+    return max(float(eps), math.ldexp(mag, -20))
+
+
+def fp32_accumulation_bound(H: np.ndarray, W: np.ndarray) -> np.ndarray:
+    """(d + 1) * 2^-24 * sum_k |H[t,k] W[e,k]|: the worst-case error of a dot
+    product of length d accumulated in fp32 in any order (gamma_d), with one
+    more rounding for fp32 products (bf16 products are exact in fp32)."""
+    d = H.shape[1]
+    return (d + 1) * 2.0 ** -24 * (np.abs(H.astype(np.float64)) @ np.abs(W.astype(np.float64)).T) + 1e-30

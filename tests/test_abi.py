@@ -62,6 +62,42 @@ def test_batched_arguments_checked_before_launch(L):
                                  ctypes.byref(st), None) == pb.BASE_ERR_WORKSPACE
 
 
+def test_stats_layout_matches_the_header(tmp_path):
+    """The ctypes mirror of base_assign_stats has the C layout of
+    include/base.h (offsets from a C compile of the header), and the first
+    six fields sit where the problem statement's struct puts them:
+    {phases, rounds, bids, eps_final, fell_back, dual_gap}, dual_gap at 32."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    fields = [f[0] for f in pb.AssignStats._fields_]
+    src = tmp_path / "off.c"
+    body = "".join(f'  printf("{f} %zu\\n", offsetof(base_assign_stats, {f}));\n' for f in fields)
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "base.h"\n'
+                   f'int main(void) {{\n{body}  printf("size %zu\\n", sizeof(base_assign_stats));\n'
+                   '  return 0;\n}\n')
+    exe = tmp_path / "off"
+    subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = dict(line.split() for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                       check=True).stdout.split("\n") if line)
+    for f in fields:
+        assert int(out[f]) == getattr(pb.AssignStats, f).offset, f
+    assert int(out["size"]) == ctypes.sizeof(pb.AssignStats)
+    assert fields[:6] == ["phases", "rounds", "bids", "eps_final", "fell_back", "dual_gap"]
+    assert pb.AssignStats.dual_gap.offset == 32
+
+
+def test_status_read_arguments_checked(L):
+    st = pb.AssignStats()
+    assert L.base_assign_status(None, 1, 8, 2, ctypes.byref(st), None) == pb.BASE_ERR_INVALID_ARG
+    assert L.base_assign_status(FAKE + 16, 1, 8, 2, ctypes.byref(st), None) == \
+        pb.BASE_ERR_INVALID_ARG
+    assert L.base_assign_status(FAKE, 0, 8, 2, ctypes.byref(st), None) == pb.BASE_ERR_INVALID_ARG
+    assert L.base_assign_status(FAKE, 1, 9, 2, ctypes.byref(st), None) == pb.BASE_ERR_INVALID_ARG
+
+
 def test_timing_record_without_launches(L):
     # Disabled or empty records need no device: nothing recorded, nothing summed.
     pb.timing_enable(0)
