@@ -288,6 +288,29 @@ int base_assign_batched(const void *S, int s_dtype, int64_t B, int64_t T, int64_
 int base_assign_status(const void *workspace, int64_t B, int64_t T, int64_t E,
                        base_assign_stats *stats, void *stream);
 
+/*
+ * base_assign_noalloc - base_assign with no workspace argument and no
+ * allocation, for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc. The solve's workspace is a library-owned device array of
+ * BASE_ASSIGN_NOALLOC_MAX_WORKSPACE bytes (32 MiB; each device the library
+ * runs on holds its own copy until the process ends). The call allocates
+ * nothing, on the device or on the host. Same algorithm, options, outputs,
+ * statistics and errors as base_assign (bit-identical results), plus:
+ *   - BASE_ERR_RANGE when base_assign_workspace_size(T, E) exceeds the
+ *     array (T = 32768 with E = 128, and T = 65536 with E = 256, fit);
+ *   - BASE_ERR_HIP when the array's device address cannot be resolved.
+ * Every call on one device shares that device's array, which keeps the
+ * last solve's state (and base_assign_status cannot read it: the address
+ * is not exported). Calls that overlap on one device -- on different
+ * streams or threads without ordering between them -- race on it and give
+ * unspecified results. The kernels run on `stream`'s device.
+ */
+#define BASE_ASSIGN_NOALLOC_MAX_WORKSPACE ((size_t)32 << 20)
+int base_assign_noalloc(const void *S, int s_dtype, int64_t T, int64_t E,
+                        const base_assign_opts *opts, int32_t *assign, int32_t *perm,
+                        void *prices, base_assign_stats *stats, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* base_permute: route rows into expert-contiguous order, or back            */
 /* ------------------------------------------------------------------------ */

@@ -45,7 +45,7 @@ BASE_ASSIGN_FULL_SCHEDULE = 16
 # Every symbol include/base.h declares.
 EXPORTED = ("base_status_string", "base_affinity", "base_affinity_gather",
             "base_assign_workspace_size", "base_assign", "base_assign_batched_workspace_size",
-            "base_assign_batched", "base_assign_status", "base_permute", "base_permute_batched",
+            "base_assign_batched", "base_assign_status", "base_assign_noalloc", "base_permute", "base_permute_batched",
             "base_greedy_workspace_size", "base_greedy_assign", "base_gate_combine",
             "base_gate_combine_batched", "base_gate_backward", "base_timing_enable",
             "base_timing_read")
@@ -101,6 +101,9 @@ def lib() -> ctypes.CDLL:
                                           vp, vp, vp, ctypes.c_size_t,
                                           ctypes.POINTER(AssignStats), vp]
         L.base_assign_batched.restype = i32
+        L.base_assign_noalloc.argtypes = [vp, i32, i64, i64, ctypes.POINTER(AssignOpts), vp, vp,
+                                          vp, ctypes.POINTER(AssignStats), vp]
+        L.base_assign_noalloc.restype = i32
         L.base_assign_status.argtypes = [vp, i64, i64, i64, ctypes.POINTER(AssignStats), vp]
         L.base_assign_status.restype = i32
         L.base_permute.argtypes = [vp, vp, vp, i64, i64, i32, i32, vp]
@@ -280,6 +283,29 @@ def assign_batched(S, *, eps_final: float = 0.0, eps_initial: float = 0.0,
     return AssignResult(out_assign, out_perm, out_prices, stats if sync_stats else None)
 
 
+NOALLOC_MAX_WORKSPACE = 32 << 20   # BASE_ASSIGN_NOALLOC_MAX_WORKSPACE
+
+
+def assign_noalloc(S, *, eps_final: float = 0.0, eps_initial: float = 0.0,
+                   eps_factor: float = 0.0, max_rounds: int = 0, flags: int = 0,
+                   sync_stats: bool = True, out_assign, out_perm, out_prices=None,
+                   stream=None) -> AssignResult:
+    """base_assign_noalloc: the solve of `assign` on the library's own
+    per-device workspace array; allocates nothing (the outputs are the
+    caller's, and must be given)."""
+    _need_device(S, out_assign, out_perm)
+    T, E = S.shape
+    opts = AssignOpts(eps_final, eps_initial, eps_factor, max_rounds,
+                      flags | (BASE_ASSIGN_SYNC_STATS if sync_stats else 0))
+    stats = AssignStats()
+    _check(lib().base_assign_noalloc(S.data_ptr(), _dtype_code(S), T, E, ctypes.byref(opts),
+                                     out_assign.data_ptr(), out_perm.data_ptr(),
+                                     0 if out_prices is None else out_prices.data_ptr(),
+                                     ctypes.byref(stats), _stream_ptr(stream)),
+           "base_assign_noalloc")
+    return AssignResult(out_assign, out_perm, out_prices, stats if sync_stats else None)
+
+
 def assign_status(workspace, T: int, E: int, B: int = 1, stream=None):
     """How the last solve on `workspace` ended (base_assign_status): waits
     for the stream and returns (status code, AssignStats) without raising.
@@ -438,5 +464,5 @@ __all__ = ["affinity", "assign", "assign_batched", "permute", "permute_batched",
            "gate_backward", "balanced_offsets", "assign_workspace_size",
            "assign_batched_workspace_size", "timing_enable",
            "timing_read", "AssignResult", "AssignOpts", "AssignStats", "BaseError", "lib",
-           "assign_status",
+           "assign_status", "assign_noalloc", "NOALLOC_MAX_WORKSPACE",
            "status_string", "EXPORTED"]

@@ -18,7 +18,8 @@ LIB = os.path.join(HERE, "libbase_mi355x.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["affinity.hip", "auction.hip", "permute.hip", "gate.hip", "abi.cpp"]
+SOURCES = ["affinity.hip", "auction.hip", "permute.hip", "gate.hip", "noalloc.hip",
+           "abi.cpp"]
 HEADERS = ["common.hpp", "internal.hpp"]
 
 # Packed fp32 instructions are kept out of the device code on purpose; the
