@@ -49,12 +49,32 @@ constexpr int kRangeBlocks = 256;   // blocks of the score-range reduction
 constexpr int kCountTile = 256;  // tokens per block in the permutation build
 constexpr int kWideLoopRounds = 1024;  // rounds one launch of the round loop may run
 constexpr int kCheckBlocks = 4096;     // largest grid of the phase check
+// Experts the shortest-path finish serves: its exchange matrix then takes 16
+// registers per thread (64 at E = 256 would leave too few for the rest of
+// the kernel at 1024 threads).
+constexpr int kSspMaxE = 128;
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Polls a grid barrier's wait makes before it gives up. BASE_TEST_BARRIER_POLLS
 // overrides the default (read at every solve): tests set it to 0 to force
 // the give-up path from the host, so that every block still exits normally.
+// Unassigned tokens of a phase below which the shortest-path finish takes
+// over (0: never). BASE_SSP_CAP overrides the default (read at every solve;
+// a tuning knob, not part of the interface).
+inline int ssp_cap_setting() {
+    const char *v = getenv("BASE_SSP_CAP");
+    if (v == nullptr || *v == 0) return 8;
+    return (int)strtol(v, nullptr, 10);
+}
+
+// BASE_TEST_SSP_FALLBACKS=1 (tests only) sends every step of the
+// shortest-path finish through its fallback paths.
+inline int ssp_fallbacks_setting() {
+    const char *v = getenv("BASE_TEST_SSP_FALLBACKS");
+    return (v != nullptr && *v == '1') ? 1 : 0;
+}
+
 inline uint32_t barrier_polls() {
     const char *v = getenv("BASE_TEST_BARRIER_POLLS");
     if (v == nullptr || *v == 0) return 1u << 24;
@@ -70,7 +90,7 @@ inline void debug_note(const char *what, hipError_t err) {
 
 struct Layout {
     size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
-        eck, ecs, ecn, sums, bar, rpart, gpart, total;
+        eck, ecs, ecn, sums, bar, rpart, gpart, sspm, sspa, total;
     int64_t cap, nblk;
 };
 
@@ -99,6 +119,11 @@ Layout make_layout(int64_t T, int64_t E) {
     L.bar = off;     off += align_up(512);                      // grid barrier words
     L.rpart = off;   off += align_up((size_t)kRangeBlocks * 12);   // score-range partials
     L.gpart = off;   off += align_up((size_t)kCheckBlocks * 8);    // phase-check partials
+    // The exchange matrix of the shortest-path finish (E <= 256 only):
+    // cheapest move from expert e to expert x and the slot of its token.
+    const int64_t Es = E <= kSspMaxE ? E : 0;
+    L.sspm = off;    off += align_up((size_t)Es * Es * 4);
+    L.sspa = off;    off += align_up((size_t)Es * Es * 2);
     L.total = off;
     return L;
 }
@@ -123,6 +148,10 @@ struct Ctx {
     uint32_t *sums;   // T x 16 words: each token's 8 best scores, their experts, a bound
     uint64_t *bar;    // grid barrier: arrivals at bar[0], release at bar[32] (own lines)
     double *gpart;    // per-block partial sums of the phase check
+    int ssp_cap;      // > 0: a phase with at most this many active tokens left is finished
+                      // by shortest augmenting paths
+    float *ssp_m;     // [E][E] min over tokens t of expert e of S[t,e] - S[t,x]
+    uint16_t *ssp_a;  // [E][E] the holder slot of that token
     int64_t ws_stride;   // bytes between the workspaces of consecutive problems of a batch
 
     // The view of problem b of a batch (blockIdx.y in every solver launch):
@@ -154,6 +183,8 @@ struct Ctx {
         r.sums = shift(sums, w);
         r.bar = shift(bar, w);
         r.gpart = shift(gpart, w);
+        r.ssp_m = shift(ssp_m, w);
+        r.ssp_a = shift(ssp_a, w);
         return r;
     }
 };
@@ -187,6 +218,9 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.sums = reinterpret_cast<uint32_t *>(ws + L.sums);
     c.bar = reinterpret_cast<uint64_t *>(ws + L.bar);
     c.gpart = reinterpret_cast<double *>(ws + L.gpart);
+    c.ssp_cap = 0;
+    c.ssp_m = reinterpret_cast<float *>(ws + L.sspm);
+    c.ssp_a = reinterpret_cast<uint16_t *>(ws + L.sspa);
     c.ws_stride = (int64_t)L.total;
     return c;
 }
@@ -2334,7 +2368,7 @@ __global__ __launch_bounds__(256) void engine_entry_kernel(Ctx<M> c0, int pf) {
         go = 0;
         if (!ctrl->done && !ctrl->all_active) {
             const int n = ld_relaxed(&ctrl->active_count[ctrl->cur]);
-            if (n > 0 && n <= c.engine_cap) go = 1;
+            if (n > c.ssp_cap && n <= c.engine_cap) go = 1;
         }
     }
     __syncthreads();
@@ -2423,7 +2457,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
         if (!ctrl->done && !ctrl->all_active) {
             s_cur = ctrl->cur;
             const int n = ld_relaxed(&ctrl->active_count[s_cur]);
-            if (n > 0 && n <= kEngCap) {
+            if (n > 0 && n > c.ssp_cap && n <= kEngCap) {
                 s_go = 1;
                 s_n = n;
             }
@@ -2497,6 +2531,7 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
     int nt_prev = 0;
     for (;;) {
         if (n == 0) break;
+        if (n <= c.ssp_cap) break;   // the shortest-path finish takes the last tokens
         if (rounds >= max_rounds_left) {
             if (tid == 0) s_stop = 1;
             break;
@@ -2658,6 +2693,713 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
             ctrl->done = 1;
         } else if (n == 0 && ctrl->last_phase) {
             ctrl->done = 1;
+        }
+    }
+}
+
+// ------------------------------------------------- shortest-path finish --
+//
+// The last few tokens of a phase (at most ssp_cap, float mode, E <= 256)
+// are not left to the auction's rounds: each would wander through many
+// experts, one eviction per round, until it meets a free slot. Instead each
+// is placed by one shortest augmenting path over the E experts, as in the
+// successive-shortest-path method for the transportation problem, starting
+// from the auction's epsilon-complementary-slack state:
+//
+//   arc e -> x   moving the cheapest token t of expert e to expert x costs
+//                w(e,x) = min_t [(S[t,e] - p_e) - (S[t,x] - p_x)]
+//                       = M(e,x) - p_e + p_x,  M(e,x) = min_t S[t,e] - S[t,x].
+//                Epsilon-CS says w >= -eps; the search uses w+ = max(w, 0).
+//   sources      every unassigned token u reaches expert x at
+//                dist0(x) = max_y (S[u,y] - p_y) - (S[u,x] - p_x) >= 0.
+//   target       the expert with a free slot at the least distance D.
+//
+// Bellman-Ford over the dense E x E arcs (all arcs relaxed in parallel, a
+// few iterations: shortest paths have few hops) gives dist(); the path is
+// applied (each expert on it hands its cheapest token to the next, the free
+// expert gains one) and every price rises by max(0, D - dist(x)). With
+// dist(x') <= dist(x) + w+(x,x') <= dist(x) + w(x,x') + eps, every arc keeps
+// w >= -eps after the rise, the moved tokens' arcs included, and the placed
+// token ends at its best value: epsilon-CS holds for every assigned token,
+// so the finished phase carries the auction's own guarantee (T * eps). Free
+// experts keep their prices (their distance is at least D).
+//
+// ssp_build_kernel computes M and the slot of its token for every expert
+// (one block per expert, reading its tokens' score rows); ssp_kernel keeps
+// M in registers (thread (x, part) holds rows [part R, part R + R) of
+// column x), the slots in LDS, and updates both after each path: an expert
+// that received a token takes the minimum with that token's row; a column
+// whose cheapest token left is recomputed over the expert's slots.
+
+constexpr int kSspThreads = 1024;
+constexpr int kSspMaxCap = 32;   // most unassigned tokens a phase hands over
+constexpr int kSspMinCap = 8;
+constexpr int kSspRc = 256;      // column recomputes taken per pass
+constexpr int kSspMnew = 8;      // path experts whose received rows go through LDS
+
+
+// Whether problem c's current phase waits for the shortest-path finish.
+template <class M>
+__device__ inline bool ssp_pending(const Ctx<M> &c, int *n_out) {
+    const SolveCtrl *ctrl = c.ctrl;
+    if (c.ssp_cap <= 0 || ctrl->done || ctrl->all_active) return false;
+    const int n = ld_relaxed(&ctrl->active_count[ctrl->cur]);
+    *n_out = n;
+    return n > 0 && n <= c.ssp_cap;
+}
+
+template <class M>
+__global__ __launch_bounds__(kSspThreads) void ssp_build_kernel(Ctx<M> c0) {
+    const Ctx<M> c = c0.at(blockIdx.y);
+    __shared__ int go;
+    __shared__ int tok[kEngMaxC];
+    __shared__ float se[kEngMaxC];
+    __shared__ float rv[kSspThreads];
+    __shared__ int rs[kSspThreads];
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        int n = 0;
+        go = ssp_pending<M>(c, &n) ? 1 : 0;
+    }
+    __syncthreads();
+    if (!go) return;
+    const int e = blockIdx.x;
+    int cnt = ld_relaxed(&c.hcount[e]);
+    if (cnt < 0 || cnt > c.C) {
+        if (tid == 0) flag_internal(c.ctrl);
+        cnt = 0;
+    }
+    const uint64_t *hold = c.holders + (int64_t)(ld_relaxed(&c.hsel[e]) & 1) * c.T + (int64_t)e * c.C;
+    for (int q = tid; q < cnt; q += kSspThreads) {
+        int t = key_token(hold[q]);
+        if (t < 0 || t >= c.T) {
+            flag_internal(c.ctrl);
+            t = 0;
+        }
+        tok[q] = t;
+        se[q] = c.S[(int64_t)t * c.E + e];
+    }
+    __syncthreads();
+    int Ep = 1;
+    while (Ep < c.E) Ep <<= 1;
+    const int subs = kSspThreads / Ep;
+    const int x = tid % Ep, sub = tid / Ep;
+    float best = INFINITY;
+    int bs = 0xffff;
+    if (x < c.E) {
+#pragma unroll 8
+        for (int q = sub; q < cnt; q += subs) {
+            const float v = se[q] - c.S[(int64_t)tok[q] * c.E + x];
+            if (v < best) {
+                best = v;
+                bs = q;
+            }
+        }
+    }
+    rv[tid] = best;
+    rs[tid] = bs;
+    __syncthreads();
+    if (sub == 0 && x < c.E) {
+        for (int j = 1; j < subs; ++j) {
+            const float v = rv[j * Ep + x];
+            const int q = rs[j * Ep + x];
+            if (v < best || (v == best && q < bs)) {
+                best = v;
+                bs = q;
+            }
+        }
+        c.ssp_m[(int64_t)e * c.E + x] = best;
+        c.ssp_a[(int64_t)e * c.E + x] = (uint16_t)bs;
+    }
+}
+
+// LDS of ssp_kernel for Ep padded experts: fixed-size arrays at offsets
+// known at compile time, then the slot matrix [E][E] (u16), the rows of the
+// unassigned tokens transposed [E][K + 1] (fp32; the odd stride keeps the
+// lanes of a wave on distinct banks both ways) and every expert's holder
+// slots [E][C] as u16 tokens (T <= 65536).
+template <int Ep>
+struct SspLds {
+    static constexpr size_t distp = 0;                       // u64 [3][Ep]
+    static constexpr size_t rckey = distp + 3 * Ep * 8;      // u64 [kSspMnew][Ep]
+    static constexpr size_t pr = rckey + kSspMnew * Ep * 8;  // f32 [Ep]
+    static constexpr size_t cnt = pr + Ep * 4;               // i32 [Ep]
+    static constexpr size_t sel = cnt + Ep * 4;
+    static constexpr size_t path = sel + Ep * 4;             // i32 [Ep + 4]
+    static constexpr size_t hslot = path + (Ep + 4) * 4;
+    static constexpr size_t htok = hslot + Ep * 4;
+    static constexpr size_t urow = htok + Ep * 4;
+    static constexpr size_t rcj = urow + Ep * 4;             // [kSspRc]
+    static constexpr size_t rcx = rcj + kSspRc * 4;
+    static constexpr size_t act = rcx + kSspRc * 4;          // [kSspMaxCap]
+    static constexpr size_t vstar = act + kSspMaxCap * 4;
+    static constexpr size_t mnew = vstar + kSspMaxCap * 4;   // f32 [kSspMnew][Ep]
+    static constexpr size_t am = mnew + kSspMnew * Ep * 4;   // u16 [Ep][Ep]
+    static constexpr size_t rows = am + (size_t)Ep * Ep * 2; // f32 [E][K + 1]
+    __host__ __device__ static size_t toks(int E, int K) {
+        return (rows + (size_t)E * (K + 1) * 4 + 15) & ~size_t(15);
+    }
+    __host__ __device__ static size_t total(int E, int K, int C) {
+        return toks(E, K) + (size_t)E * C * 2;
+    }
+};
+
+inline int ssp_pad(int E) {
+    int Ep = 32;
+    while (Ep < E) Ep <<= 1;
+    return Ep;
+}
+
+inline size_t ssp_lds_bytes(int E, int K, int C) {
+    switch (ssp_pad(E)) {
+        case 32: return SspLds<32>::total(E, K, C);
+        case 64: return SspLds<64>::total(E, K, C);
+        default: return SspLds<128>::total(E, K, C);
+    }
+}
+
+// Packed distance label: the (non-negative) distance's bits above, the
+// predecessor below (an expert, or kSspSrc + i for unassigned token i), so
+// that one 64-bit minimum keeps a distance with its predecessor.
+constexpr uint32_t kSspSrc = 0x10000u;
+__device__ inline uint64_t ssp_pack(float d, uint32_t lab) {
+    return ((uint64_t)__float_as_uint(d) << 32) | lab;
+}
+__device__ inline float ssp_dist(uint64_t v) { return __uint_as_float((uint32_t)(v >> 32)); }
+// An exchange-matrix entry with the slot of its token, ordered by value.
+__device__ inline uint64_t ssp_entry(float v, int q) {
+    return ((uint64_t)f32_ord(v) << 32) | (uint32_t)q;
+}
+
+// Wave-wide minimum of (v, i), ties to the lower i: DPP moves inside each
+// row of 16 lanes, then the four rows' results read with readlane. Every
+// lane gets the result.
+__device__ inline void wave_min_pair(float &v, int &i) {
+#define BASE_MIN_STEP(OFF)                                                \
+    {                                                                     \
+        const float ov = grp_partner<OFF>(v);                             \
+        const int oi = grp_partner<OFF>(i);                               \
+        const bool t = (ov < v) | ((ov == v) & (oi < i));                 \
+        v = t ? ov : v;                                                   \
+        i = t ? oi : i;                                                   \
+    }
+    BASE_MIN_STEP(1)
+    BASE_MIN_STEP(2)
+    BASE_MIN_STEP(4)
+    BASE_MIN_STEP(8)
+#undef BASE_MIN_STEP
+    float rv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    int ri = __builtin_amdgcn_readlane(i, 0);
+#pragma unroll
+    for (int q = 1; q < 4; ++q) {
+        const float ov = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16 * q));
+        const int oi = __builtin_amdgcn_readlane(i, 16 * q);
+        const bool t = (ov < rv) | ((ov == rv) & (oi < ri));
+        rv = t ? ov : rv;
+        ri = t ? oi : ri;
+    }
+    v = rv;
+    i = ri;
+}
+
+// Ep = 32, 64 or 128 padded experts. One wave per SIMD: wave w (of 4) owns
+// rows [w RW, w RW + RW) of the exchange matrix, lane l its columns
+// l + 64 j. (With 16 waves the per-step work of every wave queued four deep
+// on each SIMD; the relaxations themselves are few after the first step.)
+constexpr int kSspBlock = 256;
+constexpr int kSspWaves = kSspBlock / 64;
+
+// small != 0 (tests only) routes every step through the fallbacks: no
+// recompute list (whole rows instead) and received rows read by the owners.
+template <class M, int Ep>
+__global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int small) {
+    static_assert(!M::kInteger, "the shortest-path finish runs in float mode");
+    constexpr int RW = Ep / kSspWaves;           // rows per wave
+    constexpr int CL = Ep >= 64 ? Ep / 64 : 1;   // columns per lane
+    const Ctx<M> c = c0.at(blockIdx.y);
+    SolveCtrl *ctrl = c.ctrl;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    using LY = SspLds<Ep>;
+    uint64_t *distp = reinterpret_cast<uint64_t *>(smem_raw + LY::distp);
+    uint64_t *rckey = reinterpret_cast<uint64_t *>(smem_raw + LY::rckey);
+    float *pr = reinterpret_cast<float *>(smem_raw + LY::pr);
+    int *cnt = reinterpret_cast<int *>(smem_raw + LY::cnt);
+    int *sel = reinterpret_cast<int *>(smem_raw + LY::sel);
+    int *path = reinterpret_cast<int *>(smem_raw + LY::path);
+    int *hslot = reinterpret_cast<int *>(smem_raw + LY::hslot);
+    int *htok = reinterpret_cast<int *>(smem_raw + LY::htok);
+    float *urow = reinterpret_cast<float *>(smem_raw + LY::urow);
+    int *rcj = reinterpret_cast<int *>(smem_raw + LY::rcj);
+    int *rcx = reinterpret_cast<int *>(smem_raw + LY::rcx);
+    int *act = reinterpret_cast<int *>(smem_raw + LY::act);
+    float *vstar = reinterpret_cast<float *>(smem_raw + LY::vstar);
+    float *mnew = reinterpret_cast<float *>(smem_raw + LY::mnew);
+    uint16_t *am = reinterpret_cast<uint16_t *>(smem_raw + LY::am);
+    float *rowsT = reinterpret_cast<float *>(smem_raw + LY::rows);
+    __shared__ int s_go, s_n, s_cur, s_flag[3], s_L, s_i, s_u, s_err, s_nrc, s_full;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int E = c.E, C = c.C, T = c.T;
+    const int KS = K + 1;   // stride of the transposed rows
+    uint16_t *toks = reinterpret_cast<uint16_t *>(smem_raw + LY::toks(E, K));
+    const int e0 = wave * RW;   // this wave's rows
+    const int rc_cap = small ? 0 : kSspRc;
+    const int mn_cap = small ? 1 : kSspMnew;
+    if (tid == 0) {
+        int n = 0;
+        s_go = ssp_pending<M>(c, &n) && n <= K && T <= 65536 ? 1 : 0;
+        s_n = n;
+        s_cur = ctrl->cur;
+        s_err = 0;
+        s_nrc = 0;
+        s_full = 0;
+        s_flag[0] = s_flag[1] = s_flag[2] = 0;
+    }
+    __syncthreads();
+    if (!s_go) return;
+    // State into LDS and registers: prices, counts, holder selectors, every
+    // expert's held tokens, the slot matrix, the unassigned tokens' rows.
+    for (int e = tid; e < Ep; e += kSspBlock) {
+        const bool real = e < E;
+        pr[e] = real ? c.prices[e] : 0.0f;
+        int h = real ? ld_relaxed(&c.hcount[e]) : C;
+        if (h < 0 || h > C) {
+            flag_internal(ctrl);
+            s_err = 1;
+            h = C;
+        }
+        cnt[e] = h;
+        sel[e] = real ? (ld_relaxed(&c.hsel[e]) & 1) : 0;
+    }
+    __syncthreads();
+    for (int i = tid; i < E * C; i += kSspBlock) {
+        const int e = i / C, q = i - e * C;
+        int t = 0;
+        if (q < cnt[e]) {
+            t = key_token(c.holders[(int64_t)sel[e] * T + i]);
+            if (t < 0 || t >= T) {
+                flag_internal(ctrl);
+                s_err = 1;
+                t = 0;
+            }
+        }
+        toks[i] = (uint16_t)t;
+    }
+    for (int i = tid; i < E * E; i += kSspBlock) am[i] = c.ssp_a[i];
+    {
+        const int n = s_n;
+        for (int i = wave; i < n; i += kSspWaves) {
+            int t = c.active[(int64_t)s_cur * T + i];
+            if (t < 0 || t >= T) {
+                if (lane == 0) {
+                    flag_internal(ctrl);
+                    s_err = 1;
+                }
+                t = 0;
+            }
+            if (lane == 0) act[i] = t;
+            for (int y = lane; y < E; y += 64) rowsT[y * KS + i] = c.S[(int64_t)t * E + y];
+        }
+    }
+    float mreg[RW][CL];
+#pragma unroll
+    for (int r = 0; r < RW; ++r)
+#pragma unroll
+        for (int j = 0; j < CL; ++j) {
+            const int x = lane + 64 * j;
+            mreg[r][j] = (x < E && e0 + r < E) ? c.ssp_m[(int64_t)(e0 + r) * E + x] : INFINITY;
+        }
+    __syncthreads();
+    int k = s_n;
+    int augs = 0;
+    while (k > 0 && !s_err) {
+        // (1) Every unassigned token's best value (eight lanes per token),
+        // then the sources' distances (a thread per expert).
+        {
+            const int i = tid >> 3, part = tid & 7;
+            float m = -INFINITY;
+            if (i < k)
+                for (int y = part; y < E; y += 8) m = fmaxf(m, rowsT[y * KS + i] - pr[y]);
+            m = fmaxf(m, grp_partner<1>(m));
+            m = fmaxf(m, grp_partner<2>(m));
+            m = fmaxf(m, grp_partner<4>(m));
+            if (i < k && part == 0) vstar[i] = m;
+        }
+        if (tid == 0) s_flag[0] = s_flag[1] = s_flag[2] = 0;
+        __syncthreads();
+        if (tid < Ep) {
+            // Ties between tokens go to the lower token index: the list's
+            // order comes from atomics and is not reproducible.
+            const int x = tid;
+            float best = INFINITY;
+            int bi = 0, bt = 0x7fffffff;
+            if (x < E) {
+                const float px = pr[x];
+                for (int i = 0; i < k; ++i) {
+                    const float v = vstar[i] - (rowsT[x * KS + i] - px);
+                    const int ti = act[i];
+                    const bool t = (v < best) | ((v == best) & (ti < bt));
+                    best = t ? v : best;
+                    bi = t ? i : bi;
+                    bt = t ? ti : bt;
+                }
+            }
+            distp[x] = ssp_pack(best, kSspSrc + (uint32_t)bi);
+            distp[Ep + x] = ~0ull;
+        }
+        // The arcs at the current prices: M(e,x) + p_x, and -p_e per row;
+        // which of this lane's experts have room.
+        float mp[RW][CL];
+        bool room[CL];
+#pragma unroll
+        for (int j = 0; j < CL; ++j) {
+            const int x = lane + 64 * j;
+            const float px = x < E ? pr[x] : 0.0f;
+            room[j] = x < E && cnt[x] < C;
+#pragma unroll
+            for (int r = 0; r < RW; ++r) mp[r][j] = mreg[r][j] + px;
+        }
+        const float prow = lane < RW ? pr[e0 + lane] : 0.0f;   // lane r: price of row r
+        float dused = INFINITY;                                 // lane r: dist row r was relaxed at
+        __syncthreads();
+        // (2) Bellman-Ford, one synchronous step per iteration: step `it`
+        // reads buffer it % 3 and writes the next one (cleared a step
+        // ahead), into which the owners fold the current labels and the
+        // waves their strict improvements, as 64-bit minima of (distance,
+        // predecessor): equal distances keep the lower expert, whatever
+        // the order of the atomics, so the result does not depend on
+        // scheduling. Only experts nearer than the nearest expert with room
+        // (dcur, which every wave takes from the labels it reads) can lie on
+        // the path or gain a price: a wave relaxes only those of its rows,
+        // and only when their distance fell since it last relaxed them.
+        int fin = 0;     // the buffer with the converged labels
+        float D = INFINITY;
+        int f = 0x7fffffff;   // the nearest expert with room
+        for (int it = 0;; ++it) {
+            const uint64_t *cur = distp + (it % 3) * Ep;
+            uint64_t *nxt = distp + ((it + 1) % 3) * Ep;
+            if (tid < Ep) {
+                atomicMin(reinterpret_cast<unsigned long long *>(&nxt[tid]),
+                          (unsigned long long)cur[tid]);
+                distp[((it + 2) % 3) * Ep + tid] = ~0ull;
+            }
+            const float dnow = lane < RW ? ssp_dist(cur[e0 + lane]) : INFINITY;
+            float dcol[CL];
+            float dcur = INFINITY;
+            int fcur = 0x7fffffff;
+#pragma unroll
+            for (int j = 0; j < CL; ++j) {
+                const int x = lane + 64 * j;
+                dcol[j] = x < E ? ssp_dist(cur[x]) : -INFINITY;
+                const bool t = room[j] && dcol[j] < dcur;
+                dcur = t ? dcol[j] : dcur;
+                fcur = t ? x : fcur;
+            }
+            wave_min_pair(dcur, fcur);
+            const bool relax = lane < RW && dnow < dused && dnow < dcur;
+            const uint64_t todo = __ballot(relax);
+            dused = relax ? dnow : dused;
+            float best[CL];
+            int bj[CL];
+#pragma unroll
+            for (int j = 0; j < CL; ++j) {
+                best[j] = INFINITY;
+                bj[j] = 0;
+            }
+#pragma unroll
+            for (int r = 0; r < RW; ++r) {
+                if (!((todo >> r) & 1)) continue;   // uniform
+                const float de = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dnow), r));
+                const float q = de - __int_as_float(__builtin_amdgcn_readlane(__float_as_int(prow), r));
+#pragma unroll
+                for (int j = 0; j < CL; ++j) {
+                    const float cand = fmaxf(q + mp[r][j], de);
+                    const bool t = cand < best[j];
+                    best[j] = t ? cand : best[j];
+                    bj[j] = t ? e0 + r : bj[j];
+                }
+            }
+            bool imp = false;
+#pragma unroll
+            for (int j = 0; j < CL; ++j) {
+                const int x = lane + 64 * j;
+                if (best[j] < fminf(dcol[j], dcur)) {   // strict improvement (x < E)
+                    atomicMin(reinterpret_cast<unsigned long long *>(&nxt[x]),
+                              (unsigned long long)ssp_pack(best[j], (uint32_t)bj[j]));
+                    imp = true;
+                }
+            }
+            const int slot = it % 3;
+            if (__ballot(imp) != 0 && lane == 0) s_flag[slot] = 1;
+            if (tid == 0) s_flag[(it + 1) % 3] = 0;
+            __syncthreads();
+            if (!s_flag[slot]) {   // converged: cur holds the labels
+                fin = it % 3;
+                D = dcur;
+                f = fcur;
+                break;
+            }
+            if (it > Ep + 2) {   // shortest paths have at most E - 1 hops
+                if (tid == 0) {
+                    flag_internal(ctrl);
+                    s_err = 1;
+                }
+                break;
+            }
+        }
+        __syncthreads();
+        if (s_err) break;
+        const uint64_t *dfin = distp + fin * Ep;
+        // (3) The path to the nearest expert with room (one lane).
+        if (tid == 0) {
+            int L = 0;
+            bool ok = f < E && D < INFINITY;
+            if (ok) {
+                for (uint32_t lab = (uint32_t)dfin[f]; lab < kSspSrc; lab = (uint32_t)dfin[lab]) {
+                    if (lab >= (uint32_t)E || ++L > E) {
+                        ok = false;
+                        break;
+                    }
+                }
+            }
+            if (ok) {
+                int y = f;
+                for (int j = L; j > 0; --j) {
+                    path[j] = y;
+                    y = (int)(uint32_t)dfin[y];
+                }
+                path[0] = y;
+                const uint32_t i = (uint32_t)dfin[y] - kSspSrc;
+                ok = i < (uint32_t)k;
+                s_i = ok ? (int)i : 0;
+                s_u = ok ? act[s_i] : 0;
+            }
+            if (!ok) {
+                flag_internal(ctrl);
+                s_err = 1;
+            }
+            s_L = L;
+        }
+        __syncthreads();
+        if (s_err) break;
+        const int L = s_L, u = s_u, iu = s_i;
+        const int nmn = L + 1 < mn_cap ? L + 1 : mn_cap;   // path experts through LDS
+        // (A) New prices; the slot each expert on the path hands on and its
+        // token; the columns whose cheapest token leaves (queued for a
+        // recompute); the placed token's row.
+        for (int y = tid; y < E; y += kSspBlock) {
+            pr[y] = pr[y] + fmaxf(D - ssp_dist(dfin[y]), 0.0f);
+            urow[y] = rowsT[y * KS + iu];
+        }
+        for (int j = tid; j < L; j += kSspBlock) {
+            const int e = path[j];
+            const int q = am[e * E + path[j + 1]];
+            hslot[j] = q;
+            htok[j] = q < cnt[e] ? (int)toks[e * C + q] : 0;
+            if (q >= cnt[e]) {
+                flag_internal(ctrl);
+                s_err = 1;
+            }
+        }
+        for (int i = tid; i < L * E; i += kSspBlock) {
+            const int j = i / E, x = i - j * E;
+            const int e = path[j];
+            if (am[e * E + x] == am[e * E + path[j + 1]]) {
+                const int at = j < mn_cap ? atomicAdd(&s_nrc, 1) : rc_cap;
+                if (at < rc_cap) {
+                    rcj[at] = j;
+                    rcx[at] = x;
+                    rckey[j * Ep + x] = ~0ull;
+                } else {
+                    s_full = 1;   // the path's rows are recomputed whole
+                }
+            }
+        }
+        __syncthreads();
+        if (s_err) break;
+        // (B) Apply the path in the holder tables; one flat pass over every
+        // global read of the step, so that they are all in flight together:
+        // the received tokens' rows of the first kSspMnew path experts (into
+        // LDS), and each queued column's entries over its expert's slots
+        // (into a 64-bit minimum of (order-preserving value, slot)).
+        const int nrc = s_nrc < rc_cap ? s_nrc : rc_cap;
+        const int full = s_full;
+        auto token_in = [&](int j) -> int { return j == 0 ? u : htok[j - 1]; };
+        for (int j = tid; j <= L; j += kSspBlock) {
+            const int e = path[j];
+            const int q = j < L ? hslot[j] : cnt[e];
+            if (q < C) {
+                int overflow = 0;
+                uint64_t *hold = c.holders + (int64_t)sel[e] * T + (int64_t)e * C;
+                hold[q] = M::make_key(pr[e], token_in(j), &overflow);
+                if (overflow) ctrl->overflow = 1;
+            } else {
+                flag_internal(ctrl);
+                s_err = 1;
+            }
+        }
+        {
+            const int nm = nmn * E;
+            const int nitems = nm + nrc * C;
+#pragma unroll 4
+            for (int i = tid; i < nitems; i += kSspBlock) {
+                if (i < nm) {
+                    const int j = i / E, x = i - j * E;
+                    const int e = path[j];
+                    float v;
+                    if (j == 0) {
+                        v = urow[e] - urow[x];
+                    } else {
+                        const int tin = htok[j - 1];
+                        v = c.S[(int64_t)tin * E + e] - c.S[(int64_t)tin * E + x];
+                    }
+                    mnew[j * Ep + x] = v;
+                } else {
+                    const int i2 = i - nm;
+                    const int p = i2 / C, q = i2 - p * C;
+                    const int j = rcj[p], y = rcx[p];
+                    const int e = path[j];
+                    if (q < cnt[e]) {
+                        const int t = q == hslot[j] ? token_in(j) : (int)toks[e * C + q];
+                        const float v = c.S[(int64_t)t * E + e] - c.S[(int64_t)t * E + y];
+                        atomicMin(reinterpret_cast<unsigned long long *>(&rckey[j * Ep + y]),
+                                  (unsigned long long)ssp_entry(v, q));
+                    }
+                }
+            }
+        }
+        // Path experts beyond the LDS rows: their owners read directly.
+        for (int j = mn_cap; j <= L; ++j) {
+            const int e = path[j];
+            if (e < e0 || e >= e0 + RW) continue;   // uniform: rows are the wave's
+            const int rr = e - e0;
+            const int tin = token_in(j);
+            const int qin = j < L ? hslot[j] : cnt[e];
+            const float se = c.S[(int64_t)tin * E + e];
+#pragma unroll
+            for (int jj = 0; jj < CL; ++jj) {
+                const int x = lane + 64 * jj;
+                if (x >= E) continue;
+                if (j < L && am[e * E + x] == hslot[j]) continue;   // recomputed whole
+                const float v = se - c.S[(int64_t)tin * E + x];
+                float cv = 0.0f;
+#pragma unroll
+                for (int r = 0; r < RW; ++r) cv = r == rr ? mreg[r][jj] : cv;
+                if (v < cv) {
+#pragma unroll
+                    for (int r = 0; r < RW; ++r) mreg[r][jj] = r == rr ? v : mreg[r][jj];
+                    am[e * E + x] = (uint16_t)qin;
+                }
+            }
+        }
+        __syncthreads();
+        if (s_err) break;
+        // (C) Owners take, for each path expert they own, the recomputed
+        // columns and the minimum with the received row elsewhere.
+        for (int j = 0; j < nmn; ++j) {
+            const int e = path[j];
+            if (e < e0 || e >= e0 + RW) continue;   // uniform
+            const int rr = e - e0;
+            const int qin = j < L ? hslot[j] : cnt[e];
+#pragma unroll
+            for (int jj = 0; jj < CL; ++jj) {
+                const int x = lane + 64 * jj;
+                if (x >= E) continue;
+                float v;
+                int q;
+                if (j < L && am[e * E + x] == hslot[j]) {
+                    const uint64_t key = rckey[j * Ep + x];
+                    v = f32_unord((uint32_t)(key >> 32));
+                    q = (int)(uint32_t)key;
+                } else {
+                    v = mnew[j * Ep + x];
+                    q = qin;
+                    float cv = 0.0f;
+#pragma unroll
+                    for (int r = 0; r < RW; ++r) cv = r == rr ? mreg[r][jj] : cv;
+                    if (!(v < cv)) continue;
+                }
+#pragma unroll
+                for (int r = 0; r < RW; ++r) mreg[r][jj] = r == rr ? v : mreg[r][jj];
+                am[e * E + x] = (uint16_t)q;
+            }
+        }
+        if (full) {
+            // More recomputes than the list holds (or a path longer than the
+            // LDS rows): every row of the path's experts that hand on a
+            // token is recomputed, all threads splitting the slots, with one
+            // 64-bit minimum per column (distp is free until the next search).
+            for (int j = 0; j < L; ++j) {
+                const int e = path[j];
+                const int q_out = hslot[j];
+                const int t_in = token_in(j);
+                __syncthreads();
+                if (tid < E) distp[tid] = ~0ull;
+                __syncthreads();
+#pragma unroll
+                for (int jj = 0; jj < CL; ++jj) {
+                    const int x = lane + 64 * jj;
+                    if (x >= E) continue;
+                    uint64_t bk = ~0ull;
+                    for (int q = wave; q < cnt[e]; q += kSspWaves) {
+                        const int t = q == q_out ? t_in : (int)toks[e * C + q];
+                        const float v = c.S[(int64_t)t * E + e] - c.S[(int64_t)t * E + x];
+                        const uint64_t key = ssp_entry(v, q);
+                        bk = key < bk ? key : bk;
+                    }
+                    atomicMin(reinterpret_cast<unsigned long long *>(&distp[x]),
+                              (unsigned long long)bk);
+                }
+                __syncthreads();
+                if (e >= e0 && e < e0 + RW) {
+                    const int rr = e - e0;
+#pragma unroll
+                    for (int jj = 0; jj < CL; ++jj) {
+                        const int x = lane + 64 * jj;
+                        if (x >= E) continue;
+                        const uint64_t bk = distp[x];
+                        const float v = f32_unord((uint32_t)(bk >> 32));
+#pragma unroll
+                        for (int r = 0; r < RW; ++r) mreg[r][jj] = r == rr ? v : mreg[r][jj];
+                        am[e * E + x] = (uint16_t)(uint32_t)bk;
+                    }
+                }
+            }
+        }
+        // The token lists, the unassigned list and the free expert's count
+        // follow the path.
+        for (int j = tid; j <= L; j += kSspBlock) {
+            const int e = path[j];
+            const int q = j < L ? hslot[j] : cnt[e];
+            if (q < C) toks[e * C + q] = (uint16_t)token_in(j);
+        }
+        for (int y = tid; y < E; y += kSspBlock) rowsT[y * KS + iu] = rowsT[y * KS + k - 1];
+        if (tid == 0) {
+            act[iu] = act[k - 1];
+            s_nrc = 0;
+            s_full = 0;
+        }
+        __syncthreads();
+        if (tid == 0) cnt[f] += 1;
+        ++augs;
+        --k;
+    }
+    __syncthreads();
+    // Hand the state back: the phase is complete (or flagged).
+    for (int e = tid; e < E; e += kSspBlock) {
+        c.prices[e] = pr[e];
+        c.hcount[e] = cnt[e];
+    }
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) {
+        ctrl->augmentations += augs;
+        if (!s_err) {
+            ctrl->active_count[s_cur] = 0;
+            ctrl->active_count[s_cur ^ 1] = 0;
+            if (ctrl->last_phase) ctrl->done = 1;
         }
     }
 }
@@ -2954,6 +3696,44 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
         }
     }
     if (engine) c.engine_cap = kEngCap;
+    // The shortest-path finish (float mode, E <= 256, with the engine): the
+    // most unassigned tokens it takes over, as many as its LDS allows.
+    size_t ssp_bytes = 0;
+    int ssp_r = 0;
+    if constexpr (!M::kInteger) {
+        int cap = ssp_cap_setting();
+        if (engine && c.E <= kSspMaxE && c.T <= 65536 && cap > 0) {
+            int optin = 0, dev = 0;
+            if (hipGetDevice(&dev) != hipSuccess ||
+                hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) !=
+                    hipSuccess ||
+                optin <= 0)
+                optin = 64 * 1024;
+            const size_t limit = (size_t)optin - 2048;   // the kernel's static LDS
+            if (cap > kSspMaxCap) cap = kSspMaxCap;
+            if (cap < kSspMinCap) cap = kSspMinCap;
+            while (cap >= kSspMinCap && ssp_lds_bytes(c.E, cap, c.C) > limit) cap >>= 1;
+            if (cap >= kSspMinCap) {
+                ssp_r = ssp_pad(c.E);
+                ssp_bytes = ssp_lds_bytes(c.E, cap, c.C);
+                hipError_t err = hipSuccess;
+                if (ssp_bytes > 64 * 1024) {
+                    const void *fn = ssp_r == 32   ? reinterpret_cast<const void *>(&ssp_kernel<M, 32>)
+                                     : ssp_r == 64 ? reinterpret_cast<const void *>(&ssp_kernel<M, 64>)
+                                                   : reinterpret_cast<const void *>(&ssp_kernel<M, 128>);
+                    err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                              (int)ssp_bytes);
+                }
+                if (err == hipSuccess) {
+                    c.ssp_cap = cap;
+                } else {
+                    (void)hipGetLastError();
+                    debug_note("shortest-path finish LDS opt-in refused", err);
+                    ssp_r = 0;
+                }
+            }
+        }
+    }
     const size_t pr_bytes = (size_t)c.E * sizeof(value_t);
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
     // Phase slots enqueued up front; the last one continues on its own (in
@@ -3036,6 +3816,18 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
             hipLaunchKernelGGL((engine_kernel<M, G>), dim3(1, B), dim3(kEngThreads), eng_bytes, s,
                                c, p);
             if (ev1 != nullptr) (void)hipEventRecord(ev1, s);
+        }
+        if constexpr (!M::kInteger) {
+            if (ssp_r > 0) {
+                hipLaunchKernelGGL(ssp_build_kernel<M>, dim3(c.E, B), dim3(kSspThreads), 0, s, c);
+                const dim3 g(1, B), t(kSspBlock);
+                const int small = ssp_fallbacks_setting();
+                switch (ssp_r) {
+                    case 32: hipLaunchKernelGGL((ssp_kernel<M, 32>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
+                    case 64: hipLaunchKernelGGL((ssp_kernel<M, 64>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
+                    default: hipLaunchKernelGGL((ssp_kernel<M, 128>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
+                }
+            }
         }
         if (!engine || slot == slots - 1)
             hipLaunchKernelGGL((tail_kernel<M, G>), dim3(1, B), dim3(kThreads), tail_smem, s, c,
