@@ -11,6 +11,8 @@ What it computes, each function citing the passage it follows:
   solve_hungarian   the same on the expert-replicated matrix    (Sec. 3.2.1, Eq. 2)
   solve_bruteforce  the same by enumeration, tiny inputs        (Sec. 3.2.1, Eq. 2)
   greedy_argmax     test-time assignment, best expert per token (Sec. 3.2.2)
+  greedy_completion balance-keeping end of a round-bounded solve (a reading; Eq. 2's balance)
+  stable_perm_partial  sort vector of an incomplete assignment, -1 for empty rows
   dual_bound        LP-duality upper bound of Eq. 2 for prices p
   optimum_gap       second-best gap / uniqueness of an optimum
   stable_perm       sort vector grouping tokens by expert        (Fig. 2 caption)
@@ -27,11 +29,13 @@ from .assign import (
     balanced_counts_ok,
     dual_bound,
     greedy_argmax,
+    greedy_completion,
     objective,
     optimum_gap,
     solve_bruteforce,
     solve_hungarian,
     solve_ssp,
+    stable_perm_partial,
 )
 from .gate import expert_offsets, gate_backward, gate_combine
 from .permute import gather, scatter, stable_perm
@@ -49,6 +53,7 @@ __all__ = [
     "dual_bound",
     "gather",
     "greedy_argmax",
+    "greedy_completion",
     "objective",
     "optimum_gap",
     "scatter",
@@ -56,4 +61,5 @@ __all__ = [
     "solve_hungarian",
     "solve_ssp",
     "stable_perm",
+    "stable_perm_partial",
 ]

@@ -176,6 +176,56 @@ def greedy_argmax(S: np.ndarray) -> np.ndarray:
     return np.asarray(S).argmax(axis=1).astype(np.int32)
 
 
+def greedy_completion(S: np.ndarray, a: np.ndarray, p: np.ndarray) -> np.ndarray:
+    """The balance-keeping completion of a solve stopped by its round bound.
+
+    Not a step of the paper: the bounded-latency mode's reading of how to end
+    a solve early and still give every expert exactly C = T/E tokens (the
+    paper's balance constraint, Eq. 2). Every token still unassigned (a_t <
+    0), in ascending token order, takes the expert with room (fewer than C
+    tokens at that moment) that maximises S[t, e] - p[e], ties to the lowest
+    expert. The difference decides an index, so it is taken in the precision
+    the solver uses: float32 for float scores and prices, exact int64 for
+    integer ones. Returns the completed assignment (a copy)."""
+    S = np.asarray(S)
+    T, E, C = _check_shape(S)
+    out = np.asarray(a, dtype=np.int64).copy()
+    p = np.asarray(p)
+    if np.issubdtype(S.dtype, np.integer):
+        V = S.astype(np.int64) - p.astype(np.int64)[None, :]
+    else:
+        V = S.astype(np.float32) - p.astype(np.float32)[None, :]
+    count = np.bincount(out[out >= 0], minlength=E)
+    for t in range(T):
+        if out[t] >= 0:
+            continue
+        best, best_e = None, -1
+        for e in range(E):
+            if count[e] < C and (best is None or V[t, e] > best):
+                best, best_e = V[t, e], e
+        if best_e < 0:
+            raise ValueError("no expert has room for an unassigned token")
+        out[t] = best_e
+        count[best_e] += 1
+    return out.astype(np.int32)
+
+
+def stable_perm_partial(a: np.ndarray, E: int) -> np.ndarray:
+    """The sort vector of a possibly incomplete assignment (a_t < 0 for
+    unassigned tokens): rows [e C, (e + 1) C) hold expert e's tokens in
+    ascending order, then -1 for every row the expert has no token for."""
+    a = np.asarray(a, dtype=np.int64)
+    T = a.shape[0]
+    C = T // E
+    out = np.full(T, -1, dtype=np.int32)
+    for e in range(E):
+        toks = np.flatnonzero(a == e)
+        if toks.shape[0] > C:
+            raise ValueError(f"expert {e} holds more than {C} tokens")
+        out[e * C:e * C + toks.shape[0]] = toks
+    return out
+
+
 def optimum_gap(S: np.ndarray, a: np.ndarray) -> float:
     """Second-best gap of an optimal balanced assignment a.
 

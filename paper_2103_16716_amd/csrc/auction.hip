@@ -36,6 +36,10 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <map>
+#include <mutex>
+#include <tuple>
+
 #include "common.hpp"
 #include "internal.hpp"
 #include "base.h"
@@ -46,6 +50,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kCandLds = 4096;   // candidates of one expert staged in LDS when they fit
 constexpr int kRangeBlocks = 256;   // blocks of the score-range reduction
+constexpr int kPrologueBlocks = 4096;   // largest grid of the prologue (one range partial each)
 constexpr int kCountTile = 256;  // tokens per block in the permutation build
 constexpr int kWideLoopRounds = 1024;  // rounds one launch of the round loop may run
 constexpr int kCheckBlocks = 4096;     // largest grid of the phase check
@@ -117,7 +122,7 @@ Layout make_layout(int64_t T, int64_t E) {
     L.ecn = off;     off += align_up((size_t)E * 4);
     L.sums = off;    off += align_up((size_t)T * 64);          // per-token score summaries
     L.bar = off;     off += align_up(512);                      // grid barrier words
-    L.rpart = off;   off += align_up((size_t)kRangeBlocks * 12);   // score-range partials
+    L.rpart = off;   off += align_up((size_t)kPrologueBlocks * 12);   // score-range partials
     L.gpart = off;   off += align_up((size_t)kCheckBlocks * 8);    // phase-check partials
     // The exchange matrix of the shortest-path finish (E <= 256 only):
     // cheapest move from expert e to expert x and the slot of its token.
@@ -485,12 +490,53 @@ __device__ __attribute__((always_inline)) inline void group_max(typename M::valu
     if constexpr (G > 32) max_step<32, M>(bv, be);
 }
 
-// One group of G lanes per token: 9 rounds of a group maximum (ties to the
-// lowest expert) over the lanes' 8 scores each.
+// A fresh control block and the starting prices of problem b: 0, or the
+// caller's (warm start: prices only rise from any starting point, which
+// keeps every bid's complementary slackness argument intact). Called by one
+// block; prices may be NULL (control block only).
+__device__ inline void init_problem(SolveCtrl *ctrl, void *prices, int E, const AssignParams &p,
+                                    int b) {
+    if (threadIdx.x == 0) {
+        SolveCtrl z{};
+        z.smax_ord = 0u;
+        z.smin_ord = 0xffffffffu;
+        z.eps_final_eff = p.eps_final;
+        z.scale = p.scale;
+        z.integer = p.integer ? 1 : 0;
+        *ctrl = z;
+    }
+    if (prices == nullptr) return;
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        if (p.warm_prices == nullptr) {
+            reinterpret_cast<int64_t *>(prices)[e] = 0;
+        } else if (p.integer) {
+            reinterpret_cast<int64_t *>(prices)[e] =
+                reinterpret_cast<const int64_t *>(p.warm_prices)[(int64_t)b * E + e];
+        } else {
+            reinterpret_cast<float *>(prices)[e] =
+                reinterpret_cast<const float *>(p.warm_prices)[(int64_t)b * E + e];
+        }
+    }
+}
+
+// The first kernel of a solve, one group of G lanes per token:
+//   - the token's score summary: 9 rounds of a group maximum (ties to the
+//     lowest expert) over the lanes' 8 scores each;
+//   - the score range and a non-finite flag over the same loaded scores, one
+//     partial (max, min, bad) per block in rpart[3 * block] (start_kernel
+//     combines them);
+//   - assign[t] = -1 (the finalising kernels write every held token);
+//   - in block 0, a fresh control block and the starting prices.
 template <class M, int G>
-__global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
+__global__ __launch_bounds__(kThreads) void prologue_kernel(Ctx<M> c0, AssignParams p,
+                                                            int32_t *assign, uint32_t *rpart) {
     const Ctx<M> c = c0.at(blockIdx.y);
     using value_t = typename M::value_t;
+    if (blockIdx.x == 0) init_problem(c.ctrl, c.prices, c.E, p, blockIdx.y);
+    assign += (int64_t)blockIdx.y * c.T;
+    rpart = Ctx<M>::shift(rpart, (int64_t)blockIdx.y * c.ws_stride);
+    uint32_t rmx = 0u, rmn = 0xffffffffu;
+    int rbad = 0;
     const int lane = lane_id();
     const int gl = lane & (G - 1);
     const int per_block = kThreads / G;
@@ -510,9 +556,27 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
             for (int q = 0; q < 8; ++q) sv[ch][q] = M::lowest();
             if (valid && e0 < c.E) load8<M>(c.S, (int64_t)t * c.E, e0, c.E, c.scale, sv[ch]);
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
-                if (e0 + q >= c.E) sv[ch][q] = M::lowest();
+            for (int q = 0; q < 8; ++q) {
+                if (e0 + q >= c.E) {
+                    sv[ch][q] = M::lowest();
+                } else if (valid) {
+                    // range over order-preserving images; non-finite
+                    // scores only raise the flag
+                    bool fin = true;
+                    uint32_t o;
+                    if constexpr (M::kInteger) {
+                        o = (uint32_t)(int32_t)(sv[ch][q] / c.scale) ^ 0x80000000u;
+                    } else {
+                        fin = isfinite(sv[ch][q]);
+                        o = f32_ord(sv[ch][q]);
+                    }
+                    rbad |= !fin;
+                    rmx = (fin && o > rmx) ? o : rmx;
+                    rmn = (fin && o < rmn) ? o : rmn;
+                }
+            }
         }
+        if (valid && gl == 0) assign[t] = -1;
         uint32_t *out = c.sums + (int64_t)(valid ? t : 0) * kSumWords;
         uint32_t pairs[4] = {0, 0, 0, 0};
         for (int r = 0; r <= take; ++r) {
@@ -551,6 +615,32 @@ __global__ __launch_bounds__(kThreads) void summary_kernel(Ctx<M> c0) {
             for (int q = 0; q < 4; ++q) out[8 + q] = pairs[q];
             out[13] = (uint32_t)take;
         }
+    }
+    // The block's range partial.
+    __shared__ uint32_t smx[kThreads / 64], smn[kThreads / 64];
+    __shared__ int sbad[kThreads / 64];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t a = __shfl_xor(rmx, off), b = __shfl_xor(rmn, off);
+        rmx = a > rmx ? a : rmx;
+        rmn = b < rmn ? b : rmn;
+        rbad |= __shfl_xor(rbad, off);
+    }
+    if (lane == 0) {
+        smx[threadIdx.x >> 6] = rmx;
+        smn[threadIdx.x >> 6] = rmn;
+        sbad[threadIdx.x >> 6] = rbad;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < kThreads / 64; ++w) {
+            rmx = smx[w] > rmx ? smx[w] : rmx;
+            rmn = smn[w] < rmn ? smn[w] : rmn;
+            rbad |= sbad[w];
+        }
+        rpart[3 * blockIdx.x] = rmx;
+        rpart[3 * blockIdx.x + 1] = rmn;
+        rpart[3 * blockIdx.x + 2] = (uint32_t)rbad;
     }
 }
 
@@ -1142,31 +1232,7 @@ __global__ void init_kernel(SolveCtrl *ctrl, void *prices, int E, AssignParams p
                             int64_t ws_stride) {
     ctrl = Ctx<FloatMode>::shift(ctrl, (int64_t)blockIdx.y * ws_stride);
     if (prices != nullptr) prices = Ctx<FloatMode>::shift(prices, (int64_t)blockIdx.y * ws_stride);
-    const int tid = threadIdx.x;
-    if (tid == 0) {
-        SolveCtrl z{};
-        z.smax_ord = 0u;
-        z.smin_ord = 0xffffffffu;
-        z.eps_final_eff = p.eps_final;
-        z.scale = p.scale;
-        z.integer = p.integer ? 1 : 0;
-        *ctrl = z;
-    }
-    if (prices == nullptr) return;
-    // Prices start at 0, or at the caller's (warm start: prices only rise
-    // from any starting point, which keeps every bid's complementary
-    // slackness argument intact).
-    for (int e = tid; e < E; e += blockDim.x) {
-        if (p.warm_prices == nullptr) {
-            reinterpret_cast<int64_t *>(prices)[e] = 0;
-        } else if (p.integer) {
-            reinterpret_cast<int64_t *>(prices)[e] =
-                reinterpret_cast<const int64_t *>(p.warm_prices)[(int64_t)blockIdx.y * E + e];
-        } else {
-            reinterpret_cast<float *>(prices)[e] =
-                reinterpret_cast<const float *>(p.warm_prices)[(int64_t)blockIdx.y * E + e];
-        }
-    }
+    init_problem(ctrl, prices, E, p, blockIdx.y);
 }
 
 // Score range (order-preserving images) and a non-finite flag: each block
@@ -1278,21 +1344,6 @@ __global__ __launch_bounds__(256) void range_finish_kernel(SolveCtrl *ctrl, cons
         ctrl->smin_ord = mn < ctrl->smin_ord ? mn : ctrl->smin_ord;
         if (bad) ctrl->unconverged_experts |= 1 << 30;
     }
-}
-
-// Float mode: raise eps_final so that it stays far above fp32 rounding at the
-// magnitude prices and bids reach (scores plus a few score ranges).
-__global__ void eps_floor_kernel(SolveCtrl *ctrl, int integer, int64_t ws_stride) {
-    ctrl = Ctx<FloatMode>::shift(ctrl, (int64_t)blockIdx.y * ws_stride);
-    if (integer) {
-        ctrl->eps_final_eff = 1.0;
-        return;
-    }
-    const double smax = (double)f32_unord(ctrl->smax_ord);
-    const double smin = (double)f32_unord(ctrl->smin_ord);
-    const double mag = fmax(fabs(smax), fabs(smin)) + 3.0 * (smax - smin) + 1e-30;
-    const double floor_eps = ldexp(mag, -20);
-    if (ctrl->eps_final_eff < floor_eps) ctrl->eps_final_eff = floor_eps;
 }
 
 // ------------------------------------------------------------ phase check --
@@ -1464,6 +1515,67 @@ __global__ void phase_begin_kernel(Ctx<M> c0, AssignParams p, int nparts) {
     }
     __syncthreads();
     if (!begin) return;
+    for (int e = threadIdx.x; e < c.E; e += blockDim.x) {
+        c.hcount[e] = 0;
+        c.hsel[e] = 0;
+        c.bcount[e] = 0;
+    }
+}
+
+// The second kernel of a solve (one block per problem): the score range from
+// the prologue's nparts partials (and the non-finite flag), the floor of
+// eps_final in float mode, and the first epsilon phase.
+template <class M>
+__global__ __launch_bounds__(256) void start_kernel(Ctx<M> c0, AssignParams p, const uint32_t *rpart,
+                                                    int nparts) {
+    const Ctx<M> c = c0.at(blockIdx.y);
+    SolveCtrl *ctrl = c.ctrl;
+    rpart = Ctx<M>::shift(rpart, (int64_t)blockIdx.y * c.ws_stride);
+    __shared__ uint32_t smx[4], smn[4], sbad[4];
+    uint32_t mx = 0u, mn = 0xffffffffu, bad = 0u;
+    for (int i = threadIdx.x; i < nparts; i += blockDim.x) {
+        mx = rpart[3 * i] > mx ? rpart[3 * i] : mx;
+        mn = rpart[3 * i + 1] < mn ? rpart[3 * i + 1] : mn;
+        bad |= rpart[3 * i + 2];
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t a = __shfl_xor(mx, off), b = __shfl_xor(mn, off);
+        mx = a > mx ? a : mx;
+        mn = b < mn ? b : mn;
+        bad |= __shfl_xor(bad, off);
+    }
+    const int wave = threadIdx.x >> 6;
+    if (lane_id() == 0) {
+        smx[wave] = mx;
+        smn[wave] = mn;
+        sbad[wave] = bad;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < (int)(blockDim.x >> 6); ++w) {
+            mx = smx[w] > mx ? smx[w] : mx;
+            mn = smn[w] < mn ? smn[w] : mn;
+            bad |= sbad[w];
+        }
+        ctrl->smax_ord = mx;
+        ctrl->smin_ord = mn;
+        if (bad) ctrl->unconverged_experts |= 1 << 30;
+        if (M::kInteger) {
+            ctrl->eps_final_eff = 1.0;
+        } else {
+            // Raise eps_final so that it stays far above fp32 rounding at the
+            // magnitude prices and bids reach (scores plus a few score ranges).
+            const double smax = (double)f32_unord(mx);
+            const double smin = (double)f32_unord(mn);
+            const double mag = fmax(fabs(smax), fabs(smin)) + 3.0 * (smax - smin) + 1e-30;
+            const double floor_eps = ldexp(mag, -20);
+            if (ctrl->eps_final_eff < floor_eps) ctrl->eps_final_eff = floor_eps;
+        }
+        c.bar[0] = 0;    // the round loop's barrier counts from zero in every launch
+        c.bar[32] = 0;
+        begin_phase_scalar(ctrl, p, c.T);
+    }
     for (int e = threadIdx.x; e < c.E; e += blockDim.x) {
         c.hcount[e] = 0;
         c.hsel[e] = 0;
@@ -3406,11 +3518,44 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
 
 // ------------------------------------------------------------- finalising --
 
-// assign[t] = e for every held token; counts experts that are not full.
+// The finalising kernels write assign and perm from the holder tables. An
+// expert's rows of perm are its tokens in ascending order; with at most
+// kRankMaxC tokens per expert they are ranked in LDS, expert by expert
+// (larger C takes the counting sort below over assign instead).
+constexpr int kRankMaxC = 1024;
+
+// out[rank of tok[i] among tok[0..n)] = tok[i] (ascending order for distinct
+// tokens). tok has room for n rounded up to 4; entries from n on are padded
+// here. rank < n whatever the values, so the writes stay in out[0..n).
+__device__ inline void rank_write(int *tok, int n, int32_t *out) {
+    const int n4 = (n + 3) & ~3;
+    for (int i = n + (int)threadIdx.x; i < n4; i += blockDim.x) tok[i] = 0x7fffffff;
+    __syncthreads();
+    const int4 *t4 = reinterpret_cast<const int4 *>(tok);
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+        const int t = tok[i];
+        int r = 0;
+        for (int j = 0; j < n4 / 4; ++j) {
+            const int4 q = t4[j];
+            r += (q.x < t) + (q.y < t) + (q.z < t) + (q.w < t);
+        }
+        out[r] = t;
+    }
+    __syncthreads();
+}
+
+// One block per expert: assign[t] = e for every held token (the prologue set
+// every entry to -1), the expert's rows of perm when it is full and C <=
+// kRankMaxC, its price into prices_out (when not NULL), and a count of the
+// experts that are not full.
 template <class M>
-__global__ void holders_to_assign_kernel(Ctx<M> c0, int32_t *assign) {
+__global__ __launch_bounds__(256) void finalise_kernel(Ctx<M> c0, int32_t *assign, int32_t *perm,
+                                                       typename M::value_t *prices_out,
+                                                       int rank_perm) {
     const Ctx<M> c = c0.at(blockIdx.y);
     assign += (int64_t)blockIdx.y * c.T;
+    perm += (int64_t)blockIdx.y * c.T;
+    __shared__ __align__(16) int tok[kRankMaxC];
     const int e = blockIdx.x;
     int h = c.hcount[e];
     if (h < 0 || h > c.C) {
@@ -3418,12 +3563,21 @@ __global__ void holders_to_assign_kernel(Ctx<M> c0, int32_t *assign) {
         h = h < 0 ? 0 : c.C;
     }
     const uint64_t *hold = c.holders + (int64_t)(c.hsel[e] & 1) * c.T + (int64_t)e * c.C;
+    const bool ranked = rank_perm && h == c.C;
     for (int i = threadIdx.x; i < h; i += blockDim.x) {
         const int t = key_token(hold[i]);
-        if (t >= 0 && t < c.T) assign[t] = e;
+        const bool ok = t >= 0 && t < c.T;
+        if (ok) assign[t] = e;
         else flag_internal(c.ctrl);
+        if (ranked) tok[i] = ok ? t : 0x7fffffff;
     }
-    if (threadIdx.x == 0 && h != c.C) atomicAdd(&c.ctrl->unconverged_experts, 1);
+    if (threadIdx.x == 0) {
+        if (h != c.C) atomicAdd(&c.ctrl->unconverged_experts, 1);
+        if (prices_out != nullptr) prices_out[(int64_t)blockIdx.y * c.E + e] = c.prices[e];
+    }
+    if (!ranked) return;
+    __syncthreads();
+    rank_write(tok, h, perm + (int64_t)e * c.C);
 }
 
 int lanes_per_token(int64_t E);
@@ -3492,51 +3646,239 @@ hipError_t launch_dual_gap(const Ctx<M> &c, int B, const int32_t *assign, hipStr
     return hipGetLastError();
 }
 
-// Greedy completion after max_rounds (one block, sequential in token order):
-// every still-unassigned token takes its best expert among those with room.
+// Wave-wide maximum of (v, i), ties to the lower i; every lane ends with it.
+template <class V>
+__device__ inline V readlane_v(V v, int l) {
+    if constexpr (sizeof(V) == 8) {
+        uint64_t u;
+        __builtin_memcpy(&u, &v, 8);
+        const uint64_t r = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l) |
+                           ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l)
+                            << 32);
+        V out;
+        __builtin_memcpy(&out, &r, 8);
+        return out;
+    } else {
+        uint32_t u;
+        __builtin_memcpy(&u, &v, 4);
+        const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)u, l);
+        V out;
+        __builtin_memcpy(&out, &r, 4);
+        return out;
+    }
+}
+template <int OFF, class V>
+__device__ __attribute__((always_inline)) inline void max_pair_step(V &v, int &i) {
+    const V ov = grp_partner<OFF>(v);
+    const int oi = grp_partner<OFF>(i);
+    const bool t = (ov > v) | ((ov == v) & (oi < i));
+    v = t ? ov : v;
+    i = t ? oi : i;
+}
+template <class V>
+__device__ inline void wave_max_pair(V &v, int &i) {
+    max_pair_step<1>(v, i);
+    max_pair_step<2>(v, i);
+    max_pair_step<4>(v, i);
+    max_pair_step<8>(v, i);
+    V rv = readlane_v(v, 0);
+    int ri = __builtin_amdgcn_readlane(i, 0);
+#pragma unroll
+    for (int q = 1; q < 4; ++q) {
+        const V ov = readlane_v(v, 16 * q);
+        const int oi = __builtin_amdgcn_readlane(i, 16 * q);
+        const bool t = (ov > rv) | ((ov == rv) & (oi < ri));
+        rv = t ? ov : rv;
+        ri = t ? oi : ri;
+    }
+    v = rv;
+    i = ri;
+}
+
+constexpr int kCompThreads = 1024;
+constexpr int kCompStageBytes = 32 * 1024;   // score rows staged per step of the greedy walk
+constexpr int kCompMaxRows = 256;
+constexpr int kCompRegs = 2048 / 64;         // experts per lane of the walking wave (E <= 2048)
+
+__host__ __device__ inline int comp_rows(int E, int vbytes) {
+    int r = kCompStageBytes / (E * vbytes);
+    return r < 1 ? 1 : (r > kCompMaxRows ? kCompMaxRows : r);
+}
+__host__ __device__ inline size_t a16(size_t x) { return (x + 15) & ~size_t(15); }
+inline size_t comp_lds_bytes(int E, int vbytes) {
+    const int R = comp_rows(E, vbytes);
+    size_t stage = (size_t)R * E * vbytes;
+    if (stage < (size_t)kRankMaxC * 4) stage = (size_t)kRankMaxC * 4;
+    return a16((size_t)E * vbytes) + a16((size_t)E * 4) + a16((size_t)R * 4) + stage;
+}
+
+// After the finalising kernel, when some expert is not full (one block per
+// problem; returns at once otherwise):
+//   - with BASE_ASSIGN_GREEDY_FALLBACK, after max_rounds: the greedy
+//     completion. Every still-unassigned token, in ascending token order,
+//     takes its best expert by S[t,e] - p[e] (ties to the lowest expert)
+//     among those with room. The unassigned tokens are first compacted into
+//     a list (all threads); then their score rows are staged in LDS (all
+//     threads) and one wave walks them in order, keeping the experts' counts
+//     in registers. The walk's result is the sequential rule's, token by
+//     token. Placed tokens join their expert's holder table.
+//   - the rows of perm of every expert that was not full: its tokens in
+//     ascending order (when C <= kRankMaxC), then -1 for the rows it has no
+//     token for (an unconverged solve without the greedy completion).
 template <class M>
-__global__ void greedy_fill_kernel(Ctx<M> c0, int32_t *assign, uint32_t flags) {
+__global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32_t *assign,
+                                                                int32_t *perm, uint32_t flags,
+                                                                int rank_perm) {
+    using value_t = typename M::value_t;
     const Ctx<M> c = c0.at(blockIdx.y);
     assign += (int64_t)blockIdx.y * c.T;
-    using value_t = typename M::value_t;
+    perm += (int64_t)blockIdx.y * c.T;
     SolveCtrl *ctrl = c.ctrl;
-    if (!ctrl->not_converged || !(flags & BASE_ASSIGN_GREEDY_FALLBACK) || ctrl->internal_error)
-        return;
-    __shared__ int room_left;
-    if (threadIdx.x == 0) {
-        ctrl->fell_back = 1;
-        ctrl->unconverged_experts &= (1 << 30);
+    if ((ld_relaxed(&ctrl->unconverged_experts) & ~(1 << 30)) == 0) return;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    const int E = c.E, C = c.C, T = c.T;
+    const int R = comp_rows(E, (int)sizeof(value_t));
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
+    int *hc0 = reinterpret_cast<int *>(smem_raw + a16((size_t)E * sizeof(value_t)));
+    int *stok = reinterpret_cast<int *>(reinterpret_cast<unsigned char *>(hc0) + a16((size_t)E * 4));
+    value_t *vst = reinterpret_cast<value_t *>(reinterpret_cast<unsigned char *>(stok) + a16((size_t)R * 4));
+    int *tok = reinterpret_cast<int *>(vst);   // the ranking's list (after the walk)
+    int *hc1 = reinterpret_cast<int *>(pr);    // counts after the walk (prices no longer needed)
+    __shared__ int s_fill, s_n, s_wsum[kCompThreads / 64];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    for (int e = tid; e < E; e += kCompThreads) {
+        pr[e] = c.prices[e];
+        int h = c.hcount[e];
+        hc0[e] = h < 0 ? 0 : (h > C ? C : h);
     }
-    // One wave scans tokens in ascending order.
-    if (threadIdx.x >= 64) return;
-    for (int t = 0; t < c.T; ++t) {
-        if (assign[t] >= 0) continue;
-        value_t best = M::lowest();
-        int be = 0x7fffffff;
-        for (int e = threadIdx.x; e < c.E; e += 64) {
-            if (c.hcount[e] >= c.C) continue;
-            const value_t v = M::load(c.S, (int64_t)t * c.E + e, c.scale) - c.prices[e];
-            if (v > best || (v == best && e < be)) {
-                best = v;
-                be = e;
-            }
+    if (tid == 0) {
+        s_fill = ctrl->not_converged && (flags & BASE_ASSIGN_GREEDY_FALLBACK) &&
+                 !ctrl->internal_error;
+        if (s_fill) {
+            ctrl->fell_back = 1;
+            ctrl->unconverged_experts &= (1 << 30);
         }
+    }
+    __syncthreads();
+    if (s_fill) {
+        // The unassigned tokens, in ascending order, into the (no longer
+        // used) first active list: thread i counts its contiguous share,
+        // a block scan gives each share its offset.
+        int *list = c.active;
+        const int per = (T + kCompThreads - 1) / kCompThreads;
+        const int lo = tid * per < T ? tid * per : T;
+        const int hi = lo + per < T ? lo + per : T;
+        int cnt = 0;
+        for (int t = lo; t < hi; ++t) cnt += assign[t] < 0;
+        int incl = cnt;
 #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-            const value_t ob = __shfl_xor(best, off);
-            const int oe = __shfl_xor(be, off);
-            if (ob > best || (ob == best && oe < be)) {
-                best = ob;
-                be = oe;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(incl, off);
+            if (lane >= off) incl += o;
+        }
+        if (lane == 63) s_wsum[wave] = incl;
+        __syncthreads();
+        int before = 0;
+        for (int w = 0; w < wave; ++w) before += s_wsum[w];
+        if (tid == kCompThreads - 1) s_n = before + incl;
+        int at = before + incl - cnt;
+        for (int t = lo; t < hi; ++t)
+            if (assign[t] < 0) list[at++] = t;
+        __syncthreads();
+        const int n = s_n;
+        // The walking wave's experts: lane l holds experts l + 64 k.
+        int cntr[kCompRegs];
+        uint32_t selm = 0;
+        if (wave == 0) {
+#pragma unroll
+            for (int k = 0; k < kCompRegs; ++k) {
+                const int e = lane + 64 * k;
+                cntr[k] = e < E ? hc0[e] : C;
+                if (e < E) selm |= (uint32_t)(c.hsel[e] & 1) << k;
             }
         }
-        if (threadIdx.x == 0 && be < c.E) {
-            assign[t] = be;
-            c.hcount[be] += 1;
+        for (int j0 = 0; j0 < n; j0 += R) {
+            const int m = n - j0 < R ? n - j0 : R;
+            for (int r = tid; r < m; r += kCompThreads) {
+                const int t = list[j0 + r];
+                stok[r] = (t >= 0 && t < T) ? t : 0;
+            }
+            __syncthreads();
+            for (int q = tid; q < m * E; q += kCompThreads) {
+                const int r = q / E;
+                const int e = q - r * E;
+                vst[q] = M::load(c.S, (int64_t)stok[r] * E + e, c.scale) - pr[e];
+            }
+            __syncthreads();
+            if (wave == 0) {
+                for (int r = 0; r < m; ++r) {
+                    value_t bv = M::lowest();
+                    int be = 0x7fffffff;
+#pragma unroll
+                    for (int k = 0; k < kCompRegs; ++k) {
+                        if (64 * k >= E) break;
+                        const int e = lane + 64 * k;
+                        if (e < E && cntr[k] < C) {
+                            const value_t v = vst[r * E + e];
+                            if (v > bv) {
+                                bv = v;
+                                be = e;
+                            }
+                        }
+                    }
+                    wave_max_pair(bv, be);
+                    if (be < E) {
+                        const int t = stok[r];
+                        if (lane == (be & 63)) {
+                            const int kk = be >> 6;
+                            int slot = 0;
+#pragma unroll
+                            for (int k = 0; k < kCompRegs; ++k) {
+                                if (k == kk) {
+                                    slot = cntr[k];
+                                    cntr[k] = slot + 1;
+                                }
+                            }
+                            const int sel = (selm >> kk) & 1;
+                            c.holders[(int64_t)sel * T + (int64_t)be * C + slot] =
+                                (1ull << kTokBits) | (kTokMask - (uint64_t)t);
+                        }
+                        if (lane == 0) assign[t] = be;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+        if (wave == 0) {
+#pragma unroll
+            for (int k = 0; k < kCompRegs; ++k) {
+                const int e = lane + 64 * k;
+                if (e < E) {
+                    c.hcount[e] = cntr[k];
+                    hc1[e] = cntr[k];
+                }
+            }
         }
         __threadfence_block();
+        __syncthreads();
     }
-    (void)room_left;
+    for (int e = 0; e < E; ++e) {
+        if (hc0[e] >= C) continue;   // (uniform: LDS)
+        int h = s_fill ? hc1[e] : hc0[e];
+        h = h > C ? C : h;
+        int32_t *out = perm + (int64_t)e * C;
+        if (rank_perm) {
+            const uint64_t *hold = c.holders + (int64_t)(c.hsel[e] & 1) * T + (int64_t)e * C;
+            for (int i = tid; i < h; i += kCompThreads) {
+                const int t = key_token(hold[i]);
+                tok[i] = (t >= 0 && t < T) ? t : 0x7fffffff;
+            }
+            rank_write(tok, h, out);
+        }
+        for (int i = h + tid; i < C; i += kCompThreads) out[i] = -1;
+    }
 }
 
 // Per block of kCountTile tokens: how many go to each expert.
@@ -3658,72 +4000,125 @@ void timing_pair(hipEvent_t *begin, hipEvent_t *end) {
     ++g_timing.used;
 }
 
+// Per-device facts the launches depend on, looked up once per device (and
+// per kernel and LDS size): the LDS a block may opt in to, the compute
+// units, a kernel's resident blocks per compute unit, and the LDS opt-in
+// already granted to a kernel.
+constexpr int kMaxDevices = 64;
+struct DeviceFacts {
+    bool known = false;
+    int optin = 0;
+    int cus = 0;
+};
+std::mutex g_facts_mutex;
+DeviceFacts g_facts[kMaxDevices];
+std::map<std::tuple<int, const void *, int, size_t>, int> g_occupancy;
+std::map<std::pair<int, const void *>, size_t> g_lds_granted;
+
+// The current device and its facts (optin falls back to 64 KiB, cus to 0
+// when the runtime cannot tell).
+int device_facts(DeviceFacts *f) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        (void)hipGetLastError();
+        *f = DeviceFacts{true, 64 * 1024, 0};
+        return -1;
+    }
+    std::lock_guard<std::mutex> lock(g_facts_mutex);
+    if (!g_facts[dev].known) {
+        DeviceFacts d;
+        d.known = true;
+        if (hipDeviceGetAttribute(&d.optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) !=
+                hipSuccess ||
+            d.optin <= 0)
+            d.optin = 64 * 1024;
+        if (hipDeviceGetAttribute(&d.cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            d.cus = 0;
+        (void)hipGetLastError();
+        g_facts[dev] = d;
+    }
+    *f = g_facts[dev];
+    return dev;
+}
+
+// Resident blocks per compute unit of kernel fn (0 when unknown).
+int occupancy(int dev, const void *fn, int threads, size_t lds) {
+    std::lock_guard<std::mutex> lock(g_facts_mutex);
+    const auto key = std::make_tuple(dev, fn, threads, lds);
+    const auto it = g_occupancy.find(key);
+    if (it != g_occupancy.end()) return it->second;
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, lds) != hipSuccess)
+        per_cu = 0;
+    (void)hipGetLastError();
+    if (dev >= 0) g_occupancy[key] = per_cu;
+    return per_cu;
+}
+
+// Lets kernel fn take `bytes` of dynamic LDS (above the default 64 KiB); the
+// attribute is set again only for a larger size than granted before.
+hipError_t lds_optin(int dev, const void *fn, size_t bytes) {
+    if (bytes <= 64 * 1024) return hipSuccess;
+    std::lock_guard<std::mutex> lock(g_facts_mutex);
+    const auto key = std::make_pair(dev, fn);
+    const auto it = g_lds_granted.find(key);
+    if (dev >= 0 && it != g_lds_granted.end() && it->second >= bytes) return hipSuccess;
+    const hipError_t err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (err == hipSuccess && dev >= 0) g_lds_granted[key] = bytes;
+    return err;
+}
+
 template <class M, int G>
-hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t s) {
+hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *assign,
+                     uint32_t *rpart, hipStream_t s) {
     using value_t = typename M::value_t;
     Ctx<M> c = c0;
+    DeviceFacts facts;
+    const int dev = device_facts(&facts);
     // The engine's LDS: the longest per-expert lists that fit the device's
     // per-block limit (with the opt-in above the default 64 KiB).
     bool engine = c.E <= kEngMaxE && c.C <= kEngMaxC;
     size_t eng_bytes = 0;
     if (engine) {
-        int dev = 0, optin = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) != hipSuccess ||
-            optin <= 0)
-            optin = 64 * 1024;
-        const size_t limit = (size_t)optin - 1024;   // room for the kernel's static LDS
+        const size_t limit = (size_t)facts.optin - 1024;   // room for the kernel's static LDS
         int K = kEngMaxK;
         while (K >= 8 && eng_layout(c.E, (int)sizeof(value_t), K).total > limit) K >>= 1;
         if (K < 8) {
             engine = false;
         } else {
             eng_bytes = eng_layout(c.E, (int)sizeof(value_t), K).total;
-            if (eng_bytes > 64 * 1024) {
-                const hipError_t err = hipFuncSetAttribute(
-                    reinterpret_cast<const void *>(&engine_kernel<M, G>),
-                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)eng_bytes);
-                if (err != hipSuccess) {
-                    (void)hipGetLastError();
-                    debug_note("engine LDS opt-in refused", err);
-                    while (K >= 8 && eng_layout(c.E, (int)sizeof(value_t), K).total > 64 * 1024)
-                        K >>= 1;
-                    engine = K >= 8;
-                    if (engine) eng_bytes = eng_layout(c.E, (int)sizeof(value_t), K).total;
-                }
+            const hipError_t err = lds_optin(
+                dev, reinterpret_cast<const void *>(&engine_kernel<M, G>), eng_bytes);
+            if (err != hipSuccess) {
+                (void)hipGetLastError();
+                debug_note("engine LDS opt-in refused", err);
+                while (K >= 8 && eng_layout(c.E, (int)sizeof(value_t), K).total > 64 * 1024)
+                    K >>= 1;
+                engine = K >= 8;
+                if (engine) eng_bytes = eng_layout(c.E, (int)sizeof(value_t), K).total;
             }
             c.eng_k = K;
         }
     }
     if (engine) c.engine_cap = kEngCap;
-    // The shortest-path finish (float mode, E <= 256, with the engine): the
-    // most unassigned tokens it takes over, as many as its LDS allows.
+    // The shortest-path finish (float mode, E <= kSspMaxE, with the engine):
+    // the most unassigned tokens it takes over, as many as its LDS allows.
     size_t ssp_bytes = 0;
     int ssp_r = 0;
     if constexpr (!M::kInteger) {
         int cap = ssp_cap_setting();
         if (engine && c.E <= kSspMaxE && c.T <= 65536 && cap > 0) {
-            int optin = 0, dev = 0;
-            if (hipGetDevice(&dev) != hipSuccess ||
-                hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) !=
-                    hipSuccess ||
-                optin <= 0)
-                optin = 64 * 1024;
-            const size_t limit = (size_t)optin - 2048;   // the kernel's static LDS
+            const size_t limit = (size_t)facts.optin - 2048;   // the kernel's static LDS
             if (cap > kSspMaxCap) cap = kSspMaxCap;
             if (cap < kSspMinCap) cap = kSspMinCap;
             while (cap >= kSspMinCap && ssp_lds_bytes(c.E, cap, c.C) > limit) cap >>= 1;
             if (cap >= kSspMinCap) {
                 ssp_r = ssp_pad(c.E);
                 ssp_bytes = ssp_lds_bytes(c.E, cap, c.C);
-                hipError_t err = hipSuccess;
-                if (ssp_bytes > 64 * 1024) {
-                    const void *fn = ssp_r == 32   ? reinterpret_cast<const void *>(&ssp_kernel<M, 32>)
-                                     : ssp_r == 64 ? reinterpret_cast<const void *>(&ssp_kernel<M, 64>)
-                                                   : reinterpret_cast<const void *>(&ssp_kernel<M, 128>);
-                    err = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                              (int)ssp_bytes);
-                }
+                const void *fn = ssp_r == 32   ? reinterpret_cast<const void *>(&ssp_kernel<M, 32>)
+                                 : ssp_r == 64 ? reinterpret_cast<const void *>(&ssp_kernel<M, 64>)
+                                               : reinterpret_cast<const void *>(&ssp_kernel<M, 128>);
+                const hipError_t err = lds_optin(dev, fn, ssp_bytes);
                 if (err == hipSuccess) {
                     c.ssp_cap = cap;
                 } else {
@@ -3734,6 +4129,14 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
             }
         }
     }
+    // The prologue (score summaries, range partials, assign = -1, a fresh
+    // control block and starting prices) and the start of the first phase.
+    const int per_block = kThreads / G;
+    int sblocks = (int)((c.T + per_block - 1) / per_block);
+    if (sblocks > kPrologueBlocks) sblocks = kPrologueBlocks;
+    hipLaunchKernelGGL((prologue_kernel<M, G>), dim3(sblocks, B), dim3(kThreads), 0, s, c, p,
+                       assign, rpart);
+    hipLaunchKernelGGL(start_kernel<M>, dim3(1, B), dim3(256), 0, s, c, p, rpart, sblocks);
     const size_t pr_bytes = (size_t)c.E * sizeof(value_t);
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
     // Phase slots enqueued up front; the last one continues on its own (in
@@ -3754,15 +4157,9 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
         }
     }
     const int wide_rounds = engine ? 3 : 2;
-    const int per_block = kThreads / G;
     const int bid_blocks = (int)((c.T + kBidTile - 1) / kBidTile);   // one tile of the list each
     const size_t bid_bytes = bid_smem(c.E, (int)sizeof(value_t)).total;
     int upd_blocks = c.E < 2048 ? c.E : 2048;
-    {
-        int sblocks = (int)((c.T + per_block - 1) / per_block);
-        if (sblocks > 4096) sblocks = 4096;
-        hipLaunchKernelGGL((summary_kernel<M, G>), dim3(sblocks, B), dim3(kThreads), 0, s, c);
-    }
     // Round loop for phases that stay large: one block per compute unit,
     // shared out among the problems of a batch (every block of the grid must
     // be resident at once; a batch larger than the device holds skips it).
@@ -3771,17 +4168,15 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
     // slower with half).
     int coop_blocks = 0;
     {
-        int dev = 0, cus = 0, per_cu = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &per_cu, reinterpret_cast<const void *>(&wide_loop_kernel<M, G>), kThreads,
-                bid_bytes) == hipSuccess &&
-            per_cu > 0 && cus > 0) {
+        const int cus = facts.cus;
+        const int per_cu =
+            cus > 0 ? occupancy(dev, reinterpret_cast<const void *>(&wide_loop_kernel<M, G>),
+                                kThreads, bid_bytes)
+                    : 0;
+        if (per_cu > 0 && cus > 0) {
             coop_blocks = B == 1 ? cus / 2 : cus / B;
             if (coop_blocks == 0 && B <= cus * per_cu) coop_blocks = 1;
         }
-        (void)hipGetLastError();
     }
     // Each slot: the phase start (with the decision on the previous slot's
     // duality check), the wide rounds, the round loop, the engine, the
@@ -3794,8 +4189,9 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, hipStream_t
     // every launch returns at once, and fewer launches cost less), and when
     // one runs, its first rounds cost little more in the loop.
     for (int slot = 0; slot < slots; ++slot) {
-        hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1, B), dim3(1024), 0, s, c, p,
-                           checks && slot > 0 ? check_parts : 0);
+        if (slot > 0)   // (the start kernel began the first phase)
+            hipLaunchKernelGGL(phase_begin_kernel<M>, dim3(1, B), dim3(1024), 0, s, c, p,
+                               checks ? check_parts : 0);
         const int wr = (slot >= 2 && coop_blocks > 0) ? 0 : wide_rounds;
         for (int r = 0; r < wr; ++r) {
             hipLaunchKernelGGL((bid_wide_kernel<M, G>), dim3(bid_blocks, B), dim3(kThreads),
@@ -3848,51 +4244,41 @@ hipError_t solve_mode(const void *S, const AssignParams &p, int B, int32_t *assi
     const Layout L = make_layout(p.T, p.E);
     Ctx<M> c = make_ctx<M>(S, p, ws);
     const int64_t wst = c.ws_stride;
-    hipLaunchKernelGGL(init_kernel, dim3(1, B), dim3(256), 0, s, c.ctrl, (void *)c.prices, c.E, p,
-                       wst);
-    const int64_t n = p.T * p.E;
     uint32_t *rpart = reinterpret_cast<uint32_t *>(ws + L.rpart);
-    hipLaunchKernelGGL(range_kernel<M>, dim3(kRangeBlocks, B), dim3(256), 0, s, c.S, n, rpart, wst);
-    hipLaunchKernelGGL(range_finish_kernel, dim3(1, B), dim3(256), 0, s, c.ctrl, rpart,
-                       kRangeBlocks, wst);
-    hipLaunchKernelGGL(eps_floor_kernel, dim3(1, B), dim3(1), 0, s, c.ctrl, p.integer ? 1 : 0, wst);
-    hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return err;
-
+    hipError_t err = hipSuccess;
     switch (lanes_per_token(p.E)) {
-        case 1: err = run_solve<M, 1>(c, p, B, s); break;
-        case 2: err = run_solve<M, 2>(c, p, B, s); break;
-        case 4: err = run_solve<M, 4>(c, p, B, s); break;
-        case 8: err = run_solve<M, 8>(c, p, B, s); break;
-        case 16: err = run_solve<M, 16>(c, p, B, s); break;
-        case 32: err = run_solve<M, 32>(c, p, B, s); break;
-        default: err = run_solve<M, 64>(c, p, B, s); break;
+        case 1: err = run_solve<M, 1>(c, p, B, assign, rpart, s); break;
+        case 2: err = run_solve<M, 2>(c, p, B, assign, rpart, s); break;
+        case 4: err = run_solve<M, 4>(c, p, B, assign, rpart, s); break;
+        case 8: err = run_solve<M, 8>(c, p, B, assign, rpart, s); break;
+        case 16: err = run_solve<M, 16>(c, p, B, assign, rpart, s); break;
+        case 32: err = run_solve<M, 32>(c, p, B, assign, rpart, s); break;
+        default: err = run_solve<M, 64>(c, p, B, assign, rpart, s); break;
     }
     if (err != hipSuccess) {
         debug_note("solver launches", err);
         return err;
     }
 
-    int fblocks = (int)((p.T * B + 255) / 256);
-    if (fblocks > 2048) fblocks = 2048;
-    hipLaunchKernelGGL(fill_kernel, dim3(fblocks), dim3(256), 0, s, assign, p.T * B, -1);
-    hipLaunchKernelGGL(holders_to_assign_kernel<M>, dim3(c.E, B), dim3(256), 0, s, c, assign);
-    hipLaunchKernelGGL(greedy_fill_kernel<M>, dim3(1, B), dim3(64), 0, s, c, assign, p.flags);
-    int32_t *blk = reinterpret_cast<int32_t *>(ws + L.blk);
-    hipLaunchKernelGGL(block_count_kernel, dim3((unsigned)L.nblk, B), dim3(kCountTile),
-                       (size_t)p.E * sizeof(int), s, assign, c.T, c.E, blk, wst);
-    hipLaunchKernelGGL(block_scan_kernel, dim3((unsigned)p.E, B), dim3(256), 0, s, blk,
-                       (int)L.nblk, c.E, c.C, wst);
-    hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)L.nblk, B), dim3(kCountTile), 0, s,
-                       assign, c.T, c.E, blk, perm, wst);
+    // assign, perm (ranked per expert when C <= kRankMaxC) and the prices;
+    // then the greedy completion and the rows of experts that are not full.
+    const int rank_perm = c.C <= kRankMaxC ? 1 : 0;
+    hipLaunchKernelGGL(finalise_kernel<M>, dim3(c.E, B), dim3(256), 0, s, c, assign, perm,
+                       static_cast<value_t *>(prices_out), rank_perm);
+    hipLaunchKernelGGL(complete_kernel<M>, dim3(1, B), dim3(kCompThreads),
+                       comp_lds_bytes(c.E, (int)sizeof(value_t)), s, c, assign, perm, p.flags,
+                       rank_perm);
+    if (!rank_perm) {
+        int32_t *blk = reinterpret_cast<int32_t *>(ws + L.blk);
+        hipLaunchKernelGGL(block_count_kernel, dim3((unsigned)L.nblk, B), dim3(kCountTile),
+                           (size_t)p.E * sizeof(int), s, assign, c.T, c.E, blk, wst);
+        hipLaunchKernelGGL(block_scan_kernel, dim3((unsigned)p.E, B), dim3(256), 0, s, blk,
+                           (int)L.nblk, c.E, c.C, wst);
+        hipLaunchKernelGGL(perm_scatter_kernel, dim3((unsigned)L.nblk, B), dim3(kCountTile), 0, s,
+                           assign, c.T, c.E, blk, perm, wst);
+    }
     if (p.flags & BASE_ASSIGN_SYNC_STATS) {
         err = launch_dual_gap<M>(c, B, assign, s);
-        if (err != hipSuccess) return err;
-    }
-    if (prices_out != nullptr) {
-        const size_t row = (size_t)p.E * sizeof(value_t);
-        err = hipMemcpy2DAsync(prices_out, row, c.prices, (size_t)wst, row, (size_t)B,
-                               hipMemcpyDeviceToDevice, s);
         if (err != hipSuccess) return err;
     }
     return hipGetLastError();

@@ -245,6 +245,68 @@ def test_stable_perm_definition_and_routing_rule():
     np.testing.assert_array_equal(a[perm], (np.arange(T) * E) // T)
 
 
+# ---------------------------------------------- round-bounded completion ----
+
+def test_greedy_completion_hand_example_capacity_binds():
+    # worked by hand, C = 2: tokens 0 and 1 fill expert 0, so token 2 (which
+    # prefers expert 0) and token 3 go to expert 1
+    S = np.array([[1.0, 0.0], [2.0, 0.0], [3.0, 0.0], [0.0, 5.0]])
+    a = oracle.greedy_completion(S, np.full(4, -1), np.zeros(2))
+    np.testing.assert_array_equal(a, [0, 0, 1, 1])
+
+
+def test_greedy_completion_ties_and_existing_holders():
+    # ties go to the lowest expert; C = 1
+    a = oracle.greedy_completion(np.ones((2, 2)), np.full(2, -1), np.zeros(2))
+    np.testing.assert_array_equal(a, [0, 1])
+    # token 0 already holds a slot of expert 1 (C = 2): token 1 takes the
+    # other one, tokens 2 and 3 (both preferring expert 1) go to expert 0;
+    # the prices enter as S - p (expert 0 made cheaper by p = -1 changes
+    # nothing here, expert 1 made dearer by 10 sends token 1 to expert 0)
+    S = np.array([[0.0, 1.0], [0.0, 2.0], [0.0, 3.0], [0.0, 4.0]])
+    start = np.array([1, -1, -1, -1])
+    np.testing.assert_array_equal(oracle.greedy_completion(S, start, np.zeros(2)), [1, 1, 0, 0])
+    np.testing.assert_array_equal(
+        oracle.greedy_completion(S, start, np.array([-1.0, 10.0])), [1, 0, 0, 1])
+
+
+def test_greedy_completion_unconstrained_is_argmax_of_values():
+    # tokens 0..15 are unassigned and token t strongly prefers expert t % 4;
+    # every expert already holds 12 of its C = 16 slots, so each has exactly
+    # the room its 4 admirers need: the rule reduces to numpy's argmax of
+    # S - p, row by row
+    T, E = 64, 4
+    rng = np.random.default_rng(11)
+    S = rng.standard_normal((T, E)).astype(np.float32)
+    S[np.arange(16), np.arange(16) % E] += 10.0
+    p = (0.1 * rng.standard_normal(E)).astype(np.float32)
+    a = np.full(T, -1)
+    a[16:] = np.arange(T - 16) % E
+    out = oracle.greedy_completion(S, a, p)
+    np.testing.assert_array_equal(out[:16], np.argmax(S[:16] - p[None, :], axis=1))
+    np.testing.assert_array_equal(out[16:], a[16:])
+    assert oracle.balanced_counts_ok(out, E)
+    assert oracle.balanced_counts_ok(oracle.greedy_completion(S, np.full(T, -1), p), E)
+
+
+def test_greedy_completion_decides_in_float32():
+    # 1 and 1 + 2^-30 are equal in float32: the tie goes to expert 0 (an fp64
+    # comparison would pick expert 1)
+    S = np.array([[1.0, 1.0 + 2.0 ** -30], [0.0, 0.0]])
+    np.testing.assert_array_equal(oracle.greedy_completion(S, np.full(2, -1), np.zeros(2)),
+                                  [0, 1])
+    # integer scores and prices are exact
+    Si = np.array([[3, 5], [7, 2]], dtype=np.int16)
+    pi = np.array([0, 3], dtype=np.int64)
+    np.testing.assert_array_equal(oracle.greedy_completion(Si, np.full(2, -1), pi), [0, 1])
+
+
+def test_stable_perm_partial_pads_empty_rows():
+    np.testing.assert_array_equal(oracle.stable_perm_partial([1, -1, 0, 1], 2), [2, -1, 0, 3])
+    a = np.repeat(np.arange(3), 4)[np.random.default_rng(5).permutation(12)]
+    np.testing.assert_array_equal(oracle.stable_perm_partial(a, 3), oracle.stable_perm(a, 3))
+
+
 def test_gather_scatter_roundtrip_bitwise():
     T, E, d = 48, 4, 9
     rng = np.random.default_rng(4)
