@@ -2,23 +2,32 @@
 //
 // bf16 path: a tiled GEMM on the CDNA4 matrix cores (v_mfma_f32_32x32x16_bf16,
 // fp32 accumulation). The contraction dimension is the model dimension d,
-// contiguous in both H and W, so both operands are loaded the same way: eight
-// bf16 of one row per 16-byte vector. A block owns 64 tokens x 128 experts;
-// H is streamed from HBM exactly once, W (at most a few MiB) is re-read from
-// L2 by every block. The GEMM is bandwidth-bound at every shape of interest
-// (arithmetic intensity about 2E/(2+4E/d) flop per byte, well below the MFMA
-// ridge), so the kernel is organised around keeping HBM reads in flight:
-// the next K-chunk is fetched into registers while the current one is
-// multiplied out of LDS.
+// contiguous in both H and W. The GEMM is bandwidth-bound at every shape of
+// interest (arithmetic intensity about 2E/(2+4E/d) flop per byte, well below
+// the MFMA ridge): H is streamed from HBM exactly once, W (at most a few MiB)
+// is re-read from L2 by every block, and the kernel is organised around
+// keeping enough HBM reads in flight.
+//
+// With d % 64 == 0 (affinity_bf16_pipe_kernel): a block owns 128 tokens x
+// 128 experts (one block per compute unit at T = 32768), eight waves of
+// 32 x 64 outputs. Chunks of 64 elements of d of both operands go straight
+// from global memory into a ring of kStages LDS stages (16-byte LDS-direct
+// loads, no register staging), kStages - 1 chunks ahead of the one being
+// multiplied; a 16-byte slot s of LDS row r holds the row's chunk s ^ (r % 8),
+// so the matrix-core operand reads (eight rows per 128-byte row group) fall
+// on distinct banks. Otherwise (affinity_bf16_kernel) 64 x 128 blocks with
+// register-staged double buffering.
 //
 // fp32 path: a plain LDS-tiled FMA kernel (fp32 products and sums, no
 // reduced-precision matrix instructions).
 //
-// Both kernels can read H through a row index (`rows`, null for the identity):
-// output row i is then h_{rows[i]} . W^T. This is the random shuffle of tokens
-// to workers (Sec. 3.2.1, Shuffling) folded into the GEMM's loads, so the
-// shuffled copy of H is never written. An index outside [0, h_rows) gives a
-// zero row (memory-safe; not a valid shuffle).
+// Every kernel can read H through a row index (`rows`, null for the
+// identity): output row i is then h_{rows[i]} . W^T. This is the random
+// shuffle of tokens to workers (Sec. 3.2.1, Shuffling) folded into the GEMM's
+// loads, so the shuffled copy of H is never written. An index outside
+// [0, h_rows) gives a zero row (memory-safe; not a valid shuffle).
+#include <mutex>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -141,6 +150,123 @@ __global__ __launch_bounds__(256) void affinity_bf16_kernel(const uint16_t *__re
     }
 }
 
+// ---------------------------------------------------- pipelined bf16 GEMM --
+
+constexpr int kPM = 128;                    // tokens per block
+constexpr int kPN = 128;                    // experts per block
+constexpr int kPK = 64;                     // elements of d per chunk (128 bytes a row)
+constexpr int kPThreads = 512;              // 4 (tokens) x 2 (experts) waves
+constexpr int kPTile = kPM * kPK * 2;       // bytes of one operand's chunk (16 KiB)
+constexpr int kPStage = 2 * kPTile;
+constexpr int kStages = 4;
+constexpr size_t kPipeLds = (size_t)kStages * kPStage;   // 128 KiB
+#define BASE_LDS __attribute__((address_space(3)))
+
+// Waits until at most N vector-memory operations of this wave are in flight
+// (the LDS-direct loads count until their data is in LDS).
+template <int N>
+__device__ inline void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier with no memory wait of its own: each wave has already
+// waited for the loads the barrier publishes. The empty asm statements keep
+// the compiler from moving memory accesses across it.
+__device__ inline void bare_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+__global__ __launch_bounds__(kPThreads) void affinity_bf16_pipe_kernel(
+    const uint16_t *__restrict__ H, const int32_t *__restrict__ rows, int64_t h_rows,
+    const uint16_t *__restrict__ W, float *__restrict__ S, int T, int E, int d) {
+    extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int m0 = blockIdx.x * kPM;
+    const int n0 = blockIdx.y * kPN;
+    // This thread's two 16-byte slots of each operand's chunk: slot q = i *
+    // 512 + tid is row q / 8, position q % 8, and holds the row's chunk
+    // (q % 8) ^ (row % 8). Rows past T or E, and invalid source rows, read
+    // a valid row; their outputs are not stored (or stored as zero).
+    const uint16_t *ga[2], *gb[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int q = i * kPThreads + tid;
+        const int r = q >> 3;
+        const int c = (q & 7) ^ (r & 7);
+        int64_t hr = m0 + r < T ? source_row(rows, h_rows, m0 + r) : 0;
+        if (hr < 0) hr = 0;
+        const int er = n0 + r < E ? n0 + r : E - 1;
+        ga[i] = H + hr * d + c * 8;
+        gb[i] = W + (int64_t)er * d + c * 8;
+    }
+    auto issue = [&](int kc) {
+        BASE_LDS unsigned char *base = (BASE_LDS unsigned char *)lds + (kc % kStages) * kPStage;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int slot = (i * kPThreads + wave * 64) * 16;   // the wave's 1 KiB
+            __builtin_amdgcn_global_load_lds((const void *)(ga[i] + (int64_t)kc * kPK),
+                                             (BASE_LDS void *)(base + slot), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void *)(gb[i] + (int64_t)kc * kPK),
+                                             (BASE_LDS void *)(base + kPTile + slot), 16, 0, 0);
+        }
+    };
+    const int wm = wave & 3;
+    const int wn = wave >> 2;
+    const int lrow = lane & 31;
+    const int lhalf = lane >> 5;
+    f32x16_t acc[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[j][i] = 0.0f;
+    const int nk = d / kPK;
+#pragma unroll
+    for (int st = 0; st < kStages - 1; ++st)
+        if (st < nk) issue(st);
+    for (int kc = 0; kc < nk; ++kc) {
+        // Chunk kc has landed once at most the later chunks' loads (four
+        // per chunk) are in flight; after the barrier every wave's part of
+        // it is in LDS and every wave is done with the stage refilled next.
+        if (kc + kStages - 2 < nk) wait_vmcnt<4 * (kStages - 2)>();
+        else wait_vmcnt<0>();
+        bare_barrier();
+        if (kc + kStages - 1 < nk) issue(kc + kStages - 1);
+        const unsigned char *A = lds + (kc % kStages) * kPStage;
+        const unsigned char *B = A + kPTile;
+        const int ra = 32 * wm + lrow;
+#pragma unroll
+        for (int ks = 0; ks < kPK / 16; ++ks) {
+            const int c = 2 * ks + lhalf;
+            const bf16x8_t a =
+                *reinterpret_cast<const bf16x8_t *>(A + ra * 128 + ((c ^ (ra & 7)) * 16));
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int rb = 64 * wn + 32 * j + lrow;
+                const bf16x8_t b =
+                    *reinterpret_cast<const bf16x8_t *>(B + rb * 128 + ((c ^ (rb & 7)) * 16));
+                acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+            }
+        }
+    }
+    // 32x32 accumulator layout: lane holds column lane % 32; register i holds
+    // row 8 (i / 4) + 4 (lane / 32) + i % 4.
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int e = n0 + 64 * wn + 32 * j + lrow;
+        if (e >= E) continue;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int t = m0 + 32 * wm + 8 * (i >> 2) + 4 * lhalf + (i & 3);
+            if (t < T) S[(int64_t)t * E + e] = source_row(rows, h_rows, t) >= 0 ? acc[j][i] : 0.0f;
+        }
+    }
+}
+
 // fp32: 64 x 64 output tile per block, 16 x 16 threads, 4 x 4 outputs each.
 constexpr int kFT = 64;
 constexpr int kFK = 16;
@@ -200,6 +326,27 @@ __global__ __launch_bounds__(256) void affinity_f32_kernel(const float *__restri
 hipError_t launch_affinity_bf16(const uint16_t *H, const int32_t *rows, int64_t h_rows,
                                 const uint16_t *W, float *S, int64_t T, int64_t E, int64_t d,
                                 hipStream_t stream) {
+    if (d % kPK == 0) {
+        // The LDS ring is above the default 64 KiB: opted in once per device.
+        static std::mutex m;
+        static bool granted[64] = {};
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+        {
+            std::lock_guard<std::mutex> lock(m);
+            if (!granted[dev]) {
+                const hipError_t err = hipFuncSetAttribute(
+                    reinterpret_cast<const void *>(&affinity_bf16_pipe_kernel),
+                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)kPipeLds);
+                if (err != hipSuccess) return err;
+                granted[dev] = true;
+            }
+        }
+        dim3 grid((unsigned)((T + kPM - 1) / kPM), (unsigned)((E + kPN - 1) / kPN));
+        hipLaunchKernelGGL(affinity_bf16_pipe_kernel, grid, dim3(kPThreads), kPipeLds, stream, H,
+                           rows, h_rows, W, S, (int)T, (int)E, (int)d);
+        return hipGetLastError();
+    }
     dim3 grid((unsigned)((T + kBM - 1) / kBM), (unsigned)((E + kBN - 1) / kBN));
     hipLaunchKernelGGL(affinity_bf16_kernel, grid, dim3(256), 0, stream, H, rows, h_rows, W, S,
                        (int)T, (int)E, (int)d);

@@ -65,9 +65,12 @@ def check_assignment(S: np.ndarray, res, eps: float, opt=None, unique_gap=None, 
 
 # ---------------------------------------------------------------- affinity --
 
-def test_affinity_bf16_integer_inputs_bit_exact():
-    # T, E and d all ragged against the 64 x 128 x 64 tiling
-    H, W = wl.small_integer_inputs(300, 200, 264, seed=7)
+@pytest.mark.parametrize("d", [264, 256])
+def test_affinity_bf16_integer_inputs_bit_exact(d):
+    # T and E ragged against both tilings (64 x 128 and 128 x 128 tokens x
+    # experts); d = 264 takes the register-staged kernel, d = 256 (a multiple
+    # of 64) the pipelined one
+    H, W = wl.small_integer_inputs(300, 200, d, seed=7)
     S = gpu_affinity(wl.f32_to_bf16_bits(H), wl.f32_to_bf16_bits(W))
     np.testing.assert_array_equal(S.astype(np.float64), oracle.affinity(H, W))
 
@@ -78,7 +81,8 @@ def test_affinity_f32_integer_inputs_bit_exact():
     np.testing.assert_array_equal(S.astype(np.float64), oracle.affinity(H, W))
 
 
-@pytest.mark.parametrize("T,E,d", [(1000, 200, 520), (64, 128, 64), (1, 1, 8), (77, 3, 2048)])
+@pytest.mark.parametrize("T,E,d", [(1000, 200, 520), (64, 128, 64), (1, 1, 8), (77, 3, 2048),
+                                   (1000, 200, 576), (129, 257, 64), (1, 1, 64)])
 def test_affinity_bf16_random_ragged(T, E, d):
     rng = np.random.Generator(np.random.PCG64(T * 7 + E))
     Hb = wl.f32_to_bf16_bits(rng.standard_normal((T, d), dtype=np.float32))

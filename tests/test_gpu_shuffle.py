@@ -34,11 +34,12 @@ def rand_rows(rng, n, d, dtype):
     return wl.f32_to_bf16_bits(x) if dtype == "bf16" else x
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_affinity_gather(dtype):
+@pytest.mark.parametrize("dtype,d", [("bf16", 264), ("bf16", 192), ("f32", 264)])
+def test_affinity_gather(dtype, d):
     """Rows of H taken through an index with repeats, N ragged against the
-    64-row tiles, E and d ragged too."""
-    h_rows, N, E, d = 1000, 777, 200, 264
+    64- and 128-row tiles, E and d ragged too (d = 192: the pipelined bf16
+    kernel)."""
+    h_rows, N, E = 1000, 777, 200
     rng = np.random.Generator(np.random.PCG64(31))
     H = rand_rows(rng, h_rows, d, dtype)
     W = rand_rows(rng, E, d, dtype) if dtype == "bf16" else \
@@ -53,10 +54,11 @@ def test_affinity_gather(dtype):
     assert np.all(np.abs(host(S) - ref) <= bound)
 
 
-def test_affinity_gather_out_of_range_rows_are_zero():
+@pytest.mark.parametrize("d", [32, 128])
+def test_affinity_gather_out_of_range_rows_are_zero(d):
     rng = np.random.Generator(np.random.PCG64(32))
-    H = rand_rows(rng, 64, 32, "bf16")
-    W = rand_rows(rng, 16, 32, "bf16")
+    H = rand_rows(rng, 64, d, "bf16")
+    W = rand_rows(rng, 16, d, "bf16")
     rows = np.array([3, -1, 64, 63, 1 << 30, 0], dtype=np.int32)
     S = host(pb.affinity(dev(H), dev(W), rows=dev(rows)))
     assert np.all(S[[1, 2, 4]] == 0.0)
