@@ -95,7 +95,7 @@ inline void debug_note(const char *what, hipError_t err) {
 
 struct Layout {
     size_t ctrl, prices, hcount, hsel, bcount, holders, bucket, ovf_key, ovf_exp, active, blk,
-        eck, ecs, ecn, sums, bar, rpart, gpart, sspm, sspa, total;
+        eck, ecs, ecn, sums, bar, rpart, gpart, sspm, sspa, sspt, total;
     int64_t cap, nblk;
 };
 
@@ -129,6 +129,9 @@ Layout make_layout(int64_t T, int64_t E) {
     const int64_t Es = E <= kSspMaxE ? E : 0;
     L.sspm = off;    off += align_up((size_t)Es * Es * 4);
     L.sspa = off;    off += align_up((size_t)Es * Es * 2);
+    // Every expert's held tokens as uint16 in slot order (T <= 65536), in
+    // the layout the finish keeps in LDS.
+    L.sspt = off;    off += align_up(E <= kSspMaxE && T <= 65536 ? (size_t)T * 2 : 0);
     L.total = off;
     return L;
 }
@@ -157,6 +160,7 @@ struct Ctx {
                       // by shortest augmenting paths
     float *ssp_m;     // [E][E] min over tokens t of expert e of S[t,e] - S[t,x]
     uint16_t *ssp_a;  // [E][E] the holder slot of that token
+    uint16_t *ssp_t;  // [E][C] the tokens of every expert's holder slots (0 past its count)
     int64_t ws_stride;   // bytes between the workspaces of consecutive problems of a batch
 
     // The view of problem b of a batch (blockIdx.y in every solver launch):
@@ -190,6 +194,7 @@ struct Ctx {
         r.gpart = shift(gpart, w);
         r.ssp_m = shift(ssp_m, w);
         r.ssp_a = shift(ssp_a, w);
+        r.ssp_t = shift(ssp_t, w);
         return r;
     }
 };
@@ -226,6 +231,7 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.ssp_cap = 0;
     c.ssp_m = reinterpret_cast<float *>(ws + L.sspm);
     c.ssp_a = reinterpret_cast<uint16_t *>(ws + L.sspa);
+    c.ssp_t = reinterpret_cast<uint16_t *>(ws + L.sspt);
     c.ws_stride = (int64_t)L.total;
     return c;
 }
@@ -2892,6 +2898,9 @@ __global__ __launch_bounds__(kSspThreads) void ssp_build_kernel(Ctx<M> c0) {
         se[q] = c.S[(int64_t)t * c.E + e];
     }
     __syncthreads();
+    // The expert's tokens for the finish's LDS copy (uint16: T <= 65536).
+    for (int q = tid; q < c.C; q += kSspThreads)
+        c.ssp_t[(int64_t)e * c.C + q] = (uint16_t)(q < cnt ? tok[q] : 0);
     int Ep = 1;
     while (Ep < c.E) Ep <<= 1;
     const int subs = kSspThreads / Ep;
@@ -3086,20 +3095,21 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
         sel[e] = real ? (ld_relaxed(&c.hsel[e]) & 1) : 0;
     }
     __syncthreads();
-    for (int i = tid; i < E * C; i += kSspBlock) {
-        const int e = i / C, q = i - e * C;
-        int t = 0;
-        if (q < cnt[e]) {
-            t = key_token(c.holders[(int64_t)sel[e] * T + i]);
-            if (t < 0 || t >= T) {
-                flag_internal(ctrl);
-                s_err = 1;
-                t = 0;
-            }
-        }
-        toks[i] = (uint16_t)t;
+    // The token table and the slot matrix as the build kernel wrote them:
+    // 16-byte loads, all in flight together (one element at a time, the
+    // setup took 65 us of dependent loads at T = 32768).
+    {
+        const int nt16 = (E * C * 2) / 16;
+        const uint4 *src = reinterpret_cast<const uint4 *>(c.ssp_t);
+        uint4 *dst = reinterpret_cast<uint4 *>(toks);
+        for (int i = tid; i < nt16; i += kSspBlock) dst[i] = src[i];
+        for (int i = nt16 * 8 + tid; i < E * C; i += kSspBlock) toks[i] = c.ssp_t[i];
+        const int na16 = (E * E * 2) / 16;
+        const uint4 *asrc = reinterpret_cast<const uint4 *>(c.ssp_a);
+        uint4 *adst = reinterpret_cast<uint4 *>(am);
+        for (int i = tid; i < na16; i += kSspBlock) adst[i] = asrc[i];
+        for (int i = na16 * 8 + tid; i < E * E; i += kSspBlock) am[i] = c.ssp_a[i];
     }
-    for (int i = tid; i < E * E; i += kSspBlock) am[i] = c.ssp_a[i];
     {
         const int n = s_n;
         for (int i = wave; i < n; i += kSspWaves) {
