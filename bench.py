@@ -7,6 +7,13 @@ includes it). Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                     [--no-cpu-baseline] [--batch B] [--no-shuffle] [--layer]
+                    [--max-rounds R] [--seed-spread N]
+
+With --max-rounds R the timed solves stop after R bidding rounds and the
+greedy completion fills the free slots (bounded latency; the line reports
+the solve time next to the duality gap the result keeps). On the headline
+workload the line also reports the step over N mixture seeds (default 5;
+--seed-spread 0 skips it).
 
 With --batch B > 1 it measures B independent problems of the paper's
 per-worker shape (Sec. 3.2.1 Sharding; T=2048, E=128, d=2048) with the
@@ -81,6 +88,8 @@ def parse():
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--no-shuffle", action="store_true")
     ap.add_argument("--layer", action="store_true")
+    ap.add_argument("--max-rounds", type=int, default=0)
+    ap.add_argument("--seed-spread", type=int, default=-1)
     return ap.parse_args()
 
 
@@ -203,27 +212,54 @@ def bench_batched(args) -> None:
         torch.from_numpy(wl.shuffle_permutation(B * T, 2103)).cuda()
     stream = torch.cuda.current_stream()
 
-    def step():
+    def step(evs=None):
+        if evs is not None:
+            evs[0].record(stream)
         pb.affinity(H, W, out=S, rows=shuffle, stream=stream)
+        if evs is not None:
+            evs[1].record(stream)
         pb.assign_batched(S.view(B, T, E), sync_stats=False, workspace=ws, out_assign=a,
                           out_perm=perm, out_prices=prices, stream=stream)
+        if evs is not None:
+            evs[2].record(stream)
         pb.permute_batched(H, perm, shuffle=shuffle, out=X, stream=stream)
+        if evs is not None:
+            evs[3].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    pb.timing_enable(64 * args.steps)
+    torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
+    for k in range(args.steps):
+        step(events[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    eng_launches, eng_ms = pb.timing_read()
+    pb.timing_enable(0)
+    names = ["affinity", "assign", "permute"]
+    per_call_ms = {n: float(np.mean([ev[i].elapsed_time(ev[i + 1]) for ev in events]))
+                   for i, n in enumerate(names)}
+    gpu_ms = float(np.mean([ev[0].elapsed_time(ev[-1]) for ev in events]))
     res = pb.assign_batched(S.view(B, T, E), workspace=ws, out_assign=a, out_perm=perm,
                             out_prices=prices)
+    st = res.stats
     counts_ok = bool(torch.all(torch.stack([torch.bincount(a[b].long(), minlength=E)
                                             for b in range(B)]) == T // E))
+    BT = B * T
+    bytes_aff = BT * d * 2 + E * d * 2 + BT * E * 4 + BT * 4
+    bytes_perm = 2 * BT * d * 2 + BT * 4
+    bytes_assign = st.bids * (4 * E + 16) + BT * 8
+    rl = {"affinity": bytes_aff, "assign": bytes_assign, "permute": bytes_perm}
+    launches = eng_launches / args.steps if eng_launches else 0.0
+    eng_avg_ms = eng_ms / eng_launches if eng_launches else float("nan")
+    eng_bytes = st.engine_bids * (4 * E + 16) / launches if launches else 0.0
+    eng_ach = eng_bytes / (eng_avg_ms * 1e-3) / 1e9 if eng_launches else 0.0
     out = {
         "metric": f"tokens assigned/sec, {B} independent problems of T=2048,E=128,d=2048",
-        "value": B * T * args.steps / wall,
+        "value": BT * args.steps / wall,
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -236,11 +272,58 @@ def bench_batched(args) -> None:
         "data": "synthetic (seeded generator; no dataset or trained weights)",
         "config": {"workload": f"t2048-e128-d2048-worker x {B}", "B": B, "T": T, "E": E, "d": d,
                    "shuffle": shuffle is not None},
-        "assign_stats": {"phases": res.stats.phases, "rounds_max": res.stats.rounds,
-                         "bids": res.stats.bids, "converged": res.stats.converged},
+        "roofline": {"kernel": ENGINE_KERNEL, "bound": "hbm", "achieved": eng_ach,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": eng_ach / HBM_PEAK_GBS,
+                     "traffic": None,
+                     "bytes_model": "bids x (4E + 16) B over all problems: an upper bound",
+                     "algorithmic_bytes_per_launch": eng_bytes, "avg_launch_ms": eng_avg_ms,
+                     "launches_per_step": launches,
+                     "share_of_step": eng_ms / args.steps / gpu_ms if gpu_ms > 0 else None},
+        "per_call_ms": {k: round(v, 4) for k, v in per_call_ms.items()},
+        "gpu_ms_per_step": gpu_ms,
+        "per_call_roofline": {k: {"bound": "hbm",
+                                  "achieved": round(v / (per_call_ms[k] * 1e-3) / 1e9, 2),
+                                  "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                  "frac": round(v / (per_call_ms[k] * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                                4)}
+                              for k, v in rl.items()},
+        "assign_stats": {"phases": st.phases, "rounds_max": st.rounds, "bids": st.bids,
+                         "engine_bids": st.engine_bids, "converged": st.converged,
+                         "dual_gap": st.dual_gap, "eps_final": st.eps_final},
         "balanced_problems": counts_ok,
     }
+    if not args.no_cpu_baseline:
+        # A bounded sample: the oracle on the first problems of the batch.
+        sample = []
+        for b in range(min(B, 16)):
+            sample.append(wl.make_inputs(dataclasses.replace(base, seed=base.seed + 1000 * b)))
+        out["cpu_baseline"] = cpu_baseline_many(sample)
     print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_many(inps) -> dict:
+    """The CPU oracle over several independent problems (one pass each)."""
+    import oracle
+    t0 = time.perf_counter()
+    tokens = 0
+    for inp in inps:
+        S = oracle.affinity(inp.H, inp.W)
+        a, _, _ = oracle.solve_ssp(S)
+        oracle.gather(inp.H_store, oracle.stable_perm(a, inp.wl.E))
+        tokens += inp.wl.T
+    spent = time.perf_counter() - t0
+    return {"value": tokens / spent, "unit": "tokens/s", "cores": _blas_threads(),
+            "kind": "oracle",
+            "sample": f"{len(inps)} problems of {inps[0].wl.name} (the first of the batch), "
+                      f"one pass each: fp64 affinity, SSP solve, stable sort vector, gather"}
+
+
+def _blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        return int(max((i.get("num_threads", 1) for i in threadpool_info()), default=1))
+    except Exception:  # threadpoolctl missing: report the host count
+        return os.cpu_count() or 1
 
 
 def cpu_baseline(inp: wl.Inputs, min_s: float = 10.0, budget_s: float = 30.0) -> dict:
@@ -285,6 +368,62 @@ def cpu_baseline(inp: wl.Inputs, min_s: float = 10.0, budget_s: float = 30.0) ->
     }
 
 
+def seed_spread(args, w, n: int) -> dict:
+    """The whole step on n seeds of the workload's generator (the given seed
+    first, then seed + 1000 i): per seed, the median of a few timed steps."""
+    import dataclasses
+
+    import torch
+
+    import paper_2103_16716_amd as pb
+
+    T, E = w.T, w.E
+    S = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    a = torch.empty(T, dtype=torch.int32, device="cuda")
+    perm = torch.empty(T, dtype=torch.int32, device="cuda")
+    ws = torch.empty(pb.assign_workspace_size(T, E), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    rows = []
+    for i in range(n):
+        wi = dataclasses.replace(w, seed=w.seed + 1000 * i)
+        inp = wl.make_inputs(wi)
+        H = torch.from_numpy(inp.H_store.view(np.int16)).cuda().view(torch.bfloat16) \
+            if inp.H_store.dtype == np.uint16 else torch.from_numpy(inp.H_store).cuda()
+        W = torch.from_numpy(inp.W_store.view(np.int16)).cuda().view(torch.bfloat16) \
+            if inp.W_store.dtype == np.uint16 else torch.from_numpy(inp.W_store).cuda()
+        X = torch.empty_like(H)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(5)]
+
+        def step(e=None):
+            if e is not None:
+                e[0].record(stream)
+            pb.affinity(H, W, out=S, stream=stream)
+            pb.assign(S, sync_stats=False, workspace=ws, out_assign=a, out_perm=perm,
+                      stream=stream)
+            if e is not None:
+                e[1].record(stream)
+            pb.permute(H, perm, out=X, stream=stream)
+            if e is not None:
+                e[2].record(stream)
+
+        for _ in range(2):
+            step()
+        for e in ev:
+            step(e)
+        torch.cuda.synchronize()
+        step_ms = float(np.median([e[0].elapsed_time(e[2]) for e in ev]))
+        res = pb.assign(S, workspace=ws, out_assign=a, out_perm=perm)
+        ok = bool(torch.all(torch.bincount(a.long(), minlength=E) == T // E))
+        rows.append({"seed": wi.seed, "step_ms": round(step_ms, 4),
+                     "tokens_per_s": round(T / (step_ms * 1e-3)), "rounds": res.stats.rounds,
+                     "phases": res.stats.phases, "balanced": ok})
+        del H, W, X
+    tps = np.array([r["tokens_per_s"] for r in rows], dtype=np.float64)
+    return {"seeds": rows, "tokens_per_s_median": float(np.median(tps)),
+            "tokens_per_s_min": float(tps.min()), "tokens_per_s_max": float(tps.max()),
+            "note": "GPU step time (events) per seed, median of 5 steps"}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -319,6 +458,8 @@ def main():
     H, W = to_dev(inp.H_store), to_dev(inp.W_store)
     S = torch.empty((T, E), dtype=torch.float32, device="cuda")
     a = torch.empty(T, dtype=torch.int32, device="cuda")
+    # every timed solve writes its own assignment, checked after the timing
+    a_timed = torch.empty((args.steps, T), dtype=torch.int32, device="cuda")
     perm = torch.empty(T, dtype=torch.int32, device="cuda")
     prices = torch.empty(E, dtype=torch.float32, device="cuda")
     ws = torch.empty(pb.assign_workspace_size(T, E), dtype=torch.uint8, device="cuda")
@@ -328,15 +469,17 @@ def main():
 
     stream = torch.cuda.current_stream()
     n_ev = 5 if unpermute else 4
+    bounded = dict(max_rounds=args.max_rounds, flags=pb.BASE_ASSIGN_GREEDY_FALLBACK) \
+        if args.max_rounds > 0 else {}
 
-    def step(evs=None):
+    def step(evs=None, out_a=None):
         if evs is not None:
             evs[0].record(stream)
         pb.affinity(H, W, out=S, stream=stream)
         if evs is not None:
             evs[1].record(stream)
-        pb.assign(S, sync_stats=False, workspace=ws, out_assign=a, out_perm=perm,
-                  out_prices=prices, stream=stream)
+        pb.assign(S, sync_stats=False, workspace=ws, out_assign=a if out_a is None else out_a,
+                  out_perm=perm, out_prices=prices, stream=stream, **bounded)
         if evs is not None:
             evs[2].record(stream)
         pb.permute(H, perm, out=X, stream=stream)
@@ -358,11 +501,13 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        step(events[k])
+        step(events[k], a_timed[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     eng_launches, eng_ms = pb.timing_read()
     pb.timing_enable(0)
+    timed_balanced = sum(int(bool(torch.all(torch.bincount(a_timed[k].long(), minlength=E) ==
+                                            T // E))) for k in range(args.steps))
 
     names = ["affinity", "assign", "permute"] + (["unpermute"] if unpermute else [])
     per_call_ms = {n: float(np.mean([ev[i].elapsed_time(ev[i + 1]) for ev in events]))
@@ -390,7 +535,8 @@ def main():
     runs = []
     for _ in range(3):
         step()
-        res = pb.assign(S, workspace=ws, out_assign=a, out_perm=perm, out_prices=prices)
+        res = pb.assign(S, workspace=ws, out_assign=a, out_perm=perm, out_prices=prices,
+                        **bounded)
         counts = torch.bincount(a.long(), minlength=E)
         balanced += int(bool(torch.all(counts == T // E)))
         checked += 1
@@ -417,18 +563,23 @@ def main():
     if unpermute:
         rl["unpermute"] = ("hbm", bytes_perm / (per_call_ms["unpermute"] * 1e-3) / 1e9,
                            HBM_PEAK_GBS, "GB/s", bytes_perm)
-    # The dominant kernel: the engine (most of the assign call). Its
-    # algorithmic bytes per launch are the bids it places times the bytes a
-    # bid needs (the token's score row, 4E bytes, plus a 16-byte key and
-    # expert), over the launches of one solve.
+    # The dominant kernel: the engine (the largest part of the assign call).
+    # Its modelled bytes per launch are the bids it places times the bytes a
+    # bid would need if it read the token's whole score row (4E bytes) plus
+    # a 16-byte key and expert, over the launches of one solve. This is an
+    # upper bound: most bids read only the token's 64-byte summary, so the
+    # counter-measured traffic (when a summary for this source is committed)
+    # is reported beside it.
     launches_per_solve = eng_launches / args.steps if eng_launches else 0.0
     eng_avg_ms = eng_ms / eng_launches if eng_launches else float("nan")
     eng_bytes = (st.engine_bids * (4 * E + 16) / launches_per_solve
                  if launches_per_solve else 0.0)
     eng_ach = eng_bytes / (eng_avg_ms * 1e-3) / 1e9 if eng_launches else 0.0
     traffic = measured_traffic(w.name)
+    spread = args.seed_spread if args.seed_spread >= 0 else (5 if w.name == wl.HEADLINE else 0)
+    seeds_line = seed_spread(args, w, spread) if spread > 0 else None
     out = {
-        "metric": "tokens assigned/sec at T=32768,E=128,d=2048",
+        "metric": f"tokens assigned/sec at T={T},E={E},d={d}",
         "value": T * args.steps / wall,
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -441,10 +592,19 @@ def main():
         "dtype": "bf16" if bf16 else "f32",
         "data": "synthetic (seeded generator; no dataset or trained weights)",
         "config": {"workload": w.name, "T": T, "E": E, "C": T // E, "d": d, "dist": w.dist,
-                   "inputs": w.dtype, "scores": "f32", "solver": "f32 auction, eps_final=1e-4"},
+                   "inputs": w.dtype, "scores": "f32",
+                   "solver": "f32 auction, eps_final=1e-4",
+                   **({"max_rounds": args.max_rounds, "completion": "greedy"}
+                      if args.max_rounds > 0 else {}),
+                   **({"unpermute": True} if unpermute else {})},
         "roofline": {"kernel": ENGINE_KERNEL, "bound": "hbm", "achieved": eng_ach,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": eng_ach / HBM_PEAK_GBS,
-                     "traffic": traffic, "algorithmic_bytes_per_launch": eng_bytes,
+                     "traffic": traffic,
+                     "traffic_achieved_gbs": (traffic / (eng_avg_ms * 1e-3) / 1e9
+                                              if traffic and eng_launches else None),
+                     "bytes_model": "bids x (4E + 16) B: an upper bound, most bids read a "
+                                    "64 B summary instead of the 4E B row",
+                     "algorithmic_bytes_per_launch": eng_bytes,
                      "avg_launch_ms": eng_avg_ms, "launches_per_step": launches_per_solve,
                      "share_of_step": eng_ms / args.steps / gpu_ms if gpu_ms > 0 else None},
         "per_call_ms": {k: round(v, 4) for k, v in per_call_ms.items()},
@@ -462,10 +622,14 @@ def main():
                          "bids_per_token": st.bids / T, "engine_bids": st.engine_bids,
                          "eps_final": st.eps_final, "eps_last": st.eps_last,
                          "certified": st.certified, "dual_gap": st.dual_gap,
-                         "gap_bound": T * st.eps_final, "converged": st.converged},
+                         "gap_bound": T * st.eps_final, "converged": st.converged,
+                         "fell_back": st.fell_back, "augmentations": st.augmentations},
         "balanced_solves": f"{balanced}/{checked}",
+        "balanced_timed_solves": f"{timed_balanced}/{args.steps}",
         "deterministic": deterministic,
     }
+    if seeds_line is not None:
+        out["seed_spread"] = seeds_line
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inp)
     print(json.dumps(out), flush=True)

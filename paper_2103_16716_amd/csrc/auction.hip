@@ -246,6 +246,27 @@ __device__ inline int ld_relaxed(const int *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Copies n16 16-byte words from global memory to LDS with kBlock threads,
+// eight loads in flight per thread before any store (a plain loop waits for
+// each load before the next).
+template <int kBlock>
+__device__ inline void copy16_to_lds(uint4 *dst, const uint4 *src, int n16) {
+    constexpr int kU = 8;
+    for (int i0 = threadIdx.x; i0 < n16; i0 += kU * kBlock) {
+        uint4 v[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int i = i0 + u * kBlock;
+            if (i < n16) v[u] = src[i];
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const int i = i0 + u * kBlock;
+            if (i < n16) dst[i] = v[u];
+        }
+    }
+}
+
 // A consistency check failed: the access is skipped and the call reports
 // BASE_ERR_INTERNAL instead of touching memory outside the workspace. The
 // solve also ends there: every later solver kernel sees `done` and returns
@@ -2607,10 +2628,11 @@ __global__ __launch_bounds__(kEngThreads) void engine_kernel(Ctx<M> c0, AssignPa
         s.bcnt[c.E + e] = 0;
         s.bfill[e] = 0;
     }
-    for (int i = tid; i < c.E * K; i += kEngThreads) {
-        s.ck[i] = c.eng_ck[i];
-        s.cs[i] = c.eng_cs[i];
-    }
+    // The entry lists (every expert's K slots, used or not).
+    copy16_to_lds<kEngThreads>(reinterpret_cast<uint4 *>(s.ck),
+                               reinterpret_cast<const uint4 *>(c.eng_ck), c.E * K / 2);
+    copy16_to_lds<kEngThreads>(reinterpret_cast<uint4 *>(s.cs),
+                               reinterpret_cast<const uint4 *>(c.eng_cs), c.E * K / 8);
     for (int i = tid; i < s_n; i += kEngThreads) {
         const int t = c.active[(int64_t)s_cur * c.T + i];
         act[i] = (t >= 0 && t < c.T) ? t : 0;
@@ -3100,30 +3122,28 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
     // setup took 65 us of dependent loads at T = 32768).
     {
         const int nt16 = (E * C * 2) / 16;
-        const uint4 *src = reinterpret_cast<const uint4 *>(c.ssp_t);
-        uint4 *dst = reinterpret_cast<uint4 *>(toks);
-        for (int i = tid; i < nt16; i += kSspBlock) dst[i] = src[i];
+        copy16_to_lds<kSspBlock>(reinterpret_cast<uint4 *>(toks),
+                                 reinterpret_cast<const uint4 *>(c.ssp_t), nt16);
         for (int i = nt16 * 8 + tid; i < E * C; i += kSspBlock) toks[i] = c.ssp_t[i];
         const int na16 = (E * E * 2) / 16;
-        const uint4 *asrc = reinterpret_cast<const uint4 *>(c.ssp_a);
-        uint4 *adst = reinterpret_cast<uint4 *>(am);
-        for (int i = tid; i < na16; i += kSspBlock) adst[i] = asrc[i];
+        copy16_to_lds<kSspBlock>(reinterpret_cast<uint4 *>(am),
+                                 reinterpret_cast<const uint4 *>(c.ssp_a), na16);
         for (int i = na16 * 8 + tid; i < E * E; i += kSspBlock) am[i] = c.ssp_a[i];
     }
-    {
-        const int n = s_n;
-        for (int i = wave; i < n; i += kSspWaves) {
-            int t = c.active[(int64_t)s_cur * T + i];
-            if (t < 0 || t >= T) {
-                if (lane == 0) {
-                    flag_internal(ctrl);
-                    s_err = 1;
-                }
-                t = 0;
-            }
-            if (lane == 0) act[i] = t;
-            for (int y = lane; y < E; y += 64) rowsT[y * KS + i] = c.S[(int64_t)t * E + y];
+    if (tid < s_n) {
+        int t = c.active[(int64_t)s_cur * T + tid];
+        if (t < 0 || t >= T) {
+            flag_internal(ctrl);
+            s_err = 1;
+            t = 0;
         }
+        act[tid] = t;
+    }
+    __syncthreads();
+    // The unassigned tokens' rows, transposed (all loads of the pass in flight).
+    for (int q = tid; q < s_n * E; q += kSspBlock) {
+        const int i = q / E, y = q - i * E;
+        rowsT[y * KS + i] = c.S[(int64_t)act[i] * E + y];
     }
     float mreg[RW][CL];
 #pragma unroll
@@ -3706,20 +3726,48 @@ __device__ inline void wave_max_pair(V &v, int &i) {
 }
 
 constexpr int kCompThreads = 1024;
+constexpr int kCompWaves = kCompThreads / 64;
 constexpr int kCompStageBytes = 32 * 1024;   // score rows staged per step of the greedy walk
 constexpr int kCompMaxRows = 256;
-constexpr int kCompRegs = 2048 / 64;         // experts per lane of the walking wave (E <= 2048)
+constexpr int kCompScan = 32;                // tokens per thread and pass of the compaction
 
-__host__ __device__ inline int comp_rows(int E, int vbytes) {
-    int r = kCompStageBytes / (E * vbytes);
-    return r < 1 ? 1 : (r > kCompMaxRows ? kCompMaxRows : r);
-}
 __host__ __device__ inline size_t a16(size_t x) { return (x + 15) & ~size_t(15); }
-inline size_t comp_lds_bytes(int E, int vbytes) {
-    const int R = comp_rows(E, vbytes);
-    size_t stage = (size_t)R * E * vbytes;
-    if (stage < (size_t)kRankMaxC * 4) stage = (size_t)kRankMaxC * 4;
-    return a16((size_t)E * vbytes) + a16((size_t)E * 4) + a16((size_t)R * 4) + stage;
+// LDS of complete_kernel (within the default 64 KiB): prices, the counts
+// before the completion, the live counts, the holder-table selectors, the
+// staged tokens and their choices, then the staged values of R tokens (or,
+// after the walk, nrw waves' token lists for the ranking, C rounded up to 4
+// each).
+struct CompLds {
+    size_t pr, hc0, cnt, sel, stok, chs, slot, vst, total;
+    int R, nrw;
+};
+__host__ __device__ inline CompLds comp_lds(int E, int C, int vbytes) {
+    CompLds L{};
+    const size_t budget = 62 * 1024;
+    const size_t fixed = a16((size_t)E * vbytes) + 3 * a16((size_t)E * 4) +
+                         3 * a16((size_t)kCompMaxRows * 4);
+    const size_t avail = budget > fixed ? budget - fixed : 0;
+    const size_t stage_max = avail < (size_t)kCompStageBytes ? avail : (size_t)kCompStageBytes;
+    size_t r = stage_max / ((size_t)E * vbytes);
+    L.R = r < 1 ? 1 : (r > (size_t)kCompMaxRows ? kCompMaxRows : (int)r);
+    const size_t c4 = (size_t)((C + 3) & ~3);
+    const size_t rank_max = avail < 32768 ? avail : 32768;
+    size_t w = rank_max / (c4 * 4);
+    L.nrw = C > kRankMaxC ? 1 : (w < 1 ? 1 : (w > (size_t)kCompWaves ? kCompWaves : (int)w));
+    size_t stage = (size_t)L.R * E * vbytes;
+    const size_t rank = C <= kRankMaxC ? (size_t)L.nrw * c4 * 4 : 0;
+    if (stage < rank) stage = rank;
+    size_t off = 0;
+    L.pr = off;   off += a16((size_t)E * vbytes);
+    L.hc0 = off;  off += a16((size_t)E * 4);
+    L.cnt = off;  off += a16((size_t)E * 4);
+    L.sel = off;  off += a16((size_t)E * 4);
+    L.stok = off; off += a16((size_t)L.R * 4);
+    L.chs = off;  off += a16((size_t)L.R * 4);
+    L.slot = off; off += a16((size_t)L.R * 4);
+    L.vst = off;  off += stage;
+    L.total = off;
+    return L;
 }
 
 // After the finalising kernel, when some expert is not full (one block per
@@ -3728,10 +3776,14 @@ inline size_t comp_lds_bytes(int E, int vbytes) {
 //     completion. Every still-unassigned token, in ascending token order,
 //     takes its best expert by S[t,e] - p[e] (ties to the lowest expert)
 //     among those with room. The unassigned tokens are first compacted into
-//     a list (all threads); then their score rows are staged in LDS (all
-//     threads) and one wave walks them in order, keeping the experts' counts
-//     in registers. The walk's result is the sequential rule's, token by
-//     token. Placed tokens join their expert's holder table.
+//     a list (all threads; a block scan orders them). Then, chunk by chunk,
+//     their rows are staged in LDS and every wave finds each staged token's
+//     best expert among those with room at the chunk's start (all waves in
+//     parallel); one wave then walks the chunk in token order with the live
+//     counts, and a token whose expert filled earlier in the walk takes its
+//     best expert again over the experts still open. The result is the
+//     sequential rule's, token by token. Placed tokens join their expert's
+//     holder table.
 //   - the rows of perm of every expert that was not full: its tokens in
 //     ascending order (when C <= kRankMaxC), then -1 for the rows it has no
 //     token for (an unconverged solve without the greedy completion).
@@ -3747,21 +3799,28 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
     if ((ld_relaxed(&ctrl->unconverged_experts) & ~(1 << 30)) == 0) return;
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int E = c.E, C = c.C, T = c.T;
-    const int R = comp_rows(E, (int)sizeof(value_t));
-    value_t *pr = reinterpret_cast<value_t *>(smem_raw);
-    int *hc0 = reinterpret_cast<int *>(smem_raw + a16((size_t)E * sizeof(value_t)));
-    int *stok = reinterpret_cast<int *>(reinterpret_cast<unsigned char *>(hc0) + a16((size_t)E * 4));
-    value_t *vst = reinterpret_cast<value_t *>(reinterpret_cast<unsigned char *>(stok) + a16((size_t)R * 4));
-    int *tok = reinterpret_cast<int *>(vst);   // the ranking's list (after the walk)
-    int *hc1 = reinterpret_cast<int *>(pr);    // counts after the walk (prices no longer needed)
-    __shared__ int s_fill, s_n, s_wsum[kCompThreads / 64];
+    const CompLds LY = comp_lds(E, C, (int)sizeof(value_t));
+    const int R = LY.R;
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw + LY.pr);
+    int *hc0 = reinterpret_cast<int *>(smem_raw + LY.hc0);
+    int *cntl = reinterpret_cast<int *>(smem_raw + LY.cnt);
+    int *sell = reinterpret_cast<int *>(smem_raw + LY.sel);
+    int *stok = reinterpret_cast<int *>(smem_raw + LY.stok);
+    int *chs = reinterpret_cast<int *>(smem_raw + LY.chs);
+    int *slot = reinterpret_cast<int *>(smem_raw + LY.slot);
+    value_t *vst = reinterpret_cast<value_t *>(smem_raw + LY.vst);
+    int *tok = reinterpret_cast<int *>(vst);   // the ranking's lists (after the walk)
+    __shared__ int s_fill, s_base, s_wsum[kCompWaves];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     for (int e = tid; e < E; e += kCompThreads) {
         pr[e] = c.prices[e];
         int h = c.hcount[e];
-        hc0[e] = h < 0 ? 0 : (h > C ? C : h);
+        h = h < 0 ? 0 : (h > C ? C : h);
+        hc0[e] = h;
+        cntl[e] = h;
+        sell[e] = c.hsel[e] & 1;
     }
     if (tid == 0) {
         s_fill = ctrl->not_converged && (flags & BASE_ASSIGN_GREEDY_FALLBACK) &&
@@ -3770,45 +3829,54 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
             ctrl->fell_back = 1;
             ctrl->unconverged_experts &= (1 << 30);
         }
+        s_base = 0;
     }
     __syncthreads();
     if (s_fill) {
         // The unassigned tokens, in ascending order, into the (no longer
-        // used) first active list: thread i counts its contiguous share,
-        // a block scan gives each share its offset.
+        // used) first active list: per pass, thread i takes kCompScan
+        // consecutive tokens into registers (16-byte loads when the caller's
+        // buffer allows), a block scan gives each thread its offset.
         int *list = c.active;
-        const int per = (T + kCompThreads - 1) / kCompThreads;
-        const int lo = tid * per < T ? tid * per : T;
-        const int hi = lo + per < T ? lo + per : T;
-        int cnt = 0;
-        for (int t = lo; t < hi; ++t) cnt += assign[t] < 0;
-        int incl = cnt;
+        const bool vec = (reinterpret_cast<uintptr_t>(assign) & 15) == 0;
+        for (int base = 0; base < T; base += kCompThreads * kCompScan) {
+            const int lo = base + tid * kCompScan;
+            int v[kCompScan];
+            if (vec && lo + kCompScan <= T) {
 #pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const int o = __shfl_up(incl, off);
-            if (lane >= off) incl += o;
-        }
-        if (lane == 63) s_wsum[wave] = incl;
-        __syncthreads();
-        int before = 0;
-        for (int w = 0; w < wave; ++w) before += s_wsum[w];
-        if (tid == kCompThreads - 1) s_n = before + incl;
-        int at = before + incl - cnt;
-        for (int t = lo; t < hi; ++t)
-            if (assign[t] < 0) list[at++] = t;
-        __syncthreads();
-        const int n = s_n;
-        // The walking wave's experts: lane l holds experts l + 64 k.
-        int cntr[kCompRegs];
-        uint32_t selm = 0;
-        if (wave == 0) {
+                for (int j = 0; j < kCompScan / 4; ++j) {
+                    const int4 q = reinterpret_cast<const int4 *>(assign + lo)[j];
+                    v[4 * j] = q.x;
+                    v[4 * j + 1] = q.y;
+                    v[4 * j + 2] = q.z;
+                    v[4 * j + 3] = q.w;
+                }
+            } else {
 #pragma unroll
-            for (int k = 0; k < kCompRegs; ++k) {
-                const int e = lane + 64 * k;
-                cntr[k] = e < E ? hc0[e] : C;
-                if (e < E) selm |= (uint32_t)(c.hsel[e] & 1) << k;
+                for (int j = 0; j < kCompScan; ++j) v[j] = lo + j < T ? assign[lo + j] : 0;
             }
+            int cnt = 0;
+#pragma unroll
+            for (int j = 0; j < kCompScan; ++j) cnt += v[j] < 0;
+            int incl = cnt;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const int o = __shfl_up(incl, off);
+                if (lane >= off) incl += o;
+            }
+            if (lane == 63) s_wsum[wave] = incl;
+            __syncthreads();
+            int before = s_base;
+            for (int w = 0; w < wave; ++w) before += s_wsum[w];
+            int at = before + incl - cnt;
+#pragma unroll
+            for (int j = 0; j < kCompScan; ++j)
+                if (v[j] < 0) list[at++] = lo + j;
+            __syncthreads();
+            if (tid == kCompThreads - 1) s_base = at;
+            __syncthreads();
         }
+        const int n = s_base;
         for (int j0 = 0; j0 < n; j0 += R) {
             const int m = n - j0 < R ? n - j0 : R;
             for (int r = tid; r < m; r += kCompThreads) {
@@ -3816,78 +3884,122 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
                 stok[r] = (t >= 0 && t < T) ? t : 0;
             }
             __syncthreads();
+#pragma unroll 8
             for (int q = tid; q < m * E; q += kCompThreads) {
                 const int r = q / E;
                 const int e = q - r * E;
                 vst[q] = M::load(c.S, (int64_t)stok[r] * E + e, c.scale) - pr[e];
             }
             __syncthreads();
-            if (wave == 0) {
-                for (int r = 0; r < m; ++r) {
-                    value_t bv = M::lowest();
-                    int be = 0x7fffffff;
-#pragma unroll
-                    for (int k = 0; k < kCompRegs; ++k) {
-                        if (64 * k >= E) break;
-                        const int e = lane + 64 * k;
-                        if (e < E && cntr[k] < C) {
-                            const value_t v = vst[r * E + e];
-                            if (v > bv) {
-                                bv = v;
-                                be = e;
-                            }
-                        }
+            // Each staged token's best expert among those open now.
+            for (int r = wave; r < m; r += kCompWaves) {
+                value_t bv = M::lowest();
+                int be = 0x7fffffff;
+                for (int e = lane; e < E; e += 64) {
+                    const value_t v = vst[r * E + e];
+                    if (cntl[e] < C && v > bv) {
+                        bv = v;
+                        be = e;
                     }
-                    wave_max_pair(bv, be);
-                    if (be < E) {
-                        const int t = stok[r];
-                        if (lane == (be & 63)) {
-                            const int kk = be >> 6;
-                            int slot = 0;
-#pragma unroll
-                            for (int k = 0; k < kCompRegs; ++k) {
-                                if (k == kk) {
-                                    slot = cntr[k];
-                                    cntr[k] = slot + 1;
+                }
+                wave_max_pair(bv, be);
+                if (lane == 0) chs[r] = be;
+            }
+            __syncthreads();
+            // The walk in token order. Lane j of a batch of 64 holds the
+            // choice of entry j; the live counts are in LDS; lane 0 records
+            // each decision (expert and slot, into chs and slot). One wave's
+            // LDS accesses take effect in program order, so the walk needs
+            // no memory wait: the empty asm statements only keep the
+            // compiler from reordering them.
+            if (wave == 0) {
+                for (int r0 = 0; r0 < m; r0 += 64) {
+                    const int cj = r0 + lane < m ? chs[r0 + lane] : 0;
+                    const int mm = m - r0 < 64 ? m - r0 : 64;
+                    for (int j = 0; j < mm; ++j) {
+                        int e = __builtin_amdgcn_readlane(cj, j);
+                        int have = e < E ? cntl[e] : C;
+                        if (have >= C) {   // (uniform) the choice filled up: again
+                            value_t bv = M::lowest();
+                            int be = 0x7fffffff;
+                            for (int e2 = lane; e2 < E; e2 += 64) {
+                                const value_t v = vst[(r0 + j) * E + e2];
+                                if (cntl[e2] < C && v > bv) {
+                                    bv = v;
+                                    be = e2;
                                 }
                             }
-                            const int sel = (selm >> kk) & 1;
-                            c.holders[(int64_t)sel * T + (int64_t)be * C + slot] =
-                                (1ull << kTokBits) | (kTokMask - (uint64_t)t);
+                            wave_max_pair(bv, be);
+                            e = be;
+                            have = e < E ? cntl[e] : C;
                         }
-                        if (lane == 0) assign[t] = be;
+                        const bool ok = e < E && have < C;
+                        if (lane == 0) {
+                            if (ok) cntl[e] = have + 1;
+                            chs[r0 + j] = ok ? e : -1;
+                            slot[r0 + j] = have;
+                        }
+                        asm volatile("" ::: "memory");
                     }
                 }
             }
             __syncthreads();
-        }
-        if (wave == 0) {
-#pragma unroll
-            for (int k = 0; k < kCompRegs; ++k) {
-                const int e = lane + 64 * k;
-                if (e < E) {
-                    c.hcount[e] = cntr[k];
-                    hc1[e] = cntr[k];
+            // The chunk's decisions into assign and the holder tables.
+            for (int r = tid; r < m; r += kCompThreads) {
+                const int e = chs[r];
+                if (e >= 0) {
+                    const int t = stok[r];
+                    c.holders[(int64_t)sell[e] * T + (int64_t)e * C + slot[r]] =
+                        (1ull << kTokBits) | (kTokMask - (uint64_t)t);
+                    assign[t] = e;
                 }
             }
+            __syncthreads();
         }
+        for (int e = tid; e < E; e += kCompThreads) c.hcount[e] = cntl[e];
         __threadfence_block();
         __syncthreads();
     }
-    for (int e = 0; e < E; ++e) {
-        if (hc0[e] >= C) continue;   // (uniform: LDS)
-        int h = s_fill ? hc1[e] : hc0[e];
+    // One wave per expert that was not full (wave-synchronous: its tokens in
+    // the wave's slice of LDS, then ranked by counting).
+    const int nrw = LY.nrw;
+    if (wave >= nrw) return;
+    const int c4 = (C + 3) & ~3;
+    int *wtok = tok + wave * c4;
+    for (int e = wave; e < E; e += nrw) {
+        if (hc0[e] >= C) continue;   // (uniform in the wave: LDS)
+        int h = cntl[e];
         h = h > C ? C : h;
         int32_t *out = perm + (int64_t)e * C;
         if (rank_perm) {
-            const uint64_t *hold = c.holders + (int64_t)(c.hsel[e] & 1) * T + (int64_t)e * C;
-            for (int i = tid; i < h; i += kCompThreads) {
-                const int t = key_token(hold[i]);
-                tok[i] = (t >= 0 && t < T) ? t : 0x7fffffff;
+            const uint64_t *hold = c.holders + (int64_t)sell[e] * T + (int64_t)e * C;
+            const int h4 = (h + 3) & ~3;
+            for (int i = lane; i < h4; i += 64) {
+                int t = 0x7fffffff;
+                if (i < h) {
+                    t = key_token(hold[i]);
+                    t = (t >= 0 && t < T) ? t : 0x7fffffff;
+                }
+                wtok[i] = t;
             }
-            rank_write(tok, h, out);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const int4 *t4 = reinterpret_cast<const int4 *>(wtok);
+            for (int i = lane; i < h; i += 64) {
+                const int t = wtok[i];
+                int r = 0;
+                for (int j = 0; j < h4 / 4; ++j) {
+                    const int4 q = t4[j];
+                    r += (q.x < t) + (q.y < t) + (q.z < t) + (q.w < t);
+                }
+                out[r] = t;   // r < h: in the expert's rows
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         }
-        for (int i = h + tid; i < C; i += kCompThreads) out[i] = -1;
+        for (int i = h + lane; i < C; i += 64) out[i] = -1;
     }
 }
 
@@ -4276,7 +4388,7 @@ hipError_t solve_mode(const void *S, const AssignParams &p, int B, int32_t *assi
     hipLaunchKernelGGL(finalise_kernel<M>, dim3(c.E, B), dim3(256), 0, s, c, assign, perm,
                        static_cast<value_t *>(prices_out), rank_perm);
     hipLaunchKernelGGL(complete_kernel<M>, dim3(1, B), dim3(kCompThreads),
-                       comp_lds_bytes(c.E, (int)sizeof(value_t)), s, c, assign, perm, p.flags,
+                       comp_lds(c.E, c.C, (int)sizeof(value_t)).total, s, c, assign, perm, p.flags,
                        rank_perm);
     if (!rank_perm) {
         int32_t *blk = reinterpret_cast<int32_t *>(ws + L.blk);
