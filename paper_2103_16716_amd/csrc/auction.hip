@@ -73,6 +73,15 @@ inline int ssp_cap_setting() {
     return (int)strtol(v, nullptr, 10);
 }
 
+// Whether the single-workgroup rounds (small_solve_kernel) serve a shape
+// that fits them: BASE_SMALL_PATH=1 always, =0 never (read at every solve;
+// tests use it to cover both paths); unset, -1: the default rule.
+inline int small_path_setting() {
+    const char *v = getenv("BASE_SMALL_PATH");
+    if (v == nullptr || *v == 0) return -1;
+    return *v == '0' ? 0 : 1;
+}
+
 // BASE_TEST_SSP_FALLBACKS=1 (tests only) sends every step of the
 // shortest-path finish through its fallback paths.
 inline int ssp_fallbacks_setting() {
@@ -3546,6 +3555,504 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
     }
 }
 
+// Wave-wide maximum of (v, i), ties to the lower i; every lane ends with it.
+template <class V>
+__device__ inline V readlane_v(V v, int l) {
+    if constexpr (sizeof(V) == 8) {
+        uint64_t u;
+        __builtin_memcpy(&u, &v, 8);
+        const uint64_t r = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l) |
+                           ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l)
+                            << 32);
+        V out;
+        __builtin_memcpy(&out, &r, 8);
+        return out;
+    } else {
+        uint32_t u;
+        __builtin_memcpy(&u, &v, 4);
+        const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)u, l);
+        V out;
+        __builtin_memcpy(&out, &r, 4);
+        return out;
+    }
+}
+template <int OFF, class V>
+__device__ __attribute__((always_inline)) inline void max_pair_step(V &v, int &i) {
+    const V ov = grp_partner<OFF>(v);
+    const int oi = grp_partner<OFF>(i);
+    const bool t = (ov > v) | ((ov == v) & (oi < i));
+    v = t ? ov : v;
+    i = t ? oi : i;
+}
+template <class V>
+__device__ inline void wave_max_pair(V &v, int &i) {
+    max_pair_step<1>(v, i);
+    max_pair_step<2>(v, i);
+    max_pair_step<4>(v, i);
+    max_pair_step<8>(v, i);
+    V rv = readlane_v(v, 0);
+    int ri = __builtin_amdgcn_readlane(i, 0);
+#pragma unroll
+    for (int q = 1; q < 4; ++q) {
+        const V ov = readlane_v(v, 16 * q);
+        const int oi = __builtin_amdgcn_readlane(i, 16 * q);
+        const bool t = (ov > rv) | ((ov == rv) & (oi < ri));
+        rv = t ? ov : rv;
+        ri = t ? oi : ri;
+    }
+    v = rv;
+    i = ri;
+}
+
+// ------------------------------------------------- single-workgroup solve --
+//
+// A problem of at most kSmallT tokens and kSmallE experts is solved whole by
+// one workgroup (one per problem of a batch, all in one launch), with every
+// piece of mutable state in LDS: the prices, each expert's C held keys with
+// the lowest of them and its slot, the active tokens and the round's bids
+// grouped by expert. It follows the same rules as the multi-kernel path:
+// Jacobi bids from the score summaries against the prices at the start of
+// the round; an expert keeps the C largest keys of its holders and its bids
+// (streamed through "a larger key replaces the lowest held key", which gives
+// the same set for any arrival order); the lowest held key is the expert's
+// price once it is full; epsilon phases begun by begin_phase_scalar, and the
+// duality check between phases with the same allowance and decision. The
+// result is therefore deterministic and carries the same guarantee.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallWaves = kSmallThreads / 64;
+constexpr int kSmallT = 2048;
+constexpr int kSmallE = 256;
+constexpr int kSmallRows = 4;   // tokens a bidding group handles per pass (loads first)
+constexpr int kSmallBatch = 8;  // batches from this size take the single-workgroup rounds
+constexpr int kSmallSoloT = 512;   // and single problems up to this many tokens
+
+struct SmallLds {
+    size_t pr, cnt, mk, ms, bcnt, boff, bfill, tch, hk, actA, actB, bkey, bexp, bsort, total;
+};
+__host__ __device__ inline SmallLds small_lds(int T, int E, int vbytes) {
+    SmallLds L{};
+    size_t off = 0;
+    L.pr = off;    off = eng_align(off + (size_t)E * vbytes);
+    L.cnt = off;   off = eng_align(off + (size_t)E * 4);
+    L.mk = off;    off = eng_align(off + (size_t)E * 8);
+    L.ms = off;    off = eng_align(off + (size_t)E * 4);
+    L.bcnt = off;  off = eng_align(off + (size_t)E * 4);
+    L.boff = off;  off = eng_align(off + (size_t)E * 4);
+    L.bfill = off; off = eng_align(off + (size_t)E * 4);
+    L.tch = off;   off = eng_align(off + (size_t)E * 4);
+    L.hk = off;    off = eng_align(off + (size_t)T * 8);
+    L.actA = off;  off = eng_align(off + (size_t)T * 4);
+    L.actB = off;  off = eng_align(off + (size_t)T * 4);
+    L.bkey = off;  off = eng_align(off + (size_t)T * 8);
+    L.bexp = off;  off = eng_align(off + (size_t)T * 4);
+    L.bsort = off; off = eng_align(off + (size_t)T * 8);
+    L.total = off;
+    return L;
+}
+
+// Wave-wide minimum of (key, slot); every lane ends with it.
+__device__ inline void wave_min_key(uint64_t &k, int &q) {
+#define BASE_KMIN_STEP(OFF)                                  \
+    {                                                        \
+        const uint64_t ok = grp_partner<OFF>(k);             \
+        const int oq = grp_partner<OFF>(q);                  \
+        const bool t = ok < k;                               \
+        k = t ? ok : k;                                      \
+        q = t ? oq : q;                                      \
+    }
+    BASE_KMIN_STEP(1)
+    BASE_KMIN_STEP(2)
+    BASE_KMIN_STEP(4)
+    BASE_KMIN_STEP(8)
+#undef BASE_KMIN_STEP
+    uint64_t rk = readlane_v(k, 0);
+    int rq = __builtin_amdgcn_readlane(q, 0);
+#pragma unroll
+    for (int l = 1; l < 4; ++l) {
+        const uint64_t ok = readlane_v(k, 16 * l);
+        const int oq = __builtin_amdgcn_readlane(q, 16 * l);
+        const bool t = ok < rk;
+        rk = t ? ok : rk;
+        rq = t ? oq : rq;
+    }
+    k = rk;
+    q = rq;
+}
+
+// Top-2 of tokens tk[u] (valid where ok[u]) from their summaries, against
+// prices pr (the whole block calls; the summary loads go first).
+template <class M, int G>
+__device__ inline void small_top2(const Ctx<M> &c, const int (&tk)[kSmallRows],
+                                  const bool (&ok)[kSmallRows], int gl,
+                                  const typename M::value_t *pr, typename M::value_t pmin,
+                                  typename M::value_t (&v1)[kSmallRows], int (&e1)[kSmallRows],
+                                  typename M::value_t (&v2)[kSmallRows],
+                                  typename M::value_t (&s1)[kSmallRows]) {
+    uint32_t sw[kSmallRows][4];
+#pragma unroll
+    for (int u = 0; u < kSmallRows; ++u) {
+        sw[u][0] = sw[u][1] = sw[u][2] = sw[u][3] = 0;
+        if (ok[u]) load_summary(c.sums, tk[u], gl, sw[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kSmallRows; ++u)
+        top2_summary<M, G>(c, sw[u], tk[u], ok[u], gl, pr, pmin, v1[u], e1[u], v2[u], s1[u]);
+}
+
+// One launch runs from the state the control block and the holder tables
+// describe (a phase just begun, a phase the shortest-path finish completed,
+// or one in progress) through as many rounds and phases as it can: it stops
+// when the solve is done, when the round bound is reached, or when at most
+// `cap` tokens of a phase are left (cap > 0: the shortest-path finish takes
+// them; the next launch continues after it), handing the state back in the
+// multi-kernel path's layout (holder table 0, active list 0).
+template <class M, int G>
+__global__ __launch_bounds__(kSmallThreads) void small_solve_kernel(Ctx<M> c0, AssignParams p,
+                                                                    int cap) {
+    using value_t = typename M::value_t;
+    const Ctx<M> c = c0.at(blockIdx.y);
+    SolveCtrl *ctrl = c.ctrl;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    const int E = c.E, C = c.C, T = c.T;
+    const SmallLds L = small_lds(T, E, (int)sizeof(value_t));
+    value_t *pr = reinterpret_cast<value_t *>(smem_raw + L.pr);
+    int *cnt = reinterpret_cast<int *>(smem_raw + L.cnt);
+    uint64_t *mk = reinterpret_cast<uint64_t *>(smem_raw + L.mk);
+    int *ms = reinterpret_cast<int *>(smem_raw + L.ms);
+    int *bcnt = reinterpret_cast<int *>(smem_raw + L.bcnt);
+    int *boff = reinterpret_cast<int *>(smem_raw + L.boff);
+    int *bfill = reinterpret_cast<int *>(smem_raw + L.bfill);
+    int *tch = reinterpret_cast<int *>(smem_raw + L.tch);
+    uint64_t *hk = reinterpret_cast<uint64_t *>(smem_raw + L.hk);
+    int *act = reinterpret_cast<int *>(smem_raw + L.actA);
+    int *nxt = reinterpret_cast<int *>(smem_raw + L.actB);
+    uint64_t *bkey = reinterpret_cast<uint64_t *>(smem_raw + L.bkey);
+    int *bexp = reinterpret_cast<int *>(smem_raw + L.bexp);
+    uint64_t *bsort = reinterpret_cast<uint64_t *>(smem_raw + L.bsort);
+    __shared__ int s_n, s_nnext, s_ntch, s_stop, s_last;
+    __shared__ value_t s_eps;
+    __shared__ double s_part[kSmallWaves], s_pmax[kSmallWaves];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int per = kSmallThreads / G;
+    const int gid = tid / G;
+    const int gl = lane & (G - 1);
+    const bool checks = !(p.flags & BASE_ASSIGN_FULL_SCHEDULE);
+
+    __shared__ int s_all, s_cur;
+    if (tid == 0) {
+        s_stop = ctrl->done || ctrl->internal_error;
+        s_all = ctrl->all_active;
+        s_cur = ctrl->cur & 1;
+        s_n = s_all ? T : ld_relaxed(&ctrl->active_count[s_cur]);
+        if (s_n < 0 || s_n > T) {
+            flag_internal(ctrl);
+            s_stop = 1;
+        }
+        s_ntch = 0;
+        s_eps = (value_t)ctrl->eps;
+        s_last = ctrl->last_phase;
+    }
+    __syncthreads();
+    if (s_stop) return;
+    // The state: prices, every expert's holders (with the lowest key and its
+    // slot), the active tokens.
+    for (int e = tid; e < E; e += kSmallThreads) {
+        pr[e] = c.prices[e];
+        int h = s_all ? 0 : ld_relaxed(&c.hcount[e]);
+        if (h < 0 || h > C) {
+            flag_internal(ctrl);
+            h = 0;
+        }
+        cnt[e] = h;
+        bcnt[e] = 0;
+        bfill[e] = 0;
+    }
+    __syncthreads();
+    for (int i = tid; i < T; i += kSmallThreads) {
+        const int e = i / C, q = i - e * C;
+        hk[i] = q < cnt[e] ? c.holders[(int64_t)(c.hsel[e] & 1) * T + i] : ~0ull;
+        if (s_all) act[i] = i;
+        else if (i < s_n) {
+            const int t = c.active[(int64_t)s_cur * T + i];
+            act[i] = (t >= 0 && t < T) ? t : 0;
+        }
+    }
+    __syncthreads();
+    for (int e = wave; e < E; e += kSmallWaves) {
+        uint64_t m = ~0ull;
+        int mq = 0;
+        for (int q = lane; q < cnt[e]; q += 64) {
+            const uint64_t v = hk[(size_t)e * C + q];
+            if (v < m) {
+                m = v;
+                mq = q;
+            }
+        }
+        wave_min_key(m, mq);
+        if (lane == 0) {
+            mk[e] = m;
+            ms[e] = mq;
+        }
+    }
+    __syncthreads();
+    // Prices only rise: their lowest value now bounds them for the whole solve.
+    const value_t pmin = block_min_price<M>(pr, E);
+    const int ctrl_rounds0 = ctrl->rounds;
+    int rounds = 0;
+    unsigned long long bids = 0;
+    while (!s_stop) {
+        const int n = s_n;
+        if (n == 0) {
+            // The phase is complete (every expert full): stop after the last
+            // phase; otherwise the duality check, then the next phase.
+            if (s_last) {
+                if (tid == 0) ctrl->done = 1;
+                break;
+            }
+            if (checks) {
+                // D(p) - objective as a sum of per-token slacks over the held
+                // tokens (slot order), in double, in a fixed order.
+                double acc = 0.0;
+                for (int i0 = 0; i0 < T; i0 += per * kSmallRows) {
+                    value_t v1[kSmallRows], v2[kSmallRows], s1[kSmallRows];
+                    int e1[kSmallRows], tk[kSmallRows];
+                    bool ok[kSmallRows];
+#pragma unroll
+                    for (int u = 0; u < kSmallRows; ++u) {
+                        const int i = i0 + gid + u * per;
+                        int t = i < T ? key_token(hk[i]) : 0;
+                        tk[u] = (t >= 0 && t < T) ? t : 0;
+                        ok[u] = i < T;
+                    }
+                    small_top2<M, G>(c, tk, ok, gl, pr, pmin, v1, e1, v2, s1);
+#pragma unroll
+                    for (int u = 0; u < kSmallRows; ++u) {
+                        const int i = i0 + gid + u * per;
+                        if (i < T && gl == 0) {
+                            const int e = i / C;
+                            acc += (double)v1[u] -
+                                   ((double)M::load(c.S, (int64_t)tk[u] * E + e, c.scale) -
+                                    (double)pr[e]);
+                        }
+                    }
+                }
+                double pm = 0.0;
+                for (int e = tid; e < E; e += kSmallThreads) pm = fmax(pm, fabs((double)pr[e]));
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    acc += __shfl_xor(acc, off);
+                    pm = fmax(pm, __shfl_xor(pm, off));
+                }
+                if (lane == 0) {
+                    s_part[wave] = acc;
+                    s_pmax[wave] = pm;
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    double gap = 0.0, pmax = 0.0;
+                    for (int w = 0; w < kSmallWaves; ++w) {
+                        gap += s_part[w];
+                        pmax = fmax(pmax, s_pmax[w]);
+                    }
+                    double allowance = 0.0;
+                    if (!M::kInteger) {
+                        const double smax = fmax(fabs((double)f32_unord(ctrl->smax_ord)),
+                                                 fabs((double)f32_unord(ctrl->smin_ord)));
+                        allowance = (double)T * ldexp(smax + pmax, -22);
+                    }
+                    if (gap + allowance <= (double)T * ctrl->eps_final_eff) {
+                        ctrl->certified = 1;
+                        ctrl->done = 1;
+                        s_stop = 1;
+                    } else {
+                        ctrl->check_gap = gap + allowance;
+                    }
+                }
+                __syncthreads();
+                if (s_stop) break;
+            }
+            if (tid == 0) {
+                begin_phase_scalar(ctrl, p, T);
+                s_eps = (value_t)ctrl->eps;
+                s_last = ctrl->last_phase;
+                s_n = T;
+            }
+            for (int e = tid; e < E; e += kSmallThreads) {
+                cnt[e] = 0;
+                mk[e] = ~0ull;
+                ms[e] = 0;
+            }
+            for (int i = tid; i < T; i += kSmallThreads) act[i] = i;
+            __syncthreads();
+            continue;
+        }
+        if (cap > 0 && n <= cap) break;   // the shortest-path finish takes the rest
+        if (ctrl_rounds0 + rounds >= p.max_rounds) {
+            if (tid == 0) {
+                ctrl->not_converged = 1;
+                ctrl->done = 1;
+            }
+            break;
+        }
+        // (1) Bids against the prices at the start of the round.
+        const value_t eps = s_eps;
+        for (int i0 = 0; i0 < n; i0 += per * kSmallRows) {
+            value_t v1[kSmallRows], v2[kSmallRows], s1[kSmallRows];
+            int e1[kSmallRows], tk[kSmallRows];
+            bool ok[kSmallRows];
+#pragma unroll
+            for (int u = 0; u < kSmallRows; ++u) {
+                const int i = i0 + gid + u * per;
+                ok[u] = i < n;
+                tk[u] = ok[u] ? act[i] : 0;
+            }
+            small_top2<M, G>(c, tk, ok, gl, pr, pmin, v1, e1, v2, s1);
+#pragma unroll
+            for (int u = 0; u < kSmallRows; ++u) {
+                const int i = i0 + gid + u * per;
+                if (i < n && gl == 0) {
+                    int ex = e1[u];
+                    value_t sc = s1[u];
+                    if (ex >= E) {
+                        ex = 0;
+                        sc = 0;   // with v2 = lowest the bid overflows and is flagged
+                    }
+                    const value_t bid = (value_t)((sc - v2[u]) + eps);
+                    int overflow = 0;
+                    const uint64_t key = M::make_key(bid, tk[u], &overflow);
+                    if (overflow) ctrl->overflow = 1;
+                    bkey[i] = key;
+                    bexp[i] = ex;
+                    if (atomicAdd(&bcnt[ex], 1) == 0) tch[atomicAdd(&s_ntch, 1)] = ex;
+                }
+            }
+        }
+        __syncthreads();
+        const int nt = s_ntch < E ? s_ntch : E;
+        // (2) Offsets of the touched experts' bids (one wave).
+        if (wave == 0) {
+            int base = 0;
+            for (int j0 = 0; j0 < nt; j0 += 64) {
+                const int j = j0 + lane;
+                const int cj = j < nt ? bcnt[tch[j]] : 0;
+                int incl = cj;
+#pragma unroll
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int o = __shfl_up(incl, off);
+                    if (lane >= off) incl += o;
+                }
+                if (j < nt) boff[tch[j]] = base + incl - cj;
+                base += __shfl(incl, 63);
+            }
+        }
+        if (tid == 0) s_nnext = 0;
+        __syncthreads();
+        // (3) The bids grouped by expert.
+        for (int i = tid; i < n; i += kSmallThreads) {
+            const int e = bexp[i];
+            const int pos = boff[e] + atomicAdd(&bfill[e], 1);
+            if (pos < T) bsort[pos] = bkey[i];
+        }
+        __syncthreads();
+        // (4) Each touched expert streams its bids through its held keys, one
+        // wave per expert (touched experts dealt to the waves in turn: a
+        // loop whose trip count is the same for every lane of a wave, so
+        // the wave stays converged through it). Lane 0 writes the LDS state;
+        // the wave's LDS accesses take effect in program order.
+        for (int j = wave; j < nt; j += kSmallWaves) {
+            const int e = tch[j];
+            const int nb = bcnt[e];
+            const int b0 = boff[e];
+            uint64_t *h = hk + (size_t)e * C;
+            int ce = cnt[e];
+            uint64_t mke = mk[e];
+            int mse = ms[e];
+            for (int k = 0; k < nb && b0 + k < T; ++k) {
+                const uint64_t b = bsort[b0 + k];
+                int out = -1;
+                if (ce < C) {
+                    if (lane == 0) h[ce] = b;
+                    if (b < mke) {
+                        mke = b;
+                        mse = ce;
+                    }
+                    ++ce;
+                } else if (b > mke) {
+                    out = key_token(mke);
+                    if (lane == 0) h[mse] = b;
+                    asm volatile("" ::: "memory");
+                    uint64_t m = ~0ull;
+                    int mq = 0;
+                    for (int q = lane; q < C; q += 64) {
+                        const uint64_t v = h[q];
+                        if (v < m) {
+                            m = v;
+                            mq = q;
+                        }
+                    }
+                    wave_min_key(m, mq);
+                    mke = m;
+                    mse = mq;
+                } else {
+                    out = key_token(b);
+                }
+                if (out >= 0 && lane == 0) {
+                    const int at = atomicAdd(&s_nnext, 1);
+                    if (at < T && out >= 0 && out < T) nxt[at] = out;
+                    else flag_internal(ctrl);
+                }
+                asm volatile("" ::: "memory");
+            }
+            if (lane == 0) {
+                cnt[e] = ce;
+                mk[e] = mke;
+                ms[e] = mse;
+                if (ce == C) pr[e] = M::key_bid(mke);
+                bcnt[e] = 0;
+                bfill[e] = 0;
+            }
+        }
+        __syncthreads();
+        rounds += 1;
+        bids += (unsigned long long)n;
+        {
+            int *tmp = act;
+            act = nxt;
+            nxt = tmp;
+        }
+        if (tid == 0) {
+            s_n = s_nnext < T ? s_nnext : T;
+            s_ntch = 0;
+            if (ctrl->internal_error) s_stop = 1;
+        }
+        __syncthreads();
+    }
+    __syncthreads();
+    // Hand the state back in the multi-kernel path's layout (holder table 0).
+    for (int e = tid; e < E; e += kSmallThreads) {
+        c.prices[e] = pr[e];
+        c.hcount[e] = cnt[e];
+        c.hsel[e] = 0;
+        c.bcount[e] = 0;
+    }
+    for (int i = tid; i < T; i += kSmallThreads) {
+        const int e = i / C, q = i - e * C;
+        if (q < cnt[e]) c.holders[i] = hk[i];
+    }
+    for (int i = tid; i < s_n; i += kSmallThreads) c.active[i] = act[i];
+    if (tid == 0) {
+        ctrl->rounds += rounds;
+        ctrl->bids += bids;
+        ctrl->cur = 0;
+        ctrl->all_active = 0;
+        ctrl->active_count[0] = s_n;
+        ctrl->active_count[1] = 0;
+        ctrl->pad0 = 0;
+    }
+}
+
 // ------------------------------------------------------------- finalising --
 
 // The finalising kernels write assign and perm from the holder tables. An
@@ -3674,55 +4181,6 @@ hipError_t launch_dual_gap(const Ctx<M> &c, int B, const int32_t *assign, hipStr
         default: hipLaunchKernelGGL((dual_gap_kernel<M, 64>), grid, dim3(kThreads), pr_bytes, s, c, assign); break;
     }
     return hipGetLastError();
-}
-
-// Wave-wide maximum of (v, i), ties to the lower i; every lane ends with it.
-template <class V>
-__device__ inline V readlane_v(V v, int l) {
-    if constexpr (sizeof(V) == 8) {
-        uint64_t u;
-        __builtin_memcpy(&u, &v, 8);
-        const uint64_t r = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l) |
-                           ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l)
-                            << 32);
-        V out;
-        __builtin_memcpy(&out, &r, 8);
-        return out;
-    } else {
-        uint32_t u;
-        __builtin_memcpy(&u, &v, 4);
-        const uint32_t r = (uint32_t)__builtin_amdgcn_readlane((int)u, l);
-        V out;
-        __builtin_memcpy(&out, &r, 4);
-        return out;
-    }
-}
-template <int OFF, class V>
-__device__ __attribute__((always_inline)) inline void max_pair_step(V &v, int &i) {
-    const V ov = grp_partner<OFF>(v);
-    const int oi = grp_partner<OFF>(i);
-    const bool t = (ov > v) | ((ov == v) & (oi < i));
-    v = t ? ov : v;
-    i = t ? oi : i;
-}
-template <class V>
-__device__ inline void wave_max_pair(V &v, int &i) {
-    max_pair_step<1>(v, i);
-    max_pair_step<2>(v, i);
-    max_pair_step<4>(v, i);
-    max_pair_step<8>(v, i);
-    V rv = readlane_v(v, 0);
-    int ri = __builtin_amdgcn_readlane(i, 0);
-#pragma unroll
-    for (int q = 1; q < 4; ++q) {
-        const V ov = readlane_v(v, 16 * q);
-        const int oi = __builtin_amdgcn_readlane(i, 16 * q);
-        const bool t = (ov > rv) | ((ov == rv) & (oi < ri));
-        rv = t ? ov : rv;
-        ri = t ? oi : ri;
-    }
-    v = rv;
-    i = ri;
 }
 
 constexpr int kCompThreads = 1024;
@@ -4259,6 +4717,57 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *as
     hipLaunchKernelGGL((prologue_kernel<M, G>), dim3(sblocks, B), dim3(kThreads), 0, s, c, p,
                        assign, rpart);
     hipLaunchKernelGGL(start_kernel<M>, dim3(1, B), dim3(256), 0, s, c, p, rpart, sblocks);
+    // Small problems: every phase's rounds in one workgroup per problem
+    // (small_solve_kernel), the shortest-path finish after each; the last
+    // slot's launch runs every phase left to the end.
+    // By default a batch of at least kSmallBatch problems (each would get a
+    // fraction of the device in the multi-kernel path; 256 worker-shape
+    // problems take 3.9 ms this way against 12.3 ms) and very small
+    // problems; a single worker-shape problem is faster with the whole
+    // device (0.88 ms against 1.20 ms).
+    const int small_set = small_path_setting();
+    const bool small_fits = c.T <= kSmallT && c.E <= kSmallE;
+    const bool small = small_fits && (small_set == 1 ||
+                                      (small_set < 0 && (B >= kSmallBatch || c.T <= kSmallSoloT)));
+    if (small) {
+        const size_t bytes = small_lds(c.T, c.E, (int)sizeof(value_t)).total;
+        const void *fn = reinterpret_cast<const void *>(&small_solve_kernel<M, G>);
+        const hipError_t err = bytes + 1024 <= (size_t)facts.optin ? lds_optin(dev, fn, bytes)
+                                                                     : hipErrorInvalidValue;
+        if (err == hipSuccess) {
+            int nslots = (p.flags & BASE_ASSIGN_FULL_SCHEDULE) ? 6 : 5;
+            if (p.eps_initial > 0.0) {
+                double e = p.eps_initial;
+                nslots = 1;
+                while (e > p.eps_final && nslots < 64) {
+                    e /= p.eps_factor;
+                    ++nslots;
+                }
+            }
+            for (int slot = 0; slot < nslots; ++slot) {
+                const bool last = slot == nslots - 1;
+                const int cap = (!last && ssp_r > 0) ? c.ssp_cap : 0;
+                hipLaunchKernelGGL((small_solve_kernel<M, G>), dim3(1, B), dim3(kSmallThreads),
+                                   bytes, s, c, p, cap);
+                if constexpr (!M::kInteger) {
+                    if (cap > 0) {
+                        hipLaunchKernelGGL(ssp_build_kernel<M>, dim3(c.E, B), dim3(kSspThreads), 0,
+                                           s, c);
+                        const dim3 g(1, B), t(kSspBlock);
+                        const int small = ssp_fallbacks_setting();
+                        switch (ssp_r) {
+                            case 32: hipLaunchKernelGGL((ssp_kernel<M, 32>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
+                            case 64: hipLaunchKernelGGL((ssp_kernel<M, 64>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
+                            default: hipLaunchKernelGGL((ssp_kernel<M, 128>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
+                        }
+                    }
+                }
+            }
+            return hipGetLastError();
+        }
+        (void)hipGetLastError();
+        debug_note("single-workgroup solve LDS opt-in refused", err);
+    }
     const size_t pr_bytes = (size_t)c.E * sizeof(value_t);
     const size_t tail_smem = pr_bytes + (size_t)c.E * sizeof(int);
     // Phase slots enqueued up front; the last one continues on its own (in

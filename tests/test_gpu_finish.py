@@ -24,6 +24,13 @@ def _gpu():
     pb.lib()
 
 
+@pytest.fixture(autouse=True)
+def _multi_kernel_path(monkeypatch):
+    # The finish belongs to the multi-kernel path: the worker shape would
+    # otherwise take the single-workgroup solve.
+    monkeypatch.setenv("BASE_SMALL_PATH", "0")
+
+
 def _scores(name):
     inp = wl.make_inputs(name)
     S = pb.affinity(*inputs_on_device(inp))

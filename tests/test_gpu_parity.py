@@ -379,10 +379,14 @@ def _worker_batch(B, seed0):
     return torch.stack(Ss).contiguous()
 
 
-def test_assign_batched_identical_to_single_solves():
+@pytest.mark.parametrize("route", [None, "1", "0"])
+def test_assign_batched_identical_to_single_solves(monkeypatch, route):
     """Sec. 3.2.1 (Sharding): B independent worker problems in one call give,
     problem by problem, exactly what base_assign gives for each alone, and
-    each meets the oracle's bound."""
+    each meets the oracle's bound; on the default route and with the
+    single-workgroup rounds forced on and off."""
+    if route is not None:
+        monkeypatch.setenv("BASE_SMALL_PATH", route)
     B = 6
     S = _worker_batch(B, 900)
     res = pb.assign_batched(S)

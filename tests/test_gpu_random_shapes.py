@@ -3,7 +3,9 @@ E from 1 to 700 (across the engine's 512-expert limit), C = T/E from 1 to
 600 (across its 512-slot limit), float and int16 scores, clustered and
 normal score distributions, the default schedule with the duality check and
 the full schedule. Each case must be balanced, carry its sort vector, and
-meet the bound (float) or the exact optimum (integer)."""
+meet the bound (float) or the exact optimum (integer). Every case runs
+twice: on the default route (the single-workgroup solve for T <= 2048 and
+E <= 256) and with that route switched off (the multi-kernel path)."""
 import numpy as np
 import pytest
 
@@ -29,8 +31,10 @@ def _cases(n=48, seed=2103):
     return out
 
 
+@pytest.mark.parametrize("small", ["1", "0"])
 @pytest.mark.parametrize("T,E,kind,integer,full,seed", _cases())
-def test_random_shape(T, E, kind, integer, full, seed):
+def test_random_shape(monkeypatch, small, T, E, kind, integer, full, seed):
+    monkeypatch.setenv("BASE_SMALL_PATH", small)
     flags = pb.BASE_ASSIGN_FULL_SCHEDULE if full else 0
     rng = np.random.Generator(np.random.PCG64(seed))
     if integer:
