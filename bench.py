@@ -253,9 +253,12 @@ def bench_batched(args) -> None:
     bytes_perm = 2 * BT * d * 2 + BT * 4
     bytes_assign = st.bids * (4 * E + 16) + BT * 8
     rl = {"affinity": bytes_aff, "assign": bytes_assign, "permute": bytes_perm}
+    small_route = st.engine_bids == 0 and st.bids > 0
+    kernel = "small_solve_kernel" if small_route else ENGINE_KERNEL
     launches = eng_launches / args.steps if eng_launches else 0.0
-    eng_avg_ms = eng_ms / eng_launches if eng_launches else float("nan")
-    eng_bytes = st.engine_bids * (4 * E + 16) / launches if launches else 0.0
+    eng_avg_ms = eng_ms / eng_launches if eng_launches else None
+    eng_bytes = ((st.bids if small_route else st.engine_bids) * (4 * E + 16) / launches
+                 if launches else 0.0)
     eng_ach = eng_bytes / (eng_avg_ms * 1e-3) / 1e9 if eng_launches else 0.0
     out = {
         "metric": f"tokens assigned/sec, {B} independent problems of T=2048,E=128,d=2048",
@@ -272,7 +275,7 @@ def bench_batched(args) -> None:
         "data": "synthetic (seeded generator; no dataset or trained weights)",
         "config": {"workload": f"t2048-e128-d2048-worker x {B}", "B": B, "T": T, "E": E, "d": d,
                    "shuffle": shuffle is not None},
-        "roofline": {"kernel": ENGINE_KERNEL, "bound": "hbm", "achieved": eng_ach,
+        "roofline": {"kernel": kernel, "bound": "hbm", "achieved": eng_ach,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": eng_ach / HBM_PEAK_GBS,
                      "traffic": None,
                      "bytes_model": "bids x (4E + 16) B over all problems: an upper bound",
@@ -570,12 +573,17 @@ def main():
     # upper bound: most bids read only the token's 64-byte summary, so the
     # counter-measured traffic (when a summary for this source is committed)
     # is reported beside it.
+    # On the single-workgroup route (no bid placed by the engine) the timed
+    # launches are those of small_solve_kernel, which places every bid.
+    small_route = st.engine_bids == 0 and st.bids > 0
+    kernel = "small_solve_kernel" if small_route else ENGINE_KERNEL
+    kernel_bids = st.bids if small_route else st.engine_bids
     launches_per_solve = eng_launches / args.steps if eng_launches else 0.0
-    eng_avg_ms = eng_ms / eng_launches if eng_launches else float("nan")
-    eng_bytes = (st.engine_bids * (4 * E + 16) / launches_per_solve
+    eng_avg_ms = eng_ms / eng_launches if eng_launches else None
+    eng_bytes = (kernel_bids * (4 * E + 16) / launches_per_solve
                  if launches_per_solve else 0.0)
     eng_ach = eng_bytes / (eng_avg_ms * 1e-3) / 1e9 if eng_launches else 0.0
-    traffic = measured_traffic(w.name)
+    traffic = None if small_route else measured_traffic(w.name)
     spread = args.seed_spread if args.seed_spread >= 0 else (5 if w.name == wl.HEADLINE else 0)
     seeds_line = seed_spread(args, w, spread) if spread > 0 else None
     out = {
@@ -597,7 +605,7 @@ def main():
                    **({"max_rounds": args.max_rounds, "completion": "greedy"}
                       if args.max_rounds > 0 else {}),
                    **({"unpermute": True} if unpermute else {})},
-        "roofline": {"kernel": ENGINE_KERNEL, "bound": "hbm", "achieved": eng_ach,
+        "roofline": {"kernel": kernel, "bound": "hbm", "achieved": eng_ach,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": eng_ach / HBM_PEAK_GBS,
                      "traffic": traffic,
                      "traffic_achieved_gbs": (traffic / (eng_avg_ms * 1e-3) / 1e9

@@ -186,7 +186,9 @@ def greedy_completion(S: np.ndarray, a: np.ndarray, p: np.ndarray) -> np.ndarray
     tokens at that moment) that maximises S[t, e] - p[e], ties to the lowest
     expert. The difference decides an index, so it is taken in the precision
     the solver uses: float32 for float scores and prices, exact int64 for
-    integer ones. Returns the completed assignment (a copy)."""
+    integer ones. S and p are in the same units (the solver's integer mode
+    keeps prices in units of 1/K of a score: pass S * K there). Returns the
+    completed assignment (a copy)."""
     S = np.asarray(S)
     T, E, C = _check_shape(S)
     out = np.asarray(a, dtype=np.int64).copy()

@@ -201,7 +201,7 @@ int assign_entry(const void *S, int s_dtype, int64_t B, int64_t T, int64_t E,
             return BASE_ERR_INVALID_ARG;
         if (!(o.eps_final > 0.0)) o.eps_final = 1e-4;
         if (!(o.eps_factor > 1.0)) o.eps_factor = kDefaultEpsFactor;
-        if (o.max_rounds <= 0) o.max_rounds = 4000000;
+        if (o.max_rounds <= 0) o.max_rounds = kDefaultMaxRounds;
         const uint32_t known = BASE_ASSIGN_GREEDY_FALLBACK | BASE_ASSIGN_SYNC_STATS |
                                BASE_ASSIGN_CHECK_FINITE | BASE_ASSIGN_WARM_PRICES |
                                BASE_ASSIGN_FULL_SCHEDULE;

@@ -73,6 +73,15 @@ inline int ssp_cap_setting() {
     return (int)strtol(v, nullptr, 10);
 }
 
+// Phases above the last end early (see end_round) once at most T / D
+// tokens are left active (BASE_EARLY_END_DIV = D, 0: never; read at every
+// solve, a tuning knob).
+inline int early_end_tokens_setting(int64_t T) {
+    const char *v = getenv("BASE_EARLY_END_DIV");
+    const long d = (v == nullptr || *v == 0) ? 32 : strtol(v, nullptr, 10);
+    return d > 0 ? (int)(T / d) : 0;
+}
+
 // Whether the single-workgroup rounds (small_solve_kernel) serve a shape
 // that fits them: BASE_SMALL_PATH=1 always, =0 never (read at every solve;
 // tests use it to cover both paths); unset, -1: the default rule.
@@ -167,6 +176,9 @@ struct Ctx {
     double *gpart;    // per-block partial sums of the phase check
     int ssp_cap;      // > 0: a phase with at most this many active tokens left is finished
                       // by shortest augmenting paths
+    int early_n;      // > 0: a phase above the last whose epsilon exceeds kEarlyRatio
+                      // eps_final ends once at most early_n tokens are left active;
+                      // < 0: every phase above the last ends at -early_n
     float *ssp_m;     // [E][E] min over tokens t of expert e of S[t,e] - S[t,x]
     uint16_t *ssp_a;  // [E][E] the holder slot of that token
     uint16_t *ssp_t;  // [E][C] the tokens of every expert's holder slots (0 past its count)
@@ -242,6 +254,7 @@ Ctx<M> make_ctx(const void *S, const AssignParams &p, char *ws) {
     c.ssp_a = reinterpret_cast<uint16_t *>(ws + L.sspa);
     c.ssp_t = reinterpret_cast<uint16_t *>(ws + L.sspt);
     c.ws_stride = (int64_t)L.total;
+    c.early_n = 0;
     return c;
 }
 
@@ -1209,10 +1222,21 @@ __device__ void update_expert(const Ctx<M> &c, int e, int next, int novf, Update
 // ------------------------------------------------------- round bookkeeping --
 
 // Called by one thread once a round's updates are complete and visible.
-__device__ inline void end_round(SolveCtrl *ctrl, int T) {
+//
+// A phase above the last whose epsilon exceeds kEarlyRatio eps_final ends
+// as soon as at most early_n tokens are left active: its assignment is only ever used by
+// the duality check, whose gap at such an epsilon could neither certify the
+// solve nor guide the next step (the measured gap stays far above both
+// T eps_final and the guided step's reach), so placing its last tokens
+// would be wasted rounds. Its prices start the next phase, as any prices
+// may: the auction's guarantee for a phase holds from every starting price.
+constexpr double kEarlyRatio = 4096.0;
+template <class M>
+__device__ inline void end_round(const Ctx<M> &c) {
+    SolveCtrl *ctrl = c.ctrl;
     const int old = ctrl->cur;
     const int nw = old ^ 1;
-    const int n = ctrl->all_active ? T : ld_relaxed(&ctrl->active_count[old]);
+    const int n = ctrl->all_active ? c.T : ld_relaxed(&ctrl->active_count[old]);
     if (n == 0) return;
     ctrl->bids += (unsigned long long)n;
     ctrl->rounds += 1;
@@ -1220,7 +1244,15 @@ __device__ inline void end_round(SolveCtrl *ctrl, int T) {
     ctrl->cur = nw;
     ctrl->all_active = 0;
     ctrl->pad0 = 0;   // overflow list count
-    if (ld_relaxed(&ctrl->active_count[nw]) == 0 && ctrl->last_phase) ctrl->done = 1;
+    const int left = ld_relaxed(&ctrl->active_count[nw]);
+    if (left == 0) {
+        if (ctrl->last_phase) ctrl->done = 1;
+    } else if (c.early_n != 0 && !ctrl->last_phase &&
+               left <= (c.early_n > 0 ? c.early_n : -c.early_n) &&
+               (c.early_n < 0 || ctrl->early_ok)) {
+        ctrl->active_count[nw] = 0;
+        ctrl->skip_check = 1;
+    }
 }
 
 // Starts the next epsilon phase (one thread). Returns false if the solve is done.
@@ -1260,6 +1292,14 @@ __device__ inline void begin_phase_scalar(SolveCtrl *ctrl, const AssignParams &p
     ctrl->active_count[ctrl->cur] = 0;
     ctrl->active_count[ctrl->cur ^ 1] = 0;
     ctrl->pad0 = 0;
+}
+
+// The early-end state of a phase just begun by begin_phase_scalar (kept out
+// of it: the single-workgroup solver, which inlines it, never ends a phase
+// early).
+__device__ inline void begin_phase_early(SolveCtrl *ctrl) {
+    ctrl->skip_check = 0;
+    ctrl->early_ok = ctrl->eps > kEarlyRatio * ctrl->eps_final_eff ? 1 : 0;
 }
 
 // ---------------------------------------------------------------- kernels --
@@ -1406,7 +1446,7 @@ __global__ __launch_bounds__(kThreads) void phase_check_kernel(Ctx<M> c0) {
     __shared__ int go;
     if (threadIdx.x == 0) {
         go = !ctrl->done && !ctrl->last_phase && ctrl->phase > 0 && !ctrl->all_active &&
-             ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
+             !ctrl->skip_check && ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
     }
     __syncthreads();
     if (!go) return;
@@ -1530,7 +1570,7 @@ __global__ void phase_begin_kernel(Ctx<M> c0, AssignParams p, int nparts) {
     if (threadIdx.x == 0) {
         const bool finished = ctrl->phase > 0 && !ctrl->all_active &&
                               ld_relaxed(&ctrl->active_count[ctrl->cur]) == 0;
-        check = nparts > 0 && !ctrl->done && !ctrl->last_phase && finished;
+        check = nparts > 0 && !ctrl->done && !ctrl->last_phase && finished && !ctrl->skip_check;
         c.bar[0] = 0;    // the round loop's barrier counts from zero in every launch
         c.bar[32] = 0;
     }
@@ -1545,6 +1585,7 @@ __global__ void phase_begin_kernel(Ctx<M> c0, AssignParams p, int nparts) {
                 (ctrl->all_active || ld_relaxed(&ctrl->active_count[ctrl->cur]) > 0);
             if (!in_progress) {
                 begin_phase_scalar(ctrl, p, c.T);
+                begin_phase_early(ctrl);
                 begin = 1;
             }
         }
@@ -1611,6 +1652,7 @@ __global__ __launch_bounds__(256) void start_kernel(Ctx<M> c0, AssignParams p, c
         c.bar[0] = 0;    // the round loop's barrier counts from zero in every launch
         c.bar[32] = 0;
         begin_phase_scalar(ctrl, p, c.T);
+        begin_phase_early(ctrl);
     }
     for (int e = threadIdx.x; e < c.E; e += blockDim.x) {
         c.hcount[e] = 0;
@@ -1673,7 +1715,7 @@ __global__ __launch_bounds__(kThreads) void update_wide_kernel(Ctx<M> c0) {
     if (last && threadIdx.x == 0) {
         __threadfence();
         ctrl->blocks_done = 0;
-        end_round(ctrl, c.T);
+        end_round<M>(c);
     }
 }
 
@@ -1779,7 +1821,7 @@ __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c0, int max_
         if (last && tid == 0) {
             __threadfence();
             ctrl->blocks_done = 0;
-            end_round(ctrl, c.T);
+            end_round<M>(c);
         }
         target += gridDim.x;
         if (!grid_barrier(c.bar, target, ctrl, poll_limit)) return;
@@ -1818,6 +1860,7 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c0, AssignParams 
                         st_stop = 1;
                     } else {
                         begin_phase_scalar(ctrl, p, c.T);
+                        begin_phase_early(ctrl);
                         st_begin = 1;
                     }
                 } else if (ctrl->rounds >= p.max_rounds) {
@@ -1853,7 +1896,7 @@ __global__ __launch_bounds__(kThreads) void tail_kernel(Ctx<M> c0, AssignParams 
         for (int i = 0; i < nt; ++i) update_expert<M>(c, touched[i], st_cur ^ 1, novf, sm);
         __threadfence_block();
         __syncthreads();
-        if (tid == 0) end_round(ctrl, c.T);
+        if (tid == 0) end_round<M>(c);
         __threadfence_block();
         __syncthreads();
     }
@@ -4681,6 +4724,15 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *as
         }
     }
     if (engine) c.engine_cap = kEngCap;
+    {
+        // Early ends of large-epsilon phases; with the full schedule no
+        // check reads any phase above the last, so each of them may end
+        // early. Not under a caller's round bound: a bounded solve keeps
+        // the assignment its rounds built for the greedy completion.
+        const int n = early_end_tokens_setting(c.T);
+        if (n > 0 && p.max_rounds >= kDefaultMaxRounds)
+            c.early_n = (p.flags & BASE_ASSIGN_FULL_SCHEDULE) ? -n : n;
+    }
     // The shortest-path finish (float mode, E <= kSspMaxE, with the engine):
     // the most unassigned tokens it takes over, as many as its LDS allows.
     size_t ssp_bytes = 0;

@@ -35,6 +35,9 @@ struct AssignParams {
     const void *warm_prices;   // non-null: initial prices ([B][E], the prices output layout)
 };
 
+// Round bound of a solve whose caller sets none (max_rounds <= 0).
+constexpr int32_t kDefaultMaxRounds = 4000000;
+
 // Device-side solver state and statistics, at the head of the workspace.
 struct SolveCtrl {
     int32_t active_count[2];
@@ -59,11 +62,13 @@ struct SolveCtrl {
     unsigned long long engine_bids;   // bids placed inside the single-workgroup engine
     double dual_gap;        // D(p) - objective after the solve (when statistics are asked for)
     int32_t certified;      // 1: stopped after a phase whose duality gap met T eps_final
-    int32_t pad3;
+    int32_t skip_check;     // 1: the current phase ended before its last tokens were placed
     double check_gap;       // duality gap measured after the last phase (0: not measured)
     int64_t scale;          // integer mode: K (scores are scaled by it); float mode: 1
     int32_t integer;        // 1: integer mode
     int32_t augmentations;  // shortest augmenting paths run over all phases
+    int32_t early_ok;       // 1: the current phase may end early (its epsilon is large)
+    int32_t pad4;
 };
 
 // The validated assign call shared by base_assign, base_assign_batched and

@@ -45,7 +45,12 @@ def _check_completion(S, rounds):
     full = pb.assign(S, max_rounds=rounds, flags=pb.BASE_ASSIGN_GREEDY_FALLBACK)
     assert full.stats.fell_back == 1 and full.stats.converged == 1
     np.testing.assert_array_equal(host(full.prices), p0)
-    want = oracle.greedy_completion(host(S), a0, p0)
+    Sh = host(S)
+    if np.issubdtype(Sh.dtype, np.integer):
+        # integer mode: prices are in scaled units, the scores times
+        # K = 2^ceil(log2(T + 1)); the rule compares both in those units
+        Sh = Sh.astype(np.int64) * (1 << int(T).bit_length())
+    want = oracle.greedy_completion(Sh, a0, p0)
     np.testing.assert_array_equal(host(full.assign), want)
     np.testing.assert_array_equal(host(full.perm), oracle.stable_perm(want, E))
     return int((a0 < 0).sum())
