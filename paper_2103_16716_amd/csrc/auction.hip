@@ -3773,7 +3773,7 @@ __global__ __launch_bounds__(kSmallThreads) void small_solve_kernel(Ctx<M> c0, A
     int *bexp = reinterpret_cast<int *>(smem_raw + L.bexp);
     uint64_t *bsort = reinterpret_cast<uint64_t *>(smem_raw + L.bsort);
     __shared__ int s_n, s_nnext, s_ntch, s_stop, s_last;
-    __shared__ value_t s_eps;
+    __shared__ value_t s_eps, s_early_eps;
     __shared__ double s_part[kSmallWaves], s_pmax[kSmallWaves];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -3796,6 +3796,8 @@ __global__ __launch_bounds__(kSmallThreads) void small_solve_kernel(Ctx<M> c0, A
         s_ntch = 0;
         s_eps = (value_t)ctrl->eps;
         s_last = ctrl->last_phase;
+        // Phases with epsilon above this end early (see end_round).
+        s_early_eps = c.early_n < 0 ? (value_t)0 : (value_t)(kEarlyRatio * ctrl->eps_final_eff);
     }
     __syncthreads();
     if (s_stop) return;
@@ -3845,16 +3847,19 @@ __global__ __launch_bounds__(kSmallThreads) void small_solve_kernel(Ctx<M> c0, A
     const int ctrl_rounds0 = ctrl->rounds;
     int rounds = 0;
     unsigned long long bids = 0;
+    const int early_lim = c.early_n > 0 ? c.early_n : -c.early_n;
     while (!s_stop) {
         const int n = s_n;
-        if (n == 0) {
+        // A large-epsilon phase above the last ends early, unchecked (see end_round).
+        const bool early = n > 0 && n <= early_lim && !s_last && s_eps > s_early_eps;
+        if (n == 0 || early) {
             // The phase is complete (every expert full): stop after the last
             // phase; otherwise the duality check, then the next phase.
             if (s_last) {
                 if (tid == 0) ctrl->done = 1;
                 break;
             }
-            if (checks) {
+            if (checks && !early) {
                 // D(p) - objective as a sum of per-token slacks over the held
                 // tokens (slot order), in double, in a fixed order.
                 double acc = 0.0;
