@@ -1770,6 +1770,46 @@ __device__ inline bool grid_barrier(uint64_t *bar, uint64_t target, SolveCtrl *c
     return ok != 0;
 }
 
+// As grid_barrier, and the block that arrives last runs on_last() (thread 0,
+// after an acquire: every block's writes before its arrival are visible)
+// before it releases the others, which then see its writes. This folds a
+// round's closing step into the barrier that ends the round instead of a
+// separate last-block counter (one fewer chain of device atomics on one
+// address per round).
+template <class F>
+__device__ inline bool grid_barrier_last(uint64_t *bar, uint64_t target, SolveCtrl *ctrl,
+                                         uint32_t poll_limit, F on_last) {
+    __shared__ int ok;
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this thread's stores are done
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        ok = 1;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        const uint64_t arrived =
+            __hip_atomic_fetch_add(bar, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1;
+        if (arrived == target) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            on_last();
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            __hip_atomic_store(bar + 32, target, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            uint32_t polls = 0;
+            while (__hip_atomic_load(bar + 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+                if (polls >= poll_limit) {
+                    flag_internal(ctrl);
+                    ok = 0;
+                    break;
+                }
+                ++polls;
+                __builtin_amdgcn_s_sleep(2);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    __syncthreads();
+    return ok != 0;
+}
+
 template <class M, int G>
 __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c0, int max_wide,
                                                              int32_t max_rounds,
@@ -1779,7 +1819,7 @@ __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c0, int max_
     extern __shared__ __align__(16) unsigned char smem_raw[];
     value_t *pr = reinterpret_cast<value_t *>(smem_raw);
     __shared__ UpdateSmem sm;
-    __shared__ int st_go, st_cur, st_all, st_n, last;
+    __shared__ int st_go, st_cur, st_all, st_n;
     SolveCtrl *ctrl = c.ctrl;
     const int tid = threadIdx.x;
     const BidSmem B = bid_smem(c.E, (int)sizeof(value_t));
@@ -1814,17 +1854,9 @@ __global__ __launch_bounds__(kThreads) void wide_loop_kernel(Ctx<M> c0, int max_
         if (!grid_barrier(c.bar, target, ctrl, poll_limit)) return;
         const int novf = min(ld_relaxed(c.ovf_count), c.T);
         for (int e = blockIdx.x; e < c.E; e += gridDim.x) update_expert<M>(c, e, st_cur ^ 1, novf, sm);
-        __threadfence();
-        __syncthreads();
-        if (tid == 0) last = atomicAdd(&ctrl->blocks_done, 1) == (int)gridDim.x - 1;
-        __syncthreads();
-        if (last && tid == 0) {
-            __threadfence();
-            ctrl->blocks_done = 0;
-            end_round<M>(c);
-        }
         target += gridDim.x;
-        if (!grid_barrier(c.bar, target, ctrl, poll_limit)) return;
+        if (!grid_barrier_last(c.bar, target, ctrl, poll_limit, [&]() { end_round<M>(c); }))
+            return;
     }
 }
 
