@@ -4162,8 +4162,9 @@ __device__ inline void rank_write(int *tok, int n, int32_t *out) {
 }
 
 // One block per expert: assign[t] = e for every held token (the prologue set
-// every entry to -1), the expert's rows of perm when it is full and C <=
-// kRankMaxC, its price into prices_out (when not NULL), and a count of the
+// every entry to -1), the expert's rows of perm when C <= kRankMaxC (its
+// tokens in ascending order, then -1 for the rows of an expert that is not
+// full), its price into prices_out (when not NULL), and a count of the
 // experts that are not full.
 template <class M>
 __global__ __launch_bounds__(256) void finalise_kernel(Ctx<M> c0, int32_t *assign, int32_t *perm,
@@ -4180,7 +4181,7 @@ __global__ __launch_bounds__(256) void finalise_kernel(Ctx<M> c0, int32_t *assig
         h = h < 0 ? 0 : c.C;
     }
     const uint64_t *hold = c.holders + (int64_t)(c.hsel[e] & 1) * c.T + (int64_t)e * c.C;
-    const bool ranked = rank_perm && h == c.C;
+    const bool ranked = rank_perm != 0;
     for (int i = threadIdx.x; i < h; i += blockDim.x) {
         const int t = key_token(hold[i]);
         const bool ok = t >= 0 && t < c.T;
@@ -4195,6 +4196,32 @@ __global__ __launch_bounds__(256) void finalise_kernel(Ctx<M> c0, int32_t *assig
     if (!ranked) return;
     __syncthreads();
     rank_write(tok, h, perm + (int64_t)e * c.C);
+    for (int i = h + (int)threadIdx.x; i < c.C; i += blockDim.x) perm[(int64_t)e * c.C + i] = -1;
+}
+
+// After the greedy completion (one block per expert): the rows of perm of
+// every expert that took tokens in it, ranked again (complete_kernel marks
+// them in the overflow-expert list, unused once the rounds have ended).
+template <class M>
+__global__ __launch_bounds__(256) void rank_filled_kernel(Ctx<M> c0, int32_t *perm) {
+    const Ctx<M> c = c0.at(blockIdx.y);
+    perm += (int64_t)blockIdx.y * c.T;
+    __shared__ __align__(16) int tok[kRankMaxC];
+    const int e = blockIdx.x;
+    if (!ld_relaxed(&c.ctrl->fell_back) || c.ovf_exp[e] == 0) return;
+    int h = c.hcount[e];
+    if (h < 0 || h > c.C) {
+        if (threadIdx.x == 0) flag_internal(c.ctrl);
+        h = h < 0 ? 0 : c.C;
+    }
+    const uint64_t *hold = c.holders + (int64_t)(c.hsel[e] & 1) * c.T + (int64_t)e * c.C;
+    for (int i = threadIdx.x; i < h; i += blockDim.x) {
+        const int t = key_token(hold[i]);
+        tok[i] = (t >= 0 && t < c.T) ? t : 0x7fffffff;
+    }
+    __syncthreads();
+    rank_write(tok, h, perm + (int64_t)e * c.C);
+    for (int i = h + (int)threadIdx.x; i < c.C; i += blockDim.x) perm[(int64_t)e * c.C + i] = -1;
 }
 
 int lanes_per_token(int64_t E);
@@ -4272,14 +4299,12 @@ constexpr int kCompScan = 32;                // tokens per thread and pass of th
 __host__ __device__ inline size_t a16(size_t x) { return (x + 15) & ~size_t(15); }
 // LDS of complete_kernel (within the default 64 KiB): prices, the counts
 // before the completion, the live counts, the holder-table selectors, the
-// staged tokens and their choices, then the staged values of R tokens (or,
-// after the walk, nrw waves' token lists for the ranking, C rounded up to 4
-// each).
+// staged tokens and their choices, then the staged values of R tokens.
 struct CompLds {
     size_t pr, hc0, cnt, sel, stok, chs, slot, vst, total;
-    int R, nrw;
+    int R;
 };
-__host__ __device__ inline CompLds comp_lds(int E, int C, int vbytes) {
+__host__ __device__ inline CompLds comp_lds(int E, int vbytes) {
     CompLds L{};
     const size_t budget = 62 * 1024;
     const size_t fixed = a16((size_t)E * vbytes) + 3 * a16((size_t)E * 4) +
@@ -4288,13 +4313,7 @@ __host__ __device__ inline CompLds comp_lds(int E, int C, int vbytes) {
     const size_t stage_max = avail < (size_t)kCompStageBytes ? avail : (size_t)kCompStageBytes;
     size_t r = stage_max / ((size_t)E * vbytes);
     L.R = r < 1 ? 1 : (r > (size_t)kCompMaxRows ? kCompMaxRows : (int)r);
-    const size_t c4 = (size_t)((C + 3) & ~3);
-    const size_t rank_max = avail < 32768 ? avail : 32768;
-    size_t w = rank_max / (c4 * 4);
-    L.nrw = C > kRankMaxC ? 1 : (w < 1 ? 1 : (w > (size_t)kCompWaves ? kCompWaves : (int)w));
-    size_t stage = (size_t)L.R * E * vbytes;
-    const size_t rank = C <= kRankMaxC ? (size_t)L.nrw * c4 * 4 : 0;
-    if (stage < rank) stage = rank;
+    const size_t stage = (size_t)L.R * E * vbytes;
     size_t off = 0;
     L.pr = off;   off += a16((size_t)E * vbytes);
     L.hc0 = off;  off += a16((size_t)E * 4);
@@ -4308,36 +4327,31 @@ __host__ __device__ inline CompLds comp_lds(int E, int C, int vbytes) {
     return L;
 }
 
-// After the finalising kernel, when some expert is not full (one block per
-// problem; returns at once otherwise):
-//   - with BASE_ASSIGN_GREEDY_FALLBACK, after max_rounds: the greedy
-//     completion. Every still-unassigned token, in ascending token order,
-//     takes its best expert by S[t,e] - p[e] (ties to the lowest expert)
-//     among those with room. The unassigned tokens are first compacted into
-//     a list (all threads; a block scan orders them). Then, chunk by chunk,
-//     their rows are staged in LDS and every wave finds each staged token's
-//     best expert among those with room at the chunk's start (all waves in
-//     parallel); one wave then walks the chunk in token order with the live
-//     counts, and a token whose expert filled earlier in the walk takes its
-//     best expert again over the experts still open. The result is the
-//     sequential rule's, token by token. Placed tokens join their expert's
-//     holder table.
-//   - the rows of perm of every expert that was not full: its tokens in
-//     ascending order (when C <= kRankMaxC), then -1 for the rows it has no
-//     token for (an unconverged solve without the greedy completion).
+// With BASE_ASSIGN_GREEDY_FALLBACK, after the finalising kernel, when some
+// expert is not full after max_rounds (one block per problem; returns at
+// once otherwise): the greedy completion. Every still-unassigned token, in
+// ascending token order, takes its best expert by S[t,e] - p[e] (ties to
+// the lowest expert) among those with room. The unassigned tokens are first
+// compacted into a list (all threads; a block scan orders them). Then, chunk
+// by chunk, their rows are staged in LDS and every wave finds each staged
+// token's best expert among those with room at the chunk's start (all waves
+// in parallel); one wave then walks the chunk in token order with the live
+// counts, and a token whose expert filled earlier in the walk takes its best
+// expert again over the experts still open. The result is the sequential
+// rule's, token by token. Placed tokens join their expert's holder table;
+// the experts that took any are marked for rank_filled_kernel, which ranks
+// their rows of perm again (one block each).
 template <class M>
 __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32_t *assign,
-                                                                int32_t *perm, uint32_t flags,
-                                                                int rank_perm) {
+                                                                uint32_t flags) {
     using value_t = typename M::value_t;
     const Ctx<M> c = c0.at(blockIdx.y);
     assign += (int64_t)blockIdx.y * c.T;
-    perm += (int64_t)blockIdx.y * c.T;
     SolveCtrl *ctrl = c.ctrl;
     if ((ld_relaxed(&ctrl->unconverged_experts) & ~(1 << 30)) == 0) return;
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int E = c.E, C = c.C, T = c.T;
-    const CompLds LY = comp_lds(E, C, (int)sizeof(value_t));
+    const CompLds LY = comp_lds(E, (int)sizeof(value_t));
     const int R = LY.R;
     value_t *pr = reinterpret_cast<value_t *>(smem_raw + LY.pr);
     int *hc0 = reinterpret_cast<int *>(smem_raw + LY.hc0);
@@ -4347,7 +4361,6 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
     int *chs = reinterpret_cast<int *>(smem_raw + LY.chs);
     int *slot = reinterpret_cast<int *>(smem_raw + LY.slot);
     value_t *vst = reinterpret_cast<value_t *>(smem_raw + LY.vst);
-    int *tok = reinterpret_cast<int *>(vst);   // the ranking's lists (after the walk)
     __shared__ int s_fill, s_base, s_wsum[kCompWaves];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -4494,50 +4507,10 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
             }
             __syncthreads();
         }
-        for (int e = tid; e < E; e += kCompThreads) c.hcount[e] = cntl[e];
-        __threadfence_block();
-        __syncthreads();
-    }
-    // One wave per expert that was not full (wave-synchronous: its tokens in
-    // the wave's slice of LDS, then ranked by counting).
-    const int nrw = LY.nrw;
-    if (wave >= nrw) return;
-    const int c4 = (C + 3) & ~3;
-    int *wtok = tok + wave * c4;
-    for (int e = wave; e < E; e += nrw) {
-        if (hc0[e] >= C) continue;   // (uniform in the wave: LDS)
-        int h = cntl[e];
-        h = h > C ? C : h;
-        int32_t *out = perm + (int64_t)e * C;
-        if (rank_perm) {
-            const uint64_t *hold = c.holders + (int64_t)sell[e] * T + (int64_t)e * C;
-            const int h4 = (h + 3) & ~3;
-            for (int i = lane; i < h4; i += 64) {
-                int t = 0x7fffffff;
-                if (i < h) {
-                    t = key_token(hold[i]);
-                    t = (t >= 0 && t < T) ? t : 0x7fffffff;
-                }
-                wtok[i] = t;
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            const int4 *t4 = reinterpret_cast<const int4 *>(wtok);
-            for (int i = lane; i < h; i += 64) {
-                const int t = wtok[i];
-                int r = 0;
-                for (int j = 0; j < h4 / 4; ++j) {
-                    const int4 q = t4[j];
-                    r += (q.x < t) + (q.y < t) + (q.z < t) + (q.w < t);
-                }
-                out[r] = t;   // r < h: in the expert's rows
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        for (int e = tid; e < E; e += kCompThreads) {
+            c.hcount[e] = cntl[e];
+            c.ovf_exp[e] = cntl[e] != hc0[e] ? 1 : 0;   // rows for rank_filled_kernel
         }
-        for (int i = h + lane; i < C; i += 64) out[i] = -1;
     }
 }
 
@@ -4987,13 +4960,17 @@ hipError_t solve_mode(const void *S, const AssignParams &p, int B, int32_t *assi
     }
 
     // assign, perm (ranked per expert when C <= kRankMaxC) and the prices;
-    // then the greedy completion and the rows of experts that are not full.
+    // with the fallback flag, the greedy completion and the rows of perm of
+    // the experts it filled.
     const int rank_perm = c.C <= kRankMaxC ? 1 : 0;
     hipLaunchKernelGGL(finalise_kernel<M>, dim3(c.E, B), dim3(256), 0, s, c, assign, perm,
                        static_cast<value_t *>(prices_out), rank_perm);
-    hipLaunchKernelGGL(complete_kernel<M>, dim3(1, B), dim3(kCompThreads),
-                       comp_lds(c.E, c.C, (int)sizeof(value_t)).total, s, c, assign, perm, p.flags,
-                       rank_perm);
+    if (p.flags & BASE_ASSIGN_GREEDY_FALLBACK) {
+        hipLaunchKernelGGL(complete_kernel<M>, dim3(1, B), dim3(kCompThreads),
+                           comp_lds(c.E, (int)sizeof(value_t)).total, s, c, assign, p.flags);
+        if (rank_perm)
+            hipLaunchKernelGGL(rank_filled_kernel<M>, dim3(c.E, B), dim3(256), 0, s, c, perm);
+    }
     if (!rank_perm) {
         int32_t *blk = reinterpret_cast<int32_t *>(ws + L.blk);
         hipLaunchKernelGGL(block_count_kernel, dim3((unsigned)L.nblk, B), dim3(kCountTile),
