@@ -4448,7 +4448,7 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
                 int be = 0x7fffffff;
                 for (int e = lane; e < E; e += 64) {
                     const value_t v = vst[r * E + e];
-                    if (cntl[e] < C && v > bv) {
+                    if (cntl[e] < C && (v > bv || be == 0x7fffffff)) {
                         bv = v;
                         be = e;
                     }
@@ -4458,12 +4458,64 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
             }
             __syncthreads();
             // The walk in token order. Lane j of a batch of 64 holds the
-            // choice of entry j; the live counts are in LDS; lane 0 records
-            // each decision (expert and slot, into chs and slot). One wave's
-            // LDS accesses take effect in program order, so the walk needs
-            // no memory wait: the empty asm statements only keep the
-            // compiler from reordering them.
-            if (wave == 0) {
+            // choice of entry j. With E <= 128 the live counts sit in two
+            // registers (lane l: experts l and l + 64) and each decision is
+            // a few cross-lane reads; otherwise they are in LDS. Lane 0
+            // records each decision (expert and slot, into chs and slot).
+            // One wave's LDS accesses take effect in program order, so the
+            // walk needs no memory wait: the empty asm statements only keep
+            // the compiler from reordering them.
+            if (wave == 0 && E <= 128) {
+                int cnt0 = lane < E ? cntl[lane] : C;   // experts past E count as full
+                int cnt1 = lane + 64 < E ? cntl[lane + 64] : C;
+                for (int r0 = 0; r0 < m; r0 += 64) {
+                    const int cj = r0 + lane < m ? chs[r0 + lane] : 0;
+                    const int mm = m - r0 < 64 ? m - r0 : 64;
+                    int de = -1, ds = 0;   // lane j: the decision on entry j
+                    // The entry's values for a second choice, read one entry
+                    // ahead (a choice that filled up is common once few
+                    // slots are left, and the LDS read is then not waited for).
+                    value_t nv0 = vst[r0 * E + (lane < E ? lane : 0)];
+                    value_t nv1 = vst[r0 * E + (lane + 64 < E ? lane + 64 : 0)];
+                    for (int j = 0; j < mm; ++j) {
+                        const value_t v0 = nv0, v1 = nv1;
+                        if (j + 1 < mm) {
+                            nv0 = vst[(r0 + j + 1) * E + (lane < E ? lane : 0)];
+                            nv1 = vst[(r0 + j + 1) * E + (lane + 64 < E ? lane + 64 : 0)];
+                        }
+                        int e = __builtin_amdgcn_readlane(cj, j);
+                        int have = e < 64 ? __builtin_amdgcn_readlane(cnt0, e & 63)
+                                          : (e < E ? __builtin_amdgcn_readlane(cnt1, e & 63) : C);
+                        if (have >= C) {   // (uniform) the choice filled up: again
+                            const bool o0 = cnt0 < C, o1 = lane + 64 < E && cnt1 < C;
+                            value_t bv = o0 ? v0 : M::lowest();
+                            int be = o0 ? lane : 0x7fffffff;
+                            const bool t1 = o1 && v1 > bv;
+                            bv = t1 ? v1 : bv;
+                            be = t1 ? lane + 64 : be;
+                            wave_max_pair(bv, be);
+                            e = be;
+                            have = e < 64 ? __builtin_amdgcn_readlane(cnt0, e & 63)
+                                          : (e < E ? __builtin_amdgcn_readlane(cnt1, e & 63) : C);
+                        }
+                        const bool ok = e < E && have < C;
+                        if (ok && lane == (e & 63)) {
+                            if (e < 64) cnt0 += 1;
+                            else cnt1 += 1;
+                        }
+                        if (lane == j) {
+                            de = ok ? e : -1;
+                            ds = have;
+                        }
+                    }
+                    if (lane < mm) {
+                        chs[r0 + lane] = de;
+                        slot[r0 + lane] = ds;
+                    }
+                }
+                if (lane < E) cntl[lane] = cnt0;
+                if (lane + 64 < E) cntl[lane + 64] = cnt1;
+            } else if (wave == 0) {
                 for (int r0 = 0; r0 < m; r0 += 64) {
                     const int cj = r0 + lane < m ? chs[r0 + lane] : 0;
                     const int mm = m - r0 < 64 ? m - r0 : 64;
@@ -4475,7 +4527,7 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
                             int be = 0x7fffffff;
                             for (int e2 = lane; e2 < E; e2 += 64) {
                                 const value_t v = vst[(r0 + j) * E + e2];
-                                if (cntl[e2] < C && v > bv) {
+                                if (cntl[e2] < C && (v > bv || be == 0x7fffffff)) {
                                     bv = v;
                                     be = e2;
                                 }
