@@ -171,6 +171,132 @@ __global__ __launch_bounds__(1024) void greedy_offsets_kernel(int32_t *offsets, 
     }
 }
 
+// The placement after greedy_count_kernel, in one launch: every block takes
+// kPlaceTiles consecutive count tiles (one token per thread). Each block
+// reads the whole tile-count matrix (coalesced rows, many loads in flight)
+// into the experts' totals and the counts of the tiles before its own,
+// scans the totals into the expert offsets (block 0 writes offsets[0..E]),
+// and places every token at
+//     offsets[a] + (tokens of a in all earlier tiles)
+//                + (rank of t among its own tile's tokens of a),
+// the stable counting sort of greedy_scatter_kernel. E <= kPlaceMaxE.
+constexpr int kPlaceTiles = 16;
+constexpr int kPlaceThreads = kPlaceTiles * kGreedyTile;   // 1024
+constexpr int kPlaceMaxE = 512;
+
+__global__ __launch_bounds__(kPlaceThreads) void greedy_place_kernel(const int32_t *assign, int T,
+                                                                     int E, const int32_t *blk,
+                                                                     int nblk, int32_t *offsets,
+                                                                     int32_t *perm) {
+    __shared__ int tot[kPlaceMaxE];                  // totals, then exclusive offsets
+    __shared__ int own[kPlaceTiles + 1][kPlaceMaxE];  // counts before each of the block's tiles
+    __shared__ int part[kPlaceThreads / 64];
+    __shared__ int loc[kPlaceThreads];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int tile0 = blockIdx.x * kPlaceTiles;
+    for (int i = tid; i < (kPlaceTiles + 1) * kPlaceMaxE; i += kPlaceThreads) (&own[0][0])[i] = 0;
+    for (int e = tid; e < E; e += kPlaceThreads) tot[e] = 0;
+    __syncthreads();
+    // (1) Thread (c, r): column c of the counts, rows r, r + rows, ...;
+    // totals and the tiles before the block's first by LDS atomics, the
+    // block's own tiles by row. Four columns per 16-byte load when E allows.
+    if ((E & 3) == 0) {
+        const int q4 = E / 4;
+        const int rows = kPlaceThreads / q4;
+        const int c = tid % q4, r0 = tid / q4;
+        if (r0 < rows) {
+            int tb[4] = {0, 0, 0, 0}, ta[4] = {0, 0, 0, 0};
+            const int4 *b4 = reinterpret_cast<const int4 *>(blk);
+            for (int b0 = r0; b0 < nblk; b0 += 16 * rows) {
+                int4 v[16];
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const int b = b0 + u * rows;
+                    v[u] = b < nblk ? b4[(int64_t)b * q4 + c] : make_int4(0, 0, 0, 0);
+                }
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const int b = b0 + u * rows;
+                    const int w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        if (b < tile0) tb[k] += w[k];
+                        else ta[k] += w[k];
+                        if (b >= tile0 && b < tile0 + kPlaceTiles) own[b - tile0 + 1][4 * c + k] = w[k];
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                atomicAdd(&own[0][4 * c + k], tb[k]);
+                atomicAdd(&tot[4 * c + k], tb[k] + ta[k]);
+            }
+        }
+    } else {
+    const int rows = kPlaceThreads / E;   // >= 2 as E <= kPlaceMaxE
+    const int c = tid % E, r0 = tid / E;
+    if (r0 < rows) {
+        int tb = 0, ta = 0;
+        for (int b0 = r0; b0 < nblk; b0 += 8 * rows) {
+            int v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int b = b0 + u * rows;
+                v[u] = b < nblk ? blk[(int64_t)b * E + c] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int b = b0 + u * rows;
+                if (b < tile0) tb += v[u];
+                else ta += v[u];
+                if (b >= tile0 && b < tile0 + kPlaceTiles) own[b - tile0 + 1][c] = v[u];
+            }
+        }
+        atomicAdd(&own[0][c], tb);
+        atomicAdd(&tot[c], tb + ta);
+    }
+    }
+    const int t = tile0 * kGreedyTile + tid;
+    const int a = t < T ? assign[t] : -1;
+    loc[tid] = a;
+    __syncthreads();
+    // (2) own[q][e]: tokens of e in every tile before the block's tile q
+    for (int e = tid; e < E; e += kPlaceThreads) {
+        int run = own[0][e];
+        for (int q = 1; q <= kPlaceTiles; ++q) {
+            const int v = own[q][e];
+            own[q][e] = run;
+            run += v;
+        }
+        own[0][e] = 0;
+    }
+    // exclusive scan of the totals over the experts
+    {
+        const int v = tid < E ? tot[tid] : 0;
+        int incl = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(incl, off);
+            if (lane >= off) incl += o;
+        }
+        if (lane == 63) part[wave] = incl;
+        __syncthreads();
+        int base = 0;
+        for (int w = 0; w < wave; ++w) base += part[w];
+        if (tid < E) tot[tid] = base + incl - v;
+        if (blockIdx.x == 0 && tid < E) offsets[tid + 1] = base + incl;
+        if (blockIdx.x == 0 && tid == 0) offsets[0] = 0;
+    }
+    __syncthreads();
+    if (a < 0 || a >= E) return;
+    // (3) the token's place
+    const int tl = tid / kGreedyTile;
+    int pos = tot[a] + own[tl + 1][a];
+    for (int j = tl * kGreedyTile; j < tid; ++j) pos += (loc[j] == a);
+    if (pos >= 0 && pos < T) perm[pos] = t;
+}
+
 // perm[offsets[a] + blk[block][a] + rank of t among the block's tokens of a] = t.
 __global__ __launch_bounds__(kGreedyTile) void greedy_scatter_kernel(const int32_t *assign, int T,
                                                                      int E, const int32_t *blk,
@@ -387,6 +513,12 @@ hipError_t launch_greedy(const float *S, int64_t T, int64_t E, int32_t *assign, 
     int32_t *blk = static_cast<int32_t *>(workspace);
     hipLaunchKernelGGL(greedy_count_kernel, dim3(nblk), dim3(256), (size_t)E * sizeof(int), s, S,
                        (int)T, (int)E, assign, blk);
+    if (E <= kPlaceMaxE) {
+        const int pblk = (nblk + kPlaceTiles - 1) / kPlaceTiles;
+        hipLaunchKernelGGL(greedy_place_kernel, dim3(pblk), dim3(kPlaceThreads), 0, s, assign,
+                           (int)T, (int)E, blk, nblk, offsets, perm);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(greedy_scan_kernel, dim3((unsigned)E), dim3(256), 0, s, blk, nblk, (int)E,
                        offsets);
     hipLaunchKernelGGL(greedy_offsets_kernel, dim3(1), dim3(1024), 0, s, offsets, (int)E);
