@@ -57,7 +57,7 @@ constexpr int kCheckBlocks = 4096;     // largest grid of the phase check
 // Experts the shortest-path finish serves: its exchange matrix then takes 16
 // registers per thread (64 at E = 256 would leave too few for the rest of
 // the kernel at 1024 threads).
-constexpr int kSspMaxE = 128;
+constexpr int kSspMaxE = 256;
 
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -3047,6 +3047,9 @@ __global__ __launch_bounds__(kSspThreads) void ssp_build_kernel(Ctx<M> c0) {
 // slots [E][C] as u16 tokens (T <= 65536).
 template <int Ep>
 struct SspLds {
+    // Ep = 256: the slot matrix and the token lists stay in global memory
+    // (the workspace tables the build kernel wrote); they would not fit.
+    static constexpr bool kGlobal = Ep > 128;
     static constexpr size_t distp = 0;                       // u64 [3][Ep]
     static constexpr size_t rckey = distp + 3 * Ep * 8;      // u64 [kSspMnew][Ep]
     static constexpr size_t pr = rckey + kSspMnew * Ep * 8;  // f32 [Ep]
@@ -3062,12 +3065,12 @@ struct SspLds {
     static constexpr size_t vstar = act + kSspMaxCap * 4;
     static constexpr size_t mnew = vstar + kSspMaxCap * 4;   // f32 [kSspMnew][Ep]
     static constexpr size_t am = mnew + kSspMnew * Ep * 4;   // u16 [Ep][Ep]
-    static constexpr size_t rows = am + (size_t)Ep * Ep * 2; // f32 [E][K + 1]
+    static constexpr size_t rows = am + (kGlobal ? 0 : (size_t)Ep * Ep * 2); // f32 [E][K + 1]
     __host__ __device__ static size_t toks(int E, int K) {
         return (rows + (size_t)E * (K + 1) * 4 + 15) & ~size_t(15);
     }
     __host__ __device__ static size_t total(int E, int K, int C) {
-        return toks(E, K) + (size_t)E * C * 2;
+        return toks(E, K) + (kGlobal ? 0 : (size_t)E * C * 2);
     }
 };
 
@@ -3081,7 +3084,8 @@ inline size_t ssp_lds_bytes(int E, int K, int C) {
     switch (ssp_pad(E)) {
         case 32: return SspLds<32>::total(E, K, C);
         case 64: return SspLds<64>::total(E, K, C);
-        default: return SspLds<128>::total(E, K, C);
+        case 128: return SspLds<128>::total(E, K, C);
+        default: return SspLds<256>::total(E, K, C);
     }
 }
 
@@ -3134,15 +3138,22 @@ __device__ inline void wave_min_pair(float &v, int &i) {
 // l + 64 j. (With 16 waves the per-step work of every wave queued four deep
 // on each SIMD; the relaxations themselves are few after the first step.)
 constexpr int kSspBlock = 256;
-constexpr int kSspWaves = kSspBlock / 64;
+// Ep = 256: eight waves (two per SIMD), 32 rows of 4 columns each in
+// registers per lane; the arcs' M(e,x) + p_x are formed where they are used
+// instead of kept in a second array (registers).
+template <int Ep>
+constexpr int ssp_block() { return Ep > 128 ? 512 : kSspBlock; }
 
 // small != 0 (tests only) routes every step through the fallbacks: no
 // recompute list (whole rows instead) and received rows read by the owners.
 template <class M, int Ep>
-__global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int small) {
+__global__ __launch_bounds__(ssp_block<Ep>()) void ssp_kernel(Ctx<M> c0, int K, int small) {
     static_assert(!M::kInteger, "the shortest-path finish runs in float mode");
-    constexpr int RW = Ep / kSspWaves;           // rows per wave
+    constexpr int kBlk = ssp_block<Ep>();
+    constexpr int kW = kBlk / 64;
+    constexpr int RW = Ep / kW;                  // rows per wave
     constexpr int CL = Ep >= 64 ? Ep / 64 : 1;   // columns per lane
+    constexpr bool kG = SspLds<Ep>::kGlobal;
     const Ctx<M> c = c0.at(blockIdx.y);
     SolveCtrl *ctrl = c.ctrl;
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -3161,7 +3172,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
     int *act = reinterpret_cast<int *>(smem_raw + LY::act);
     float *vstar = reinterpret_cast<float *>(smem_raw + LY::vstar);
     float *mnew = reinterpret_cast<float *>(smem_raw + LY::mnew);
-    uint16_t *am = reinterpret_cast<uint16_t *>(smem_raw + LY::am);
+    uint16_t *am = kG ? c.ssp_a : reinterpret_cast<uint16_t *>(smem_raw + LY::am);
     float *rowsT = reinterpret_cast<float *>(smem_raw + LY::rows);
     __shared__ int s_go, s_n, s_cur, s_flag[3], s_L, s_i, s_u, s_err, s_nrc, s_full;
 
@@ -3170,7 +3181,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
     const int wave = tid >> 6;
     const int E = c.E, C = c.C, T = c.T;
     const int KS = K + 1;   // stride of the transposed rows
-    uint16_t *toks = reinterpret_cast<uint16_t *>(smem_raw + LY::toks(E, K));
+    uint16_t *toks = kG ? c.ssp_t : reinterpret_cast<uint16_t *>(smem_raw + LY::toks(E, K));
     const int e0 = wave * RW;   // this wave's rows
     const int rc_cap = small ? 0 : kSspRc;
     const int mn_cap = small ? 1 : kSspMnew;
@@ -3188,7 +3199,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
     if (!s_go) return;
     // State into LDS and registers: prices, counts, holder selectors, every
     // expert's held tokens, the slot matrix, the unassigned tokens' rows.
-    for (int e = tid; e < Ep; e += kSspBlock) {
+    for (int e = tid; e < Ep; e += kBlk) {
         const bool real = e < E;
         pr[e] = real ? c.prices[e] : 0.0f;
         int h = real ? ld_relaxed(&c.hcount[e]) : C;
@@ -3204,15 +3215,15 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
     // The token table and the slot matrix as the build kernel wrote them:
     // 16-byte loads, all in flight together (one element at a time, the
     // setup took 65 us of dependent loads at T = 32768).
-    {
+    if constexpr (!kG) {
         const int nt16 = (E * C * 2) / 16;
-        copy16_to_lds<kSspBlock>(reinterpret_cast<uint4 *>(toks),
-                                 reinterpret_cast<const uint4 *>(c.ssp_t), nt16);
-        for (int i = nt16 * 8 + tid; i < E * C; i += kSspBlock) toks[i] = c.ssp_t[i];
+        copy16_to_lds<kBlk>(reinterpret_cast<uint4 *>(toks),
+                            reinterpret_cast<const uint4 *>(c.ssp_t), nt16);
+        for (int i = nt16 * 8 + tid; i < E * C; i += kBlk) toks[i] = c.ssp_t[i];
         const int na16 = (E * E * 2) / 16;
-        copy16_to_lds<kSspBlock>(reinterpret_cast<uint4 *>(am),
-                                 reinterpret_cast<const uint4 *>(c.ssp_a), na16);
-        for (int i = na16 * 8 + tid; i < E * E; i += kSspBlock) am[i] = c.ssp_a[i];
+        copy16_to_lds<kBlk>(reinterpret_cast<uint4 *>(am),
+                            reinterpret_cast<const uint4 *>(c.ssp_a), na16);
+        for (int i = na16 * 8 + tid; i < E * E; i += kBlk) am[i] = c.ssp_a[i];
     }
     if (tid < s_n) {
         int t = c.active[(int64_t)s_cur * T + tid];
@@ -3225,7 +3236,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
     }
     __syncthreads();
     // The unassigned tokens' rows, transposed (all loads of the pass in flight).
-    for (int q = tid; q < s_n * E; q += kSspBlock) {
+    for (int q = tid; q < s_n * E; q += kBlk) {
         const int i = q / E, y = q - i * E;
         rowsT[y * KS + i] = c.S[(int64_t)act[i] * E + y];
     }
@@ -3277,15 +3288,19 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
         }
         // The arcs at the current prices: M(e,x) + p_x, and -p_e per row;
         // which of this lane's experts have room.
-        float mp[RW][CL];
+        float mp[kG ? 1 : RW][CL];
+        float pxl[CL];
         bool room[CL];
 #pragma unroll
         for (int j = 0; j < CL; ++j) {
             const int x = lane + 64 * j;
             const float px = x < E ? pr[x] : 0.0f;
+            pxl[j] = px;
             room[j] = x < E && cnt[x] < C;
+            if constexpr (!kG) {
 #pragma unroll
-            for (int r = 0; r < RW; ++r) mp[r][j] = mreg[r][j] + px;
+                for (int r = 0; r < RW; ++r) mp[r][j] = mreg[r][j] + px;
+            }
         }
         const float prow = lane < RW ? pr[e0 + lane] : 0.0f;   // lane r: price of row r
         float dused = INFINITY;                                 // lane r: dist row r was relaxed at
@@ -3341,7 +3356,8 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
                 const float q = de - __int_as_float(__builtin_amdgcn_readlane(__float_as_int(prow), r));
 #pragma unroll
                 for (int j = 0; j < CL; ++j) {
-                    const float cand = fmaxf(q + mp[r][j], de);
+                    const float mpv = kG ? mreg[r][j] + pxl[j] : mp[kG ? 0 : r][j];
+                    const float cand = fmaxf(q + mpv, de);
                     const bool t = cand < best[j];
                     best[j] = t ? cand : best[j];
                     bj[j] = t ? e0 + r : bj[j];
@@ -3415,11 +3431,11 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
         // (A) New prices; the slot each expert on the path hands on and its
         // token; the columns whose cheapest token leaves (queued for a
         // recompute); the placed token's row.
-        for (int y = tid; y < E; y += kSspBlock) {
+        for (int y = tid; y < E; y += kBlk) {
             pr[y] = pr[y] + fmaxf(D - ssp_dist(dfin[y]), 0.0f);
             urow[y] = rowsT[y * KS + iu];
         }
-        for (int j = tid; j < L; j += kSspBlock) {
+        for (int j = tid; j < L; j += kBlk) {
             const int e = path[j];
             const int q = am[e * E + path[j + 1]];
             hslot[j] = q;
@@ -3429,7 +3445,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
                 s_err = 1;
             }
         }
-        for (int i = tid; i < L * E; i += kSspBlock) {
+        for (int i = tid; i < L * E; i += kBlk) {
             const int j = i / E, x = i - j * E;
             const int e = path[j];
             if (am[e * E + x] == am[e * E + path[j + 1]]) {
@@ -3453,7 +3469,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
         const int nrc = s_nrc < rc_cap ? s_nrc : rc_cap;
         const int full = s_full;
         auto token_in = [&](int j) -> int { return j == 0 ? u : htok[j - 1]; };
-        for (int j = tid; j <= L; j += kSspBlock) {
+        for (int j = tid; j <= L; j += kBlk) {
             const int e = path[j];
             const int q = j < L ? hslot[j] : cnt[e];
             if (q < C) {
@@ -3470,7 +3486,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
             const int nm = nmn * E;
             const int nitems = nm + nrc * C;
 #pragma unroll 4
-            for (int i = tid; i < nitems; i += kSspBlock) {
+            for (int i = tid; i < nitems; i += kBlk) {
                 if (i < nm) {
                     const int j = i / E, x = i - j * E;
                     const int e = path[j];
@@ -3569,7 +3585,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
                     const int x = lane + 64 * jj;
                     if (x >= E) continue;
                     uint64_t bk = ~0ull;
-                    for (int q = wave; q < cnt[e]; q += kSspWaves) {
+                    for (int q = wave; q < cnt[e]; q += kW) {
                         const int t = q == q_out ? t_in : (int)toks[e * C + q];
                         const float v = c.S[(int64_t)t * E + e] - c.S[(int64_t)t * E + x];
                         const uint64_t key = ssp_entry(v, q);
@@ -3596,12 +3612,12 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
         }
         // The token lists, the unassigned list and the free expert's count
         // follow the path.
-        for (int j = tid; j <= L; j += kSspBlock) {
+        for (int j = tid; j <= L; j += kBlk) {
             const int e = path[j];
             const int q = j < L ? hslot[j] : cnt[e];
             if (q < C) toks[e * C + q] = (uint16_t)token_in(j);
         }
-        for (int y = tid; y < E; y += kSspBlock) rowsT[y * KS + iu] = rowsT[y * KS + k - 1];
+        for (int y = tid; y < E; y += kBlk) rowsT[y * KS + iu] = rowsT[y * KS + k - 1];
         if (tid == 0) {
             act[iu] = act[k - 1];
             s_nrc = 0;
@@ -3614,7 +3630,7 @@ __global__ __launch_bounds__(kSspBlock) void ssp_kernel(Ctx<M> c0, int K, int sm
     }
     __syncthreads();
     // Hand the state back: the phase is complete (or flagged).
-    for (int e = tid; e < E; e += kSspBlock) {
+    for (int e = tid; e < E; e += kBlk) {
         c.prices[e] = pr[e];
         c.hcount[e] = cnt[e];
     }
@@ -4753,6 +4769,19 @@ hipError_t lds_optin(int dev, const void *fn, size_t bytes) {
     return err;
 }
 
+// The shortest-path finish for Ep padded experts (one block per problem).
+template <class M>
+void launch_ssp(const Ctx<M> &c, int B, int ssp_r, size_t ssp_bytes, hipStream_t s) {
+    const dim3 g(1, B);
+    const int small = ssp_fallbacks_setting();
+    switch (ssp_r) {
+        case 32: hipLaunchKernelGGL((ssp_kernel<M, 32>), g, dim3(ssp_block<32>()), ssp_bytes, s, c, c.ssp_cap, small); break;
+        case 64: hipLaunchKernelGGL((ssp_kernel<M, 64>), g, dim3(ssp_block<64>()), ssp_bytes, s, c, c.ssp_cap, small); break;
+        case 128: hipLaunchKernelGGL((ssp_kernel<M, 128>), g, dim3(ssp_block<128>()), ssp_bytes, s, c, c.ssp_cap, small); break;
+        default: hipLaunchKernelGGL((ssp_kernel<M, 256>), g, dim3(ssp_block<256>()), ssp_bytes, s, c, c.ssp_cap, small); break;
+    }
+}
+
 template <class M, int G>
 hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *assign,
                      uint32_t *rpart, hipStream_t s) {
@@ -4810,9 +4839,10 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *as
             if (cap >= kSspMinCap) {
                 ssp_r = ssp_pad(c.E);
                 ssp_bytes = ssp_lds_bytes(c.E, cap, c.C);
-                const void *fn = ssp_r == 32   ? reinterpret_cast<const void *>(&ssp_kernel<M, 32>)
-                                 : ssp_r == 64 ? reinterpret_cast<const void *>(&ssp_kernel<M, 64>)
-                                               : reinterpret_cast<const void *>(&ssp_kernel<M, 128>);
+                const void *fn = ssp_r == 32    ? reinterpret_cast<const void *>(&ssp_kernel<M, 32>)
+                                 : ssp_r == 64  ? reinterpret_cast<const void *>(&ssp_kernel<M, 64>)
+                                 : ssp_r == 128 ? reinterpret_cast<const void *>(&ssp_kernel<M, 128>)
+                                                : reinterpret_cast<const void *>(&ssp_kernel<M, 256>);
                 const hipError_t err = lds_optin(dev, fn, ssp_bytes);
                 if (err == hipSuccess) {
                     c.ssp_cap = cap;
@@ -4873,13 +4903,7 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *as
                     if (cap > 0) {
                         hipLaunchKernelGGL(ssp_build_kernel<M>, dim3(c.E, B), dim3(kSspThreads), 0,
                                            s, c);
-                        const dim3 g(1, B), t(kSspBlock);
-                        const int small = ssp_fallbacks_setting();
-                        switch (ssp_r) {
-                            case 32: hipLaunchKernelGGL((ssp_kernel<M, 32>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
-                            case 64: hipLaunchKernelGGL((ssp_kernel<M, 64>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
-                            default: hipLaunchKernelGGL((ssp_kernel<M, 128>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
-                        }
+                        launch_ssp<M>(c, B, ssp_r, ssp_bytes, s);
                     }
                 }
             }
@@ -4967,13 +4991,7 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *as
         if constexpr (!M::kInteger) {
             if (ssp_r > 0) {
                 hipLaunchKernelGGL(ssp_build_kernel<M>, dim3(c.E, B), dim3(kSspThreads), 0, s, c);
-                const dim3 g(1, B), t(kSspBlock);
-                const int small = ssp_fallbacks_setting();
-                switch (ssp_r) {
-                    case 32: hipLaunchKernelGGL((ssp_kernel<M, 32>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
-                    case 64: hipLaunchKernelGGL((ssp_kernel<M, 64>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
-                    default: hipLaunchKernelGGL((ssp_kernel<M, 128>), g, t, ssp_bytes, s, c, c.ssp_cap, small); break;
-                }
+                launch_ssp<M>(c, B, ssp_r, ssp_bytes, s);
             }
         }
         if (!engine || slot == slots - 1)
