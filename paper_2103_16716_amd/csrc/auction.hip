@@ -2960,6 +2960,9 @@ constexpr int kSspMaxCap = 32;   // most unassigned tokens a phase hands over
 constexpr int kSspMinCap = 8;
 constexpr int kSspRc = 256;      // column recomputes taken per pass
 constexpr int kSspMnew = 8;      // path experts whose received rows go through LDS
+// (sixteen with 256 experts, whose paths run longer)
+template <int Ep>
+constexpr int ssp_mnew() { return Ep > 128 ? 2 * kSspMnew : kSspMnew; }
 
 
 // Whether problem c's current phase waits for the shortest-path finish.
@@ -3051,8 +3054,8 @@ struct SspLds {
     // (the workspace tables the build kernel wrote); they would not fit.
     static constexpr bool kGlobal = Ep > 128;
     static constexpr size_t distp = 0;                       // u64 [3][Ep]
-    static constexpr size_t rckey = distp + 3 * Ep * 8;      // u64 [kSspMnew][Ep]
-    static constexpr size_t pr = rckey + kSspMnew * Ep * 8;  // f32 [Ep]
+    static constexpr size_t rckey = distp + 3 * Ep * 8;      // u64 [ssp_mnew][Ep]
+    static constexpr size_t pr = rckey + ssp_mnew<Ep>() * Ep * 8;  // f32 [Ep]
     static constexpr size_t cnt = pr + Ep * 4;               // i32 [Ep]
     static constexpr size_t sel = cnt + Ep * 4;
     static constexpr size_t path = sel + Ep * 4;             // i32 [Ep + 4]
@@ -3063,8 +3066,8 @@ struct SspLds {
     static constexpr size_t rcx = rcj + kSspRc * 4;
     static constexpr size_t act = rcx + kSspRc * 4;          // [kSspMaxCap]
     static constexpr size_t vstar = act + kSspMaxCap * 4;
-    static constexpr size_t mnew = vstar + kSspMaxCap * 4;   // f32 [kSspMnew][Ep]
-    static constexpr size_t am = mnew + kSspMnew * Ep * 4;   // u16 [Ep][Ep]
+    static constexpr size_t mnew = vstar + kSspMaxCap * 4;   // f32 [ssp_mnew][Ep]
+    static constexpr size_t am = mnew + ssp_mnew<Ep>() * Ep * 4;   // u16 [Ep][Ep]
     static constexpr size_t rows = am + (kGlobal ? 0 : (size_t)Ep * Ep * 2); // f32 [E][K + 1]
     __host__ __device__ static size_t toks(int E, int K) {
         return (rows + (size_t)E * (K + 1) * 4 + 15) & ~size_t(15);
@@ -3184,7 +3187,7 @@ __global__ __launch_bounds__(ssp_block<Ep>()) void ssp_kernel(Ctx<M> c0, int K, 
     uint16_t *toks = kG ? c.ssp_t : reinterpret_cast<uint16_t *>(smem_raw + LY::toks(E, K));
     const int e0 = wave * RW;   // this wave's rows
     const int rc_cap = small ? 0 : kSspRc;
-    const int mn_cap = small ? 1 : kSspMnew;
+    const int mn_cap = small ? 1 : ssp_mnew<Ep>();
     if (tid == 0) {
         int n = 0;
         s_go = ssp_pending<M>(c, &n) && n <= K && T <= 65536 ? 1 : 0;
