@@ -3105,47 +3105,18 @@ __device__ inline uint64_t ssp_entry(float v, int q) {
     return ((uint64_t)f32_ord(v) << 32) | (uint32_t)q;
 }
 
-// Wave-wide minimum of (v, i), ties to the lower i: DPP moves inside each
-// row of 16 lanes, then the four rows' results read with readlane. Every
-// lane gets the result.
-__device__ inline void wave_min_pair(float &v, int &i) {
-#define BASE_MIN_STEP(OFF)                                                \
-    {                                                                     \
-        const float ov = grp_partner<OFF>(v);                             \
-        const int oi = grp_partner<OFF>(i);                               \
-        const bool t = (ov < v) | ((ov == v) & (oi < i));                 \
-        v = t ? ov : v;                                                   \
-        i = t ? oi : i;                                                   \
-    }
-    BASE_MIN_STEP(1)
-    BASE_MIN_STEP(2)
-    BASE_MIN_STEP(4)
-    BASE_MIN_STEP(8)
-#undef BASE_MIN_STEP
-    float rv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-    int ri = __builtin_amdgcn_readlane(i, 0);
-#pragma unroll
-    for (int q = 1; q < 4; ++q) {
-        const float ov = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16 * q));
-        const int oi = __builtin_amdgcn_readlane(i, 16 * q);
-        const bool t = (ov < rv) | ((ov == rv) & (oi < ri));
-        rv = t ? ov : rv;
-        ri = t ? oi : ri;
-    }
-    v = rv;
-    i = ri;
-}
-
-// Ep = 32, 64 or 128 padded experts. One wave per SIMD: wave w (of 4) owns
-// rows [w RW, w RW + RW) of the exchange matrix, lane l its columns
-// l + 64 j. (With 16 waves the per-step work of every wave queued four deep
-// on each SIMD; the relaxations themselves are few after the first step.)
-constexpr int kSspBlock = 256;
-// Ep = 256: eight waves (two per SIMD), 32 rows of 4 columns each in
-// registers per lane; the arcs' M(e,x) + p_x are formed where they are used
-// instead of kept in a second array (registers).
+// Sixteen waves (four per SIMD) for every Ep: wave w owns rows
+// [w RW, w RW + RW) of the exchange matrix (RW = Ep / 16), lane l its
+// columns l + 64 j. A Bellman-Ford step costs each wave one uniform test
+// per row it owns, relaxed or not, and a wave issues one instruction at a
+// time: few rows per wave, with four waves interleaved on each SIMD, keep
+// the steps short (with four waves of 32 rows a step took about 3000
+// cycles, most of them in the test chain). For Ep = 256 the arcs'
+// M(e,x) + p_x are formed where they are used instead of kept in a second
+// array (registers).
+constexpr int kSspBlock = 1024;
 template <int Ep>
-constexpr int ssp_block() { return Ep > 128 ? 512 : kSspBlock; }
+constexpr int ssp_block() { return kSspBlock; }
 
 // small != 0 (tests only) routes every step through the fallbacks: no
 // recompute list (whole rows instead) and received rows read by the owners.
@@ -3178,6 +3149,10 @@ __global__ __launch_bounds__(ssp_block<Ep>()) void ssp_kernel(Ctx<M> c0, int K, 
     uint16_t *am = kG ? c.ssp_a : reinterpret_cast<uint16_t *>(smem_raw + LY::am);
     float *rowsT = reinterpret_cast<float *>(smem_raw + LY::rows);
     __shared__ int s_go, s_n, s_cur, s_flag[3], s_L, s_i, s_u, s_err, s_nrc, s_full;
+    // The nearest expert with room at each step's labels, as a 64-bit
+    // minimum of (distance, expert) beside the label buffers: the waves read
+    // it instead of each reducing the labels of every expert.
+    __shared__ uint64_t s_rkey[3];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -3267,7 +3242,10 @@ __global__ __launch_bounds__(ssp_block<Ep>()) void ssp_kernel(Ctx<M> c0, int K, 
             m = fmaxf(m, grp_partner<4>(m));
             if (i < k && part == 0) vstar[i] = m;
         }
-        if (tid == 0) s_flag[0] = s_flag[1] = s_flag[2] = 0;
+        if (tid == 0) {
+            s_flag[0] = s_flag[1] = s_flag[2] = 0;
+            s_rkey[0] = s_rkey[1] = s_rkey[2] = ~0ull;
+        }
         __syncthreads();
         if (tid < Ep) {
             // Ties between tokens go to the lower token index: the list's
@@ -3288,6 +3266,9 @@ __global__ __launch_bounds__(ssp_block<Ep>()) void ssp_kernel(Ctx<M> c0, int K, 
             }
             distp[x] = ssp_pack(best, kSspSrc + (uint32_t)bi);
             distp[Ep + x] = ~0ull;
+            if (x < E && cnt[x] < C)
+                atomicMin(reinterpret_cast<unsigned long long *>(&s_rkey[0]),
+                          (unsigned long long)ssp_pack(best, (uint32_t)x));
         }
         // The arcs at the current prices: M(e,x) + p_x, and -p_e per row;
         // which of this lane's experts have room.
@@ -3329,19 +3310,21 @@ __global__ __launch_bounds__(ssp_block<Ep>()) void ssp_kernel(Ctx<M> c0, int K, 
                           (unsigned long long)cur[tid]);
                 distp[((it + 2) % 3) * Ep + tid] = ~0ull;
             }
+            if (tid == 0) {
+                atomicMin(reinterpret_cast<unsigned long long *>(&s_rkey[(it + 1) % 3]),
+                          (unsigned long long)s_rkey[it % 3]);
+                s_rkey[(it + 2) % 3] = ~0ull;
+            }
             const float dnow = lane < RW ? ssp_dist(cur[e0 + lane]) : INFINITY;
             float dcol[CL];
-            float dcur = INFINITY;
-            int fcur = 0x7fffffff;
 #pragma unroll
             for (int j = 0; j < CL; ++j) {
                 const int x = lane + 64 * j;
                 dcol[j] = x < E ? ssp_dist(cur[x]) : -INFINITY;
-                const bool t = room[j] && dcol[j] < dcur;
-                dcur = t ? dcol[j] : dcur;
-                fcur = t ? x : fcur;
             }
-            wave_min_pair(dcur, fcur);
+            const uint64_t rk = s_rkey[it % 3];
+            const float dcur = rk == ~0ull ? INFINITY : ssp_dist(rk);
+            const int fcur = rk == ~0ull ? 0x7fffffff : (int)(uint32_t)rk;
             const bool relax = lane < RW && dnow < dused && dnow < dcur;
             const uint64_t todo = __ballot(relax);
             dused = relax ? dnow : dused;
@@ -3373,6 +3356,9 @@ __global__ __launch_bounds__(ssp_block<Ep>()) void ssp_kernel(Ctx<M> c0, int K, 
                 if (best[j] < fminf(dcol[j], dcur)) {   // strict improvement (x < E)
                     atomicMin(reinterpret_cast<unsigned long long *>(&nxt[x]),
                               (unsigned long long)ssp_pack(best[j], (uint32_t)bj[j]));
+                    if (room[j])
+                        atomicMin(reinterpret_cast<unsigned long long *>(&s_rkey[(it + 1) % 3]),
+                                  (unsigned long long)ssp_pack(best[j], (uint32_t)x));
                     imp = true;
                 }
             }
