@@ -4299,34 +4299,45 @@ constexpr int kCompThreads = 1024;
 constexpr int kCompWaves = kCompThreads / 64;
 constexpr int kCompStageBytes = 32 * 1024;   // score rows staged per step of the greedy walk
 constexpr int kCompMaxRows = 256;
-constexpr int kCompScan = 32;                // tokens per thread and pass of the compaction
+static_assert(kCompMaxRows <= kCompThreads, "a chunk token per thread");
 
 __host__ __device__ inline size_t a16(size_t x) { return (x + 15) & ~size_t(15); }
+
 // LDS of complete_kernel (within the default 64 KiB): prices, the counts
 // before the completion, the live counts, the holder-table selectors, the
-// staged tokens and their choices, then the staged values of R tokens.
+// staged tokens and their choices, the open experts and the tokens' orders
+// of preference over them, then the staged values: R tokens' rows of E, or
+// R64 tokens' values at the (at most 64) open experts.
+constexpr int kCompOrdRows = 128;
+constexpr int kCompOpenStride = 65;   // staged open-expert values per token (odd: no bank conflicts)
 struct CompLds {
-    size_t pr, hc0, cnt, sel, stok, chs, slot, vst, total;
-    int R;
+    size_t pr, hc0, cnt, sel, stok, chs, slot, oe, ord, vst, total;
+    int R, R64;
 };
 __host__ __device__ inline CompLds comp_lds(int E, int vbytes) {
     CompLds L{};
     const size_t budget = 62 * 1024;
     const size_t fixed = a16((size_t)E * vbytes) + 3 * a16((size_t)E * 4) +
-                         3 * a16((size_t)kCompMaxRows * 4);
+                         3 * a16((size_t)kCompMaxRows * 4) + a16(64 * 4) + kCompOrdRows * 64;
     const size_t avail = budget > fixed ? budget - fixed : 0;
     const size_t stage_max = avail < (size_t)kCompStageBytes ? avail : (size_t)kCompStageBytes;
     size_t r = stage_max / ((size_t)E * vbytes);
     L.R = r < 1 ? 1 : (r > (size_t)kCompMaxRows ? kCompMaxRows : (int)r);
-    const size_t stage = (size_t)L.R * E * vbytes;
+    const size_t r64 = stage_max / ((size_t)kCompOpenStride * vbytes);
+    L.R64 = r64 < 1 ? 1 : (r64 > (size_t)kCompOrdRows ? kCompOrdRows : (int)r64);
+    const int rows = L.R > L.R64 ? L.R : L.R64;
+    const size_t sa = (size_t)L.R * E * vbytes, sb = (size_t)L.R64 * kCompOpenStride * vbytes;
+    const size_t stage = sa > sb ? sa : sb;
     size_t off = 0;
     L.pr = off;   off += a16((size_t)E * vbytes);
     L.hc0 = off;  off += a16((size_t)E * 4);
     L.cnt = off;  off += a16((size_t)E * 4);
     L.sel = off;  off += a16((size_t)E * 4);
-    L.stok = off; off += a16((size_t)L.R * 4);
-    L.chs = off;  off += a16((size_t)L.R * 4);
-    L.slot = off; off += a16((size_t)L.R * 4);
+    L.stok = off; off += a16((size_t)rows * 4);
+    L.chs = off;  off += a16((size_t)rows * 4);
+    L.slot = off; off += a16((size_t)rows * 4);
+    L.oe = off;   off += a16(64 * 4);
+    L.ord = off;  off += kCompOrdRows * 64;
     L.vst = off;  off += stage;
     L.total = off;
     return L;
@@ -4338,12 +4349,15 @@ __host__ __device__ inline CompLds comp_lds(int E, int vbytes) {
 // ascending token order, takes its best expert by S[t,e] - p[e] (ties to
 // the lowest expert) among those with room. The unassigned tokens are first
 // compacted into a list (all threads; a block scan orders them). Then, chunk
-// by chunk, their rows are staged in LDS and every wave finds each staged
-// token's best expert among those with room at the chunk's start (all waves
-// in parallel); one wave then walks the chunk in token order with the live
-// counts, and a token whose expert filled earlier in the walk takes its best
-// expert again over the experts still open. The result is the sequential
-// rule's, token by token. Placed tokens join their expert's holder table;
+// by chunk: with at most 64 experts open at the chunk's start (float
+// scores), each token's open experts are sorted by preference (all waves in
+// parallel) and one wave walks the tokens in order, each taking its first
+// entry that is not full. Otherwise the tokens' rows are staged in LDS,
+// every wave finds each token's best expert among those with room at the
+// chunk's start, and one wave walks the chunk with the live counts: a token
+// whose expert filled earlier in the walk takes its best expert again over
+// the experts still open. Either way the result is the sequential rule's,
+// token by token. Placed tokens join their expert's holder table;
 // the experts that took any are marked for rank_filled_kernel, which ranks
 // their rows of perm again (one block each).
 template <class M>
@@ -4365,8 +4379,10 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
     int *stok = reinterpret_cast<int *>(smem_raw + LY.stok);
     int *chs = reinterpret_cast<int *>(smem_raw + LY.chs);
     int *slot = reinterpret_cast<int *>(smem_raw + LY.slot);
+    int *oel = reinterpret_cast<int *>(smem_raw + LY.oe);
+    uint8_t *ordl = reinterpret_cast<uint8_t *>(smem_raw + LY.ord);
     value_t *vst = reinterpret_cast<value_t *>(smem_raw + LY.vst);
-    __shared__ int s_fill, s_base, s_wsum[kCompWaves];
+    __shared__ int s_fill, s_base, s_no, s_wsum[kCompWaves];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
@@ -4390,164 +4406,299 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
     __syncthreads();
     if (s_fill) {
         // The unassigned tokens, in ascending order, into the (no longer
-        // used) first active list: per pass, thread i takes kCompScan
-        // consecutive tokens into registers (16-byte loads when the caller's
-        // buffer allows), a block scan gives each thread its offset.
+        // used) first active list. A pass covers kCompThreads * 32 tokens:
+        // wave w the 2048 from base + 2048 w, in eight steps of 256 in which
+        // lane l holds four consecutive tokens (one 16-byte load when the
+        // caller's buffer allows: each load of a wave reads a contiguous
+        // KiB). Offsets inside a wave come from ballots of the lanes' counts
+        // (0..4, three bits), across waves from their totals.
         int *list = c.active;
+        const int one_chunk = R > LY.R64 ? R : LY.R64;   // the rows of stok
         const bool vec = (reinterpret_cast<uintptr_t>(assign) & 15) == 0;
-        for (int base = 0; base < T; base += kCompThreads * kCompScan) {
-            const int lo = base + tid * kCompScan;
-            int v[kCompScan];
-            if (vec && lo + kCompScan <= T) {
+        const uint64_t lt = (1ull << lane) - 1;
+        for (int base = 0; base < T; base += kCompThreads * 32) {
+            const int wb = base + wave * 2048 + 4 * lane;
+            int4 q[8];
 #pragma unroll
-                for (int j = 0; j < kCompScan / 4; ++j) {
-                    const int4 q = reinterpret_cast<const int4 *>(assign + lo)[j];
-                    v[4 * j] = q.x;
-                    v[4 * j + 1] = q.y;
-                    v[4 * j + 2] = q.z;
-                    v[4 * j + 3] = q.w;
+            for (int k = 0; k < 8; ++k) {
+                const int t0 = wb + k * 256;
+                if (vec && t0 + 4 <= T) {
+                    q[k] = *reinterpret_cast<const int4 *>(assign + t0);
+                } else {
+                    q[k].x = t0 < T ? assign[t0] : 0;
+                    q[k].y = t0 + 1 < T ? assign[t0 + 1] : 0;
+                    q[k].z = t0 + 2 < T ? assign[t0 + 2] : 0;
+                    q[k].w = t0 + 3 < T ? assign[t0 + 3] : 0;
                 }
-            } else {
-#pragma unroll
-                for (int j = 0; j < kCompScan; ++j) v[j] = lo + j < T ? assign[lo + j] : 0;
             }
-            int cnt = 0;
+            int pre[8];
+            int wtot = 0;
 #pragma unroll
-            for (int j = 0; j < kCompScan; ++j) cnt += v[j] < 0;
-            int incl = cnt;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const int o = __shfl_up(incl, off);
-                if (lane >= off) incl += o;
+            for (int k = 0; k < 8; ++k) {
+                const int cnt = (q[k].x < 0) + (q[k].y < 0) + (q[k].z < 0) + (q[k].w < 0);
+                const uint64_t b0 = __builtin_amdgcn_ballot_w64((cnt & 1) != 0);
+                const uint64_t b1 = __builtin_amdgcn_ballot_w64((cnt & 2) != 0);
+                const uint64_t b2 = __builtin_amdgcn_ballot_w64((cnt & 4) != 0);
+                pre[k] = wtot + __popcll(b0 & lt) + 2 * __popcll(b1 & lt) + 4 * __popcll(b2 & lt);
+                wtot += __popcll(b0) + 2 * __popcll(b1) + 4 * __popcll(b2);
             }
-            if (lane == 63) s_wsum[wave] = incl;
+            if (lane == 0) s_wsum[wave] = wtot;
             __syncthreads();
-            int before = s_base;
-            for (int w = 0; w < wave; ++w) before += s_wsum[w];
-            int at = before + incl - cnt;
+            // The waves' totals: one read per lane, summed from registers.
+            const int wsv = lane < kCompWaves ? s_wsum[lane] : 0;
+            int before = s_base, all = 0;
 #pragma unroll
-            for (int j = 0; j < kCompScan; ++j)
-                if (v[j] < 0) list[at++] = lo + j;
+            for (int w = 0; w < kCompWaves; ++w) {
+                const int x = __builtin_amdgcn_readlane(wsv, w);
+                before += w < wave ? x : 0;
+                all += x;
+            }
+            // All of them in one pass and within the rows of the chunks'
+            // token array: straight into it (LDS), not the list.
+            int *dst = T <= kCompThreads * 32 && all <= one_chunk ? stok : list;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int4 v = q[k];
+                if ((v.x | v.y | v.z | v.w) >= 0) continue;   // none of the four
+                const int t0 = wb + k * 256;
+                int at = before + pre[k];
+                if (v.x < 0) dst[at++] = t0;
+                if (v.y < 0) dst[at++] = t0 + 1;
+                if (v.z < 0) dst[at++] = t0 + 2;
+                if (v.w < 0) dst[at++] = t0 + 3;
+            }
             __syncthreads();
-            if (tid == kCompThreads - 1) s_base = at;
+            if (tid == 0) {
+                int tot = s_base;
+                for (int w = 0; w < kCompWaves; ++w) tot += s_wsum[w];
+                s_base = tot;
+            }
             __syncthreads();
         }
         const int n = s_base;
-        for (int j0 = 0; j0 < n; j0 += R) {
-            const int m = n - j0 < R ? n - j0 : R;
-            for (int r = tid; r < m; r += kCompThreads) {
-                const int t = list[j0 + r];
-                stok[r] = (t >= 0 && t < T) ? t : 0;
-            }
-            __syncthreads();
-#pragma unroll 8
-            for (int q = tid; q < m * E; q += kCompThreads) {
-                const int r = q / E;
-                const int e = q - r * E;
-                vst[q] = M::load(c.S, (int64_t)stok[r] * E + e, c.scale) - pr[e];
-            }
-            __syncthreads();
-            // Each staged token's best expert among those open now.
-            for (int r = wave; r < m; r += kCompWaves) {
-                value_t bv = M::lowest();
-                int be = 0x7fffffff;
-                for (int e = lane; e < E; e += 64) {
-                    const value_t v = vst[r * E + e];
-                    if (cntl[e] < C && (v > bv || be == 0x7fffffff)) {
-                        bv = v;
-                        be = e;
-                    }
+        const bool in_lds = T <= kCompThreads * 32 && n <= one_chunk;   // the tokens are in stok
+        for (int j0 = 0; j0 < n;) {
+            if (wave == 0) {
+                // The experts open at the chunk's start, ascending (the
+                // first 64 of them, and how many there are).
+                int no = 0;
+                for (int e0 = 0; e0 < E; e0 += 64) {
+                    const int e = e0 + lane;
+                    const bool open = e < E && cntl[e] < C;
+                    const uint64_t bm = __ballot(open);
+                    const int at = no + __popcll(bm & ((1ull << lane) - 1));
+                    if (open && at < 64) oel[at] = e;
+                    no += __popcll(bm);
                 }
-                wave_max_pair(bv, be);
-                if (lane == 0) chs[r] = be;
+                if (lane == 0) s_no = no;
             }
             __syncthreads();
-            // The walk in token order. Lane j of a batch of 64 holds the
-            // choice of entry j. With E <= 128 the live counts sit in two
-            // registers (lane l: experts l and l + 64) and each decision is
-            // a few cross-lane reads; otherwise they are in LDS. Lane 0
-            // records each decision (expert and slot, into chs and slot).
-            // One wave's LDS accesses take effect in program order, so the
-            // walk needs no memory wait: the empty asm statements only keep
-            // the compiler from reordering them.
-            if (wave == 0 && E <= 128) {
-                int cnt0 = lane < E ? cntl[lane] : C;   // experts past E count as full
-                int cnt1 = lane + 64 < E ? cntl[lane + 64] : C;
-                for (int r0 = 0; r0 < m; r0 += 64) {
-                    const int cj = r0 + lane < m ? chs[r0 + lane] : 0;
-                    const int mm = m - r0 < 64 ? m - r0 : 64;
-                    int de = -1, ds = 0;   // lane j: the decision on entry j
-                    // The entry's values for a second choice, read one entry
-                    // ahead (a choice that filled up is common once few
-                    // slots are left, and the LDS read is then not waited for).
-                    value_t nv0 = vst[r0 * E + (lane < E ? lane : 0)];
-                    value_t nv1 = vst[r0 * E + (lane + 64 < E ? lane + 64 : 0)];
-                    for (int j = 0; j < mm; ++j) {
-                        const value_t v0 = nv0, v1 = nv1;
-                        if (j + 1 < mm) {
-                            nv0 = vst[(r0 + j + 1) * E + (lane < E ? lane : 0)];
-                            nv1 = vst[(r0 + j + 1) * E + (lane + 64 < E ? lane + 64 : 0)];
-                        }
-                        int e = __builtin_amdgcn_readlane(cj, j);
-                        int have = e < 64 ? __builtin_amdgcn_readlane(cnt0, e & 63)
-                                          : (e < E ? __builtin_amdgcn_readlane(cnt1, e & 63) : C);
-                        if (have >= C) {   // (uniform) the choice filled up: again
-                            const bool o0 = cnt0 < C, o1 = lane + 64 < E && cnt1 < C;
-                            value_t bv = o0 ? v0 : M::lowest();
-                            int be = o0 ? lane : 0x7fffffff;
-                            const bool t1 = o1 && v1 > bv;
-                            bv = t1 ? v1 : bv;
-                            be = t1 ? lane + 64 : be;
-                            wave_max_pair(bv, be);
-                            e = be;
-                            have = e < 64 ? __builtin_amdgcn_readlane(cnt0, e & 63)
-                                          : (e < E ? __builtin_amdgcn_readlane(cnt1, e & 63) : C);
-                        }
-                        const bool ok = e < E && have < C;
-                        if (ok && lane == (e & 63)) {
-                            if (e < 64) cnt0 += 1;
-                            else cnt1 += 1;
-                        }
-                        if (lane == j) {
-                            de = ok ? e : -1;
-                            ds = have;
-                        }
-                    }
-                    if (lane < mm) {
-                        chs[r0 + lane] = de;
-                        slot[r0 + lane] = ds;
-                    }
+            const int no = s_no;
+            const bool fast = !M::kInteger && no <= 64;
+            const int cap = fast ? LY.R64 : R;
+            const int m = n - j0 < cap ? n - j0 : cap;
+            // The chunk's tokens to the front of stok (m <= kCompMaxRows <
+            // kCompThreads: one each).
+            int t = 0;
+            if (tid < m) t = in_lds ? stok[j0 + tid] : list[j0 + tid];
+            if (in_lds) __syncthreads();
+            if (tid < m) stok[tid] = (t >= 0 && t < T) ? t : 0;
+            __syncthreads();
+            if (fast) {
+                // At most 64 experts open (a completion never reopens one):
+                // only their values are staged; each token's open experts
+                // are ranked by preference (value, then the lower expert):
+                // every (token, open expert) pair counts the entries that
+                // precede it, and the token's order lists them by rank. The
+                // walk then takes each token's first entry that is not full,
+                // from a 64-bit mask of the full ones (no reduction per
+                // token).
+                for (int q = tid; q < m * no; q += kCompThreads) {
+                    const int r = q / no;
+                    const int i = q - r * no;
+                    const int e = oel[i];
+                    vst[r * kCompOpenStride + i] =
+                        M::load(c.S, (int64_t)stok[r] * E + e, c.scale) - pr[e];
                 }
-                if (lane < E) cntl[lane] = cnt0;
-                if (lane + 64 < E) cntl[lane + 64] = cnt1;
-            } else if (wave == 0) {
-                for (int r0 = 0; r0 < m; r0 += 64) {
-                    const int cj = r0 + lane < m ? chs[r0 + lane] : 0;
-                    const int mm = m - r0 < 64 ? m - r0 : 64;
-                    for (int j = 0; j < mm; ++j) {
-                        int e = __builtin_amdgcn_readlane(cj, j);
-                        int have = e < E ? cntl[e] : C;
-                        if (have >= C) {   // (uniform) the choice filled up: again
-                            value_t bv = M::lowest();
-                            int be = 0x7fffffff;
-                            for (int e2 = lane; e2 < E; e2 += 64) {
-                                const value_t v = vst[(r0 + j) * E + e2];
-                                if (cntl[e2] < C && (v > bv || be == 0x7fffffff)) {
-                                    bv = v;
-                                    be = e2;
+                __syncthreads();
+                for (int q = tid; q < m * no; q += kCompThreads) {
+                    const int r = q / no;
+                    const int i = q - r * no;
+                    const value_t *row = vst + r * kCompOpenStride;
+                    const value_t v = row[i];
+                    int rank = 0;
+                    for (int k = 0; k < no; ++k) {
+                        const value_t w = row[k];
+                        rank += (w > v || (w == v && k < i)) ? 1 : 0;
+                    }
+                    ordl[r * 64 + rank] = (uint8_t)i;
+                }
+                __syncthreads();
+                if (wave == 0) {
+                    // Lane i: the count of open expert i; bit i of full: it
+                    // is full (lanes past the list count as full). An
+                    // order's entries past no are stale, and masked.
+                    // Lane i: the slots left at open expert i (none past the
+                    // list); full follows from one ballot of them, off the
+                    // read of the slot a token takes.
+                    int rem = lane < no ? C - cntl[oel[lane]] : 0;
+                    const uint64_t inl = no >= 64 ? ~0ull : (1ull << no) - 1;   // entries of the order
+                    uint64_t full = __builtin_amdgcn_ballot_w64(rem <= 0);
+                    for (int b0 = 0; b0 < m; b0 += 64) {
+                        const int mb = m - b0 < 64 ? m - b0 : 64;
+                        int di = -1, ds = 0;   // lane j: the decision on entry b0 + j (open index, slot)
+                        // Two tokens a step, both against the same mask: the
+                        // second chooses again only when the first has just
+                        // filled the expert it picked.
+                        int na = ordl[b0 * 64 + lane];
+                        int nb = ordl[(b0 + (mb > 1 ? 1 : 0)) * 64 + lane];
+                        for (int j = 0; j < mb; j += 2) {
+                            const int ia = na, ib = nb;   // lane k: the tokens' k-th choices
+                            const int j2 = j + 2 < mb ? j + 2 : mb - 1;
+                            const int j3 = j + 3 < mb ? j + 3 : mb - 1;
+                            na = ordl[(b0 + j2) * 64 + lane];
+                            nb = ordl[(b0 + j3) * 64 + lane];
+                            const uint64_t ra = __builtin_amdgcn_ballot_w64(((full >> ia) & 1) == 0) & inl;
+                            const uint64_t rb = __builtin_amdgcn_ballot_w64(((full >> ib) & 1) == 0) & inl;
+                            if (ra == 0) continue;   // (uniform) no expert has room: nor for the next
+                            const int ea = __builtin_amdgcn_readlane(ia, (int)__builtin_ctzll(ra));
+                            const int la = __builtin_amdgcn_readlane(rem, ea);
+                            rem -= lane == ea ? 1 : 0;
+                            di = lane == j ? ea : di;
+                            ds = lane == j ? C - la : ds;
+                            if (j + 1 < mb) {
+                                int eb = __builtin_amdgcn_readlane(ib, (int)__builtin_ctzll(rb));
+                                if (eb == ea && la == 1) {   // the first filled it: again
+                                    full = __builtin_amdgcn_ballot_w64(rem <= 0);
+                                    const uint64_t r2 = __builtin_amdgcn_ballot_w64(((full >> ib) & 1) == 0) & inl;
+                                    eb = r2 != 0 ? __builtin_amdgcn_readlane(ib, (int)__builtin_ctzll(r2)) : -1;
+                                }
+                                if (eb >= 0) {
+                                    const int lb = __builtin_amdgcn_readlane(rem, eb);
+                                    rem -= lane == eb ? 1 : 0;
+                                    di = lane == j + 1 ? eb : di;
+                                    ds = lane == j + 1 ? C - lb : ds;
                                 }
                             }
-                            wave_max_pair(bv, be);
-                            e = be;
-                            have = e < E ? cntl[e] : C;
+                            full = __builtin_amdgcn_ballot_w64(rem <= 0);
                         }
-                        const bool ok = e < E && have < C;
-                        if (lane == 0) {
-                            if (ok) cntl[e] = have + 1;
-                            chs[r0 + j] = ok ? e : -1;
-                            slot[r0 + j] = have;
+                        if (lane < mb) {
+                            chs[b0 + lane] = di >= 0 ? oel[di] : -1;
+                            slot[b0 + lane] = ds;
                         }
-                        asm volatile("" ::: "memory");
+                    }
+                    if (lane < no) cntl[oel[lane]] = C - rem;
+                }
+            } else {
+#pragma unroll 8
+                for (int q = tid; q < m * E; q += kCompThreads) {
+                    const int r = q / E;
+                    const int e = q - r * E;
+                    vst[q] = M::load(c.S, (int64_t)stok[r] * E + e, c.scale) - pr[e];
+                }
+                __syncthreads();
+                // Each staged token's best expert among those open now.
+                for (int r = wave; r < m; r += kCompWaves) {
+                    value_t bv = M::lowest();
+                    int be = 0x7fffffff;
+                    for (int e = lane; e < E; e += 64) {
+                        const value_t v = vst[r * E + e];
+                        if (cntl[e] < C && (v > bv || be == 0x7fffffff)) {
+                            bv = v;
+                            be = e;
+                        }
+                    }
+                    wave_max_pair(bv, be);
+                    if (lane == 0) chs[r] = be;
+                }
+                __syncthreads();
+                // The walk in token order. Lane j of a batch of 64 holds the
+                // choice of entry j. With E <= 128 the live counts sit in two
+                // registers (lane l: experts l and l + 64) and each decision is
+                // a few cross-lane reads; otherwise they are in LDS. Lane 0
+                // records each decision (expert and slot, into chs and slot).
+                // One wave's LDS accesses take effect in program order, so the
+                // walk needs no memory wait: the empty asm statements only keep
+                // the compiler from reordering them.
+                if (wave == 0 && E <= 128) {
+                    int cnt0 = lane < E ? cntl[lane] : C;   // experts past E count as full
+                    int cnt1 = lane + 64 < E ? cntl[lane + 64] : C;
+                    for (int r0 = 0; r0 < m; r0 += 64) {
+                        const int cj = r0 + lane < m ? chs[r0 + lane] : 0;
+                        const int mm = m - r0 < 64 ? m - r0 : 64;
+                        int de = -1, ds = 0;   // lane j: the decision on entry j
+                        // The entry's values for a second choice, read one entry
+                        // ahead (a choice that filled up is common once few
+                        // slots are left, and the LDS read is then not waited for).
+                        value_t nv0 = vst[r0 * E + (lane < E ? lane : 0)];
+                        value_t nv1 = vst[r0 * E + (lane + 64 < E ? lane + 64 : 0)];
+                        for (int j = 0; j < mm; ++j) {
+                            const value_t v0 = nv0, v1 = nv1;
+                            if (j + 1 < mm) {
+                                nv0 = vst[(r0 + j + 1) * E + (lane < E ? lane : 0)];
+                                nv1 = vst[(r0 + j + 1) * E + (lane + 64 < E ? lane + 64 : 0)];
+                            }
+                            int e = __builtin_amdgcn_readlane(cj, j);
+                            int have = e < 64 ? __builtin_amdgcn_readlane(cnt0, e & 63)
+                                              : (e < E ? __builtin_amdgcn_readlane(cnt1, e & 63) : C);
+                            if (have >= C) {   // (uniform) the choice filled up: again
+                                const bool o0 = cnt0 < C, o1 = lane + 64 < E && cnt1 < C;
+                                value_t bv = o0 ? v0 : M::lowest();
+                                int be = o0 ? lane : 0x7fffffff;
+                                const bool t1 = o1 && v1 > bv;
+                                bv = t1 ? v1 : bv;
+                                be = t1 ? lane + 64 : be;
+                                wave_max_pair(bv, be);
+                                e = be;
+                                have = e < 64 ? __builtin_amdgcn_readlane(cnt0, e & 63)
+                                              : (e < E ? __builtin_amdgcn_readlane(cnt1, e & 63) : C);
+                            }
+                            const bool ok = e < E && have < C;
+                            if (ok && lane == (e & 63)) {
+                                if (e < 64) cnt0 += 1;
+                                else cnt1 += 1;
+                            }
+                            if (lane == j) {
+                                de = ok ? e : -1;
+                                ds = have;
+                            }
+                        }
+                        if (lane < mm) {
+                            chs[r0 + lane] = de;
+                            slot[r0 + lane] = ds;
+                        }
+                    }
+                    if (lane < E) cntl[lane] = cnt0;
+                    if (lane + 64 < E) cntl[lane + 64] = cnt1;
+                } else if (wave == 0) {
+                    for (int r0 = 0; r0 < m; r0 += 64) {
+                        const int cj = r0 + lane < m ? chs[r0 + lane] : 0;
+                        const int mm = m - r0 < 64 ? m - r0 : 64;
+                        for (int j = 0; j < mm; ++j) {
+                            int e = __builtin_amdgcn_readlane(cj, j);
+                            int have = e < E ? cntl[e] : C;
+                            if (have >= C) {   // (uniform) the choice filled up: again
+                                value_t bv = M::lowest();
+                                int be = 0x7fffffff;
+                                for (int e2 = lane; e2 < E; e2 += 64) {
+                                    const value_t v = vst[(r0 + j) * E + e2];
+                                    if (cntl[e2] < C && (v > bv || be == 0x7fffffff)) {
+                                        bv = v;
+                                        be = e2;
+                                    }
+                                }
+                                wave_max_pair(bv, be);
+                                e = be;
+                                have = e < E ? cntl[e] : C;
+                            }
+                            const bool ok = e < E && have < C;
+                            if (lane == 0) {
+                                if (ok) cntl[e] = have + 1;
+                                chs[r0 + j] = ok ? e : -1;
+                                slot[r0 + j] = have;
+                            }
+                            asm volatile("" ::: "memory");
+                        }
                     }
                 }
             }
@@ -4563,6 +4714,7 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
                 }
             }
             __syncthreads();
+            j0 += m;
         }
         for (int e = tid; e < E; e += kCompThreads) {
             c.hcount[e] = cntl[e];

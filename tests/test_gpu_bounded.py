@@ -58,8 +58,10 @@ def _check_completion(S, rounds):
 
 @pytest.mark.parametrize("name,rounds", [("t32768-e128-d2048-mix8", 20), ("t8192-e64-d1024", 20),
                                          ("t4096-e16-d512", 3), ("t2048-e128-d2048-worker", 6),
-                                         ("t512-e8-d128-f32", 1)])
+                                         ("t2048-e128-d2048-worker", 1), ("t512-e8-d128-f32", 1)])
 def test_greedy_completion_matches_the_sequential_rule(name, rounds):
+    """Few experts open (the sorted-preference walk) and many (after one
+    round: the re-choosing walk)."""
     _check_completion(_scores(name), rounds)
 
 
