@@ -186,8 +186,18 @@ __global__ __launch_bounds__(kPThreads) void affinity_bf16_pipe_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int m0 = blockIdx.x * kPM;
-    const int n0 = blockIdx.y * kPN;
+    // Blocks go to the eight XCDs in turn (block L to XCD L % 8). The nn
+    // expert tiles of a token tile are placed on one XCD one after another
+    // (the same L % 8, consecutive L / 8), so that the token tile's rows of H
+    // come from memory once and from that XCD's L2 for the other expert
+    // tiles. With one expert tile this is the identity.
+    const int nn = (E + kPN - 1) / kPN;
+    const int L = blockIdx.x;
+    const int u = L >> 3;
+    const int mt = (u / nn) * 8 + (L & 7);
+    if (mt * kPM >= T) return;   // padding of the grid to whole groups of eight
+    const int m0 = mt * kPM;
+    const int n0 = (u % nn) * kPN;
     // This thread's two 16-byte slots of each operand's chunk: slot q = i *
     // 512 + tid is row q / 8, position q % 8, and holds the row's chunk
     // (q % 8) ^ (row % 8). Rows past T or E, and invalid source rows, read
@@ -342,9 +352,10 @@ hipError_t launch_affinity_bf16(const uint16_t *H, const int32_t *rows, int64_t 
                 granted[dev] = true;
             }
         }
-        dim3 grid((unsigned)((T + kPM - 1) / kPM), (unsigned)((E + kPN - 1) / kPN));
-        hipLaunchKernelGGL(affinity_bf16_pipe_kernel, grid, dim3(kPThreads), kPipeLds, stream, H,
-                           rows, h_rows, W, S, (int)T, (int)E, (int)d);
+        const int64_t nm8 = ((T + kPM - 1) / kPM + 7) / 8 * 8;   // token tiles, whole eights
+        const int64_t nn = (E + kPN - 1) / kPN;
+        hipLaunchKernelGGL(affinity_bf16_pipe_kernel, dim3((unsigned)(nm8 * nn)), dim3(kPThreads),
+                           kPipeLds, stream, H, rows, h_rows, W, S, (int)T, (int)E, (int)d);
         return hipGetLastError();
     }
     dim3 grid((unsigned)((T + kBM - 1) / kBM), (unsigned)((E + kBN - 1) / kBN));
