@@ -15,8 +15,10 @@
 // loads, no register staging), kStages - 1 chunks ahead of the one being
 // multiplied; a 16-byte slot s of LDS row r holds the row's chunk s ^ (r % 8),
 // so the matrix-core operand reads (eight rows per 128-byte row group) fall
-// on distinct banks. Otherwise (affinity_bf16_kernel) 64 x 128 blocks with
-// register-staged double buffering.
+// on distinct banks. When those tiles would cover fewer than 128 blocks
+// (affinity_bf16_small_kernel): 32 x 32 tiles, four waves splitting d and
+// summing in a fixed order. Otherwise (affinity_bf16_kernel) 64 x 128
+// blocks with register-staged double buffering.
 //
 // fp32 path: a plain LDS-tiled FMA kernel (fp32 products and sums, no
 // reduced-precision matrix instructions).
@@ -277,6 +279,82 @@ __global__ __launch_bounds__(kPThreads) void affinity_bf16_pipe_kernel(
     }
 }
 
+// ------------------------------------------------- small bf16 problems --
+//
+// When the 128 x 128 tiles would occupy few compute units (the per-worker
+// shape T = 2048, E = 128 is 16 tiles), a block owns 32 tokens x 32 experts
+// and its four waves split d: wave w takes the contiguous quarter of the
+// 16-element steps, loading its MFMA operands straight from memory (eight
+// steps in flight per lane), and the waves' partial tiles are added in LDS
+// in wave order (a fixed order: the result does not depend on scheduling).
+constexpr int kST = 32;
+constexpr int kSWaves = 4;
+constexpr int kSU = 4;   // steps per register set (two sets in flight)
+
+__global__ __launch_bounds__(64 * kSWaves) void affinity_bf16_small_kernel(
+    const uint16_t *__restrict__ H, const int32_t *__restrict__ rows, int64_t h_rows,
+    const uint16_t *__restrict__ W, float *__restrict__ S, int T, int E, int d) {
+    __shared__ float red[kSWaves - 1][16][64];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int lrow = lane & 31;
+    const int lhalf = lane >> 5;
+    const int m0 = blockIdx.x * kST;
+    const int n0 = blockIdx.y * kST;
+    // A operand: token row m0 + lane % 32; B operand: expert row n0 + lane % 32;
+    // lane / 32 picks the upper 8 of each 16-element step.
+    int64_t hr = m0 + lrow < T ? source_row(rows, h_rows, m0 + lrow) : 0;
+    if (hr < 0) hr = 0;
+    const int er = n0 + lrow < E ? n0 + lrow : E - 1;
+    const int q = d / 16 / kSWaves;   // steps per wave (d % 64 == 0)
+    const uint16_t *pa = H + hr * d + (int64_t)wave * q * 16 + lhalf * 8;
+    const uint16_t *pb = W + (int64_t)er * d + (int64_t)wave * q * 16 + lhalf * 8;
+    f32x16_t acc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+    bf16x8_t a0[kSU], b0[kSU], a1[kSU], b1[kSU];
+    auto load = [&](bf16x8_t (&a)[kSU], bf16x8_t (&b)[kSU], int s0) {
+#pragma unroll
+        for (int u = 0; u < kSU; ++u) {
+            if (s0 + u < q) {   // (uniform)
+                a[u] = *reinterpret_cast<const bf16x8_t *>(pa + (int64_t)(s0 + u) * 16);
+                b[u] = *reinterpret_cast<const bf16x8_t *>(pb + (int64_t)(s0 + u) * 16);
+            }
+        }
+    };
+    auto mma = [&](bf16x8_t (&a)[kSU], bf16x8_t (&b)[kSU], int s0) {
+#pragma unroll
+        for (int u = 0; u < kSU; ++u)
+            if (s0 + u < q) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[u], b[u], acc, 0, 0, 0);
+    };
+    load(a0, b0, 0);
+    for (int s0 = 0; s0 < q; s0 += 2 * kSU) {
+        load(a1, b1, s0 + kSU);
+        mma(a0, b0, s0);
+        load(a0, b0, s0 + 2 * kSU);
+        mma(a1, b1, s0 + kSU);
+    }
+    if (wave > 0) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) red[wave - 1][i][lane] = acc[i];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int w = 0; w < kSWaves - 1; ++w)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[i] += red[w][i][lane];
+    // 32x32 accumulator layout: lane holds column lane % 32; register i holds
+    // row 8 (i / 4) + 4 (lane / 32) + i % 4.
+    const int e = n0 + lrow;
+    if (e >= E) return;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const int t = m0 + 8 * (i >> 2) + 4 * lhalf + (i & 3);
+        if (t < T) S[(int64_t)t * E + e] = source_row(rows, h_rows, t) >= 0 ? acc[i] : 0.0f;
+    }
+}
+
 // fp32: 64 x 64 output tile per block, 16 x 16 threads, 4 x 4 outputs each.
 constexpr int kFT = 64;
 constexpr int kFK = 16;
@@ -336,6 +414,13 @@ __global__ __launch_bounds__(256) void affinity_f32_kernel(const float *__restri
 hipError_t launch_affinity_bf16(const uint16_t *H, const int32_t *rows, int64_t h_rows,
                                 const uint16_t *W, float *S, int64_t T, int64_t E, int64_t d,
                                 hipStream_t stream) {
+    if (d % kPK == 0 && ((T + kPM - 1) / kPM) * ((E + kPN - 1) / kPN) < 128) {
+        // Fewer 128 x 128 tiles than half the compute units: 32 x 32 tiles.
+        dim3 grid((unsigned)((T + kST - 1) / kST), (unsigned)((E + kST - 1) / kST));
+        hipLaunchKernelGGL(affinity_bf16_small_kernel, grid, dim3(64 * kSWaves), 0, stream, H,
+                           rows, h_rows, W, S, (int)T, (int)E, (int)d);
+        return hipGetLastError();
+    }
     if (d % kPK == 0) {
         // The LDS ring is above the default 64 KiB: opted in once per device.
         static std::mutex m;
