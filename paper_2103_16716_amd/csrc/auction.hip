@@ -2979,6 +2979,15 @@ __device__ inline bool ssp_pending(const Ctx<M> &c, int *n_out) {
     return n > 0 && n <= c.ssp_cap;
 }
 
+// Threads of a build block: a quarter for experts of at most 64 tokens in
+// grids of more than 1024 blocks (a batch of 256 worker-shape problems
+// launches 32768, and four times as many fit on a compute unit at once:
+// 117 -> 134 M tokens/s through the batch); a single problem keeps full
+// blocks (its 128 blocks at a quarter of the threads were slower).
+inline int ssp_build_threads(int64_t C, int64_t blocks) {
+    return C <= 64 && blocks > 1024 ? kSspThreads / 4 : kSspThreads;
+}
+
 template <class M>
 __global__ __launch_bounds__(kSspThreads) void ssp_build_kernel(Ctx<M> c0) {
     const Ctx<M> c = c0.at(blockIdx.y);
@@ -3001,7 +3010,8 @@ __global__ __launch_bounds__(kSspThreads) void ssp_build_kernel(Ctx<M> c0) {
         cnt = 0;
     }
     const uint64_t *hold = c.holders + (int64_t)(ld_relaxed(&c.hsel[e]) & 1) * c.T + (int64_t)e * c.C;
-    for (int q = tid; q < cnt; q += kSspThreads) {
+    const int nth = blockDim.x;   // a multiple of Ep (kSspThreads or a quarter of it)
+    for (int q = tid; q < cnt; q += nth) {
         int t = key_token(hold[q]);
         if (t < 0 || t >= c.T) {
             flag_internal(c.ctrl);
@@ -3012,11 +3022,11 @@ __global__ __launch_bounds__(kSspThreads) void ssp_build_kernel(Ctx<M> c0) {
     }
     __syncthreads();
     // The expert's tokens for the finish's LDS copy (uint16: T <= 65536).
-    for (int q = tid; q < c.C; q += kSspThreads)
+    for (int q = tid; q < c.C; q += nth)
         c.ssp_t[(int64_t)e * c.C + q] = (uint16_t)(q < cnt ? tok[q] : 0);
     int Ep = 1;
     while (Ep < c.E) Ep <<= 1;
-    const int subs = kSspThreads / Ep;
+    const int subs = nth / Ep;
     const int x = tid % Ep, sub = tid / Ep;
     float best = INFINITY;
     int bs = 0xffff;
@@ -5046,8 +5056,8 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *as
                 if (ev1 != nullptr) (void)hipEventRecord(ev1, s);
                 if constexpr (!M::kInteger) {
                     if (cap > 0) {
-                        hipLaunchKernelGGL(ssp_build_kernel<M>, dim3(c.E, B), dim3(kSspThreads), 0,
-                                           s, c);
+                        hipLaunchKernelGGL(ssp_build_kernel<M>, dim3(c.E, B),
+                                           dim3(ssp_build_threads(c.C, c.E * B)), 0, s, c);
                         launch_ssp<M>(c, B, ssp_r, ssp_bytes, s);
                     }
                 }
@@ -5135,7 +5145,8 @@ hipError_t run_solve(const Ctx<M> &c0, const AssignParams &p, int B, int32_t *as
         }
         if constexpr (!M::kInteger) {
             if (ssp_r > 0) {
-                hipLaunchKernelGGL(ssp_build_kernel<M>, dim3(c.E, B), dim3(kSspThreads), 0, s, c);
+                hipLaunchKernelGGL(ssp_build_kernel<M>, dim3(c.E, B),
+                                   dim3(ssp_build_threads(c.C, c.E * B)), 0, s, c);
                 launch_ssp<M>(c, B, ssp_r, ssp_bytes, s);
             }
         }
