@@ -19,8 +19,12 @@ namespace {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int kPerThread = 4;                          // 16-byte chunks in flight per thread
-constexpr int kChunksPerBlock = kThreads * kPerThread; // 16 KiB per block
+// 16-byte chunks in flight per thread. Two (8 KiB blocks) against four
+// (16 KiB): 59 -> 53 us for 32768 rows of 4 KiB, 199 -> 184 us for 65536
+// rows of 8 KiB, 921 -> 808 us for 256 shuffled problems of 2048 rows (one
+// chunk, or 128-thread blocks, about the same as two; eight slower).
+constexpr int kPerThread = 2;
+constexpr int kChunksPerBlock = kThreads * kPerThread; // 8 KiB per block
 
 // Source row of routed row k (see above), or -1 when an index is out of range.
 __device__ inline int64_t routed_source(const int32_t *__restrict__ perm,
