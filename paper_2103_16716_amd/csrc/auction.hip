@@ -4549,12 +4549,11 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
                 }
                 __syncthreads();
                 if (wave == 0) {
-                    // Lane i: the count of open expert i; bit i of full: it
-                    // is full (lanes past the list count as full). An
-                    // order's entries past no are stale, and masked.
                     // Lane i: the slots left at open expert i (none past the
-                    // list); full follows from one ballot of them, off the
-                    // read of the slot a token takes.
+                    // list, which therefore counts as full); bit i of full:
+                    // none left, one ballot of them, off the read of the slot
+                    // a token takes. An order's entries past no are stale,
+                    // and masked.
                     int rem = lane < no ? C - cntl[oel[lane]] : 0;
                     const uint64_t inl = no >= 64 ? ~0ull : (1ull << no) - 1;   // entries of the order
                     uint64_t full = __builtin_amdgcn_ballot_w64(rem <= 0);
@@ -4567,30 +4566,31 @@ __global__ __launch_bounds__(kCompThreads) void complete_kernel(Ctx<M> c0, int32
                         int na = ordl[b0 * 64 + lane];
                         int nb = ordl[(b0 + (mb > 1 ? 1 : 0)) * 64 + lane];
                         for (int j = 0; j < mb; j += 2) {
-                            const int ia = na, ib = nb;   // lane k: the tokens' k-th choices
+                            const int orda = na, ordb = nb;   // lane k: the tokens' k-th choices
                             const int j2 = j + 2 < mb ? j + 2 : mb - 1;
                             const int j3 = j + 3 < mb ? j + 3 : mb - 1;
                             na = ordl[(b0 + j2) * 64 + lane];
                             nb = ordl[(b0 + j3) * 64 + lane];
-                            const uint64_t ra = __builtin_amdgcn_ballot_w64(((full >> ia) & 1) == 0) & inl;
-                            const uint64_t rb = __builtin_amdgcn_ballot_w64(((full >> ib) & 1) == 0) & inl;
+                            const uint64_t ra = __builtin_amdgcn_ballot_w64(((full >> orda) & 1) == 0) & inl;
+                            const uint64_t rb = __builtin_amdgcn_ballot_w64(((full >> ordb) & 1) == 0) & inl;
                             if (ra == 0) continue;   // (uniform) no expert has room: nor for the next
-                            const int ea = __builtin_amdgcn_readlane(ia, (int)__builtin_ctzll(ra));
-                            const int la = __builtin_amdgcn_readlane(rem, ea);
-                            rem -= lane == ea ? 1 : 0;
-                            di = lane == j ? ea : di;
+                            // oa, ob: the open-list indices the two tokens take
+                            const int oa = __builtin_amdgcn_readlane(orda, (int)__builtin_ctzll(ra));
+                            const int la = __builtin_amdgcn_readlane(rem, oa);
+                            rem -= lane == oa ? 1 : 0;
+                            di = lane == j ? oa : di;
                             ds = lane == j ? C - la : ds;
                             if (j + 1 < mb) {
-                                int eb = __builtin_amdgcn_readlane(ib, (int)__builtin_ctzll(rb));
-                                if (eb == ea && la == 1) {   // the first filled it: again
+                                int ob = __builtin_amdgcn_readlane(ordb, (int)__builtin_ctzll(rb));
+                                if (ob == oa && la == 1) {   // the first filled it: again
                                     full = __builtin_amdgcn_ballot_w64(rem <= 0);
-                                    const uint64_t r2 = __builtin_amdgcn_ballot_w64(((full >> ib) & 1) == 0) & inl;
-                                    eb = r2 != 0 ? __builtin_amdgcn_readlane(ib, (int)__builtin_ctzll(r2)) : -1;
+                                    const uint64_t r2 = __builtin_amdgcn_ballot_w64(((full >> ordb) & 1) == 0) & inl;
+                                    ob = r2 != 0 ? __builtin_amdgcn_readlane(ordb, (int)__builtin_ctzll(r2)) : -1;
                                 }
-                                if (eb >= 0) {
-                                    const int lb = __builtin_amdgcn_readlane(rem, eb);
-                                    rem -= lane == eb ? 1 : 0;
-                                    di = lane == j + 1 ? eb : di;
+                                if (ob >= 0) {
+                                    const int lb = __builtin_amdgcn_readlane(rem, ob);
+                                    rem -= lane == ob ? 1 : 0;
+                                    di = lane == j + 1 ? ob : di;
                                     ds = lane == j + 1 ? C - lb : ds;
                                 }
                             }
