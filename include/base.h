@@ -370,8 +370,15 @@ int base_permute_batched(const void *in, const int32_t *perm, const int32_t *shu
  *             ascending, tokens ascending within an expert)
  *   offsets   [device] int32 [E + 1] out: expert e's rows of the routed order
  *             are [offsets[e], offsets[e + 1])
- *   workspace [device] base_greedy_workspace_size(T, E) bytes, 256-aligned
+ *   workspace [device] base_greedy_workspace_size(T, E) bytes, 256-aligned;
+ *             any contents at entry. Calls that overlap in time (other
+ *             streams) need workspaces of their own.
  *   0 < T < 2^31, 0 < E <= 2048.
+ * With E <= 512 the call is one launch whose blocks meet at a grid barrier;
+ * it launches no more blocks than the device holds at once. Its waits are
+ * bounded: should one give up (a block never scheduled, e.g. while another
+ * stream's kernel holds every compute unit indefinitely), the tokens of the
+ * blocks that gave up are left unplaced and get assign[t] = -1.
  * Errors: BASE_ERR_INVALID_ARG, BASE_ERR_RANGE, BASE_ERR_WORKSPACE, BASE_ERR_HIP.
  *
  * base_gate_combine - Sec. 3.1, Eq. 1, fused into the return to token order:

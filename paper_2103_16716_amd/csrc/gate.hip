@@ -9,8 +9,12 @@
 // S[t, a_t] already computed for the routing.
 //
 // Kernels:
+//   greedy_route_kernel    E <= 512: the whole routing in one launch (argmax,
+//                          counts, grid barrier, offsets, placement), see below
+//   otherwise, or when the device cannot hold the blocks at once:
 //   greedy_count_kernel    argmax per token (16 lanes per token, 8 experts
 //                          per lane per chunk of 128) + per-block expert counts
+//   greedy_place_kernel    E <= 512: offsets and placement in one launch
 //   greedy_scan_kernel     per-expert exclusive scan over the blocks
 //   greedy_offsets_kernel  exclusive scan of the expert totals -> offsets
 //   greedy_scatter_kernel  stable counting sort -> perm
@@ -22,6 +26,12 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
+
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <mutex>
+#include <random>
 
 #include "base.h"
 #include "internal.hpp"
@@ -297,6 +307,239 @@ __global__ __launch_bounds__(kPlaceThreads) void greedy_place_kernel(const int32
     if (pos >= 0 && pos < T) perm[pos] = t;
 }
 
+// Greedy routing in one launch (E <= kPlaceMaxE): block b takes tokens
+// [b TB, (b + 1) TB), TB a multiple of kRouteTile.
+//   (1) argmax, 8 lanes per token (up to four 16-byte loads per lane in
+//       flight), the block's expert counts (LDS) to row b of the count
+//       matrix, and each token's expert kept in LDS;
+//   (2) a grid barrier;
+//   (3) every block sums the count matrix into the experts' totals and the
+//       counts of the blocks before its own, scans the totals into the
+//       offsets (block 0 writes them) and places each token at
+//           offsets[a] + (tokens of a in earlier blocks)
+//                      + (tokens of a before t in its own block),
+//       the same stable counting sort as the multi-launch path.
+// The host launches no more blocks than are resident at once, so every
+// block reaches the barrier. Its words sit in the workspace header and hold
+// anything at entry: block 0 clears the arrival count and the release word
+// and then publishes the launch's tag (nonzero); the other blocks arrive
+// only after they see the tag, the last arrival stores the tag into the
+// release word (on its own line, so the waits do not slow the arrivals),
+// and block 0 clears the published tag once every block has arrived, so
+// the next launch on the stream starts from a clean one. Waits are bounded: a block
+// that gives up (a block never scheduled) leaves its tokens unplaced and
+// marks them assign[t] = -1.
+constexpr int kRouteThreads = 1024;
+constexpr int kRouteLanes = 8;                                  // lanes per token
+constexpr int kRouteTile = kRouteThreads / kRouteLanes;         // 128 tokens per pass
+constexpr int kRouteMaxTB = 4096;                               // tokens per block (LDS)
+// Blocks per launch: more compute units read the scores sooner, more blocks
+// make the barrier and every block's read of the count matrix longer; the
+// measured optimum at 32768 x 128 and 65536 x 256 scores lies near 128-192.
+constexpr int kRouteMaxBlocks = 192;
+constexpr size_t kRouteHeader = 1024;                           // barrier words
+constexpr uint32_t kRoutePolls = 1u << 24;
+
+__device__ inline bool route_wait(const uint64_t *w, uint64_t want) {
+    for (uint32_t polls = 0;; ++polls) {
+        if (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == want) return true;
+        if (polls >= kRoutePolls) return false;
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+__global__ __launch_bounds__(kRouteThreads) void greedy_route_kernel(
+    const float *S, int T, int E, int TB, int32_t *assign, int32_t *perm, int32_t *offsets,
+    uint64_t *bar, int32_t *cnt, uint64_t tag) {
+    __shared__ int hist[kPlaceMaxE];   // the block's counts
+    __shared__ int pre[kPlaceMaxE];    // counts of the blocks before this one
+    __shared__ int tot[kPlaceMaxE];    // totals, then exclusive offsets
+    __shared__ int loc[kRouteMaxTB];   // experts of the block's tokens (-1: none)
+    __shared__ int part[kRouteThreads / 64];
+    __shared__ int ok;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.x, G = gridDim.x;
+    uint64_t *arrivals = bar;        // own 256-byte lines
+    uint64_t *armed = bar + 32;
+    uint64_t *release = bar + 64;
+    if (b == 0 && tid == 0) {
+        __hip_atomic_store(arrivals, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(release, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __hip_atomic_store(armed, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    for (int e = tid; e < E; e += kRouteThreads) { hist[e] = 0; pre[e] = 0; tot[e] = 0; }
+    __syncthreads();
+    // (1)
+    const int g = tid / kRouteLanes, gl = tid % kRouteLanes;
+    const int t0 = b * TB;
+    for (int i0 = 0; i0 < TB; i0 += kRouteTile) {
+        const int i = i0 + g;
+        const int t = t0 + i;
+        float best = -INFINITY;
+        int be = 0x7fffffff;
+        if (t < T) {
+            const float *row = S + (int64_t)t * E;
+            if ((E & 3) == 0) {
+                for (int base = 0; base < E; base += 16 * kRouteLanes) {
+                    float4 v[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int e = base + 4 * (kRouteLanes * u + gl);
+                        v[u] = e < E ? *reinterpret_cast<const float4 *>(row + e)
+                                     : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {   // ascending: ties keep the lower expert
+                        const int e = base + 4 * (kRouteLanes * u + gl);
+                        const float x[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const bool better = (e + q < E) & (x[q] > best);
+                            best = better ? x[q] : best;
+                            be = better ? e + q : be;
+                        }
+                    }
+                }
+            } else {
+                for (int e = gl; e < E; e += kRouteLanes) {
+                    const float x = row[e];
+                    const bool better = x > best;
+                    best = better ? x : best;
+                    be = better ? e : be;
+                }
+            }
+        }
+#pragma unroll
+        for (int off = kRouteLanes / 2; off > 0; off >>= 1) {
+            const float ob = __shfl_xor(best, off);
+            const int oe = __shfl_xor(be, off);
+            const bool take = (ob > best) | ((ob == best) & (oe < be));
+            best = take ? ob : best;
+            be = take ? oe : be;
+        }
+        if (gl == 0) {
+            int a = -1;
+            if (t < T) {
+                a = (be >= 0 && be < E) ? be : 0;   // a row of NaN/-inf goes to expert 0
+                assign[t] = a;
+                atomicAdd(&hist[a], 1);
+            }
+            loc[i] = a;
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += kRouteThreads) cnt[(int64_t)b * E + e] = hist[e];
+    // (2)
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this thread's stores are done
+    __syncthreads();
+    if (tid == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        bool fine = b == 0 || route_wait(armed, tag);
+        if (fine) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            const uint64_t arrived = __hip_atomic_fetch_add(arrivals, 1ull, __ATOMIC_RELAXED,
+                                                            __HIP_MEMORY_SCOPE_AGENT) + 1;
+            if (arrived == (uint64_t)G) {   // the last arrival releases the others
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                __hip_atomic_store(release, tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                fine = route_wait(release, tag);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        if (fine && b == 0)   // every block has arrived, so none still waits for the tag
+            __hip_atomic_store(armed, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = fine ? 1 : 0;
+    }
+    __syncthreads();
+    if (!ok) {
+        for (int i = tid; i < TB; i += kRouteThreads)
+            if (t0 + i < T) assign[t0 + i] = -1;
+        return;
+    }
+    // (3) thread (c, r): column c of the counts, rows r, r + rows, ...
+    if ((E & 3) == 0) {
+        const int q4 = E / 4;
+        const int rows = kRouteThreads / q4;
+        const int c = tid % q4, r0 = tid / q4;
+        if (r0 < rows) {
+            int tb[4] = {0, 0, 0, 0}, ta[4] = {0, 0, 0, 0};
+            const int4 *c4 = reinterpret_cast<const int4 *>(cnt);
+            for (int k0 = r0; k0 < G; k0 += 8 * rows) {
+                int4 v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int k = k0 + u * rows;
+                    v[u] = k < G ? c4[(int64_t)k * q4 + c] : make_int4(0, 0, 0, 0);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int k = k0 + u * rows;
+                    const int w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (k < b) tb[q] += w[q];
+                        ta[q] += w[q];
+                    }
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                atomicAdd(&pre[4 * c + q], tb[q]);
+                atomicAdd(&tot[4 * c + q], ta[q]);
+            }
+        }
+    } else {
+        const int rows = kRouteThreads / E;   // >= 2 as E <= kPlaceMaxE
+        const int c = tid % E, r0 = tid / E;
+        if (r0 < rows) {
+            int tb = 0, ta = 0;
+            for (int k = r0; k < G; k += rows) {
+                const int v = cnt[(int64_t)k * E + c];
+                if (k < b) tb += v;
+                ta += v;
+            }
+            atomicAdd(&pre[c], tb);
+            atomicAdd(&tot[c], ta);
+        }
+    }
+    __syncthreads();
+    {   // exclusive scan of the totals over the experts
+        const int v = tid < E ? tot[tid] : 0;
+        int incl = v;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(incl, off);
+            if (lane >= off) incl += o;
+        }
+        if (lane == 63) part[wave] = incl;
+        __syncthreads();
+        int base = 0;
+        for (int w = 0; w < wave; ++w) base += part[w];
+        if (tid < E) tot[tid] = base + incl - v + pre[tid];
+        if (b == 0 && tid < E) offsets[tid + 1] = base + incl;
+        if (b == 0 && tid == 0) offsets[0] = 0;
+    }
+    __syncthreads();
+    // rank within the block: the token's 8 lanes split the earlier tokens
+    for (int i0 = 0; i0 < TB; i0 += kRouteTile) {
+        const int i = i0 + g;
+        const int a = loc[i];
+        int r = 0;
+        if (a >= 0)
+            for (int j = gl; j < i; j += kRouteLanes) r += loc[j] == a;
+#pragma unroll
+        for (int off = kRouteLanes / 2; off > 0; off >>= 1) r += __shfl_xor(r, off);
+        if (gl == 0 && a >= 0) {
+            const int pos = tot[a] + r;
+            if (pos >= 0 && pos < T) perm[pos] = t0 + i;
+        }
+    }
+}
+
 // perm[offsets[a] + blk[block][a] + rank of t among the block's tokens of a] = t.
 __global__ __launch_bounds__(kGreedyTile) void greedy_scatter_kernel(const int32_t *assign, int T,
                                                                      int E, const int32_t *blk,
@@ -504,13 +747,71 @@ __global__ __launch_bounds__(64 * kDwWaves) void gate_dw_kernel(const void *H, c
 
 size_t greedy_workspace_size(int64_t T, int64_t E) {
     const int64_t nblk = (T + kGreedyTile - 1) / kGreedyTile;
-    return (size_t)(nblk * E * 4 + 255) & ~size_t(255);
+    return kRouteHeader + ((size_t)(nblk * E * 4 + 255) & ~size_t(255));
 }
+
+namespace {
+
+// Compute units and resident blocks of greedy_route_kernel per compute unit
+// on the current device (0 when the runtime cannot tell), looked up once.
+int route_capacity() {
+    constexpr int kDevices = 64;
+    static std::mutex mu;
+    static int known[kDevices] = {}, cap[kDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevices) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    std::lock_guard<std::mutex> lock(mu);
+    if (!known[dev]) {
+        int cus = 0, per_cu = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            cus = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu, reinterpret_cast<const void *>(greedy_route_kernel), kRouteThreads, 0) !=
+            hipSuccess)
+            per_cu = 0;
+        (void)hipGetLastError();
+        cap[dev] = cus > 0 && per_cu > 0 ? cus * per_cu : 0;
+        known[dev] = 1;
+    }
+    return cap[dev];
+}
+
+// A nonzero tag per launch, from a per-process random start.
+uint64_t route_tag() {
+    static std::atomic<uint64_t> next{[] {
+        std::random_device rd;
+        const uint64_t r = ((uint64_t)rd() << 32) ^ rd();
+        return r ^ (uint64_t)std::chrono::steady_clock::now().time_since_epoch().count();
+    }()};
+    const uint64_t t = next.fetch_add(1, std::memory_order_relaxed);
+    return t == 0 ? 1 : t;
+}
+
+}  // namespace
 
 hipError_t launch_greedy(const float *S, int64_t T, int64_t E, int32_t *assign, int32_t *perm,
                          int32_t *offsets, void *workspace, hipStream_t s) {
     const int nblk = (int)((T + kGreedyTile - 1) / kGreedyTile);
-    int32_t *blk = static_cast<int32_t *>(workspace);
+    uint64_t *bar = static_cast<uint64_t *>(workspace);
+    int32_t *blk = reinterpret_cast<int32_t *>(static_cast<char *>(workspace) + kRouteHeader);
+    if (E <= kPlaceMaxE) {
+        // One launch when every block can be resident: as few blocks as keep
+        // the tokens per block within the LDS list.
+        const int64_t cap = std::min<int64_t>(route_capacity(), kRouteMaxBlocks);
+        const int64_t tiles = (T + kRouteTile - 1) / kRouteTile;
+        if (cap > 0 && tiles <= cap * (kRouteMaxTB / kRouteTile)) {
+            const int64_t per = (tiles + cap - 1) / cap;          // passes per block
+            const int64_t TB = per * kRouteTile;
+            const int64_t G = (T + TB - 1) / TB;                  // <= cap, <= nblk
+            hipLaunchKernelGGL(greedy_route_kernel, dim3((unsigned)G), dim3(kRouteThreads), 0, s,
+                               S, (int)T, (int)E, (int)TB, assign, perm, offsets, bar, blk,
+                               route_tag());
+            return hipGetLastError();
+        }
+    }
     hipLaunchKernelGGL(greedy_count_kernel, dim3(nblk), dim3(256), (size_t)E * sizeof(int), s, S,
                        (int)T, (int)E, assign, blk);
     if (E <= kPlaceMaxE) {

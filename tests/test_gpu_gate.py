@@ -43,16 +43,38 @@ def test_greedy_routing_bit_exact(name):
     np.testing.assert_array_equal(host(off), oracle.expert_offsets(a_ref, Sh.shape[1]))
 
 
-@pytest.mark.parametrize("T,E", [(1000, 70), (257, 3), (64, 1), (5000, 2048)])
+@pytest.mark.parametrize("T,E", [(1000, 70), (257, 3), (64, 1), (5000, 2048), (300000, 16),
+                                 (4099, 512), (2000, 500), (3001, 513), (77, 130)])
 def test_greedy_routing_ragged(T, E):
+    """Single-launch routing (E <= 512: several token passes per block at T =
+    300000, the widest E, E/4 not a power of two, scalar loads for E % 4 != 0)
+    and the multi-launch path (E > 512)."""
     rng = np.random.Generator(np.random.PCG64(T + E))
     S = rng.standard_normal((T, E), dtype=np.float32)
     S[::7, :] = np.round(S[::7, :])          # ties: the lowest expert must win
+    S[T // 2, :] = -np.inf                   # a row with no finite score: expert 0
+    S[T // 3, :] = -np.inf
+    S[T // 3, E - 1] = 0.0
     a, perm, off = pb.greedy_assign(dev(S))
     a_ref = oracle.greedy_argmax(S)
     np.testing.assert_array_equal(host(a), a_ref)
     np.testing.assert_array_equal(host(perm), oracle.stable_perm(a_ref, E))
     np.testing.assert_array_equal(host(off), oracle.expert_offsets(a_ref, E))
+
+
+def test_greedy_routing_reuses_a_workspace():
+    """The workspace holds anything at the first call (here all bytes 0xA5)
+    and one workspace serves calls of different shapes in a row."""
+    n = int(pb.lib().base_greedy_workspace_size(40000, 128))
+    ws = torch.full((n,), 0xA5, dtype=torch.uint8, device="cuda")
+    for T, E in ((40000, 128), (40000, 128), (1000, 64), (33333, 100)):
+        rng = np.random.Generator(np.random.PCG64(7 * T + E))
+        S = rng.standard_normal((T, E), dtype=np.float32)
+        a, perm, off = pb.greedy_assign(dev(S), workspace=ws)
+        a_ref = oracle.greedy_argmax(S)
+        np.testing.assert_array_equal(host(a), a_ref)
+        np.testing.assert_array_equal(host(perm), oracle.stable_perm(a_ref, E))
+        np.testing.assert_array_equal(host(off), oracle.expert_offsets(a_ref, E))
 
 
 def _routing(kind, S):
