@@ -118,13 +118,17 @@ def bench_layer(args) -> None:
     offsets = pb.balanced_offsets(T, E, H.device)
     gws = torch.empty(max(int(pb.lib().base_greedy_workspace_size(T, E)), 256),
                       dtype=torch.uint8, device="cuda")
+    ga = torch.empty(T, dtype=torch.int32, device="cuda")
+    gp = torch.empty(T, dtype=torch.int32, device="cuda")
+    go = torch.empty(E + 1, dtype=torch.int32, device="cuda")
     stream = torch.cuda.current_stream()
     names = ("greedy", "combine", "backward")
 
     def step(evs=None):
         if evs is not None:
             evs[0].record(stream)
-        pb.greedy_assign(S, workspace=gws, stream=stream)
+        pb.greedy_assign(S, workspace=gws, stream=stream, out_assign=ga, out_perm=gp,
+                         out_offsets=go)
         if evs is not None:
             evs[1].record(stream)
         pb.gate_combine(F, H, S, r.assign, r.perm, out=Y, stream=stream)

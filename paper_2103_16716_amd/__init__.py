@@ -357,16 +357,27 @@ def permute_batched(x, perm, shuffle=None, inverse: bool = False, out=None, stre
     return out
 
 
-def greedy_assign(S, workspace=None, stream=None):
+def greedy_assign(S, workspace=None, stream=None, out_assign=None, out_perm=None,
+                  out_offsets=None):
     """Test-time routing (base_greedy_assign): (assign [T], perm [T],
-    offsets [E + 1]) with every token at its best expert."""
+    offsets [E + 1]) with every token at its best expert. The out_* tensors
+    (int32, contiguous, on S's device), when given, receive the results, so
+    a loop of calls allocates nothing."""
     torch = _torch()
     _need_device(S)
     T, E = S.shape
     dev = S.device
-    a = torch.empty(T, dtype=torch.int32, device=dev)
-    perm = torch.empty(T, dtype=torch.int32, device=dev)
-    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+
+    def out(x, n):
+        if x is None:
+            return torch.empty(n, dtype=torch.int32, device=dev)
+        if x.dtype != torch.int32 or x.numel() != n or not x.is_contiguous() or x.device != dev:
+            raise ValueError(f"greedy_assign: an output needs {n} contiguous int32 on {dev}")
+        return x
+
+    a = out(out_assign, T)
+    perm = out(out_perm, T)
+    offsets = out(out_offsets, E + 1)
     n = int(lib().base_greedy_workspace_size(T, E))
     if workspace is None:
         workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)

@@ -64,13 +64,17 @@ def test_greedy_routing_ragged(T, E):
 
 def test_greedy_routing_reuses_a_workspace():
     """The workspace holds anything at the first call (here all bytes 0xA5)
-    and one workspace serves calls of different shapes in a row."""
+    and one workspace serves calls of different shapes in a row; the results
+    go to the caller's output tensors."""
     n = int(pb.lib().base_greedy_workspace_size(40000, 128))
     ws = torch.full((n,), 0xA5, dtype=torch.uint8, device="cuda")
     for T, E in ((40000, 128), (40000, 128), (1000, 64), (33333, 100)):
         rng = np.random.Generator(np.random.PCG64(7 * T + E))
         S = rng.standard_normal((T, E), dtype=np.float32)
-        a, perm, off = pb.greedy_assign(dev(S), workspace=ws)
+        outs = [torch.full((n,), -7, dtype=torch.int32, device="cuda") for n in (T, T, E + 1)]
+        a, perm, off = pb.greedy_assign(dev(S), workspace=ws, out_assign=outs[0],
+                                        out_perm=outs[1], out_offsets=outs[2])
+        assert all(x is y for x, y in zip((a, perm, off), outs))
         a_ref = oracle.greedy_argmax(S)
         np.testing.assert_array_equal(host(a), a_ref)
         np.testing.assert_array_equal(host(perm), oracle.stable_perm(a_ref, E))
