@@ -43,12 +43,15 @@ def test_greedy_routing_bit_exact(name):
     np.testing.assert_array_equal(host(off), oracle.expert_offsets(a_ref, Sh.shape[1]))
 
 
-@pytest.mark.parametrize("T,E", [(1000, 70), (257, 3), (64, 1), (5000, 2048), (300000, 16),
-                                 (4099, 512), (2000, 500), (3001, 513), (77, 130)])
+@pytest.mark.parametrize("T,E", [(1000, 70), (257, 3), (64, 1), (1, 5), (5000, 2048),
+                                 (300000, 16), (4099, 512), (2000, 500), (3001, 513), (77, 130),
+                                 (800000, 8)])
 def test_greedy_routing_ragged(T, E):
     """Single-launch routing (E <= 512: several token passes per block at T =
     300000, the widest E, E/4 not a power of two, scalar loads for E % 4 != 0)
-    and the multi-launch path (E > 512)."""
+    and the multi-launch paths: count + place (E <= 512 with more tokens than
+    192 blocks of 4096 hold, T = 800000) and count + scan + offsets + scatter
+    (E > 512)."""
     rng = np.random.Generator(np.random.PCG64(T + E))
     S = rng.standard_normal((T, E), dtype=np.float32)
     S[::7, :] = np.round(S[::7, :])          # ties: the lowest expert must win
