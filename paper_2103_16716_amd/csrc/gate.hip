@@ -626,6 +626,8 @@ __global__ __launch_bounds__(256) void gate_combine_kernel(const void *F, const 
 // Backward per routed row k (one block per row, grid-stride): with t =
 // perm[k], a = assign[t], g = sigmoid(S[t, a]):
 //   dS[t] = g (1 - g) (dY[t] . F[k]);  dF[k] = g dY[t];  dH[t] = dY[t] + dS[t] W[a].
+constexpr int kRowRegs = 2;   // 16-byte chunks of a row a thread keeps in registers
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void gate_rows_kernel(const void *dY, const void *F,
                                                         const void *W, const float *S,
@@ -634,6 +636,65 @@ __global__ __launch_bounds__(256) void gate_rows_kernel(const void *dY, const vo
                                                         float *dS, int T, int E, int ncs) {
     using Ck = Chunk<BF16>;
     __shared__ float part[4];
+    if (ncs <= kRowRegs * (int)blockDim.x) {
+        // The row fits the block's registers: dY, F and W are loaded once,
+        // before the reduction, and dF needs no dS, so it is stored first;
+        // after the reduction only dH remains. Same arithmetic, same order.
+        for (int k = blockIdx.x; k < T; k += gridDim.x) {
+            const int t = perm[k];
+            const bool ok = t >= 0 && t < T;
+            const int tt = ok ? t : 0;
+            int a = assign[tt];
+            a = (a >= 0 && a < E) ? a : 0;
+            const float g = gate_of(S[(int64_t)tt * E + a]);
+            float y[kRowRegs][8], f[kRowRegs][8], w[kRowRegs][8];
+#pragma unroll
+            for (int r = 0; r < kRowRegs; ++r) {
+                const int j = threadIdx.x + r * blockDim.x;
+                if (j < ncs) {
+                    Ck::load(dY, (int64_t)tt * ncs + j, y[r]);
+                    Ck::load(F, (int64_t)k * ncs + j, f[r]);
+                    Ck::load(W, (int64_t)a * ncs + j, w[r]);
+                }
+            }
+            float dot = 0.0f;
+#pragma unroll
+            for (int r = 0; r < kRowRegs; ++r) {
+                const int j = threadIdx.x + r * blockDim.x;
+                if (j < ncs) {
+#pragma unroll
+                    for (int q = 0; q < Ck::kN; ++q) dot = fmaf(y[r][q], f[r][q], dot);
+                    if (ok) {
+                        float o[8];
+#pragma unroll
+                        for (int q = 0; q < Ck::kN; ++q) o[q] = g * y[r][q];
+                        Ck::store(dF, (int64_t)k * ncs + j, o);
+                    }
+                }
+            }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
+            if (lane_of() == 0) part[threadIdx.x >> 6] = dot;
+            __syncthreads();
+            dot = 0.0f;
+            for (int v = 0; v < (int)(blockDim.x >> 6); ++v) dot += part[v];
+            __syncthreads();
+            const float ds = g * (1.0f - g) * dot;
+            if (!ok) continue;
+            if (threadIdx.x == 0) dS[t] = ds;
+#pragma unroll
+            for (int r = 0; r < kRowRegs; ++r) {
+                const int j = threadIdx.x + r * blockDim.x;
+                if (j < ncs) {
+                    float o[8];
+#pragma unroll
+                    for (int q = 0; q < Ck::kN; ++q) o[q] = fmaf(ds, w[r][q], y[r][q]);
+                    Ck::store(dH, (int64_t)t * ncs + j, o);
+                }
+            }
+        }
+        return;
+    }
     for (int k = blockIdx.x; k < T; k += gridDim.x) {
         const int t = perm[k];
         const bool ok = t >= 0 && t < T;
